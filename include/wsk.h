@@ -1,0 +1,293 @@
+/*
+ * wsk.h -- C ABI of a partitioned KV cache for CPU-GPU split decode attention
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * The cache follows the format of Yu, Dong, Liao, "Physically Partitioned
+ * KVCache Format for CPU-GPU Load Balancing in MoE Inference":
+ *
+ *   - Sec. 3 and Sec. 4.3 (i): every cached byte gets its one physical home
+ *     when it is written, and placed data never moves afterwards.  Here a
+ *     sequence's CPU partition is the prefix [0, s) and its GPU partition the
+ *     suffix [s, L); s is fixed when the sequence is opened.
+ *   - Sec. 4.1: each partition is made of fixed-size blocks of block_tokens
+ *     tokens on an absolute grid (block k holds positions [k*Bk, (k+1)*Bk)).
+ *     A block straddling s has a slot in both pools, each holding only its
+ *     own side's positions.
+ *   - Sec. 4.3: the interface is a PartitionSpec plus init / append / views
+ *     (and flush, which this library does not implement: it has no D-window
+ *     eviction).  The GPU side additionally attends its own range and merges
+ *     partial results (Sec. 4.2, last paragraph; Sec. 5.1).
+ *
+ * Conventions for every call:
+ *   - The return value is a status: WSK_OK (0) or a negative WSK_E* code.
+ *     wsk_last_error() returns a message for the calling thread's last
+ *     failure.  No C++ exception crosses this boundary.
+ *   - A failed call changes no cache state and enqueues no GPU work, except
+ *     WSK_EHIP, which reports a HIP runtime failure after the fact.
+ *   - "stream" is a hipStream_t passed as void* (NULL = the legacy default
+ *     stream).  GPU work is enqueued on it in call order; results in device
+ *     memory are ready when the stream reaches that point.
+ *   - bf16 values are raw IEEE bfloat16 bits (uint16_t storage).
+ *   - A cache is not thread-safe: serialise calls on one cache.
+ */
+#ifndef WSK_H
+#define WSK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define WSK_OK 0
+#define WSK_EINVAL (-1) /* malformed argument or spec                         */
+#define WSK_ENOMEM (-2) /* a block pool (or a host allocation) is exhausted   */
+#define WSK_ERANGE (-3) /* a position or range outside what the call allows   */
+#define WSK_EHIP (-4)   /* the HIP runtime reported an error                  */
+#define WSK_ESTATE (-5) /* wrong state: sequence not open / already open, or
+                           a GPU call on a cache created without a device      */
+
+#define WSK_KIND_GQA 0 /* per-head K and V rows, grouped-query attention     */
+#define WSK_KIND_MLA 1 /* one compressed latent row per token (MLA)          */
+
+#define WSK_PART_CPU 0
+#define WSK_PART_GPU 1
+
+/* Largest number of query heads one KV head may serve in a GQA cache.       */
+#define WSK_MAX_GROUP 64
+
+/*
+ * PartitionSpec (Sec. 4.3): the physical layout of one layer's cache.  The
+ * paper's spec also carries the roofline parameters of its split policy;
+ * this library takes the split per sequence instead (wsk_seq_open).
+ *
+ *   kind               WSK_KIND_GQA or WSK_KIND_MLA
+ *   n_q_heads          query heads (MLA: heads sharing the latent)
+ *   n_kv_heads         GQA: KV heads, dividing n_q_heads with
+ *                      n_q_heads / n_kv_heads <= WSK_MAX_GROUP; MLA: 1
+ *   head_dim           GQA: K/V width, must be 128.  MLA: ignored.
+ *   latent_dim         MLA: compressed latent width, must be 512.  GQA: 0.
+ *   rope_dim           MLA: decoupled RoPE key width, must be 64.  GQA: 0.
+ *   block_tokens       tokens per block: 64, 128 or 256 (each divides the
+ *                      paper's eviction batch of 256, Sec. 4.2)
+ *   max_seqs           sequence ids are 0 .. max_seqs-1
+ *   max_seq_len        positions per sequence, >= 1
+ *   device_pool_blocks slots in the GPU pool (HBM), >= 0
+ *   host_pool_blocks   slots in the CPU pool (pageable host memory), >= 0
+ *   softmax_scale      multiplier of q.k before the softmax, finite and > 0
+ *
+ * Slot layout, identical in both pools (bf16):
+ *   GQA  slot = [n_kv_heads][2][block_tokens][head_dim]   (index 0 = K, 1 = V)
+ *   MLA  slot = [block_tokens][latent_dim + rope_dim]     (latent | rope)
+ */
+typedef struct wsk_partition_spec {
+    int32_t kind;
+    int32_t n_q_heads;
+    int32_t n_kv_heads;
+    int32_t head_dim;
+    int32_t latent_dim;
+    int32_t rope_dim;
+    int32_t block_tokens;
+    int32_t max_seqs;
+    int32_t max_seq_len;
+    int32_t reserved; /* must be 0 */
+    int64_t device_pool_blocks;
+    int64_t host_pool_blocks;
+    float softmax_scale;
+} wsk_partition_spec;
+
+typedef struct wsk_cache wsk_cache;
+
+/* Where one cached position lives (wsk_route). */
+typedef struct wsk_loc {
+    int32_t part;          /* WSK_PART_CPU or WSK_PART_GPU            */
+    int32_t logical_block; /* pos / block_tokens                      */
+    int32_t slot;          /* slot index in that partition's pool     */
+    int32_t offset;        /* pos % block_tokens: row within the slot */
+} wsk_loc;
+
+/*
+ * Zero-copy view of one partition of one sequence (Sec. 4.3 (iii)).
+ * Token p of the partition (start <= p < end), KV head g, lives at
+ *   (char*)pool + table[p / block_tokens] * slot_bytes + g * head_bytes
+ *                + (p % block_tokens) * row_bytes            (K, or MLA row)
+ * and its V row at that address + v_bytes (GQA only).
+ * CPU views hold host addresses; GPU views hold device addresses (the table
+ * too).  The pointers are borrowed: they stay valid until wsk_destroy,
+ * because placed blocks never move (Sec. 4.2).
+ */
+typedef struct wsk_view {
+    void *pool;
+    const int32_t *table; /* this sequence's row: slot per logical block, -1 = none */
+    int64_t slot_bytes;
+    int64_t head_bytes;
+    int64_t v_bytes;
+    int64_t row_bytes;
+    int32_t start, end;   /* positions held: CPU [0, min(s, L)), GPU [min(s, L), L) */
+    int32_t block_tokens;
+    int32_t is_device;
+} wsk_view;
+
+/* Message of the calling thread's last failure ("" if none). */
+const char *wsk_last_error(void);
+
+/*
+ * Validate *spec and build a cache (Sec. 4.3 "init").  device >= 0 selects
+ * the HIP device that owns the GPU pool; both pools and the block tables
+ * are allocated here, once, and zero-filled.  device = -1 builds a
+ * host-only cache that never calls HIP: routing, wsk_reserve, wsk_route
+ * and CPU views work; every call that moves data to or computes on the GPU
+ * returns WSK_ESTATE.  The library owns the cache; free it with wsk_destroy.
+ * Errors: EINVAL (spec), ENOMEM (host allocation), EHIP (device allocation).
+ */
+int wsk_init(const wsk_partition_spec *spec, int device, wsk_cache **out);
+
+/* Free both pools and tables.  The caller must have synchronised every
+ * stream that still uses the cache.  NULL is accepted. */
+int wsk_destroy(wsk_cache *cache);
+
+/* Copy of the cache's spec. */
+int wsk_get_spec(const wsk_cache *cache, wsk_partition_spec *out);
+
+/*
+ * Open sequence seq with split s >= 0: positions p < s will live in the CPU
+ * partition and p >= s in the GPU partition (the paper's sequence-dimension
+ * split, Sec. 5.1, fixed at write time).  Errors: EINVAL (seq or s out of
+ * range), ESTATE (already open).
+ */
+int wsk_seq_open(wsk_cache *cache, int32_t seq, int32_t split);
+
+/* Close seq and return all its slots to the free sets (in-place block
+ * reclamation at session end, Sec. 4.2).  Work already enqueued that reads
+ * those slots must be ordered before any later write that reuses them.
+ * Errors: EINVAL, ESTATE (not open). */
+int wsk_seq_close(wsk_cache *cache, int32_t seq);
+
+/* Current length L and split s of an open sequence. */
+int wsk_seq_info(const wsk_cache *cache, int32_t seq, int32_t *length, int32_t *split);
+
+/*
+ * Routing decision only (Sec. 4.3 (i), "append is the routing decision"):
+ * give positions [L, L+n) of seq their homes, taking slots lowest-free-first,
+ * and set L += n, without writing data.  The rows hold whatever the slot held
+ * before (zeros for never-used slots) until the caller fills them, e.g.
+ * through wsk_views.  All-or-nothing: ENOMEM leaves the cache unchanged.
+ * Errors: EINVAL (n < 0 or past max_seq_len), ESTATE, ENOMEM.
+ */
+int wsk_reserve(wsk_cache *cache, int32_t seq, int32_t n);
+
+/*
+ * Bulk write of positions [pos0, pos0+n) of seq (prefill routed in one shot,
+ * Sec. 4.2): each row goes to its partition's pool.  pos0 must equal the
+ * current length L.  k, v are HOST pointers, token-major:
+ *   GQA  k, v: bf16 [n][n_kv_heads][head_dim]
+ *   MLA  k:    bf16 [n][latent_dim + rope_dim], v must be NULL
+ * CPU rows are copied with memcpy; GPU rows go host -> device through a
+ * staging buffer and a scatter kernel on stream.  The call returns after the
+ * data is in place (it synchronises stream), so k and v may be freed at once.
+ * All-or-nothing for routing (ENOMEM changes nothing).
+ * Errors: EINVAL, ESTATE, ERANGE (pos0 != L), ENOMEM, EHIP.
+ */
+int wsk_write(wsk_cache *cache, int32_t seq, int32_t pos0, int32_t n,
+              const void *k, const void *v, void *stream);
+
+/*
+ * Decode append (Sec. 4.2: new entries join the GPU side at no transfer
+ * cost): one new row at position L of each listed sequence, then L += 1.
+ * seq_ids is a HOST array of n distinct open sequences; k_new, v_new are
+ * DEVICE pointers, row i for seq_ids[i]:
+ *   GQA  k_new, v_new: bf16 [n][n_kv_heads][head_dim]
+ *   MLA  k_new:        bf16 [n][latent_dim + rope_dim], v_new NULL
+ * Routing (slot allocation) happens on the host during the call; the copy
+ * runs asynchronously on stream, and the inputs must stay valid until the
+ * stream reaches it.  Every appended position must be in the GPU partition
+ * (L >= s); rows below the split are written with wsk_write.
+ * Errors: EINVAL (n <= 0, duplicate or bad ids), ESTATE, ERANGE (position
+ * below the split or past max_seq_len), ENOMEM, EHIP.
+ */
+int wsk_append(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
+               const void *k_new, const void *v_new, void *stream);
+
+/* Home of position pos of seq.  Errors: EINVAL, ESTATE, ERANGE (pos >= L). */
+int wsk_route(const wsk_cache *cache, int32_t seq, int32_t pos, wsk_loc *out);
+
+/* Zero-copy views of both partitions of seq (Sec. 4.3 "views").  Either
+ * output pointer may be NULL.  The GPU view of a host-only cache has NULL
+ * pool and table.  Errors: EINVAL, ESTATE. */
+int wsk_views(const wsk_cache *cache, int32_t seq, wsk_view *cpu, wsk_view *gpu);
+
+/*
+ * Bytes of device workspace wsk_attend needs for the same sequences and
+ * ranges (the split-KV chunk partials).  Same argument rules as wsk_attend.
+ */
+int wsk_attend_workspace(const wsk_cache *cache, int32_t n, const int32_t *seq_ids,
+                         const int32_t *start, const int32_t *end, size_t *bytes);
+
+/*
+ * Decode attention over the GPU partition (the GPU engine of Sec. 5.1): for
+ * each i < n, every query head of seq_ids[i] attends positions
+ * [start[i], end[i]), which must lie in the GPU partition:
+ * min(s, L) <= start <= end <= L.  The output
+ * is a normalised partial and its log-sum-exp (Sec. 4.2 last paragraph):
+ *   O[i][h]   = sum_j softmax_j(scale * q.k_j) v_j
+ *   LSE[i][h] = ln sum_j exp(scale * q.k_j)
+ * An empty range gives O = 0, LSE = -inf and reads no KV.
+ * Query head h reads KV head floor(h / (n_q_heads / n_kv_heads)).
+ * seq_ids, start, end: HOST arrays (seq ids need not be distinct).
+ * q, o, lse, ws: DEVICE pointers owned by the caller:
+ *   GQA  q bf16 [n][n_q_heads][head_dim]       o fp32 [n][n_q_heads][head_dim]
+ *   MLA  q bf16 [n][n_q_heads][latent+rope]    o fp32 [n][n_q_heads][latent_dim]
+ *        (the absorbed query q_lat | q_rope)   (the latent output, before expansion)
+ *   lse fp32 [n][n_q_heads] (natural log)
+ *   ws   at least wsk_attend_workspace() bytes, 256-byte aligned
+ * Softmax and accumulation are fp32 from bf16 inputs.
+ * Errors: EINVAL, ESTATE, ERANGE (range outside the GPU partition), EHIP.
+ */
+int wsk_attend(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
+               const int32_t *start, const int32_t *end, const void *q,
+               float *o, float *lse, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * LSE merge of two partials over disjoint key sets (Sec. 4.2, Sec. 5.1),
+ * row by row, on the GPU:
+ *   m = max(lse_a, lse_b);  m = -inf  ->  O = 0, LSE = -inf
+ *   otherwise w_x = exp(lse_x - m),  O = (w_a O_a + w_b O_b) / (w_a + w_b),
+ *   LSE = m + ln(w_a + w_b)
+ * All pointers are DEVICE pointers: o_* fp32 [rows][width], lse_* fp32
+ * [rows].  o_out/lse_out may alias o_b/lse_b (or o_a/lse_a).  o_bf16, if not
+ * NULL, also receives O rounded to bf16 (nearest-even), [rows][width].
+ * Errors: EINVAL (rows < 0, width <= 0 or width % 4 != 0), EHIP.
+ */
+int wsk_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a,
+              const float *o_b, const float *lse_b, float *o_out, float *lse_out,
+              uint16_t *o_bf16, void *stream);
+
+/*
+ * MLA query-side projection (Sec. 6.1, compressed-MLA variant): for each of
+ * n tokens and H heads, q_lat[h] = W_UK[h]^T q_nope[h] with fp32
+ * accumulation, rounded once to bf16 (nearest-even).  DEVICE pointers:
+ *   q_nope bf16 [n][H][dn], w_uk bf16 [H][dn][dl],
+ *   out: row (i, h) is written at out + (i*H + h) * out_stride elements
+ *   (out_stride >= dl; pass latent+rope to fill the first dl elements of an
+ *   attend query buffer in place).
+ * Supported: dl % 64 == 0, 1 <= dn <= 256.  Errors: EINVAL, EHIP.
+ */
+int wsk_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t *q_nope,
+                   const uint16_t *w_uk, uint16_t *out, int64_t out_stride, void *stream);
+
+/*
+ * MLA output-side expansion (Sec. 6.1): O[i][h] = W_UV[h]^T O_lat[i][h],
+ * fp32 accumulation.  DEVICE pointers: o_lat fp32 [n][H][dl],
+ * w_uv bf16 [H][dl][dv], o fp32 [n][H][dv].
+ * Supported: dv % 64 == 0, 1 <= dl <= 1024.  Errors: EINVAL, EHIP.
+ */
+int wsk_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat,
+                   const uint16_t *w_uv, float *o, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WSK_H */

@@ -1,0 +1,288 @@
+// Small kernels of the decode path, gfx950: chunk combine, LSE merge,
+// decode append, bulk scatter, MLA query absorption and output expansion.
+
+#include "wsk_internal.h"
+
+namespace wsk {
+namespace {
+
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// ---------------------------------------------------------------------------
+// Chunk combine: O = sum_c w_c O_c / sum_c w_c, w_c = exp(lse_c - max lse),
+// LSE = max + ln sum w_c.  One wavefront per (sequence, head); each lane owns
+// WIDTH/64 consecutive output elements.  No chunk (empty range): O = 0,
+// LSE = -inf.
+// ---------------------------------------------------------------------------
+template <int WIDTH>
+__global__ __launch_bounds__(64) void combine_kernel(const CombineParams p) {
+    constexpr int PER = WIDTH / 64;
+    const int row = blockIdx.x;                 // i * H + h
+    const int i = row / p.n_q_heads;
+    const int h = row - i * p.n_q_heads;
+    const int c0 = p.chunk_begin[i];
+    const int nc = p.chunk_begin[i + 1] - c0;
+    const int lane = threadIdx.x;
+    float acc[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+    if (nc == 0) {
+#pragma unroll
+        for (int e = 0; e < PER; ++e) p.o[(int64_t)row * WIDTH + lane * PER + e] = 0.f;
+        if (lane == 0) p.lse[row] = -INFINITY;
+        return;
+    }
+    const float *pl = p.part_lse + (int64_t)c0 * p.n_q_heads + h;
+    float m = -INFINITY;
+    for (int c = 0; c < nc; ++c) m = fmaxf(m, pl[(int64_t)c * p.n_q_heads]);
+    float den = 0.f;
+    for (int c = 0; c < nc; ++c) {
+        const float w = __expf(pl[(int64_t)c * p.n_q_heads] - m);
+        den += w;
+        const float *po = p.part_o + ((int64_t)(c0 + c) * p.n_q_heads + h) * WIDTH + lane * PER;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) acc[e] = fmaf(w, po[e], acc[e]);
+    }
+    const float inv = 1.f / den;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) p.o[(int64_t)row * WIDTH + lane * PER + e] = acc[e] * inv;
+    if (lane == 0) p.lse[row] = m + __logf(den);
+}
+
+// ---------------------------------------------------------------------------
+// LSE merge of two partials, 4 elements per thread.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void merge_kernel(int32_t rows, int32_t width, const float *o_a,
+                                                    const float *lse_a, const float *o_b,
+                                                    const float *lse_b, float *o_out, uint16_t *o_bf16) {
+    const int64_t q4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // float4 index
+    const int64_t total4 = (int64_t)rows * width / 4;
+    if (q4 >= total4) return;
+    const int64_t e0 = q4 * 4;
+    const int64_t r = e0 / width;
+    const float la = lse_a[r], lb = lse_b[r];
+    const float m = fmaxf(la, lb);
+    // The row's LSE is written by merge_lse_kernel afterwards: lse_out may
+    // alias lse_a or lse_b, which every element of the row reads here.
+    f32x4 y;
+    if (m == -INFINITY) {
+        y = f32x4{0.f, 0.f, 0.f, 0.f};
+    } else {
+        const float wa = __expf(la - m), wb = __expf(lb - m);
+        const float inv = 1.f / (wa + wb);
+        const f32x4 a = *reinterpret_cast<const f32x4 *>(o_a + e0);
+        const f32x4 b = *reinterpret_cast<const f32x4 *>(o_b + e0);
+        y = (wa * a + wb * b) * inv;
+    }
+    *reinterpret_cast<f32x4 *>(o_out + e0) = y;
+    if (o_bf16) {
+        uint16_t *d = o_bf16 + e0;
+        d[0] = f32_to_bf16(y.x);
+        d[1] = f32_to_bf16(y.y);
+        d[2] = f32_to_bf16(y.z);
+        d[3] = f32_to_bf16(y.w);
+    }
+}
+
+__global__ __launch_bounds__(256) void merge_lse_kernel(int32_t rows, const float *lse_a,
+                                                        const float *lse_b, float *lse_out) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= rows) return;
+    const float la = lse_a[r], lb = lse_b[r];
+    const float m = fmaxf(la, lb);
+    lse_out[r] = (m == -INFINITY) ? -INFINITY : m + __logf(__expf(la - m) + __expf(lb - m));
+}
+
+// ---------------------------------------------------------------------------
+// Decode append: one workgroup per appended row (all KV heads, K and V).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void append_kernel(const AppendParams p) {
+    const int r = blockIdx.x;
+    const int64_t dst0 = p.dst[r];
+    if (threadIdx.x == 0 && p.tab_index[r] >= 0) p.table[p.tab_index[r]] = p.tab_slot[r];
+    const int row16 = p.row_elems / 8;                 // 16-byte pieces per row
+    if (p.kind == 0) {
+        // source [n][Hkv][D]; destination head g at dst0 + g*2*Bk*D (K), + Bk*D (V)
+        const int pieces = p.n_kv_heads * row16;
+        for (int t = threadIdx.x; t < 2 * pieces; t += blockDim.x) {
+            const int which = t / pieces;              // 0 = K, 1 = V
+            const int q = t - which * pieces;
+            const int g = q / row16;
+            const int k = q - g * row16;
+            const uint16_t *src = (which ? p.v_new : p.k_new) + ((int64_t)r * p.n_kv_heads + g) * p.row_elems;
+            uint16_t *dst = p.pool + dst0 + (int64_t)g * 2 * p.block_tokens * p.row_elems +
+                            (int64_t)which * p.block_tokens * p.row_elems;
+            reinterpret_cast<u32x4 *>(dst)[k] = reinterpret_cast<const u32x4 *>(src)[k];
+        }
+    } else {
+        const uint16_t *src = p.k_new + (int64_t)r * p.row_elems;
+        for (int k = threadIdx.x; k < row16; k += blockDim.x)
+            reinterpret_cast<u32x4 *>(p.pool + dst0)[k] = reinterpret_cast<const u32x4 *>(src)[k];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Bulk scatter of staged rows into the GPU partition.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void scatter_kernel(const ScatterParams p) {
+    const int row16 = p.row_elems / 8;
+    const int per_pos = (p.kind == 0) ? 2 * p.n_kv_heads * row16 : row16;
+    const int64_t total = (int64_t)p.m * per_pos;
+    const int bshift = __builtin_ctz(p.block_tokens);
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+         t += (int64_t)gridDim.x * blockDim.x) {
+        const int j = (int)(t / per_pos);
+        int q = (int)(t - (int64_t)j * per_pos);
+        const int pos = p.p0 + j;
+        const int blk = pos >> bshift;
+        const int off = pos - (blk << bshift);
+        const int64_t slot = p.table_row[blk];
+        if (p.kind == 0) {
+            const int which = q / (p.n_kv_heads * row16);
+            q -= which * p.n_kv_heads * row16;
+            const int g = q / row16;
+            const int k = q - g * row16;
+            const uint16_t *src = (which ? p.src_v : p.src_k) + ((int64_t)j * p.n_kv_heads + g) * p.row_elems;
+            uint16_t *dst = p.pool + slot * p.slot_elems +
+                            ((int64_t)(g * 2 + which) * p.block_tokens + off) * p.row_elems;
+            reinterpret_cast<u32x4 *>(dst)[k] = reinterpret_cast<const u32x4 *>(src)[k];
+        } else {
+            const uint16_t *src = p.src_k + (int64_t)j * p.row_elems;
+            uint16_t *dst = p.pool + slot * p.slot_elems + (int64_t)off * p.row_elems;
+            reinterpret_cast<u32x4 *>(dst)[q] = reinterpret_cast<const u32x4 *>(src)[q];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// MLA absorption: q_lat[i][h][l] = sum_k q_nope[i][h][k] * W_UK[h][k][l],
+// fp32 accumulation, one bf16 rounding.  Workgroup = (head, 64 latent
+// columns, 8 tokens); W_UK is read once per workgroup, coalesced over l.
+// ---------------------------------------------------------------------------
+constexpr int kAbsorbTok = 8;
+
+__global__ __launch_bounds__(64) void absorb_kernel(int32_t n, int32_t H, int32_t dn, int32_t dl,
+                                                    const uint16_t *q_nope, const uint16_t *w_uk,
+                                                    uint16_t *out, int64_t out_stride) {
+    __shared__ float sq[kAbsorbTok][256];
+    const int h = blockIdx.x;
+    const int l = blockIdx.y * 64 + threadIdx.x;
+    const int i0 = blockIdx.z * kAbsorbTok;
+    const int nt = min(kAbsorbTok, n - i0);
+    for (int t = threadIdx.x; t < kAbsorbTok * dn; t += 64) {
+        const int ii = t / dn, k = t - ii * dn;
+        sq[ii][k] = ii < nt ? bf16_to_f32(q_nope[((int64_t)(i0 + ii) * H + h) * dn + k]) : 0.f;
+    }
+    __syncthreads();
+    float acc[kAbsorbTok];
+#pragma unroll
+    for (int ii = 0; ii < kAbsorbTok; ++ii) acc[ii] = 0.f;
+    const uint16_t *w = w_uk + (int64_t)h * dn * dl + l;
+    for (int k = 0; k < dn; ++k) {
+        const float wv = bf16_to_f32(w[(int64_t)k * dl]);
+#pragma unroll
+        for (int ii = 0; ii < kAbsorbTok; ++ii) acc[ii] = fmaf(sq[ii][k], wv, acc[ii]);
+    }
+    for (int ii = 0; ii < nt; ++ii) out[((int64_t)(i0 + ii) * H + h) * out_stride + l] = f32_to_bf16(acc[ii]);
+}
+
+// ---------------------------------------------------------------------------
+// MLA expansion: o[i][h][j] = sum_l o_lat[i][h][l] * W_UV[h][l][j], fp32.
+// Workgroup = (head, 64 output columns, 8 tokens).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void expand_kernel(int32_t n, int32_t H, int32_t dl, int32_t dv,
+                                                    const float *o_lat, const uint16_t *w_uv, float *o) {
+    __shared__ float so[kAbsorbTok][1024];
+    const int h = blockIdx.x;
+    const int j = blockIdx.y * 64 + threadIdx.x;
+    const int i0 = blockIdx.z * kAbsorbTok;
+    const int nt = min(kAbsorbTok, n - i0);
+    for (int t = threadIdx.x; t < kAbsorbTok * dl; t += 64) {
+        const int ii = t / dl, l = t - ii * dl;
+        so[ii][l] = ii < nt ? o_lat[((int64_t)(i0 + ii) * H + h) * dl + l] : 0.f;
+    }
+    __syncthreads();
+    float acc[kAbsorbTok];
+#pragma unroll
+    for (int ii = 0; ii < kAbsorbTok; ++ii) acc[ii] = 0.f;
+    const uint16_t *w = w_uv + (int64_t)h * dl * dv + j;
+    for (int l = 0; l < dl; ++l) {
+        const float wv = bf16_to_f32(w[(int64_t)l * dv]);
+#pragma unroll
+        for (int ii = 0; ii < kAbsorbTok; ++ii) acc[ii] = fmaf(so[ii][l], wv, acc[ii]);
+    }
+    for (int ii = 0; ii < nt; ++ii) o[((int64_t)(i0 + ii) * H + h) * dv + j] = acc[ii];
+}
+
+}  // namespace
+
+hipError_t launch_combine(const CombineParams &p, int width, hipStream_t s) {
+    if (p.n <= 0) return hipSuccess;
+    const dim3 grid(p.n * p.n_q_heads), block(64);
+    switch (width) {
+        case 128: hipLaunchKernelGGL(combine_kernel<128>, grid, block, 0, s, p); break;
+        case 512: hipLaunchKernelGGL(combine_kernel<512>, grid, block, 0, s, p); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a,
+                        const float *o_b, const float *lse_b, float *o_out, float *lse_out,
+                        uint16_t *o_bf16, hipStream_t s) {
+    if (rows <= 0) return hipSuccess;
+    const int64_t total4 = (int64_t)rows * width / 4;
+    const int64_t blocks = (total4 + 255) / 256;
+    hipLaunchKernelGGL(merge_kernel, dim3((unsigned)blocks), dim3(256), 0, s, rows, width, o_a, lse_a,
+                       o_b, lse_b, o_out, o_bf16);
+    // The row LSEs are written in a second pass, after every element of every
+    // row has read them: o_out/lse_out may alias the inputs.
+    hipLaunchKernelGGL(merge_lse_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, rows, lse_a, lse_b,
+                       lse_out);
+    return hipGetLastError();
+}
+
+hipError_t launch_append(const AppendParams &p, hipStream_t s) {
+    if (p.n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(append_kernel, dim3(p.n), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_scatter(const ScatterParams &p, hipStream_t s) {
+    if (p.m <= 0) return hipSuccess;
+    const int row16 = p.row_elems / 8;
+    const int64_t per_pos = (p.kind == 0) ? 2 * p.n_kv_heads * row16 : row16;
+    int64_t blocks = ((int64_t)p.m * per_pos + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t *q_nope,
+                             const uint16_t *w_uk, uint16_t *out, int64_t out_stride, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const dim3 grid(H, dl / 64, (n + kAbsorbTok - 1) / kAbsorbTok);
+    hipLaunchKernelGGL(absorb_kernel, grid, dim3(64), 0, s, n, H, dn, dl, q_nope, w_uk, out, out_stride);
+    return hipGetLastError();
+}
+
+hipError_t launch_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat,
+                             const uint16_t *w_uv, float *o, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const dim3 grid(H, dv / 64, (n + kAbsorbTok - 1) / kAbsorbTok);
+    hipLaunchKernelGGL(expand_kernel, grid, dim3(64), 0, s, n, H, dl, dv, o_lat, w_uv, o);
+    return hipGetLastError();
+}
+
+}  // namespace wsk

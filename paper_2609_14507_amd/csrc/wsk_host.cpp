@@ -1,0 +1,703 @@
+// Host side of the partitioned KV cache: spec validation, block pools, the
+// deterministic slot allocator (write-time routing), views, and the launch
+// plumbing of the decode-path kernels.  Implements include/wsk.h.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <functional>
+#include <new>
+#include <queue>
+#include <string>
+#include <vector>
+
+#include "../../include/wsk.h"
+#include "wsk_internal.h"
+
+using namespace wsk;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(WSK_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Makes the cache's device current for the duration of a call and restores
+// the caller's device afterwards.
+struct DeviceGuard {
+    int prev = -1;
+    hipError_t err = hipSuccess;
+    explicit DeviceGuard(int dev) {
+        if (dev < 0) return;
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        if (prev != dev) err = hipSetDevice(dev);
+    }
+    ~DeviceGuard() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+typedef std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> MinHeap;
+
+// Bytes of device staging used by wsk_write for the GPU partition's rows.
+constexpr size_t kStageBytes = 64u << 20;
+
+}  // namespace
+
+struct wsk_cache {
+    wsk_partition_spec spec;
+    int device = -1;
+    int32_t max_blocks = 0;       // logical blocks per sequence
+    int32_t row_elems = 0;        // bf16 elements of one cached row (one head's K, or one MLA row)
+    int32_t rows_per_pos = 0;     // rows one position stores (GQA: 2 * Hkv; MLA: 1)
+    int64_t slot_elems = 0;       // bf16 elements per slot
+    uint16_t *hpool = nullptr;    // CPU partition pool (pageable, 64-byte aligned)
+    uint16_t *dpool = nullptr;    // GPU partition pool (HBM)
+    int32_t *dtab = nullptr;      // device copy of the GPU block table
+    uint16_t *dstage = nullptr;   // device staging for wsk_write
+    std::vector<int32_t> htab[2]; // host block tables [part][seq * max_blocks + k]
+    std::vector<uint8_t> is_open;
+    std::vector<int32_t> split, length;
+    MinHeap free_slots[2];
+};
+
+namespace {
+
+struct Pending {
+    int part;
+    int32_t seq;
+    int32_t blk;
+    int32_t slot;
+};
+
+int validate_spec(const wsk_partition_spec *s) {
+    if (!s) return fail(WSK_EINVAL, "spec is NULL");
+    if (s->reserved != 0) return fail(WSK_EINVAL, "spec.reserved must be 0");
+    if (s->kind != WSK_KIND_GQA && s->kind != WSK_KIND_MLA) return fail(WSK_EINVAL, "spec.kind %d", s->kind);
+    if (s->n_q_heads <= 0 || s->n_kv_heads <= 0) return fail(WSK_EINVAL, "head counts must be positive");
+    if (s->block_tokens != 64 && s->block_tokens != 128 && s->block_tokens != 256)
+        return fail(WSK_EINVAL, "block_tokens must be 64, 128 or 256 (got %d)", s->block_tokens);
+    if (s->max_seqs <= 0 || s->max_seq_len <= 0) return fail(WSK_EINVAL, "max_seqs and max_seq_len must be positive");
+    if (s->device_pool_blocks < 0 || s->host_pool_blocks < 0 || s->device_pool_blocks > INT32_MAX ||
+        s->host_pool_blocks > INT32_MAX)
+        return fail(WSK_EINVAL, "pool sizes must be in [0, 2^31)");
+    if (!(std::isfinite(s->softmax_scale) && s->softmax_scale > 0.f))
+        return fail(WSK_EINVAL, "softmax_scale must be finite and positive");
+    if ((int64_t)s->max_seqs * ((s->max_seq_len + s->block_tokens - 1) / s->block_tokens) > INT32_MAX)
+        return fail(WSK_EINVAL, "block table too large");
+    if (s->kind == WSK_KIND_GQA) {
+        if (s->n_q_heads % s->n_kv_heads) return fail(WSK_EINVAL, "n_q_heads must be a multiple of n_kv_heads");
+        if (s->n_q_heads / s->n_kv_heads > WSK_MAX_GROUP) return fail(WSK_EINVAL, "group size above %d", WSK_MAX_GROUP);
+        if (s->head_dim != kHeadDim) return fail(WSK_EINVAL, "GQA head_dim must be %d", kHeadDim);
+        if (s->latent_dim != 0 || s->rope_dim != 0) return fail(WSK_EINVAL, "GQA latent_dim/rope_dim must be 0");
+    } else {
+        if (s->n_kv_heads != 1) return fail(WSK_EINVAL, "MLA n_kv_heads must be 1");
+        if (s->latent_dim != kLatent || s->rope_dim != kRope)
+            return fail(WSK_EINVAL, "MLA latent_dim/rope_dim must be %d/%d", kLatent, kRope);
+        if (s->n_q_heads > 16) return fail(WSK_EINVAL, "MLA supports at most 16 heads");
+    }
+    return WSK_OK;
+}
+
+int check_seq(const wsk_cache *c, int32_t seq) {
+    if (!c) return fail(WSK_EINVAL, "cache is NULL");
+    if (seq < 0 || seq >= c->spec.max_seqs) return fail(WSK_EINVAL, "sequence id %d out of range", seq);
+    if (!c->is_open[seq]) return fail(WSK_ESTATE, "sequence %d is not open", seq);
+    return WSK_OK;
+}
+
+inline int32_t &tab(wsk_cache *c, int part, int32_t seq, int32_t blk) {
+    return c->htab[part][(size_t)seq * c->max_blocks + blk];
+}
+
+void undo(wsk_cache *c, const std::vector<Pending> &pend) {
+    for (const Pending &p : pend) c->free_slots[p.part].push(p.slot);
+}
+
+// Routing decision for positions [pos0, pos0+n) of seq: every (partition,
+// logical block) touched for the first time takes the lowest free slot of its
+// pool, blocks in ascending order (CPU side of a straddling block first).
+int plan(wsk_cache *c, int32_t seq, int32_t pos0, int32_t n, std::vector<Pending> &pend) {
+    if (n <= 0) return WSK_OK;
+    const int bk = c->spec.block_tokens;
+    const int32_t s = c->split[seq];
+    const int32_t end = pos0 + n;
+    for (int32_t blk = pos0 / bk; blk <= (end - 1) / bk; ++blk) {
+        const int32_t lo = std::max(pos0, blk * bk), hi = std::min(end, (blk + 1) * bk);
+        for (int part = WSK_PART_CPU; part <= WSK_PART_GPU; ++part) {
+            const bool touched = part == WSK_PART_CPU ? lo < s : hi > s;
+            if (!touched || tab(c, part, seq, blk) >= 0) continue;
+            bool pending_already = false;
+            for (const Pending &p : pend)
+                if (p.part == part && p.seq == seq && p.blk == blk) pending_already = true;
+            if (pending_already) continue;
+            if (c->free_slots[part].empty()) {
+                undo(c, pend);
+                pend.clear();
+                return fail(WSK_ENOMEM, "%s pool exhausted", part == WSK_PART_CPU ? "CPU" : "GPU");
+            }
+            pend.push_back({part, seq, blk, c->free_slots[part].top()});
+            c->free_slots[part].pop();
+        }
+    }
+    return WSK_OK;
+}
+
+void commit(wsk_cache *c, const std::vector<Pending> &pend) {
+    for (const Pending &p : pend) tab(c, p.part, p.seq, p.blk) = p.slot;
+}
+
+// Offset (elements) of position pos, KV head g, K (which = 0) or V (1), in its slot.
+inline int64_t row_offset(const wsk_cache *c, int32_t pos, int g, int which) {
+    const int bk = c->spec.block_tokens;
+    const int off = pos % bk;
+    if (c->spec.kind == WSK_KIND_MLA) return (int64_t)off * c->row_elems;
+    return ((int64_t)(g * 2 + which) * bk + off) * c->row_elems;
+}
+
+// Split-KV chunking of one attend call.  Chunks are whole 64-token tiles of
+// the absolute tile grid; every call with the same arguments yields the same
+// layout, so wsk_attend_workspace and wsk_attend agree.
+struct AttendPlan {
+    int32_t tiles_per_chunk = 4;
+    int heads_per_wg = 1;
+    int head_groups = 1;
+    std::vector<int32_t> nchunks;   // per sequence
+    int64_t partials = 0;           // sum of nchunks
+    size_t part_o_bytes = 0;
+    size_t bytes = 0;
+};
+
+int64_t n_tiles(int32_t a, int32_t e) { return e > a ? (int64_t)((e - 1) / kTile - a / kTile + 1) : 0; }
+
+int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
+              AttendPlan &pl) {
+    if (n < 0) return fail(WSK_EINVAL, "n < 0");
+    if (n > 0 && (!ids || !start || !end)) return fail(WSK_EINVAL, "seq_ids/start/end must not be NULL");
+    int64_t total_tiles = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        int rc = check_seq(c, ids[i]);
+        if (rc) return rc;
+        const int32_t L = c->length[ids[i]], s = std::min(c->split[ids[i]], L);
+        if (!(s <= start[i] && start[i] <= end[i] && end[i] <= L))
+            return fail(WSK_ERANGE, "range [%d, %d) of sequence %d outside its GPU partition [%d, %d)", start[i],
+                        end[i], ids[i], s, L);
+        total_tiles += n_tiles(start[i], end[i]);
+    }
+    const wsk_partition_spec &sp = c->spec;
+    int units = 1;
+    if (sp.kind == WSK_KIND_GQA) {
+        const int G = sp.n_q_heads / sp.n_kv_heads;
+        pl.heads_per_wg = gqa_heads_per_wg(G);
+        pl.head_groups = G / pl.heads_per_wg;
+        units = sp.n_kv_heads * pl.head_groups;
+    }
+    // About 2048 workgroups keep every CU busy through several rounds while
+    // each wavefront still streams several tiles; at least 4 tiles per chunk
+    // (one per wavefront), at most 64.
+    int64_t want = (total_tiles * units + 2047) / 2048;
+    int64_t tpc = std::max<int64_t>(4, std::min<int64_t>(64, want));
+    tpc = (tpc + 3) / 4 * 4;
+    pl.tiles_per_chunk = (int32_t)tpc;
+    pl.nchunks.assign(n, 0);
+    pl.partials = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        pl.nchunks[i] = (int32_t)((n_tiles(start[i], end[i]) + tpc - 1) / tpc);
+        pl.partials += pl.nchunks[i];
+    }
+    const int width = sp.kind == WSK_KIND_GQA ? kHeadDim : kLatent;
+    pl.part_o_bytes = ((size_t)pl.partials * sp.n_q_heads * width * sizeof(float) + 255) / 256 * 256;
+    pl.bytes = pl.part_o_bytes + ((size_t)pl.partials * sp.n_q_heads * sizeof(float) + 255) / 256 * 256;
+    return WSK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *wsk_last_error(void) { return g_err.c_str(); }
+
+int wsk_init(const wsk_partition_spec *spec, int device, wsk_cache **out) {
+    if (!out) return fail(WSK_EINVAL, "out is NULL");
+    *out = nullptr;
+    int rc = validate_spec(spec);
+    if (rc) return rc;
+    if (device < -1) return fail(WSK_EINVAL, "device %d", device);
+    wsk_cache *c = new (std::nothrow) wsk_cache();
+    if (!c) return fail(WSK_ENOMEM, "host allocation failed");
+    c->spec = *spec;
+    c->device = device;
+    c->max_blocks = (spec->max_seq_len + spec->block_tokens - 1) / spec->block_tokens;
+    if (spec->kind == WSK_KIND_GQA) {
+        c->row_elems = spec->head_dim;
+        c->rows_per_pos = 2 * spec->n_kv_heads;
+    } else {
+        c->row_elems = spec->latent_dim + spec->rope_dim;
+        c->rows_per_pos = 1;
+    }
+    c->slot_elems = (int64_t)c->rows_per_pos * spec->block_tokens * c->row_elems;
+    try {
+        const size_t tab_n = (size_t)spec->max_seqs * c->max_blocks;
+        c->htab[0].assign(tab_n, -1);
+        c->htab[1].assign(tab_n, -1);
+        c->is_open.assign(spec->max_seqs, 0);
+        c->split.assign(spec->max_seqs, 0);
+        c->length.assign(spec->max_seqs, 0);
+        std::vector<int32_t> h(spec->host_pool_blocks), d(spec->device_pool_blocks);
+        for (int32_t i = 0; i < (int32_t)h.size(); ++i) h[i] = i;
+        for (int32_t i = 0; i < (int32_t)d.size(); ++i) d[i] = i;
+        c->free_slots[0] = MinHeap(std::greater<int32_t>(), std::move(h));
+        c->free_slots[1] = MinHeap(std::greater<int32_t>(), std::move(d));
+    } catch (const std::bad_alloc &) {
+        delete c;
+        return fail(WSK_ENOMEM, "host allocation failed");
+    }
+    const size_t slot_bytes = (size_t)c->slot_elems * 2;
+    if (spec->host_pool_blocks > 0) {
+        const size_t bytes = ((size_t)spec->host_pool_blocks * slot_bytes + 63) / 64 * 64;
+        c->hpool = (uint16_t *)aligned_alloc(64, bytes);
+        if (!c->hpool) {
+            delete c;
+            return fail(WSK_ENOMEM, "host pool of %zu bytes", bytes);
+        }
+        memset(c->hpool, 0, bytes);
+    }
+    if (device >= 0) {
+        DeviceGuard guard(device);
+        if (guard.err != hipSuccess) {
+            wsk_destroy(c);
+            return hip_fail(guard.err, "hipSetDevice");
+        }
+        hipError_t e = hipSuccess;
+        const size_t pool_bytes = (size_t)spec->device_pool_blocks * slot_bytes;
+        if (pool_bytes) e = hipMalloc((void **)&c->dpool, pool_bytes);
+        if (e == hipSuccess && pool_bytes) e = hipMemset(c->dpool, 0, pool_bytes);
+        const size_t tab_bytes = c->htab[1].size() * sizeof(int32_t);
+        if (e == hipSuccess) e = hipMalloc((void **)&c->dtab, tab_bytes);
+        if (e == hipSuccess) e = hipMemset(c->dtab, 0xff, tab_bytes);
+        if (e == hipSuccess) e = hipMalloc((void **)&c->dstage, kStageBytes);
+        if (e == hipSuccess) e = hipDeviceSynchronize();
+        if (e != hipSuccess) {
+            const int r = hip_fail(e, "device allocation");
+            wsk_destroy(c);
+            return r;
+        }
+    }
+    *out = c;
+    return WSK_OK;
+}
+
+int wsk_destroy(wsk_cache *c) {
+    if (!c) return WSK_OK;
+    if (c->device >= 0) {
+        DeviceGuard guard(c->device);
+        if (c->dpool) (void)hipFree(c->dpool);
+        if (c->dtab) (void)hipFree(c->dtab);
+        if (c->dstage) (void)hipFree(c->dstage);
+    }
+    free(c->hpool);
+    delete c;
+    return WSK_OK;
+}
+
+int wsk_get_spec(const wsk_cache *c, wsk_partition_spec *out) {
+    if (!c || !out) return fail(WSK_EINVAL, "NULL argument");
+    *out = c->spec;
+    return WSK_OK;
+}
+
+int wsk_seq_open(wsk_cache *c, int32_t seq, int32_t split) {
+    if (!c) return fail(WSK_EINVAL, "cache is NULL");
+    if (seq < 0 || seq >= c->spec.max_seqs) return fail(WSK_EINVAL, "sequence id %d out of range", seq);
+    if (split < 0) return fail(WSK_EINVAL, "split %d < 0", split);
+    if (c->is_open[seq]) return fail(WSK_ESTATE, "sequence %d already open", seq);
+    c->is_open[seq] = 1;
+    c->split[seq] = split;
+    c->length[seq] = 0;
+    return WSK_OK;
+}
+
+int wsk_seq_close(wsk_cache *c, int32_t seq) {
+    int rc = check_seq(c, seq);
+    if (rc) return rc;
+    for (int part = 0; part < 2; ++part)
+        for (int32_t k = 0; k < c->max_blocks; ++k) {
+            int32_t &t = tab(c, part, seq, k);
+            if (t >= 0) {
+                c->free_slots[part].push(t);
+                t = -1;
+            }
+        }
+    c->is_open[seq] = 0;
+    c->length[seq] = 0;
+    c->split[seq] = 0;
+    return WSK_OK;
+}
+
+int wsk_seq_info(const wsk_cache *c, int32_t seq, int32_t *length, int32_t *split) {
+    int rc = check_seq(c, seq);
+    if (rc) return rc;
+    if (length) *length = c->length[seq];
+    if (split) *split = c->split[seq];
+    return WSK_OK;
+}
+
+int wsk_reserve(wsk_cache *c, int32_t seq, int32_t n) {
+    int rc = check_seq(c, seq);
+    if (rc) return rc;
+    if (n < 0 || (int64_t)c->length[seq] + n > c->spec.max_seq_len)
+        return fail(WSK_EINVAL, "reserve of %d positions past max_seq_len", n);
+    std::vector<Pending> pend;
+    rc = plan(c, seq, c->length[seq], n, pend);
+    if (rc) return rc;
+    // the device table must follow for GPU blocks
+    if (c->device >= 0) {
+        bool any_gpu = false;
+        for (const Pending &p : pend) any_gpu |= p.part == WSK_PART_GPU;
+        if (any_gpu) {
+            DeviceGuard guard(c->device);
+            hipError_t e = guard.err;
+            for (const Pending &p : pend) {
+                if (p.part != WSK_PART_GPU || e != hipSuccess) continue;
+                e = hipMemcpy(c->dtab + (size_t)p.seq * c->max_blocks + p.blk, &p.slot, sizeof(int32_t),
+                              hipMemcpyHostToDevice);
+            }
+            if (e != hipSuccess) {
+                undo(c, pend);
+                return hip_fail(e, "block table update");
+            }
+        }
+    }
+    commit(c, pend);
+    c->length[seq] += n;
+    return WSK_OK;
+}
+
+int wsk_write(wsk_cache *c, int32_t seq, int32_t pos0, int32_t n, const void *k, const void *v, void *stream) {
+    int rc = check_seq(c, seq);
+    if (rc) return rc;
+    const wsk_partition_spec &sp = c->spec;
+    if (n < 0) return fail(WSK_EINVAL, "n < 0");
+    if (pos0 != c->length[seq]) return fail(WSK_ERANGE, "write at %d, sequence %d has length %d", pos0, seq, c->length[seq]);
+    if ((int64_t)pos0 + n > sp.max_seq_len) return fail(WSK_EINVAL, "write past max_seq_len");
+    if (n == 0) return WSK_OK;
+    if (!k) return fail(WSK_EINVAL, "k is NULL");
+    if (sp.kind == WSK_KIND_GQA && !v) return fail(WSK_EINVAL, "v is NULL");
+    if (sp.kind == WSK_KIND_MLA && v) return fail(WSK_EINVAL, "MLA caches take no v");
+    const int32_t s = c->split[seq];
+    const int32_t end = pos0 + n;
+    const bool has_gpu = end > s;
+    if (has_gpu && c->device < 0) return fail(WSK_ESTATE, "host-only cache cannot hold GPU-partition rows");
+
+    std::vector<Pending> pend;
+    rc = plan(c, seq, pos0, n, pend);
+    if (rc) return rc;
+    commit(c, pend);
+
+    const int hkv = sp.kind == WSK_KIND_GQA ? sp.n_kv_heads : 1;
+    const int nsrc = sp.kind == WSK_KIND_GQA ? 2 : 1;
+    const size_t row_bytes = (size_t)c->row_elems * 2;
+    const size_t pos_bytes = (size_t)hkv * row_bytes;   // one source position of K (or V)
+    const uint16_t *src[2] = {(const uint16_t *)k, (const uint16_t *)v};
+
+    // CPU partition rows: memcpy into the host pool
+    for (int32_t p = pos0; p < std::min(end, s); ++p) {
+        const int32_t slot = tab(c, WSK_PART_CPU, seq, p / sp.block_tokens);
+        uint16_t *base = c->hpool + (int64_t)slot * c->slot_elems;
+        for (int w = 0; w < nsrc; ++w)
+            for (int g = 0; g < hkv; ++g)
+                memcpy(base + row_offset(c, p, g, w), src[w] + ((int64_t)(p - pos0) * hkv + g) * c->row_elems,
+                       row_bytes);
+    }
+    if (!has_gpu) {
+        c->length[seq] = end;
+        return WSK_OK;
+    }
+
+    // GPU partition rows: table update, then H2D through staging + scatter
+    DeviceGuard guard(c->device);
+    if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+    hipStream_t st = (hipStream_t)stream;
+    const int32_t g0 = std::max(pos0, s);
+    const int32_t b0 = g0 / sp.block_tokens, b1 = (end - 1) / sp.block_tokens;
+    hipError_t e = hipMemcpyAsync(c->dtab + (size_t)seq * c->max_blocks + b0, &tab(c, WSK_PART_GPU, seq, b0),
+                                  (size_t)(b1 - b0 + 1) * sizeof(int32_t), hipMemcpyHostToDevice, st);
+    const size_t per_piece = kStageBytes / (nsrc * pos_bytes);
+    uint16_t *stage[2] = {c->dstage, c->dstage + (kStageBytes / 2) / 2};
+    for (int32_t p = g0; p < end && e == hipSuccess; p += (int32_t)per_piece) {
+        const int32_t m = (int32_t)std::min<int64_t>(per_piece, end - p);
+        for (int w = 0; w < nsrc && e == hipSuccess; ++w)
+            e = hipMemcpyAsync(stage[w], src[w] + (int64_t)(p - pos0) * hkv * c->row_elems, (size_t)m * pos_bytes,
+                               hipMemcpyHostToDevice, st);
+        if (e != hipSuccess) break;
+        ScatterParams sc{};
+        sc.src_k = stage[0];
+        sc.src_v = stage[1];
+        sc.pool = c->dpool;
+        sc.table_row = c->dtab + (size_t)seq * c->max_blocks;
+        sc.slot_elems = c->slot_elems;
+        sc.p0 = p;
+        sc.m = m;
+        sc.kind = sp.kind;
+        sc.n_kv_heads = hkv;
+        sc.block_tokens = sp.block_tokens;
+        sc.row_elems = c->row_elems;
+        e = launch_scatter(sc, st);
+    }
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    c->length[seq] = end;
+    if (e != hipSuccess) return hip_fail(e, "wsk_write");
+    return WSK_OK;
+}
+
+int wsk_append(wsk_cache *c, int32_t n, const int32_t *ids, const void *k_new, const void *v_new, void *stream) {
+    if (!c) return fail(WSK_EINVAL, "cache is NULL");
+    const wsk_partition_spec &sp = c->spec;
+    if (n <= 0 || !ids) return fail(WSK_EINVAL, "n must be positive and seq_ids non-NULL");
+    if (!k_new) return fail(WSK_EINVAL, "k_new is NULL");
+    if (sp.kind == WSK_KIND_GQA && !v_new) return fail(WSK_EINVAL, "v_new is NULL");
+    if (sp.kind == WSK_KIND_MLA && v_new) return fail(WSK_EINVAL, "MLA caches take no v_new");
+    if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
+    std::vector<int32_t> order(n);
+    for (int32_t i = 0; i < n; ++i) {
+        int rc = check_seq(c, ids[i]);
+        if (rc) return rc;
+        order[i] = i;
+    }
+    std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return ids[a] < ids[b]; });
+    for (int32_t j = 1; j < n; ++j)
+        if (ids[order[j]] == ids[order[j - 1]]) return fail(WSK_EINVAL, "sequence %d listed twice", ids[order[j]]);
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t sq = ids[i];
+        if (c->length[sq] >= sp.max_seq_len) return fail(WSK_ERANGE, "sequence %d is full", sq);
+        if (c->length[sq] < c->split[sq])
+            return fail(WSK_ERANGE, "position %d of sequence %d is below its split %d", c->length[sq], sq, c->split[sq]);
+    }
+    std::vector<Pending> pend;
+    for (int32_t j = 0; j < n; ++j) {
+        const int32_t sq = ids[order[j]];
+        int rc = plan(c, sq, c->length[sq], 1, pend);
+        if (rc) return rc;
+    }
+    commit(c, pend);
+
+    DeviceGuard guard(c->device);
+    if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+    hipStream_t st = (hipStream_t)stream;
+    const int hkv = sp.kind == WSK_KIND_GQA ? sp.n_kv_heads : 1;
+    hipError_t e = hipSuccess;
+    for (int32_t r0 = 0; r0 < n && e == hipSuccess; r0 += kMaxLaunchSeqs) {
+        const int32_t m = std::min(kMaxLaunchSeqs, n - r0);
+        AppendParams ap{};
+        ap.k_new = (const uint16_t *)k_new + (int64_t)r0 * hkv * c->row_elems;
+        ap.v_new = v_new ? (const uint16_t *)v_new + (int64_t)r0 * hkv * c->row_elems : nullptr;
+        ap.pool = c->dpool;
+        ap.table = c->dtab;
+        ap.n = m;
+        ap.kind = sp.kind;
+        ap.n_kv_heads = hkv;
+        ap.block_tokens = sp.block_tokens;
+        ap.row_elems = c->row_elems;
+        for (int32_t r = 0; r < m; ++r) {
+            const int32_t sq = ids[r0 + r];
+            const int32_t pos = c->length[sq];
+            const int32_t blk = pos / sp.block_tokens;
+            const int32_t slot = tab(c, WSK_PART_GPU, sq, blk);
+            ap.dst[r] = (int64_t)slot * c->slot_elems + row_offset(c, pos, 0, 0);
+            ap.tab_index[r] = -1;
+            for (const Pending &p : pend)
+                if (p.seq == sq && p.part == WSK_PART_GPU && p.blk == blk) {
+                    ap.tab_index[r] = (int32_t)((size_t)sq * c->max_blocks + blk);
+                    ap.tab_slot[r] = slot;
+                }
+        }
+        e = launch_append(ap, st);
+    }
+    for (int32_t i = 0; i < n; ++i) c->length[ids[i]] += 1;
+    if (e != hipSuccess) return hip_fail(e, "wsk_append");
+    return WSK_OK;
+}
+
+int wsk_route(const wsk_cache *c, int32_t seq, int32_t pos, wsk_loc *out) {
+    int rc = check_seq(c, seq);
+    if (rc) return rc;
+    if (!out) return fail(WSK_EINVAL, "out is NULL");
+    if (pos < 0 || pos >= c->length[seq]) return fail(WSK_ERANGE, "position %d outside [0, %d)", pos, c->length[seq]);
+    const int part = pos < c->split[seq] ? WSK_PART_CPU : WSK_PART_GPU;
+    const int32_t blk = pos / c->spec.block_tokens;
+    out->part = part;
+    out->logical_block = blk;
+    out->slot = c->htab[part][(size_t)seq * c->max_blocks + blk];
+    out->offset = pos % c->spec.block_tokens;
+    return WSK_OK;
+}
+
+int wsk_views(const wsk_cache *c, int32_t seq, wsk_view *cpu, wsk_view *gpu) {
+    int rc = check_seq(c, seq);
+    if (rc) return rc;
+    const int64_t slot_bytes = c->slot_elems * 2;
+    const int64_t row_bytes = (int64_t)c->row_elems * 2;
+    const bool gqa = c->spec.kind == WSK_KIND_GQA;
+    const int32_t s = c->split[seq], L = c->length[seq];
+    for (int side = 0; side < 2; ++side) {
+        wsk_view *v = side == 0 ? cpu : gpu;
+        if (!v) continue;
+        v->slot_bytes = slot_bytes;
+        v->head_bytes = gqa ? 2 * c->spec.block_tokens * row_bytes : 0;
+        v->v_bytes = gqa ? c->spec.block_tokens * row_bytes : 0;
+        v->row_bytes = row_bytes;
+        v->block_tokens = c->spec.block_tokens;
+        if (side == 0) {
+            v->pool = c->hpool;
+            v->table = c->htab[0].data() + (size_t)seq * c->max_blocks;
+            v->start = 0;
+            v->end = std::min(s, L);
+            v->is_device = 0;
+        } else {
+            v->pool = c->dpool;
+            v->table = c->dtab ? c->dtab + (size_t)seq * c->max_blocks : nullptr;
+            v->start = std::min(s, L);
+            v->end = L;
+            v->is_device = 1;
+        }
+    }
+    return WSK_OK;
+}
+
+int wsk_attend_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start,
+                         const int32_t *end, size_t *bytes) {
+    if (!c || !bytes) return fail(WSK_EINVAL, "NULL argument");
+    AttendPlan pl;
+    int rc = make_plan(c, n, ids, start, end, pl);
+    if (rc) return rc;
+    *bytes = pl.bytes;
+    return WSK_OK;
+}
+
+int wsk_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
+               const void *q, float *o, float *lse, void *ws, size_t ws_bytes, void *stream) {
+    if (!c) return fail(WSK_EINVAL, "cache is NULL");
+    AttendPlan pl;
+    int rc = make_plan(c, n, ids, start, end, pl);
+    if (rc) return rc;
+    if (n == 0) return WSK_OK;
+    if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
+    if (!q || !o || !lse) return fail(WSK_EINVAL, "q/o/lse must not be NULL");
+    if (pl.bytes && (!ws || ws_bytes < pl.bytes)) return fail(WSK_EINVAL, "workspace of %zu bytes needed", pl.bytes);
+    if (((uintptr_t)ws & 255) != 0) return fail(WSK_EINVAL, "workspace must be 256-byte aligned");
+    const wsk_partition_spec &sp = c->spec;
+    const bool gqa = sp.kind == WSK_KIND_GQA;
+    const int width = gqa ? kHeadDim : kLatent;
+    const int qw = gqa ? kHeadDim : kLatent + kRope;
+    DeviceGuard guard(c->device);
+    if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+    hipStream_t st = (hipStream_t)stream;
+    float *part_o = (float *)ws;
+    float *part_lse = (float *)((char *)ws + pl.part_o_bytes);
+    hipError_t e = hipSuccess;
+    int64_t part_base = 0;
+    for (int32_t i0 = 0; i0 < n && e == hipSuccess; i0 += kMaxLaunchSeqs) {
+        const int32_t m = std::min(kMaxLaunchSeqs, n - i0);
+        AttendParams ap{};
+        CombineParams cp{};
+        ap.pool = c->dpool;
+        ap.table = c->dtab;
+        ap.q = (const uint16_t *)q + (int64_t)i0 * sp.n_q_heads * qw;
+        ap.part_o = part_o + part_base * sp.n_q_heads * width;
+        ap.part_lse = part_lse + part_base * sp.n_q_heads;
+        ap.slot_elems = c->slot_elems;
+        ap.q_row = (int64_t)sp.n_q_heads * qw;
+        ap.table_stride = c->max_blocks;
+        ap.n_q_heads = sp.n_q_heads;
+        ap.n_kv_heads = gqa ? sp.n_kv_heads : 1;
+        ap.group = sp.n_q_heads / ap.n_kv_heads;
+        ap.head_groups = gqa ? pl.head_groups : 1;
+        ap.block_tokens = sp.block_tokens;
+        ap.tiles_per_chunk = pl.tiles_per_chunk;
+        ap.n = m;
+        ap.scale_log2 = sp.softmax_scale * 1.4426950408889634f;
+        const int units = ap.n_kv_heads * ap.head_groups;
+        ap.wg_begin[0] = 0;
+        ap.chunk_begin[0] = 0;
+        for (int32_t r = 0; r < m; ++r) {
+            ap.seq[r] = ids[i0 + r];
+            ap.start[r] = start[i0 + r];
+            ap.end[r] = end[i0 + r];
+            const int32_t nc = pl.nchunks[i0 + r];
+            ap.wg_begin[r + 1] = ap.wg_begin[r] + nc * units;
+            ap.chunk_begin[r + 1] = ap.chunk_begin[r] + nc;
+        }
+        for (int32_t r = m + 1; r <= kMaxLaunchSeqs; ++r) {
+            ap.wg_begin[r] = ap.wg_begin[m];
+            ap.chunk_begin[r] = ap.chunk_begin[m];
+        }
+        const int n_wg = ap.wg_begin[m];
+        if (gqa)
+            e = launch_gqa_attend(ap, pl.heads_per_wg, n_wg, st);
+        else
+            e = launch_mla_attend(ap, n_wg, st);
+        if (e != hipSuccess) break;
+        cp.part_o = ap.part_o;
+        cp.part_lse = ap.part_lse;
+        cp.o = o + (int64_t)i0 * sp.n_q_heads * width;
+        cp.lse = lse + (int64_t)i0 * sp.n_q_heads;
+        cp.n = m;
+        cp.n_q_heads = sp.n_q_heads;
+        for (int32_t r = 0; r <= kMaxLaunchSeqs; ++r) cp.chunk_begin[r] = ap.chunk_begin[r];
+        e = launch_combine(cp, width, st);
+        part_base += ap.chunk_begin[m];
+    }
+    if (e != hipSuccess) return hip_fail(e, "wsk_attend");
+    return WSK_OK;
+}
+
+int wsk_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a, const float *o_b,
+              const float *lse_b, float *o_out, float *lse_out, uint16_t *o_bf16, void *stream) {
+    if (rows < 0 || width <= 0 || width % 4) return fail(WSK_EINVAL, "rows %d width %d", rows, width);
+    if (rows == 0) return WSK_OK;
+    if (!o_a || !lse_a || !o_b || !lse_b || !o_out || !lse_out) return fail(WSK_EINVAL, "NULL pointer");
+    hipError_t e = launch_merge(rows, width, o_a, lse_a, o_b, lse_b, o_out, lse_out, o_bf16, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "wsk_merge");
+    return WSK_OK;
+}
+
+int wsk_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t *q_nope, const uint16_t *w_uk,
+                   uint16_t *out, int64_t out_stride, void *stream) {
+    if (n < 0 || H <= 0 || dn < 1 || dn > 256 || dl <= 0 || dl % 64 || out_stride < dl)
+        return fail(WSK_EINVAL, "absorb sizes n=%d H=%d dn=%d dl=%d stride=%lld", n, H, dn, dl, (long long)out_stride);
+    if (n == 0) return WSK_OK;
+    if (!q_nope || !w_uk || !out) return fail(WSK_EINVAL, "NULL pointer");
+    hipError_t e = launch_mla_absorb(n, H, dn, dl, q_nope, w_uk, out, out_stride, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "wsk_mla_absorb");
+    return WSK_OK;
+}
+
+int wsk_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat, const uint16_t *w_uv, float *o,
+                   void *stream) {
+    if (n < 0 || H <= 0 || dl < 1 || dl > 1024 || dv <= 0 || dv % 64)
+        return fail(WSK_EINVAL, "expand sizes n=%d H=%d dl=%d dv=%d", n, H, dl, dv);
+    if (n == 0) return WSK_OK;
+    if (!o_lat || !w_uv || !o) return fail(WSK_EINVAL, "NULL pointer");
+    hipError_t e = launch_mla_expand(n, H, dl, dv, o_lat, w_uv, o, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "wsk_mla_expand");
+    return WSK_OK;
+}
+
+}  // extern "C"

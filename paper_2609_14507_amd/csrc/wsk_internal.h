@@ -1,0 +1,117 @@
+// Internal declarations shared by the host library (wsk_host.cpp) and the
+// HIP kernels.  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wsk {
+
+// Sequences handled by one kernel launch; a call with more is split.
+constexpr int kMaxLaunchSeqs = 64;
+// Tokens per attention tile: one token per lane of a 64-wide wavefront.
+constexpr int kTile = 64;
+// GQA key/value width.
+constexpr int kHeadDim = 128;
+// MLA latent and RoPE widths.
+constexpr int kLatent = 512;
+constexpr int kRope = 64;
+
+// ---------------------------------------------------------------------------
+// Split-KV attention (pass 1).  One workgroup = (sequence i, KV head g, query
+// head group hg, chunk c); a chunk is tiles_per_chunk consecutive 64-token
+// tiles of [start, end) on the absolute tile grid.  Each workgroup writes a
+// normalised partial O and its LSE for its heads into part_o / part_lse at
+// partial index chunk_begin[i] + c.
+// ---------------------------------------------------------------------------
+struct AttendParams {
+    const uint16_t *pool;    // device pool base (bf16)
+    const int32_t *table;    // device block table [max_seqs][table_stride]
+    const uint16_t *q;       // launch-local query rows: row i at q + i * q_row
+    float *part_o;           // [partials][n_q_heads][width]
+    float *part_lse;         // [partials][n_q_heads]
+    int64_t slot_elems;      // bf16 elements per slot
+    int64_t q_row;           // bf16 elements per query row (n_q_heads * q width)
+    int32_t table_stride;
+    int32_t n_q_heads;
+    int32_t n_kv_heads;
+    int32_t group;           // query heads per KV head
+    int32_t head_groups;     // workgroups per KV head along the query heads
+    int32_t block_tokens;
+    int32_t tiles_per_chunk;
+    int32_t n;
+    float scale_log2;        // softmax scale * log2(e)
+    int32_t seq[kMaxLaunchSeqs];
+    int32_t start[kMaxLaunchSeqs];
+    int32_t end[kMaxLaunchSeqs];
+    int32_t wg_begin[kMaxLaunchSeqs + 1];
+    int32_t chunk_begin[kMaxLaunchSeqs + 1];
+};
+
+// Chunk combine (pass 2): merges the partials of each (sequence, head).
+struct CombineParams {
+    const float *part_o;
+    const float *part_lse;
+    float *o;                // launch-local [n][n_q_heads][width]
+    float *lse;              // launch-local [n][n_q_heads]
+    int32_t n;
+    int32_t n_q_heads;
+    int32_t chunk_begin[kMaxLaunchSeqs + 1];
+};
+
+// Decode append: row r of the source goes to the pool at dst[r] (elements);
+// GQA rows carry K and V for every KV head.  tab_index[r] >= 0 also stores
+// tab_slot[r] into the device table (a newly opened block).
+struct AppendParams {
+    const uint16_t *k_new;
+    const uint16_t *v_new;   // GQA only
+    uint16_t *pool;
+    int32_t *table;
+    int32_t n;
+    int32_t kind;
+    int32_t n_kv_heads;
+    int32_t block_tokens;
+    int32_t row_elems;       // GQA: head_dim; MLA: latent + rope
+    int64_t dst[kMaxLaunchSeqs];
+    int32_t tab_index[kMaxLaunchSeqs];
+    int32_t tab_slot[kMaxLaunchSeqs];
+};
+
+// Bulk scatter of staged rows [p0, p0 + m) of one sequence into its GPU
+// partition, slots taken from the device table row.
+struct ScatterParams {
+    const uint16_t *src_k;   // staged [m][n_kv_heads][head_dim] or [m][row]
+    const uint16_t *src_v;   // GQA only
+    uint16_t *pool;
+    const int32_t *table_row;
+    int64_t slot_elems;
+    int32_t p0;
+    int32_t m;
+    int32_t kind;
+    int32_t n_kv_heads;
+    int32_t block_tokens;
+    int32_t row_elems;
+};
+
+hipError_t launch_gqa_attend(const AttendParams &p, int heads_per_wg, int n_wg, hipStream_t s);
+hipError_t launch_mla_attend(const AttendParams &p, int n_wg, hipStream_t s);
+hipError_t launch_combine(const CombineParams &p, int width, hipStream_t s);
+hipError_t launch_append(const AppendParams &p, hipStream_t s);
+hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
+hipError_t launch_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a,
+                        const float *o_b, const float *lse_b, float *o_out, float *lse_out,
+                        uint16_t *o_bf16, hipStream_t s);
+hipError_t launch_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t *q_nope,
+                             const uint16_t *w_uk, uint16_t *out, int64_t out_stride, hipStream_t s);
+hipError_t launch_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat,
+                             const uint16_t *w_uv, float *o, hipStream_t s);
+
+// Heads per workgroup used by the GQA kernel for a group size G: the largest
+// divisor of G that is at most 8.
+inline int gqa_heads_per_wg(int G) {
+    for (int d = 8; d >= 1; --d)
+        if (G % d == 0) return d;
+    return 1;
+}
+
+}  // namespace wsk

@@ -1,0 +1,227 @@
+"""Python binding of the C ABI in include/wsk.h (argument marshalling only).
+
+Every function here has the name of the C entry point it calls.  Device
+buffers are torch tensors (PyTorch supplies device memory and the HIP stream);
+host buffers are numpy arrays.  All compute runs in libwsk.so: if the library
+is missing this module raises instead of falling back to anything.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libwsk.so")
+
+WSK_OK, WSK_EINVAL, WSK_ENOMEM, WSK_ERANGE, WSK_EHIP, WSK_ESTATE = 0, -1, -2, -3, -4, -5
+ERROR_NAMES = {WSK_EINVAL: "EINVAL", WSK_ENOMEM: "ENOMEM", WSK_ERANGE: "ERANGE",
+               WSK_EHIP: "EHIP", WSK_ESTATE: "ESTATE"}
+KIND_GQA, KIND_MLA = 0, 1
+PART_CPU, PART_GPU = 0, 1
+
+
+class WskError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        self.code = code
+        self.name = ERROR_NAMES.get(code, str(code))
+        super().__init__("%s: %s" % (self.name, msg))
+
+
+class wsk_partition_spec(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("latent_dim", ctypes.c_int32), ("rope_dim", ctypes.c_int32),
+                ("block_tokens", ctypes.c_int32), ("max_seqs", ctypes.c_int32), ("max_seq_len", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("device_pool_blocks", ctypes.c_int64),
+                ("host_pool_blocks", ctypes.c_int64), ("softmax_scale", ctypes.c_float)]
+
+
+class wsk_loc(ctypes.Structure):
+    _fields_ = [("part", ctypes.c_int32), ("logical_block", ctypes.c_int32), ("slot", ctypes.c_int32),
+                ("offset", ctypes.c_int32)]
+
+
+class wsk_view(ctypes.Structure):
+    _fields_ = [("pool", ctypes.c_void_p), ("table", ctypes.POINTER(ctypes.c_int32)),
+                ("slot_bytes", ctypes.c_int64), ("head_bytes", ctypes.c_int64), ("v_bytes", ctypes.c_int64),
+                ("row_bytes", ctypes.c_int64), ("start", ctypes.c_int32), ("end", ctypes.c_int32),
+                ("block_tokens", ctypes.c_int32), ("is_device", ctypes.c_int32)]
+
+
+_lib = None
+_VP, _I32, _I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+_PI32 = ctypes.POINTER(ctypes.c_int32)
+_SIGS = {
+    "wsk_last_error": ([], ctypes.c_char_p),
+    "wsk_init": ([ctypes.POINTER(wsk_partition_spec), ctypes.c_int, ctypes.POINTER(_VP)], ctypes.c_int),
+    "wsk_destroy": ([_VP], ctypes.c_int),
+    "wsk_get_spec": ([_VP, ctypes.POINTER(wsk_partition_spec)], ctypes.c_int),
+    "wsk_seq_open": ([_VP, _I32, _I32], ctypes.c_int),
+    "wsk_seq_close": ([_VP, _I32], ctypes.c_int),
+    "wsk_seq_info": ([_VP, _I32, _PI32, _PI32], ctypes.c_int),
+    "wsk_reserve": ([_VP, _I32, _I32], ctypes.c_int),
+    "wsk_write": ([_VP, _I32, _I32, _I32, _VP, _VP, _VP], ctypes.c_int),
+    "wsk_append": ([_VP, _I32, _PI32, _VP, _VP, _VP], ctypes.c_int),
+    "wsk_route": ([_VP, _I32, _I32, ctypes.POINTER(wsk_loc)], ctypes.c_int),
+    "wsk_views": ([_VP, _I32, ctypes.POINTER(wsk_view), ctypes.POINTER(wsk_view)], ctypes.c_int),
+    "wsk_attend_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+    "wsk_attend": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
+    "wsk_merge": ([_I32, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP], ctypes.c_int),
+    "wsk_mla_absorb": ([_I32, _I32, _I32, _I32, _VP, _VP, _VP, _I64, _VP], ctypes.c_int),
+    "wsk_mla_expand": ([_I32, _I32, _I32, _I32, _VP, _VP, _VP, _VP], ctypes.c_int),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """Load libwsk.so (built by paper_2609_14507_amd.build); raise if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libwsk.so is not built (%s): run __graft_entry__.build()" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != WSK_OK:
+        raise WskError(rc, lib().wsk_last_error().decode())
+
+
+def _ptr(t) -> Optional[int]:
+    """Device pointer of a torch tensor (None passes NULL)."""
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    """hipStream_t handle: the given one, else torch's current stream once torch has
+    initialised the GPU, else NULL (the legacy default stream)."""
+    if stream is not None:
+        return stream
+    import torch
+    if torch.cuda.is_initialized():
+        return torch.cuda.current_stream().cuda_stream
+    return None
+
+
+def _i32_array(xs: Sequence[int]):
+    a = (ctypes.c_int32 * max(1, len(xs)))(*[int(x) for x in xs])
+    return a
+
+
+def wsk_last_error() -> str:
+    return lib().wsk_last_error().decode()
+
+
+def make_spec(kind: int, n_q_heads: int, n_kv_heads: int, head_dim: int, block_tokens: int, max_seqs: int,
+              max_seq_len: int, device_pool_blocks: int, host_pool_blocks: int, softmax_scale: float,
+              latent_dim: int = 0, rope_dim: int = 0) -> wsk_partition_spec:
+    return wsk_partition_spec(kind, n_q_heads, n_kv_heads, head_dim, latent_dim, rope_dim, block_tokens,
+                              max_seqs, max_seq_len, 0, device_pool_blocks, host_pool_blocks, softmax_scale)
+
+
+def wsk_init(spec: wsk_partition_spec, device: int) -> int:
+    h = ctypes.c_void_p()
+    _check(lib().wsk_init(ctypes.byref(spec), device, ctypes.byref(h)))
+    return h.value
+
+
+def wsk_destroy(h: int):
+    _check(lib().wsk_destroy(h))
+
+
+def wsk_get_spec(h: int) -> wsk_partition_spec:
+    s = wsk_partition_spec()
+    _check(lib().wsk_get_spec(h, ctypes.byref(s)))
+    return s
+
+
+def wsk_seq_open(h: int, seq: int, split: int):
+    _check(lib().wsk_seq_open(h, seq, split))
+
+
+def wsk_seq_close(h: int, seq: int):
+    _check(lib().wsk_seq_close(h, seq))
+
+
+def wsk_seq_info(h: int, seq: int) -> Tuple[int, int]:
+    L, s = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().wsk_seq_info(h, seq, ctypes.byref(L), ctypes.byref(s)))
+    return L.value, s.value
+
+
+def wsk_reserve(h: int, seq: int, n: int):
+    _check(lib().wsk_reserve(h, seq, n))
+
+
+def wsk_write(h: int, seq: int, pos0: int, k: np.ndarray, v: Optional[np.ndarray], stream=None):
+    """k, v: host uint16 (bf16 bits), token-major [n, Hkv, D] (MLA: k [n, row], v None)."""
+    k = np.ascontiguousarray(k, dtype=np.uint16)
+    v = None if v is None else np.ascontiguousarray(v, dtype=np.uint16)
+    n = k.shape[0]
+    _check(lib().wsk_write(h, seq, pos0, n, k.ctypes.data, None if v is None else v.ctypes.data,
+                           _stream(stream) if n else None))
+
+
+def wsk_append(h: int, seq_ids: Sequence[int], k_new, v_new=None, stream=None):
+    """k_new, v_new: device tensors (bf16), row i for seq_ids[i]."""
+    ids = _i32_array(seq_ids)
+    _check(lib().wsk_append(h, len(seq_ids), ids, _ptr(k_new), _ptr(v_new), _stream(stream)))
+
+
+def wsk_route(h: int, seq: int, pos: int) -> Tuple[int, int, int, int]:
+    loc = wsk_loc()
+    _check(lib().wsk_route(h, seq, pos, ctypes.byref(loc)))
+    return loc.part, loc.logical_block, loc.slot, loc.offset
+
+
+def wsk_views(h: int, seq: int) -> Tuple[wsk_view, wsk_view]:
+    cpu, gpu = wsk_view(), wsk_view()
+    _check(lib().wsk_views(h, seq, ctypes.byref(cpu), ctypes.byref(gpu)))
+    return cpu, gpu
+
+
+def wsk_attend_workspace(h: int, seq_ids, start, end) -> int:
+    b = ctypes.c_size_t()
+    _check(lib().wsk_attend_workspace(h, len(seq_ids), _i32_array(seq_ids), _i32_array(start),
+                                      _i32_array(end), ctypes.byref(b)))
+    return b.value
+
+
+def wsk_attend(h: int, seq_ids, start, end, q, o, lse, ws, stream=None):
+    """q: device bf16 [n, H, qwidth]; o: fp32 [n, H, width]; lse fp32 [n, H]; ws: device uint8 buffer."""
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().wsk_attend(h, len(seq_ids), _i32_array(seq_ids), _i32_array(start), _i32_array(end),
+                            _ptr(q), _ptr(o), _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
+
+
+def wsk_merge(o_a, lse_a, o_b, lse_b, o_out, lse_out, o_bf16=None, stream=None):
+    """Row-wise LSE merge of fp32 device partials [rows, width] / [rows]."""
+    width = o_a.shape[-1]
+    rows = o_a.numel() // width
+    _check(lib().wsk_merge(rows, width, _ptr(o_a), _ptr(lse_a), _ptr(o_b), _ptr(lse_b), _ptr(o_out),
+                           _ptr(lse_out), _ptr(o_bf16), _stream(stream)))
+
+
+def wsk_mla_absorb(q_nope, w_uk, out, out_stride: int, stream=None):
+    """q_nope bf16 [n, H, dn], w_uk bf16 [H, dn, dl]; out bf16 rows at stride out_stride."""
+    n, H, dn = q_nope.shape
+    dl = w_uk.shape[2]
+    _check(lib().wsk_mla_absorb(n, H, dn, dl, _ptr(q_nope), _ptr(w_uk), _ptr(out), out_stride, _stream(stream)))
+
+
+def wsk_mla_expand(o_lat, w_uv, o, stream=None):
+    """o_lat fp32 [n, H, dl], w_uv bf16 [H, dl, dv] -> o fp32 [n, H, dv]."""
+    n, H, dl = o_lat.shape
+    dv = w_uv.shape[2]
+    _check(lib().wsk_mla_expand(n, H, dl, dv, _ptr(o_lat), _ptr(w_uv), _ptr(o), _stream(stream)))

@@ -1,0 +1,358 @@
+"""GPU parity of the GQA decode path against the fp64 oracle (runs on an MI355X).
+
+Routing and pool bytes are compared bit for bit with the oracle's routing
+model; attention outputs and merged results within max_abs <= 1e-2 and
+L1-ratio <= 1e-3 (bf16 inputs, fp32 accumulation).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.route import CPU, GPU, RouteModel
+from paper_2609_14507_amd import workloads as wl
+from paper_2609_14507_amd import wsk
+from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
+from tests.gpu_util import assert_close, assert_lse, d2h, say
+
+pytestmark = pytest.mark.gpu
+DEV = 0
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    torch.cuda.set_device(DEV)
+    yield
+    torch.cuda.synchronize()
+
+
+def _kv_full(prefill, steps_k, steps_v, b):
+    """Token-major K, V of sequence b including appended rows."""
+    k = prefill.k[b]
+    v = prefill.v[b]
+    if steps_k:
+        k = np.concatenate([k] + [s[b][None] for s in steps_k])
+        v = np.concatenate([v] + [s[b][None] for s in steps_v])
+    return k, v
+
+
+def _oracle_partial(w, q_b, k, v, a, e):
+    return oracle.attend(q_b, k, v, a, e, w.softmax_scale, w.group)
+
+
+def _check_step(w, sess, q, ks, vs, prefill, o_gpu, lse_gpu, o_m, lse_m, ranges, label, sample=None):
+    """Compare the GPU partial over `ranges` and the merged result with the oracle."""
+    bs = range(sess.B) if sample is None else sample
+    og, lg, om, lm, rg, rl, rm, rml = [], [], [], [], [], [], [], []
+    for b in bs:
+        k, v = _kv_full(prefill, ks, vs, b)
+        a, e = ranges[b]
+        o_r, l_r = _oracle_partial(w, q[b], k, v, a, e)
+        o_f, l_f = _oracle_partial(w, q[b], k, v, 0, e)
+        og.append(o_gpu[b]); lg.append(lse_gpu[b]); rg.append(o_r); rl.append(l_r)
+        if o_m is not None:
+            om.append(o_m[b]); lm.append(lse_m[b]); rm.append(o_f); rml.append(l_f)
+    assert_close(np.stack(og), np.stack(rg), label + " gpu partial")
+    assert_lse(np.stack(lg), np.stack(rl), label + " gpu partial")
+    if o_m is not None:
+        assert_close(np.stack(om), np.stack(rm), label + " merged")
+        assert_lse(np.stack(lm), np.stack(rml), label + " merged")
+
+
+def _cpu_partial_dev(w, q, prefill, splits, dev):
+    """The CPU-range partial (oracle, fp64 -> fp32) copied to the device."""
+    os_, ls_ = [], []
+    for b in range(len(splits)):
+        o, l = _oracle_partial(w, q[b], prefill.k[b], prefill.v[b], 0, splits[b])
+        os_.append(o)
+        ls_.append(l)
+    return (torch.from_numpy(np.stack(os_).astype(np.float32)).to(dev),
+            torch.from_numpy(np.stack(ls_).astype(np.float32)).to(dev))
+
+
+def _check_routing_and_bytes(sess, model, prefill, ks, vs, full_pool=False):
+    """Bit-exact routing against the oracle model, and the bytes at every routed
+    GPU address equal the source rows; optionally every other pool byte is zero."""
+    w = sess.w
+    cpu_v, gpu_v = wsk.wsk_views(sess.h, 0)
+    slot_bytes = gpu_v.slot_bytes
+    dev_slots = sess.spec.device_pool_blocks
+    pool = d2h(gpu_v.pool, slot_bytes * dev_slots).view(np.uint16)
+    touched = np.zeros(pool.shape, bool) if full_pool else None
+    mism = 0
+    for b in range(sess.B):
+        k, v = _kv_full(prefill, ks, vs, b)
+        L = sess.lengths[b]
+        assert k.shape[0] == L
+        for p in range(L):
+            r = wsk.wsk_route(sess.h, b, p)
+            assert r == model.route(b, p), (b, p, r, model.route(b, p))
+        # bytes of the GPU partition, block by block
+        s = min(sess.splits[b], L)
+        for p0 in range(s, L, sess.spec.block_tokens):
+            part, blk, slot, off = wsk.wsk_route(sess.h, b, p0)
+            p1 = min(L, (blk + 1) * sess.spec.block_tokens)
+            n = p1 - p0
+            for g in range(w.n_kv_heads):
+                for which, src in ((0, k), (1, v)):
+                    a = (slot * slot_bytes + g * gpu_v.head_bytes + which * gpu_v.v_bytes +
+                         off * gpu_v.row_bytes) // 2
+                    got = pool[a:a + n * w.head_dim].reshape(n, w.head_dim)
+                    mism += int(np.count_nonzero(got != src[p0:p1, g]))
+                    if touched is not None:
+                        touched[a:a + n * w.head_dim] = True
+    assert mism == 0, mism
+    if touched is not None:
+        assert not pool[~touched].any()
+
+
+def _model_for(sess, prefill, appended_steps):
+    m = RouteModel(sess.spec.block_tokens, sess.spec.host_pool_blocks, sess.spec.device_pool_blocks)
+    for b in range(sess.B):
+        m.open(b, sess.splits[b])
+        m.write(b, 0, prefill.lengths[b])
+    for _ in range(appended_steps):
+        m.append(list(range(sess.B)))
+    return m
+
+
+# ---------------------------------------------------------------------------
+# Tiny config: one sequence, L = 2048, split 1024; attend, merge, 1-token append
+# ---------------------------------------------------------------------------
+
+def test_c1_attend_merge_append():
+    w = wl.C1
+    say("case c1", w.name)
+    pf = wl.make_prefill(w)
+    st = wl.draw_step(w, pf.gen)
+    dev = torch.device("cuda", DEV)
+    with DecodeSession(w, pf, DEV) as sess:
+        q = to_device_bf16(st.q, dev)
+        o_cpu, l_cpu = _cpu_partial_dev(w, st.q, pf, pf.splits, dev)
+        # attend the GPU partition [s, L), merge with the CPU partial
+        o_g, l_g = sess.attend(q)
+        o_m, l_m = sess.merge(o_cpu, l_cpu, o_g, l_g)
+        ranges = [sess.gpu_range(b) for b in range(sess.B)]
+        _check_step(w, sess, st.q, [], [], pf, o_g.cpu().numpy(), l_g.cpu().numpy(), o_m.cpu().numpy(),
+                    l_m.cpu().numpy(), ranges, "c1")
+        # then append one token and check routing + every byte of the device pool
+        sess.append(to_device_bf16(st.k_new, dev), to_device_bf16(st.v_new, dev))
+        model = _model_for(sess, pf, 1)
+        _check_routing_and_bytes(sess, model, pf, [st.k_new], [st.v_new], full_pool=True)
+        # canonical step order: append first, then attend [s, L+1) and merge
+        o_g2, l_g2 = sess.attend(q)
+        o_m2, l_m2 = sess.merge(o_cpu, l_cpu, o_g2, l_g2)
+        ranges = [sess.gpu_range(b) for b in range(sess.B)]
+        _check_step(w, sess, st.q, [st.k_new], [st.v_new], pf, o_g2.cpu().numpy(), l_g2.cpu().numpy(),
+                    o_m2.cpu().numpy(), l_m2.cpu().numpy(), ranges, "c1 after append")
+
+
+# ---------------------------------------------------------------------------
+# Edge cases on small caches
+# ---------------------------------------------------------------------------
+
+def _small(Hq, Hkv, lengths, splits, seed, bk=64, std=1.0):
+    w = wl.Workload("edge", wl.GQA, batch=len(lengths), n_q_heads=Hq, n_kv_heads=Hkv, head_dim=128,
+                    context=max(lengths), seed=seed, block_tokens=bk, kv_std=std)
+    gen = torch.Generator().manual_seed(seed)
+    ks = [wl.draw_bf16(gen, (L, Hkv, 128), std) for L in lengths]
+    vs = [wl.draw_bf16(gen, (L, Hkv, 128), std) for L in lengths]
+    pf = wl.Prefill(list(lengths), list(splits), ks, vs, gen)
+    return w, pf
+
+
+@pytest.mark.parametrize("Hq,Hkv,bk", [(8, 2, 64), (32, 4, 64), (4, 4, 64), (32, 2, 128), (24, 4, 256),
+                                        (6, 2, 64)])
+def test_ranges_and_group_sizes(Hq, Hkv, bk):
+    """Unaligned, single-token, single-tile, empty and tail ranges; G = 1, 3, 4, 6, 8, 16."""
+    lengths = [1000, 700, 130, 64, 5000, 1]
+    splits = [0, 333, 65, 64, 1234, 0]
+    w, pf = _small(Hq, Hkv, lengths, splits, seed=Hq * 7 + bk)
+    say("case ranges Hq=%d Hkv=%d bk=%d" % (Hq, Hkv, bk))
+    dev = torch.device("cuda", DEV)
+    q_bits = wl.draw_bf16(pf.gen, (len(lengths), Hq, 128))
+    with DecodeSession(w, pf, DEV, extra_tokens=0, block_tokens=bk) as sess:
+        q = to_device_bf16(q_bits, dev)
+        cases = [
+            [(0, 1000), (333, 700), (65, 130), (64, 64), (1234, 5000), (0, 1)],       # whole GPU ranges
+            [(999, 1000), (333, 334), (100, 101), (64, 64), (4999, 5000), (1, 1)],   # one token / empty
+            [(10, 63), (400, 450), (65, 129), (64, 64), (1300, 1400), (0, 0)],       # inside one tile
+            [(63, 65), (383, 385), (127, 130), (64, 64), (1279, 4097), (0, 1)],      # tile boundaries
+        ]
+        for ranges in cases:
+            start = [a for a, _ in ranges]
+            end = [e for _, e in ranges]
+            o, l = sess.attend(q, start, end)
+            o, l = o.cpu().numpy(), l.cpu().numpy()
+            for b, (a, e) in enumerate(ranges):
+                o_r, l_r = oracle.attend(q_bits[b], pf.k[b], pf.v[b], a, e, w.softmax_scale, w.group)
+                if e == a:
+                    assert np.all(o[b] == 0) and np.all(np.isneginf(l[b])), (b, a, e)
+                    continue
+                assert_close(o[b], o_r, "b%d [%d,%d)" % (b, a, e))
+                assert_lse(l[b], l_r, "b%d [%d,%d)" % (b, a, e))
+
+
+def test_garbage_outside_range_is_ignored():
+    """Rows outside [start, end) in the same tiles hold NaN/Inf: the result is unaffected."""
+    Hq, Hkv = 8, 2
+    L = 600
+    w, pf = _small(Hq, Hkv, [L], [0], seed=11)
+    nan_k = pf.k[0].copy()
+    nan_v = pf.v[0].copy()
+    for p in list(range(0, 70)) + list(range(530, 600)):
+        nan_k[p] = 0x7FC0 if p % 2 else 0x7F80     # NaN / +Inf
+        nan_v[p] = 0x7FC0 if p % 3 else 0xFF80
+    pf2 = wl.Prefill([L], [0], [nan_k], [nan_v], pf.gen)
+    q_bits = wl.draw_bf16(pf.gen, (1, Hq, 128))
+    dev = torch.device("cuda", DEV)
+    say("case garbage rows")
+    with DecodeSession(w, pf2, DEV, extra_tokens=0) as sess:
+        o, l = sess.attend(to_device_bf16(q_bits, dev), [70], [530])
+        o_r, l_r = oracle.attend(q_bits[0], pf.k[0], pf.v[0], 70, 530, w.softmax_scale, w.group)
+        assert_close(o.cpu().numpy()[0], o_r, "garbage outside")
+        assert_lse(l.cpu().numpy()[0], l_r, "garbage outside")
+
+
+def test_many_sequences_split_launches_and_duplicates():
+    """More sequences than one launch carries (64), repeated ids, mixed ranges."""
+    n = 70
+    lengths = [int(x) for x in np.random.default_rng(4).integers(1, 400, n)]
+    splits = [int(L * f) for L, f in zip(lengths, np.random.default_rng(5).uniform(0, 1, n))]
+    w, pf = _small(16, 4, lengths, splits, seed=21)
+    dev = torch.device("cuda", DEV)
+    say("case many sequences n=%d" % n)
+    ids = list(range(n)) + [3, 3, 69]
+    q_bits = wl.draw_bf16(pf.gen, (len(ids), 16, 128))
+    with DecodeSession(w, pf, DEV, extra_tokens=0) as sess:
+        start = [sess.gpu_range(b)[0] for b in ids]
+        end = [sess.lengths[b] for b in ids]
+        # the repeated ids attend sub-ranges of their GPU partition
+        for i in (n, n + 1):
+            a, e = sess.gpu_range(3)
+            start[i], end[i] = a + (e - a) // 3 * (i - n), a + (e - a) // 2 * (i - n + 1)
+        o, l = sess.attend(to_device_bf16(q_bits, dev), start, end, ids=ids)
+        o, l = o.cpu().numpy(), l.cpu().numpy()
+        ref_o, ref_l, got_o, got_l = [], [], [], []
+        for i, b in enumerate(ids):
+            o_r, l_r = oracle.attend(q_bits[i], pf.k[b], pf.v[b], start[i], end[i], w.softmax_scale, w.group)
+            if end[i] == start[i]:
+                assert np.all(o[i] == 0) and np.all(np.isneginf(l[i]))
+                continue
+            ref_o.append(o_r); ref_l.append(l_r); got_o.append(o[i]); got_l.append(l[i])
+        assert_close(np.stack(got_o), np.stack(ref_o), "70 sequences")
+        assert_lse(np.stack(got_l), np.stack(ref_l), "70 sequences")
+
+
+def test_merge_kernel_cases():
+    rng = np.random.default_rng(9)
+    dev = torch.device("cuda", DEV)
+    rows, width = 300, 128
+    oa = rng.standard_normal((rows, width)).astype(np.float32)
+    ob = rng.standard_normal((rows, width)).astype(np.float32)
+    la = (rng.standard_normal(rows) * 5).astype(np.float32)
+    lb = (rng.standard_normal(rows) * 5).astype(np.float32)
+    la[:10] = -np.inf                      # empty CPU side
+    lb[10:20] = -np.inf                    # empty GPU side
+    la[20:25] = -np.inf
+    lb[20:25] = -np.inf                    # both empty
+    lb[25:30] = la[25:30] + 80             # one side dominates
+    say("case merge kernel")
+    ro, rl = oracle.merge(oa.astype(np.float64), la.astype(np.float64), ob.astype(np.float64), lb.astype(np.float64))
+    t = lambda x: torch.from_numpy(x).to(dev)
+    o_out, l_out = torch.empty(rows, width, device=dev), torch.empty(rows, device=dev)
+    bf = torch.empty(rows, width, dtype=torch.int16, device=dev)
+    wsk.wsk_merge(t(oa), t(la), t(ob), t(lb), o_out, l_out, bf)
+    got = o_out.cpu().numpy()
+    assert np.array_equal(got[:10], ob[:10]) and np.array_equal(got[10:20], oa[10:20])
+    assert np.all(got[20:25] == 0) and np.all(np.isneginf(l_out.cpu().numpy()[20:25]))
+    assert np.max(np.abs(got - ro)) < 1e-5
+    assert_lse(l_out.cpu().numpy(), rl, "merge")
+    bits = bf.cpu().numpy().view(np.uint16)
+    assert np.array_equal(bits, oracle.round_bf16(got.astype(np.float64)))
+    # in place into the b side
+    ob_d, lb_d = t(ob), t(lb)
+    wsk.wsk_merge(t(oa), t(la), ob_d, lb_d, ob_d, lb_d)
+    assert np.max(np.abs(ob_d.cpu().numpy() - ro)) < 1e-5
+    assert_lse(lb_d.cpu().numpy(), rl, "merge in place")
+
+
+# ---------------------------------------------------------------------------
+# Full-size configurations
+# ---------------------------------------------------------------------------
+
+def test_c2_qwen3_full():
+    w = wl.C2
+    say("case c2", w.name)
+    pf = wl.make_prefill(w)
+    st = wl.draw_step(w, pf.gen)
+    dev = torch.device("cuda", DEV)
+    with DecodeSession(w, pf, DEV) as sess:
+        sess.append(to_device_bf16(st.k_new, dev), to_device_bf16(st.v_new, dev))
+        q = to_device_bf16(st.q, dev)
+        o_g, l_g = sess.attend(q)
+        o_cpu, l_cpu = _cpu_partial_dev(w, st.q, pf, pf.splits, dev)
+        o_m, l_m = sess.merge(o_cpu, l_cpu, o_g, l_g)
+        ranges = [sess.gpu_range(b) for b in range(sess.B)]
+        _check_step(w, sess, st.q, [st.k_new], [st.v_new], pf, o_g.cpu().numpy(), l_g.cpu().numpy(),
+                    o_m.cpu().numpy(), l_m.cpu().numpy(), ranges, "c2")
+        model = _model_for(sess, pf, 1)
+        for b in (0, 7, 15):
+            for p in (0, 9829, 9830, 9831, 32767, 32768):
+                assert wsk.wsk_route(sess.h, b, p) == model.route(b, p)
+
+
+def test_c3_mixtral_sweep_without_data_movement():
+    """The CPU share moves over {0, .25, .5, .75} on one cache written once with s = 0:
+    only the attend range changes, and the device pool's bytes stay identical."""
+    w = wl.C3
+    say("case c3", w.name)
+    pf = wl.make_prefill(w)
+    st = wl.draw_step(w, pf.gen)
+    dev = torch.device("cuda", DEV)
+    with DecodeSession(w, pf, DEV, extra_tokens=0) as sess:
+        _, gpu_v = wsk.wsk_views(sess.h, 0)
+        nbytes = gpu_v.slot_bytes * sess.spec.device_pool_blocks
+        import hashlib
+        before = hashlib.blake2b(d2h(gpu_v.pool, nbytes).tobytes(), digest_size=16).hexdigest()
+        q = to_device_bf16(st.q, dev)
+        L = w.context
+        for share in w.sweep:
+            s = wl.split_point(share, L)
+            o_g, l_g = sess.attend(q, [s] * sess.B, [L] * sess.B)
+            o_cpu, l_cpu = _cpu_partial_dev(w, st.q, pf, [s] * sess.B, dev)
+            o_m, l_m = sess.merge(o_cpu, l_cpu, o_g, l_g)
+            _check_step(w, sess, st.q, [], [], pf, o_g.cpu().numpy(), l_g.cpu().numpy(), o_m.cpu().numpy(),
+                        l_m.cpu().numpy(), [(s, L)] * sess.B, "c3 r=%.2f" % share)
+        after = hashlib.blake2b(d2h(gpu_v.pool, nbytes).tobytes(), digest_size=16).hexdigest()
+        assert before == after
+
+
+def test_c5_ragged_64_steps():
+    w = wl.C5
+    say("case c5", w.name)
+    pf = wl.make_prefill(w)
+    dev = torch.device("cuda", DEV)
+    ks, vs = [], []
+    with DecodeSession(w, pf, DEV) as sess:
+        model = _model_for(sess, pf, 0)
+        for step in range(w.steps):
+            st = wl.draw_step(w, pf.gen)
+            sess.append(to_device_bf16(st.k_new, dev), to_device_bf16(st.v_new, dev))
+            model.append(list(range(sess.B)))
+            ks.append(st.k_new)
+            vs.append(st.v_new)
+            for b in range(sess.B):
+                p = sess.lengths[b] - 1
+                assert wsk.wsk_route(sess.h, b, p) == model.route(b, p)
+            q = to_device_bf16(st.q, dev)
+            o_g, l_g = sess.attend(q)
+            if step in (0, 31, 63):
+                o_cpu, l_cpu = _cpu_partial_dev(w, st.q, pf, pf.splits, dev)
+                o_m, l_m = sess.merge(o_cpu, l_cpu, o_g, l_g)
+                ranges = [sess.gpu_range(b) for b in range(sess.B)]
+                _check_step(w, sess, st.q, ks, vs, pf, o_g.cpu().numpy(), l_g.cpu().numpy(), o_m.cpu().numpy(),
+                            l_m.cpu().numpy(), ranges, "c5 step %d" % step)
