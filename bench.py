@@ -1,0 +1,217 @@
+"""Benchmark of the GPU-partition decode step on one MI355X.
+
+One step = the whole hot path over one batch: append the new token's K/V of
+every sequence into its GPU partition, split-KV attention over the GPU range
+(pass 1 + chunk combine), LSE merge with the CPU-range partial.  Inputs are
+seeded synthetic tensors already resident in HBM; the CPU-range partial fed
+to the merge is a seeded synthetic (O, LSE) pair (the merge's cost does not
+depend on its values).
+
+Timing: W untimed warmup steps, then K timed steps.  Before each step a
+512 MB buffer is rewritten so the 256 MB Infinity Cache holds no KV; HIP
+events on the stream the kernels run on bracket each step (and the attend
+call inside it), outside the flush.  The algorithmic bytes of a step are the
+bf16 K and V rows of every attended position, read once.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "GPU-partition decode attention effective KV GB/s and % of HBM peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor()
+
+
+def cpu_baseline(w, pf, steps_inputs, budget_s: float):
+    """The fp64 oracle, as it stands, over the GPU range of decode step 0, on the
+    host's cores.  Sequences are taken in order until the time budget is spent."""
+    import oracle
+    st = steps_inputs[0]
+    t_total, nbytes, done = 0.0, 0, 0
+    for b in range(len(pf.lengths)):
+        k = np.concatenate([pf.k[b], st.k_new[b][None]])
+        v = np.concatenate([pf.v[b], st.v_new[b][None]])
+        s, L = min(pf.splits[b], k.shape[0]), k.shape[0]
+        t0 = time.perf_counter()
+        oracle.attend(st.q[b], k, v, s, L, w.softmax_scale, w.group)
+        t_total += time.perf_counter() - t0
+        nbytes += (L - s) * w.token_bytes
+        done += 1
+        if t_total >= budget_s:
+            break
+    return {
+        "value": nbytes / t_total / 1e9,
+        "unit": "GB/s",
+        "cores": oracle.max_threads(),
+        "kind": "oracle",
+        "sample": "fp64 oracle over the GPU range of decode step 0 for %d of %d sequences "
+                  "(%.2f GB of KV, %.1f s); CPU: %s" % (done, len(pf.lengths), nbytes / 1e9, t_total, cpu_model()),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c2", help="workload: c2 (default, the metric's), c1, c3, c4, c5")
+    ap.add_argument("--share", type=float, default=None, help="override the CPU share (sweep configs)")
+    ap.add_argument("--no-flush", action="store_true", help="skip the Infinity Cache flush between steps")
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_14507_amd import workloads as wl
+    from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
+
+    w = wl.CONFIGS[args.config]
+    if w.kind == wl.MLA:
+        raise SystemExit("MLA bench is not wired yet")
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    K, W = args.steps, args.warmup
+
+    log("bench: drawing %s" % w.name)
+    pf = wl.make_prefill(w)
+    splits = pf.splits
+    if args.share is not None:
+        splits = [wl.split_point(args.share, L) for L in pf.lengths]
+        pf = wl.Prefill(pf.lengths, splits, pf.k, pf.v, pf.gen)
+    steps_in = [wl.draw_step(w, pf.gen) for _ in range(W + K)]
+    log("bench: routing the prefill into the cache")
+    sess = DecodeSession(w, pf, 0, extra_tokens=W + K)
+    B, H, D = sess.B, w.n_q_heads, w.head_dim
+    qs = [to_device_bf16(s.q, dev) for s in steps_in]
+    kn = [to_device_bf16(s.k_new, dev) for s in steps_in]
+    vn = [to_device_bf16(s.v_new, dev) for s in steps_in]
+    o_c, l_c = wl.draw_cpu_partial(pf.gen, B * H, D)
+    o_cpu = torch.from_numpy(o_c).to(dev).view(B, H, D)
+    l_cpu = torch.from_numpy(l_c).to(dev).view(B, H)
+    o_g = torch.empty(B, H, D, device=dev)
+    l_g = torch.empty(B, H, device=dev)
+    o_m = torch.empty(B, H, D, device=dev)
+    l_m = torch.empty(B, H, device=dev)
+    sess.workspace(sess.ids, [min(s, L) for s, L in zip(splits, pf.lengths)], list(pf.lengths))
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev):
+        if not args.no_flush:
+            flush.add_(1)
+        ev[0].record(stream)
+        sess.append(kn[i], vn[i])
+        ev[1].record(stream)
+        sess.attend(qs[i], o=o_g, lse=l_g)
+        ev[2].record(stream)
+        sess.merge(o_cpu, l_cpu, o_g, l_g, o_m, l_m)
+        ev[3].record(stream)
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(W + K)]
+    nbytes = []
+    log("bench: %d warmup + %d timed steps" % (W, K))
+    for i in range(W):
+        step(i, events[i])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(W, W + K):
+        nbytes.append(sum((sess.lengths[b] + 1 - min(splits[b], sess.lengths[b])) * w.token_bytes
+                          for b in range(B)))
+        step(i, events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = np.array([events[i][0].elapsed_time(events[i][3]) for i in range(W, W + K)])
+    att_ms = np.array([events[i][1].elapsed_time(events[i][2]) for i in range(W, W + K)])
+    app_ms = np.array([events[i][0].elapsed_time(events[i][1]) for i in range(W, W + K)])
+    mrg_ms = np.array([events[i][2].elapsed_time(events[i][3]) for i in range(W, W + K)])
+    nbytes = np.array(nbytes, dtype=np.float64)
+    value = float(nbytes.sum() / (step_ms.sum() * 1e-3) / 1e9)
+    att_gbs = float(nbytes.sum() / (att_ms.sum() * 1e-3) / 1e9)
+    log("bench: step %.1f us (append %.1f, attend %.1f, merge %.1f); attend %.0f GB/s; wall %.1f ms/step"
+        % (step_ms.mean() * 1e3, app_ms.mean() * 1e3, att_ms.mean() * 1e3, mrg_ms.mean() * 1e3, att_gbs,
+           wall / K * 1e3))
+    sess.close()
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(float(step_ms.mean()), 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "batch": B,
+            "q_heads": w.n_q_heads,
+            "kv_heads": w.n_kv_heads,
+            "head_dim": w.head_dim,
+            "context": w.context if w.context else [w.ragged_lo, w.ragged_hi],
+            "cpu_share": args.share if args.share is not None else (w.cpu_share or [w.share_lo, w.share_hi]),
+            "gpu_tokens_per_step": int(nbytes.mean() / w.token_bytes),
+            "kv_bytes_per_step": int(nbytes.mean()),
+            "step": "append + attend (pass 1 + chunk combine) + LSE merge",
+            "cache_flush_between_steps": not args.no_flush,
+        },
+        "breakdown_us": {
+            "append": round(float(app_ms.mean() * 1e3), 2),
+            "attend": round(float(att_ms.mean() * 1e3), 2),
+            "merge": round(float(mrg_ms.mean() * 1e3), 2),
+            "step_p10": round(float(np.percentile(step_ms, 10) * 1e3), 2),
+            "step_p90": round(float(np.percentile(step_ms, 90) * 1e3), 2),
+            "wall_per_step_incl_flush": round(wall / K * 1e6, 1),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "wsk_attend (gqa_attend_kernel + combine_kernel)",
+            "achieved": round(att_gbs, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(att_gbs / HBM_PEAK_GBS, 4),
+            "traffic": None,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the oracle on the host (%.0f s budget)" % args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(w, pf, steps_in, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -78,9 +78,15 @@ extern "C" {
  *   host_pool_blocks   slots in the CPU pool (pageable host memory), >= 0
  *   softmax_scale      multiplier of q.k before the softmax, finite and > 0
  *
- * Slot layout, identical in both pools (bf16):
- *   GQA  slot = [n_kv_heads][2][block_tokens][head_dim]   (index 0 = K, 1 = V)
- *   MLA  slot = [block_tokens][latent_dim + rope_dim]     (latent | rope)
+ * Slot layouts (bf16).  Each partition's layout is fixed by the format for
+ * the engine that reads it (Sec. 4.3 (ii)):
+ *   GQA, CPU pool  slot = [n_kv_heads][2][block_tokens][head_dim]
+ *                  (per head: K rows, then V rows; token-major)
+ *   GQA, GPU pool  slot = [n_kv_heads][ K: block_tokens x head_dim |
+ *                                       V^T: head_dim x block_tokens ]
+ *                  (per head: K rows token-major, then V transposed so that
+ *                  consecutive tokens of one dim are contiguous)
+ *   MLA, both      slot = [block_tokens][latent_dim + rope_dim]  (latent | rope)
  */
 typedef struct wsk_partition_spec {
     int32_t kind;
@@ -110,10 +116,13 @@ typedef struct wsk_loc {
 
 /*
  * Zero-copy view of one partition of one sequence (Sec. 4.3 (iii)).
- * Token p of the partition (start <= p < end), KV head g, lives at
- *   (char*)pool + table[p / block_tokens] * slot_bytes + g * head_bytes
- *                + (p % block_tokens) * row_bytes            (K, or MLA row)
- * and its V row at that address + v_bytes (GQA only).
+ * Token p of the partition (start <= p < end), KV head g, has its K row (or
+ * MLA row) at
+ *   head = (char*)pool + table[p / block_tokens] * slot_bytes + g * head_bytes
+ *   K    = head + (p % block_tokens) * row_bytes
+ * and (GQA only) its V element d at
+ *   head + v_bytes + (p % block_tokens) * row_bytes + 2 * d          if !v_transposed
+ *   head + v_bytes + (d * block_tokens + p % block_tokens) * 2        if v_transposed
  * CPU views hold host addresses; GPU views hold device addresses (the table
  * too).  The pointers are borrowed: they stay valid until wsk_destroy,
  * because placed blocks never move (Sec. 4.2).
@@ -128,6 +137,8 @@ typedef struct wsk_view {
     int32_t start, end;   /* positions held: CPU [0, min(s, L)), GPU [min(s, L), L) */
     int32_t block_tokens;
     int32_t is_device;
+    int32_t v_transposed; /* 1: V stored [head_dim][block_tokens] (GQA GPU pool) */
+    int32_t reserved;
 } wsk_view;
 
 /* Message of the calling thread's last failure ("" if none). */

@@ -1,85 +1,62 @@
 // Split-KV decode attention over a GQA partition (pass 1), gfx950.
 //
-// Computes, for every query head of a KV head, the exact softmax attention
-// over one chunk of the sequence range (the GPU engine of Sec. 5.1), and
-// writes the normalised partial output and its natural-log LSE (the
-// "partial output and normaliser" of Sec. 4.2).
+// For every query head served by one KV head, computes the exact softmax
+// attention over one chunk of the sequence range (the GPU engine of
+// Sec. 5.1) and writes the normalised partial output and its natural-log LSE
+// (the "partial output and normaliser" merged by LSE, Sec. 4.2).
 //
-// Work mapping (one workgroup = 4 wavefronts):
-//   workgroup -> (sequence, KV head, group of GH query heads, chunk of tiles)
-//   wavefront -> every 4th 64-token tile of the chunk, own online softmax
-// Per tile and wavefront:
-//   1. K tile (64 tokens x 128 bf16 = 16 KB) is read with coalesced 16-byte
-//      loads (each instruction covers 4 full rows) and stored to LDS with the
-//      16-byte chunk index XOR-ed by the row, so that reading one whole row
-//      per lane hits distinct banks.
-//   2. QK: lane j owns token j.  v_dot2 bf16 products with fp32 accumulation;
-//      the query rows stay uniform across the wave (scalar registers).
-//   3. Tile max per head with DPP row reductions + 4 readlanes; exp2-domain
-//      online softmax (scale folded with log2 e).
-//   4. P·V: lane (row group r, 16-byte chunk c) owns dims 8c..8c+7 for rows
-//      r, r+4, ...; V comes straight from HBM in 16-byte loads; probabilities
-//      are broadcast from LDS.  fp32 FMA, fp32 probabilities.
-// The next tile's K and V loads are issued while the current tile computes.
-// At the end the four wavefront states are merged through LDS.
+// The G query heads of a KV head share every K and V row, so both products
+// are dense contractions and run on the matrix cores
+// (v_mfma_f32_16x16x32_bf16, query heads padded to 16 rows):
+//
+//   S^T [64 tokens x 16 heads] = K [64 x 128] . Q^T [128 x 16]
+//   O   [16 heads x 128]      += P [16 x 64]  . V [64 x 128]
+//
+// Layouts chosen so every operand comes straight from HBM in 16-byte loads:
+//   - K rows are token-major (as written); the QK A-operand of lane l is 16
+//     bytes of one token row.
+//   - V is stored transposed in the GPU pool (per block: [head_dim][tokens]),
+//     so the P.V B-operand (8 consecutive tokens of one dim) is 16 contiguous
+//     bytes.
+//   - The 16 tokens of each QK M-tile are permuted so that the QK output of a
+//     lane already holds, per K-step of P.V, the 8 consecutive tokens its P
+//     A-operand needs: no data moves between the two products.
+// P is split into bf16 hi + lo parts (two MFMAs), which keeps the P.V
+// product accurate to ~2^-16 relative, like fp32 probabilities.
+//
+// Work mapping: workgroup = (sequence, KV head, group of GH <= 16 query
+// heads, chunk of 64-token tiles); its 4 wavefronts take every 4th tile of the
+// chunk with their own online softmax and are merged through LDS at the end.
 
 #include "wsk_internal.h"
 
 namespace wsk {
 namespace {
 
-typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
-
-__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
-                                           __builtin_bit_cast(bf16x2_t, b), c, false);
-}
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-template <int CTRL>
-__device__ __forceinline__ float dpp_f(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
-}
-__device__ __forceinline__ float lane_f(float v, int l) {
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
-}
-
-// DPP controls: quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror.
-// Applied in this order they pair every lane of a 16-lane row with each other lane.
-__device__ __forceinline__ float wave_max(float v) {
-    v = fmaxf(v, dpp_f<0xB1>(v));
-    v = fmaxf(v, dpp_f<0x4E>(v));
-    v = fmaxf(v, dpp_f<0x141>(v));
-    v = fmaxf(v, dpp_f<0x140>(v));
-    return fmaxf(fmaxf(lane_f(v, 0), lane_f(v, 16)), fmaxf(lane_f(v, 32), lane_f(v, 48)));
-}
-__device__ __forceinline__ float wave_sum(float v) {
-    v += dpp_f<0xB1>(v);
-    v += dpp_f<0x4E>(v);
-    v += dpp_f<0x141>(v);
-    v += dpp_f<0x140>(v);
-    return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
-}
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 
 constexpr int kWaves = 4;
-constexpr int kChunks = kHeadDim * 2 / 16;   // 16-byte chunks per row: 16
 
-// Up to 4 heads per workgroup fit two workgroups per CU (<= 256 registers per
-// lane); 5-8 heads need the whole register file (one workgroup per CU).
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Token (0..63) of row r (0..15) of QK M-tile mt (0..3).  Rows 4g..4g+3 of
+// M-tiles 2k and 2k+1 are tokens 32k + 8g .. 32k + 8g + 7.
+__device__ __forceinline__ int tile_token(int mt, int r) {
+    return 32 * (mt >> 1) + 8 * (r >> 2) + 4 * (mt & 1) + (r & 3);
+}
+
 template <int GH>
-__global__ __launch_bounds__(256, (GH <= 4 ? 2 : 1)) void gqa_attend_kernel(const AttendParams p) {
-    __shared__ u32x4 s_k[kWaves][kTile * kChunks];   // 4 x 16 KB
-    __shared__ float s_p[kWaves][kTile][8];           // 4 x 2 KB
-    __shared__ float s_m[kWaves][8];
-    __shared__ float s_l[kWaves][8];
+__global__ __launch_bounds__(256, 2) void gqa_attend_kernel(const AttendParams p) {
+    __shared__ float s_o[kWaves][GH][kHeadDim];
+    __shared__ float s_m[kWaves][GH];
+    __shared__ float s_l[kWaves][GH];
 
     const int lane = threadIdx.x & 63;
-    // uniform within a wavefront; readfirstlane tells the compiler so, which
-    // keeps all tile addressing on the scalar unit
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int n = lane & 15;     // MFMA column: query head (QK) / dim within an N-tile (P.V)
+    const int grp = lane >> 4;   // MFMA k-group 0..3
 
     // ---- work item of this workgroup (uniform) ----
     const int wg = blockIdx.x;
@@ -97,174 +74,151 @@ __global__ __launch_bounds__(256, (GH <= 4 ? 2 : 1)) void gqa_attend_kernel(cons
     const int tile0 = (t_start >> 6) + c * p.tiles_per_chunk;
     const int tile_end = min(tile0 + p.tiles_per_chunk, ((t_end - 1) >> 6) + 1);
     const int h0 = g * p.group + hg * GH;
-    // The query rows are read-only for the whole kernel: read them through the
-    // constant address space so they are fetched with scalar loads into SGPRs.
-    typedef const __attribute__((address_space(4))) uint32_t cu32;
-    cu32 *qw = (cu32 *)(p.q + (int64_t)i * p.q_row + (int64_t)h0 * kHeadDim);
     typedef const __attribute__((address_space(4))) int32_t ci32;
     ci32 *trow = (ci32 *)(p.table + (int64_t)seq * p.table_stride);   // read-only here
     const int bk = p.block_tokens;
-    const int bshift = __builtin_ctz(bk);     // block_tokens is a power of two
+    const int bshift = __builtin_ctz(bk);
     const int64_t head_off = (int64_t)g * 2 * bk * kHeadDim;
+    const int head_bytes = 2 * bk * kHeadDim * 2;     // K rows then V^T of one head in one slot
+    const int vt_bytes = bk * kHeadDim * 2;           // offset of V^T from the K rows
 
-    // Buffer descriptor over the K and V rows of KV head g in the slot of
-    // tile tt (2 * block_tokens rows of 256 bytes); soffset selects the tile's
-    // first row.  Accesses past the descriptor's extent read zero.
-    const int head_bytes = 2 * bk * kHeadDim * 2;
-    auto tile_rsrc = [&](int tt, int &row_bytes0) -> __amdgpu_buffer_rsrc_t {
-        const int tok0 = tt * kTile;
+    // Q^T operand (constant): lane (grp, n) holds q[h0 + n][32ks + 8grp .. +8]
+    bf16x8 qop[4];
+    {
+        const u32x4 *qrow = reinterpret_cast<const u32x4 *>(p.q + (int64_t)i * p.q_row +
+                                                            (int64_t)(h0 + (n < GH ? n : 0)) * kHeadDim);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const u32x4 v = qrow[ks * 4 + grp];
+            qop[ks] = as_bf16x8(n < GH ? v : u32x4{0u, 0u, 0u, 0u});
+        }
+    }
+
+    // lane parts of the load offsets (bytes within one (slot, head) region)
+    int koff[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) koff[mt] = tile_token(mt, n) * (kHeadDim * 2) + 16 * grp;
+    const int voff = n * bk * 2 + 16 * grp;
+
+    float m_run = -INFINITY;   // running max of head n (exp2 domain)
+    float l_lane = 0.f;        // this lane's share of head n's normaliser
+    f32x4 o[8];
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int t = tile0 + wave; t < tile_end; t += kWaves) {
+        const int tok0 = t * kTile;
         const int blk = tok0 >> bshift;
-        row_bytes0 = (tok0 - (blk << bshift)) * (kHeadDim * 2);
+        const int row0 = tok0 - (blk << bshift);
         const int slot = __builtin_amdgcn_readfirstlane(trow[blk]);
         const uint16_t *base = p.pool + (int64_t)slot * p.slot_elems + head_off;
-        return __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, head_bytes, 0x00020000);
-    };
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, head_bytes, 0x00020000);
 
-    float m_run[GH], l_lane[GH], o[GH][8];
+        // ---- loads: K A-operands [mt][ks], V^T B-operands [nt][ks] ----
+        u32x4 ka[4][4], vb[8][2];
 #pragma unroll
-    for (int h = 0; h < GH; ++h) {
-        m_run[h] = -INFINITY;
-        l_lane[h] = 0.f;
+        for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
-    }
+            for (int ks = 0; ks < 4; ++ks)
+                ka[mt][ks] = __builtin_amdgcn_raw_buffer_load_b128(rs, koff[mt] + 64 * ks, row0 * (kHeadDim * 2), 0);
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt)
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks)
+                vb[nt][ks] = __builtin_amdgcn_raw_buffer_load_b128(
+                    rs, voff + 64 * ks, vt_bytes + row0 * 2 + nt * 16 * bk * 2, 0);
 
-    const int rgrp = lane >> 4;   // row group 0..3 (rows rgrp, rgrp+4, ...)
-    const int chk = lane & 15;    // 16-byte chunk within a row
-    u32x4 vreg[16];
-    u32x4 *sk = s_k[wave];
-    typedef __attribute__((address_space(3))) void lds_void;
-    // K tile -> LDS by DMA.  Instruction ii fills LDS slots ii*64 .. ii*64+63;
-    // slot (row r, position pc) receives logical chunk pc ^ (r & 15) of row r,
-    // so the 16 lanes of a row still read that row's 256 contiguous bytes.
-    int koff[4];                                    // lane part of the K DMA source
+        // ---- QK on the matrix cores ----
+        f32x4 s[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) koff[j] = rgrp * 256 + ((chk ^ (j * 4 + rgrp)) * 16);
-    const int voff = lane * 16;
-    auto issue_k = [&](int tt) {
-        int rb0;
-        const __amdgpu_buffer_rsrc_t rs = tile_rsrc(tt, rb0);
+        for (int mt = 0; mt < 4; ++mt) {
+            s[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ii = 0; ii < 16; ++ii)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)(sk + ii * 64), 16, koff[ii & 3],
-                                                     rb0 + ii * 1024, 0, 0);
-    };
-    // V rows outside [start, end) may hold anything (even NaN bit patterns);
-    // they are read from an offset past the descriptor's extent, which the
-    // hardware returns as zeros, so their zero probability adds exactly nothing.
-    auto issue_v = [&](int tt) {
-        int rb0;
-        const __amdgpu_buffer_rsrc_t rs = tile_rsrc(tt, rb0);
-        const int vb0 = rb0 + bk * kHeadDim * 2;
-        const int tok_l = tt * kTile + rgrp;
-#pragma unroll
-        for (int ii = 0; ii < 16; ++ii) {
-            const int tok = tok_l + ii * 4;
-            const int off = (tok >= t_start && tok < t_end) ? voff : 0x40000000;
-            vreg[ii] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, vb0 + ii * 1024, 0);
+            for (int ks = 0; ks < 4; ++ks)
+                s[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka[mt][ks]), qop[ks], s[mt], 0, 0, 0);
         }
-    };
 
-    int t = tile0 + wave;
-    if (t < tile_end) {
-        issue_k(t);
-        issue_v(t);
-    }
-    for (; t < tile_end; t += kWaves) {
-        const int tn = t + kWaves;
-        // 2. QK: lane = token.  The query pointer is made opaque per tile so the
-        // compiler re-reads the (scalar-cache resident) query inside the loop
-        // instead of hoisting GH*64 dwords into scalar registers.
-        cu32 *qt = qw;
-        asm volatile("" : "+s"(qt));
-        float acc[GH];
+        // ---- online softmax (exp2 domain) for head n over this tile ----
+        const bool partial = tok0 < t_start || tok0 + kTile > t_end;
+        float sv[4][4];
+        float mloc = -INFINITY;
 #pragma unroll
-        for (int h = 0; h < GH; ++h) acc[h] = 0.f;
-#pragma unroll 2
-        for (int ch = 0; ch < kChunks; ++ch) {
-            const u32x4 kk = sk[lane * kChunks + (ch ^ (lane & 15))];
+        for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-            for (int h = 0; h < GH; ++h) {
-                cu32 *qh = qt + h * (kHeadDim / 2) + ch * 4;
-                acc[h] = dot2_bf16(qh[0], kk.x, acc[h]);
-                acc[h] = dot2_bf16(qh[1], kk.y, acc[h]);
-                acc[h] = dot2_bf16(qh[2], kk.z, acc[h]);
-                acc[h] = dot2_bf16(qh[3], kk.w, acc[h]);
+            for (int r = 0; r < 4; ++r) {
+                const int tok = tok0 + 32 * (mt >> 1) + 8 * grp + 4 * (mt & 1) + r;
+                const bool ok = !partial || (tok >= t_start && tok < t_end);
+                sv[mt][r] = ok ? s[mt][r] * p.scale_log2 : -INFINITY;
+                mloc = fmaxf(mloc, sv[mt][r]);
+            }
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+        const float m_new = fmaxf(m_run, mloc);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        float psum = 0.f;
+        bf16x8 phi[2], plo[2];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float pv = __builtin_amdgcn_exp2f(sv[2 * ks + (j >> 2)][j & 3] - m_new);
+                psum += pv;
+                const __bf16 hi = (__bf16)pv;
+                phi[ks][j] = hi;
+                plo[ks][j] = (__bf16)(pv - (float)hi);
+            }
+        l_lane = fmaf(l_lane, alpha, psum);
+
+        // rows of O are heads 4grp..4grp+3: fetch their rescale factors
+        float alpha_r[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) alpha_r[r] = __shfl(alpha, 4 * grp + r);
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) o[nt][r] *= alpha_r[r];
+
+        // rows outside [start, end) may hold anything (even NaN): zero their V
+        if (partial) {
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                uint32_t mask[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int tk = tok0 + 32 * ks + 8 * grp + 2 * e;
+                    mask[e] = ((tk >= t_start && tk < t_end) ? 0x0000ffffu : 0u) |
+                              ((tk + 1 >= t_start && tk + 1 < t_end) ? 0xffff0000u : 0u);
+                }
+#pragma unroll
+                for (int nt = 0; nt < 8; ++nt) vb[nt][ks] &= u32x4{mask[0], mask[1], mask[2], mask[3]};
             }
         }
 
-        // every lane has read its K row: the buffer may be refilled
-        __builtin_amdgcn_wave_barrier();
-        if (tn < tile_end) issue_k(tn);
-
-        // 3. online softmax in the exp2 domain
-        const int tok = t * kTile + lane;
-        const bool valid = tok >= t_start && tok < t_end;
-        float pr[GH], alpha[GH];
+        // ---- P.V on the matrix cores ----
 #pragma unroll
-        for (int h = 0; h < GH; ++h) {
-            const float s = valid ? acc[h] * p.scale_log2 : -INFINITY;
-            const float mn = fmaxf(m_run[h], wave_max(s));
-            alpha[h] = __builtin_amdgcn_exp2f(m_run[h] - mn);
-            pr[h] = __builtin_amdgcn_exp2f(s - mn);
-            l_lane[h] = fmaf(l_lane[h], alpha[h], pr[h]);
-            m_run[h] = mn;
-        }
-        float *prow = s_p[wave][lane];
+        for (int nt = 0; nt < 8; ++nt)
 #pragma unroll
-        for (int h = 0; h < GH; ++h) prow[h] = pr[h];
-        __builtin_amdgcn_wave_barrier();
-
-        // 4. P·V
-#pragma unroll
-        for (int h = 0; h < GH; ++h)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) o[h][e] *= alpha[h];
-#pragma unroll
-        for (int ii = 0; ii < 16; ++ii) {
-            const int r = ii * 4 + rgrp;
-            float pv[GH];
-            const float *pp = s_p[wave][r];
-            if constexpr (GH == 8) {
-                const f32x4 a = *reinterpret_cast<const f32x4 *>(pp);
-                const f32x4 b = *reinterpret_cast<const f32x4 *>(pp + 4);
-                pv[0] = a.x; pv[1] = a.y; pv[2] = a.z; pv[3] = a.w;
-                pv[4] = b.x; pv[5] = b.y; pv[6] = b.z; pv[7] = b.w;
-            } else {
-#pragma unroll
-                for (int h = 0; h < GH; ++h) pv[h] = pp[h];
+            for (int ks = 0; ks < 2; ++ks) {
+                o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(phi[ks], as_bf16x8(vb[nt][ks]), o[nt], 0, 0, 0);
+                o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo[ks], as_bf16x8(vb[nt][ks]), o[nt], 0, 0, 0);
             }
-            const u32x4 w4 = vreg[ii];
-            const float vf[8] = {bf16_lo(w4.x), bf16_hi(w4.x), bf16_lo(w4.y), bf16_hi(w4.y),
-                                 bf16_lo(w4.z), bf16_hi(w4.z), bf16_lo(w4.w), bf16_hi(w4.w)};
-#pragma unroll
-            for (int h = 0; h < GH; ++h)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) o[h][e] = fmaf(pv[h], vf[e], o[h][e]);
-            // keep each row step's probability reads and conversions next to
-            // their FMAs (hoisting them all needs > 100 extra registers)
-            if constexpr (GH > 2) __builtin_amdgcn_sched_barrier(0);
-        }
-        if (tn < tile_end) issue_v(tn);
-        __builtin_amdgcn_wave_barrier();
     }
 
-    // ---- merge the four wavefront states ----
-    float l_w[GH];
-#pragma unroll
-    for (int h = 0; h < GH; ++h) l_w[h] = wave_sum(l_lane[h]);
-    float *red = reinterpret_cast<float *>(sk);   // [4 row groups][GH][128] fp32 <= 16 KB
-#pragma unroll
-    for (int h = 0; h < GH; ++h) {
-        f32x4 *dst = reinterpret_cast<f32x4 *>(red + (rgrp * GH + h) * kHeadDim + chk * 8);
-        dst[0] = f32x4{o[h][0], o[h][1], o[h][2], o[h][3]};
-        dst[1] = f32x4{o[h][4], o[h][5], o[h][6], o[h][7]};
+    // ---- merge the four wavefront states through LDS ----
+    float l_tot = l_lane + __shfl_xor(l_lane, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    if (grp == 0 && n < GH) {
+        s_m[wave][n] = m_run;
+        s_l[wave][n] = l_tot;
     }
-    if (lane == 0) {
 #pragma unroll
-        for (int h = 0; h < GH; ++h) {
-            s_m[wave][h] = m_run[h];
-            s_l[wave][h] = l_w[h];
+    for (int r = 0; r < 4; ++r) {
+        const int h = 4 * grp + r;
+        if (h < GH) {
+#pragma unroll
+            for (int nt = 0; nt < 8; ++nt) s_o[wave][h][16 * nt + n] = o[nt][r];
         }
     }
     __syncthreads();
@@ -280,11 +234,7 @@ __global__ __launch_bounds__(256, (GH <= 4 ? 2 : 1)) void gqa_attend_kernel(cons
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) {
             const float a = __builtin_amdgcn_exp2f(s_m[w][h] - M);
-            const float *rw = reinterpret_cast<const float *>(s_k[w]);
-            float sum = 0.f;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) sum += rw[(r * GH + h) * kHeadDim + d];
-            num = fmaf(a, sum, num);
+            num = fmaf(a, s_o[w][h][d], num);
             den = fmaf(a, s_l[w][h], den);
         }
         const int64_t row = (int64_t)part * p.n_q_heads + h0 + h;
@@ -301,12 +251,9 @@ hipError_t launch_gqa_attend(const AttendParams &p, int heads_per_wg, int n_wg, 
     switch (heads_per_wg) {
         case 1: hipLaunchKernelGGL(gqa_attend_kernel<1>, grid, block, 0, s, p); break;
         case 2: hipLaunchKernelGGL(gqa_attend_kernel<2>, grid, block, 0, s, p); break;
-        case 3: hipLaunchKernelGGL(gqa_attend_kernel<3>, grid, block, 0, s, p); break;
         case 4: hipLaunchKernelGGL(gqa_attend_kernel<4>, grid, block, 0, s, p); break;
-        case 5: hipLaunchKernelGGL(gqa_attend_kernel<5>, grid, block, 0, s, p); break;
-        case 6: hipLaunchKernelGGL(gqa_attend_kernel<6>, grid, block, 0, s, p); break;
-        case 7: hipLaunchKernelGGL(gqa_attend_kernel<7>, grid, block, 0, s, p); break;
         case 8: hipLaunchKernelGGL(gqa_attend_kernel<8>, grid, block, 0, s, p); break;
+        case 16: hipLaunchKernelGGL(gqa_attend_kernel<16>, grid, block, 0, s, p); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

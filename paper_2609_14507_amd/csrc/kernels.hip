@@ -22,98 +22,108 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 // ---------------------------------------------------------------------------
 // Chunk combine: O = sum_c w_c O_c / sum_c w_c, w_c = exp(lse_c - max lse),
 // LSE = max + ln sum w_c.  One wavefront per (sequence, head); each lane owns
-// WIDTH/64 consecutive output elements.  No chunk (empty range): O = 0,
-// LSE = -inf.
+// WIDTH/64 consecutive output elements; chunk loads are unrolled so many are
+// in flight at once.  No chunk (empty range): O = 0, LSE = -inf.
 // ---------------------------------------------------------------------------
 template <int WIDTH>
 __global__ __launch_bounds__(64) void combine_kernel(const CombineParams p) {
     constexpr int PER = WIDTH / 64;
+    typedef __attribute__((ext_vector_type(PER))) float fv;
     const int row = blockIdx.x;                 // i * H + h
     const int i = row / p.n_q_heads;
     const int h = row - i * p.n_q_heads;
     const int c0 = p.chunk_begin[i];
     const int nc = p.chunk_begin[i + 1] - c0;
     const int lane = threadIdx.x;
-    float acc[PER];
-#pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+    fv *out = reinterpret_cast<fv *>(p.o + (int64_t)row * WIDTH) + lane;
     if (nc == 0) {
-#pragma unroll
-        for (int e = 0; e < PER; ++e) p.o[(int64_t)row * WIDTH + lane * PER + e] = 0.f;
+        *out = fv{};
         if (lane == 0) p.lse[row] = -INFINITY;
         return;
     }
     const float *pl = p.part_lse + (int64_t)c0 * p.n_q_heads + h;
     float m = -INFINITY;
+#pragma unroll 8
     for (int c = 0; c < nc; ++c) m = fmaxf(m, pl[(int64_t)c * p.n_q_heads]);
     float den = 0.f;
+    fv acc = fv{};
+    const fv *po = reinterpret_cast<const fv *>(p.part_o + ((int64_t)c0 * p.n_q_heads + h) * WIDTH) + lane;
+    const int64_t cstride = (int64_t)p.n_q_heads * WIDTH / PER;
+#pragma unroll 8
     for (int c = 0; c < nc; ++c) {
         const float w = __expf(pl[(int64_t)c * p.n_q_heads] - m);
         den += w;
-        const float *po = p.part_o + ((int64_t)(c0 + c) * p.n_q_heads + h) * WIDTH + lane * PER;
-#pragma unroll
-        for (int e = 0; e < PER; ++e) acc[e] = fmaf(w, po[e], acc[e]);
+        acc += w * po[c * cstride];
     }
-    const float inv = 1.f / den;
-#pragma unroll
-    for (int e = 0; e < PER; ++e) p.o[(int64_t)row * WIDTH + lane * PER + e] = acc[e] * inv;
+    *out = acc * (1.f / den);
     if (lane == 0) p.lse[row] = m + __logf(den);
 }
 
 // ---------------------------------------------------------------------------
-// LSE merge of two partials, 4 elements per thread.
+// LSE merge of two partials.  A workgroup owns whole rows: thread t first
+// reads the LSEs of row t into LDS and writes that row's merged LSE, so
+// lse_out may alias lse_a or lse_b; O is then merged 4 elements per thread.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void merge_kernel(int32_t rows, int32_t width, const float *o_a,
-                                                    const float *lse_a, const float *o_b,
-                                                    const float *lse_b, float *o_out, uint16_t *o_bf16) {
-    const int64_t q4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // float4 index
-    const int64_t total4 = (int64_t)rows * width / 4;
-    if (q4 >= total4) return;
-    const int64_t e0 = q4 * 4;
-    const int64_t r = e0 / width;
-    const float la = lse_a[r], lb = lse_b[r];
-    const float m = fmaxf(la, lb);
-    // The row's LSE is written by merge_lse_kernel afterwards: lse_out may
-    // alias lse_a or lse_b, which every element of the row reads here.
-    f32x4 y;
-    if (m == -INFINITY) {
-        y = f32x4{0.f, 0.f, 0.f, 0.f};
-    } else {
-        const float wa = __expf(la - m), wb = __expf(lb - m);
-        const float inv = 1.f / (wa + wb);
-        const f32x4 a = *reinterpret_cast<const f32x4 *>(o_a + e0);
-        const f32x4 b = *reinterpret_cast<const f32x4 *>(o_b + e0);
-        y = (wa * a + wb * b) * inv;
+__global__ __launch_bounds__(256) void merge_kernel(int32_t rows, int32_t width, int32_t rows_per_wg,
+                                                    const float *o_a, const float *lse_a, const float *o_b,
+                                                    const float *lse_b, float *o_out, float *lse_out,
+                                                    uint16_t *o_bf16) {
+    __shared__ float s_wa[256], s_wb[256];
+    const int r0 = blockIdx.x * rows_per_wg;
+    const int nr = min(rows_per_wg, rows - r0);
+    if ((int)threadIdx.x < nr) {
+        const int r = r0 + threadIdx.x;
+        const float la = lse_a[r], lb = lse_b[r];
+        const float m = fmaxf(la, lb);
+        float wa = 0.f, wb = 0.f, lo = -INFINITY;
+        if (m != -INFINITY) {
+            wa = __expf(la - m);
+            wb = __expf(lb - m);
+            lo = m + __logf(wa + wb);
+            const float inv = 1.f / (wa + wb);
+            wa *= inv;
+            wb *= inv;
+        }
+        s_wa[threadIdx.x] = wa;
+        s_wb[threadIdx.x] = wb;
+        lse_out[r] = lo;
     }
-    *reinterpret_cast<f32x4 *>(o_out + e0) = y;
-    if (o_bf16) {
-        uint16_t *d = o_bf16 + e0;
-        d[0] = f32_to_bf16(y.x);
-        d[1] = f32_to_bf16(y.y);
-        d[2] = f32_to_bf16(y.z);
-        d[3] = f32_to_bf16(y.w);
+    __syncthreads();
+    const int w4 = width / 4;
+    for (int f = threadIdx.x; f < nr * w4; f += blockDim.x) {
+        const int rr = f / w4;
+        const int64_t e0 = (int64_t)(r0 + rr) * width + (int64_t)(f - rr * w4) * 4;
+        const float wa = s_wa[rr], wb = s_wb[rr];
+        f32x4 y = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (wa != 0.f || wb != 0.f) {
+            // a side with zero weight is not read: an empty partial's O may be anything
+            const f32x4 a = wa != 0.f ? *reinterpret_cast<const f32x4 *>(o_a + e0) : f32x4{0.f, 0.f, 0.f, 0.f};
+            const f32x4 b = wb != 0.f ? *reinterpret_cast<const f32x4 *>(o_b + e0) : f32x4{0.f, 0.f, 0.f, 0.f};
+            y = wa * a + wb * b;
+        }
+        *reinterpret_cast<f32x4 *>(o_out + e0) = y;
+        if (o_bf16) {
+            uint16_t *d = o_bf16 + e0;
+            d[0] = f32_to_bf16(y.x);
+            d[1] = f32_to_bf16(y.y);
+            d[2] = f32_to_bf16(y.z);
+            d[3] = f32_to_bf16(y.w);
+        }
     }
-}
-
-__global__ __launch_bounds__(256) void merge_lse_kernel(int32_t rows, const float *lse_a,
-                                                        const float *lse_b, float *lse_out) {
-    const int r = blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= rows) return;
-    const float la = lse_a[r], lb = lse_b[r];
-    const float m = fmaxf(la, lb);
-    lse_out[r] = (m == -INFINITY) ? -INFINITY : m + __logf(__expf(la - m) + __expf(lb - m));
 }
 
 // ---------------------------------------------------------------------------
 // Decode append: one workgroup per appended row (all KV heads, K and V).
+// GPU-pool GQA slot per KV head: K rows [Bk][D], then V transposed [D][Bk].
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void append_kernel(const AppendParams p) {
     const int r = blockIdx.x;
-    const int64_t dst0 = p.dst[r];
+    const int64_t slot0 = p.slot_elem0[r];
+    const int row = p.row[r];
     if (threadIdx.x == 0 && p.tab_index[r] >= 0) p.table[p.tab_index[r]] = p.tab_slot[r];
     const int row16 = p.row_elems / 8;                 // 16-byte pieces per row
+    const int bk = p.block_tokens;
     if (p.kind == 0) {
-        // source [n][Hkv][D]; destination head g at dst0 + g*2*Bk*D (K), + Bk*D (V)
         const int pieces = p.n_kv_heads * row16;
         for (int t = threadIdx.x; t < 2 * pieces; t += blockDim.x) {
             const int which = t / pieces;              // 0 = K, 1 = V
@@ -121,25 +131,36 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendParams p) {
             const int g = q / row16;
             const int k = q - g * row16;
             const uint16_t *src = (which ? p.v_new : p.k_new) + ((int64_t)r * p.n_kv_heads + g) * p.row_elems;
-            uint16_t *dst = p.pool + dst0 + (int64_t)g * 2 * p.block_tokens * p.row_elems +
-                            (int64_t)which * p.block_tokens * p.row_elems;
-            reinterpret_cast<u32x4 *>(dst)[k] = reinterpret_cast<const u32x4 *>(src)[k];
+            uint16_t *head = p.pool + slot0 + (int64_t)g * 2 * bk * p.row_elems;
+            const u32x4 v = reinterpret_cast<const u32x4 *>(src)[k];
+            if (which == 0) {
+                reinterpret_cast<u32x4 *>(head + (int64_t)row * p.row_elems)[k] = v;
+            } else {
+                uint16_t *vt = head + (int64_t)bk * p.row_elems + row;   // column `row` of V^T
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    vt[(int64_t)(8 * k + 2 * e) * bk] = (uint16_t)(v[e] & 0xffffu);
+                    vt[(int64_t)(8 * k + 2 * e + 1) * bk] = (uint16_t)(v[e] >> 16);
+                }
+            }
         }
     } else {
         const uint16_t *src = p.k_new + (int64_t)r * p.row_elems;
+        uint16_t *dst = p.pool + slot0 + (int64_t)row * p.row_elems;
         for (int k = threadIdx.x; k < row16; k += blockDim.x)
-            reinterpret_cast<u32x4 *>(p.pool + dst0)[k] = reinterpret_cast<const u32x4 *>(src)[k];
+            reinterpret_cast<u32x4 *>(dst)[k] = reinterpret_cast<const u32x4 *>(src)[k];
     }
 }
 
 // ---------------------------------------------------------------------------
-// Bulk scatter of staged rows into the GPU partition.
+// Bulk scatter of staged rows into the GPU partition (same slot layout).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void scatter_kernel(const ScatterParams p) {
     const int row16 = p.row_elems / 8;
     const int per_pos = (p.kind == 0) ? 2 * p.n_kv_heads * row16 : row16;
     const int64_t total = (int64_t)p.m * per_pos;
-    const int bshift = __builtin_ctz(p.block_tokens);
+    const int bk = p.block_tokens;
+    const int bshift = __builtin_ctz(bk);
     for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
          t += (int64_t)gridDim.x * blockDim.x) {
         const int j = (int)(t / per_pos);
@@ -154,9 +175,18 @@ __global__ __launch_bounds__(256) void scatter_kernel(const ScatterParams p) {
             const int g = q / row16;
             const int k = q - g * row16;
             const uint16_t *src = (which ? p.src_v : p.src_k) + ((int64_t)j * p.n_kv_heads + g) * p.row_elems;
-            uint16_t *dst = p.pool + slot * p.slot_elems +
-                            ((int64_t)(g * 2 + which) * p.block_tokens + off) * p.row_elems;
-            reinterpret_cast<u32x4 *>(dst)[k] = reinterpret_cast<const u32x4 *>(src)[k];
+            uint16_t *head = p.pool + slot * p.slot_elems + (int64_t)g * 2 * bk * p.row_elems;
+            const u32x4 v = reinterpret_cast<const u32x4 *>(src)[k];
+            if (which == 0) {
+                reinterpret_cast<u32x4 *>(head + (int64_t)off * p.row_elems)[k] = v;
+            } else {
+                uint16_t *vt = head + (int64_t)bk * p.row_elems + off;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    vt[(int64_t)(8 * k + 2 * e) * bk] = (uint16_t)(v[e] & 0xffffu);
+                    vt[(int64_t)(8 * k + 2 * e + 1) * bk] = (uint16_t)(v[e] >> 16);
+                }
+            }
         } else {
             const uint16_t *src = p.src_k + (int64_t)j * p.row_elems;
             uint16_t *dst = p.pool + slot * p.slot_elems + (int64_t)off * p.row_elems;
@@ -242,14 +272,12 @@ hipError_t launch_merge(int32_t rows, int32_t width, const float *o_a, const flo
                         const float *o_b, const float *lse_b, float *o_out, float *lse_out,
                         uint16_t *o_bf16, hipStream_t s) {
     if (rows <= 0) return hipSuccess;
-    const int64_t total4 = (int64_t)rows * width / 4;
-    const int64_t blocks = (total4 + 255) / 256;
-    hipLaunchKernelGGL(merge_kernel, dim3((unsigned)blocks), dim3(256), 0, s, rows, width, o_a, lse_a,
-                       o_b, lse_b, o_out, o_bf16);
-    // The row LSEs are written in a second pass, after every element of every
-    // row has read them: o_out/lse_out may alias the inputs.
-    hipLaunchKernelGGL(merge_lse_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, rows, lse_a, lse_b,
-                       lse_out);
+    int rpw = 1024 / width;
+    if (rpw < 1) rpw = 1;
+    if (rpw > 256) rpw = 256;
+    const int blocks = (rows + rpw - 1) / rpw;
+    hipLaunchKernelGGL(merge_kernel, dim3(blocks), dim3(256), 0, s, rows, width, rpw, o_a, lse_a, o_b, lse_b,
+                       o_out, lse_out, o_bf16);
     return hipGetLastError();
 }
 

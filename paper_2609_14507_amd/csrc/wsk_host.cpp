@@ -164,7 +164,9 @@ void commit(wsk_cache *c, const std::vector<Pending> &pend) {
     for (const Pending &p : pend) tab(c, p.part, p.seq, p.blk) = p.slot;
 }
 
-// Offset (elements) of position pos, KV head g, K (which = 0) or V (1), in its slot.
+// Offset (elements) of position pos, KV head g, K (which = 0) or V (1), in
+// its slot of the CPU pool, where every row is token-major.  (The GPU pool
+// stores GQA V transposed; its rows are placed by the append/scatter kernels.)
 inline int64_t row_offset(const wsk_cache *c, int32_t pos, int g, int which) {
     const int bk = c->spec.block_tokens;
     const int off = pos % bk;
@@ -520,7 +522,8 @@ int wsk_append(wsk_cache *c, int32_t n, const int32_t *ids, const void *k_new, c
             const int32_t pos = c->length[sq];
             const int32_t blk = pos / sp.block_tokens;
             const int32_t slot = tab(c, WSK_PART_GPU, sq, blk);
-            ap.dst[r] = (int64_t)slot * c->slot_elems + row_offset(c, pos, 0, 0);
+            ap.slot_elem0[r] = (int64_t)slot * c->slot_elems;
+            ap.row[r] = pos % sp.block_tokens;
             ap.tab_index[r] = -1;
             for (const Pending &p : pend)
                 if (p.seq == sq && p.part == WSK_PART_GPU && p.blk == blk) {
@@ -564,6 +567,8 @@ int wsk_views(const wsk_cache *c, int32_t seq, wsk_view *cpu, wsk_view *gpu) {
         v->v_bytes = gqa ? c->spec.block_tokens * row_bytes : 0;
         v->row_bytes = row_bytes;
         v->block_tokens = c->spec.block_tokens;
+        v->v_transposed = (gqa && side == 1) ? 1 : 0;
+        v->reserved = 0;
         if (side == 0) {
             v->pool = c->hpool;
             v->table = c->htab[0].data() + (size_t)seq * c->max_blocks;

@@ -59,8 +59,9 @@ struct CombineParams {
     int32_t chunk_begin[kMaxLaunchSeqs + 1];
 };
 
-// Decode append: row r of the source goes to the pool at dst[r] (elements);
-// GQA rows carry K and V for every KV head.  tab_index[r] >= 0 also stores
+// Decode append: row r of the source goes to row row[r] of the slot whose
+// first element is slot_elem0[r]; GQA rows carry K and V for every KV head
+// (V stored transposed in the GPU pool).  tab_index[r] >= 0 also stores
 // tab_slot[r] into the device table (a newly opened block).
 struct AppendParams {
     const uint16_t *k_new;
@@ -72,7 +73,8 @@ struct AppendParams {
     int32_t n_kv_heads;
     int32_t block_tokens;
     int32_t row_elems;       // GQA: head_dim; MLA: latent + rope
-    int64_t dst[kMaxLaunchSeqs];
+    int64_t slot_elem0[kMaxLaunchSeqs];
+    int32_t row[kMaxLaunchSeqs];
     int32_t tab_index[kMaxLaunchSeqs];
     int32_t tab_slot[kMaxLaunchSeqs];
 };
@@ -107,9 +109,9 @@ hipError_t launch_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const
                              const uint16_t *w_uv, float *o, hipStream_t s);
 
 // Heads per workgroup used by the GQA kernel for a group size G: the largest
-// divisor of G that is at most 8.
+// power of two dividing G, at most 16 (the matrix-core tile height).
 inline int gqa_heads_per_wg(int G) {
-    for (int d = 8; d >= 1; --d)
+    for (int d = 16; d > 1; d >>= 1)
         if (G % d == 0) return d;
     return 1;
 }

@@ -72,9 +72,13 @@ class DecodeSession:
             self.lengths[b] += 1
 
     def workspace(self, ids, start, end) -> torch.Tensor:
+        """Device workspace for an attend call; grown with room for one more chunk
+        partial per sequence, so that decode steps that cross into a new chunk do
+        not allocate."""
         need = wsk.wsk_attend_workspace(self.h, ids, start, end)
         if self._ws.numel() < need:
-            self._ws = torch.empty(need, dtype=torch.uint8, device=self.dev)
+            spare = len(ids) * self.w.n_q_heads * (self.out_width + 1) * 4 + 512
+            self._ws = torch.empty(need + spare, dtype=torch.uint8, device=self.dev)
         return self._ws
 
     def attend(self, q: torch.Tensor, start: Optional[Sequence[int]] = None, end: Optional[Sequence[int]] = None,

@@ -47,7 +47,8 @@ class wsk_view(ctypes.Structure):
     _fields_ = [("pool", ctypes.c_void_p), ("table", ctypes.POINTER(ctypes.c_int32)),
                 ("slot_bytes", ctypes.c_int64), ("head_bytes", ctypes.c_int64), ("v_bytes", ctypes.c_int64),
                 ("row_bytes", ctypes.c_int64), ("start", ctypes.c_int32), ("end", ctypes.c_int32),
-                ("block_tokens", ctypes.c_int32), ("is_device", ctypes.c_int32)]
+                ("block_tokens", ctypes.c_int32), ("is_device", ctypes.c_int32),
+                ("v_transposed", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 _lib = None

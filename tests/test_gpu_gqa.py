@@ -96,14 +96,19 @@ def _check_routing_and_bytes(sess, model, prefill, ks, vs, full_pool=False):
             part, blk, slot, off = wsk.wsk_route(sess.h, b, p0)
             p1 = min(L, (blk + 1) * sess.spec.block_tokens)
             n = p1 - p0
+            bk = sess.spec.block_tokens
+            assert gpu_v.v_transposed == 1
             for g in range(w.n_kv_heads):
-                for which, src in ((0, k), (1, v)):
-                    a = (slot * slot_bytes + g * gpu_v.head_bytes + which * gpu_v.v_bytes +
-                         off * gpu_v.row_bytes) // 2
-                    got = pool[a:a + n * w.head_dim].reshape(n, w.head_dim)
-                    mism += int(np.count_nonzero(got != src[p0:p1, g]))
-                    if touched is not None:
-                        touched[a:a + n * w.head_dim] = True
+                head = (slot * slot_bytes + g * gpu_v.head_bytes) // 2
+                a = head + off * w.head_dim                      # K rows, token-major
+                got = pool[a:a + n * w.head_dim].reshape(n, w.head_dim)
+                mism += int(np.count_nonzero(got != k[p0:p1, g]))
+                vt = head + gpu_v.v_bytes // 2                   # V^T [head_dim][bk]
+                idx = vt + np.arange(w.head_dim)[:, None] * bk + np.arange(off, off + n)[None, :]
+                mism += int(np.count_nonzero(pool[idx] != v[p0:p1, g].T))
+                if touched is not None:
+                    touched[a:a + n * w.head_dim] = True
+                    touched[idx] = True
     assert mism == 0, mism
     if touched is not None:
         assert not pool[~touched].any()
