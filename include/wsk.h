@@ -55,6 +55,9 @@ extern "C" {
 #define WSK_PART_CPU 0
 #define WSK_PART_GPU 1
 
+#define WSK_LAYOUT_ROWS 0    /* token-major rows                               */
+#define WSK_LAYOUT_TILED64 1 /* GQA GPU pool: 64-token tiles in matrix-core order */
+
 /* Largest number of query heads one KV head may serve in a GQA cache.       */
 #define WSK_MAX_GROUP 64
 
@@ -82,10 +85,14 @@ extern "C" {
  * the engine that reads it (Sec. 4.3 (ii)):
  *   GQA, CPU pool  slot = [n_kv_heads][2][block_tokens][head_dim]
  *                  (per head: K rows, then V rows; token-major)
- *   GQA, GPU pool  slot = [n_kv_heads][ K: block_tokens x head_dim |
- *                                       V^T: head_dim x block_tokens ]
- *                  (per head: K rows token-major, then V transposed so that
- *                  consecutive tokens of one dim are contiguous)
+ *   GQA, GPU pool  slot = [n_kv_heads][block_tokens / 64 tiles][K: 1024 | V: 1024]
+ *                  16-byte pieces, each piece 8 bf16, in the order the GPU
+ *                  kernel's matrix-core lanes read them (WSK_LAYOUT_TILED64):
+ *                  token t of a tile (0..63), dim d (0..127):
+ *                    K: piece (4*mt + d/32)*64 + 16*((d%32)/8) + nk, elem d%8,
+ *                       mt = 2*(t/32) + (t%8)/4,  nk = 4*((t%32)/8) + t%4
+ *                    V: piece (2*(d/16) + t/32)*64 + 16*((t%32)/8) + d%16,
+ *                       elem t%8
  *   MLA, both      slot = [block_tokens][latent_dim + rope_dim]  (latent | rope)
  */
 typedef struct wsk_partition_spec {
@@ -116,13 +123,14 @@ typedef struct wsk_loc {
 
 /*
  * Zero-copy view of one partition of one sequence (Sec. 4.3 (iii)).
- * Token p of the partition (start <= p < end), KV head g, has its K row (or
- * MLA row) at
- *   head = (char*)pool + table[p / block_tokens] * slot_bytes + g * head_bytes
- *   K    = head + (p % block_tokens) * row_bytes
- * and (GQA only) its V element d at
- *   head + v_bytes + (p % block_tokens) * row_bytes + 2 * d          if !v_transposed
- *   head + v_bytes + (d * block_tokens + p % block_tokens) * 2        if v_transposed
+ * For token p of the partition (start <= p < end) and KV head g, let
+ *   head = (char*)pool + table[p / block_tokens] * slot_bytes + g * head_bytes.
+ * layout WSK_LAYOUT_ROWS: the K row (or MLA row) is at
+ *   head + (p % block_tokens) * row_bytes,
+ *   and (GQA) the V row at head + v_bytes + (p % block_tokens) * row_bytes.
+ * layout WSK_LAYOUT_TILED64 (GQA GPU pool): tile k = (p % block_tokens) / 64
+ *   starts at head + k * 32768; its K pieces follow, then its V pieces at
+ *   + 16384, placed as described for the slot layout above.
  * CPU views hold host addresses; GPU views hold device addresses (the table
  * too).  The pointers are borrowed: they stay valid until wsk_destroy,
  * because placed blocks never move (Sec. 4.2).
@@ -137,7 +145,7 @@ typedef struct wsk_view {
     int32_t start, end;   /* positions held: CPU [0, min(s, L)), GPU [min(s, L), L) */
     int32_t block_tokens;
     int32_t is_device;
-    int32_t v_transposed; /* 1: V stored [head_dim][block_tokens] (GQA GPU pool) */
+    int32_t layout;       /* WSK_LAYOUT_ROWS or WSK_LAYOUT_TILED64 */
     int32_t reserved;
 } wsk_view;
 

@@ -12,21 +12,25 @@
 //   S^T [64 tokens x 16 heads] = K [64 x 128] . Q^T [128 x 16]
 //   O   [16 heads x 128]      += P [16 x 64]  . V [64 x 128]
 //
-// Layouts chosen so every operand comes straight from HBM in 16-byte loads:
-//   - K rows are token-major (as written); the QK A-operand of lane l is 16
-//     bytes of one token row.
-//   - V is stored transposed in the GPU pool (per block: [head_dim][tokens]),
-//     so the P.V B-operand (8 consecutive tokens of one dim) is 16 contiguous
-//     bytes.
-//   - The 16 tokens of each QK M-tile are permuted so that the QK output of a
-//     lane already holds, per K-step of P.V, the 8 consecutive tokens its P
-//     A-operand needs: no data moves between the two products.
-// P is split into bf16 hi + lo parts (two MFMAs), which keeps the P.V
-// product accurate to ~2^-16 relative, like fp32 probabilities.
+// The GPU pool keeps each 64-token tile of a KV head as 2 x 1024 16-byte
+// pieces in exactly the order the matrix-core lanes consume them (the
+// TILED64 format, fixed when the rows are written): every operand load is
+// one 16-byte load per lane and 1 KB contiguous per wavefront instruction.
+//   - QK A-operand (mt, ks), lane (grp, n): K[token tile_token(mt, n)]
+//     [dims 32ks + 8grp .. +8]
+//   - P.V B-operand (nt, ks), lane (grp, n): V[tokens 32ks + 8grp .. +8]
+//     [dim 16nt + n]
+// tile_token() permutes the tokens of each QK M-tile so that the QK output of
+// a lane already holds, per K-step of P.V, the 8 consecutive tokens its P
+// A-operand needs: nothing moves between the two products.  P is split into
+// bf16 hi + lo parts (two MFMAs), which keeps P.V accurate to ~2^-16
+// relative, like fp32 probabilities.
 //
 // Work mapping: workgroup = (sequence, KV head, group of GH <= 16 query
 // heads, chunk of 64-token tiles); its 4 wavefronts take every 4th tile of the
 // chunk with their own online softmax and are merged through LDS at the end.
+// Each wavefront issues the next tile's K loads as soon as QK has consumed
+// the current ones, and the next V loads right after P.V.
 
 #include "wsk_internal.h"
 
@@ -38,6 +42,7 @@ typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 
 constexpr int kWaves = 4;
+constexpr int kTileBytes = 2 * kTile * kHeadDim * 2;   // K and V pieces of one 64-token tile: 32 KB
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -71,16 +76,16 @@ __global__ __launch_bounds__(256, 2) void gqa_attend_kernel(const AttendParams p
     const int seq = p.seq[i];
     const int t_start = p.start[i];
     const int t_end = p.end[i];
-    const int tile0 = (t_start >> 6) + c * p.tiles_per_chunk;
-    const int tile_end = min(tile0 + p.tiles_per_chunk, ((t_end - 1) >> 6) + 1);
+    const int tpc = p.tpc[i];
+    const int tile0 = (t_start >> 6) + c * tpc;
+    const int tile_end = min(tile0 + tpc, ((t_end - 1) >> 6) + 1);
     const int h0 = g * p.group + hg * GH;
     typedef const __attribute__((address_space(4))) int32_t ci32;
     ci32 *trow = (ci32 *)(p.table + (int64_t)seq * p.table_stride);   // read-only here
     const int bk = p.block_tokens;
     const int bshift = __builtin_ctz(bk);
     const int64_t head_off = (int64_t)g * 2 * bk * kHeadDim;
-    const int head_bytes = 2 * bk * kHeadDim * 2;     // K rows then V^T of one head in one slot
-    const int vt_bytes = bk * kHeadDim * 2;           // offset of V^T from the K rows
+    const int head_bytes = 2 * bk * kHeadDim * 2;     // all tiles of one head in one slot
 
     // Q^T operand (constant): lane (grp, n) holds q[h0 + n][32ks + 8grp .. +8]
     bf16x8 qop[4];
@@ -94,40 +99,53 @@ __global__ __launch_bounds__(256, 2) void gqa_attend_kernel(const AttendParams p
         }
     }
 
-    // lane parts of the load offsets (bytes within one (slot, head) region)
-    int koff[4];
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt) koff[mt] = tile_token(mt, n) * (kHeadDim * 2) + 16 * grp;
-    const int voff = n * bk * 2 + 16 * grp;
-
     float m_run = -INFINITY;   // running max of head n (exp2 domain)
     float l_lane = 0.f;        // this lane's share of head n's normaliser
     f32x4 o[8];
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int t = tile0 + wave; t < tile_end; t += kWaves) {
+    // Buffer descriptor over the tiles of KV head g in the slot holding tile
+    // t; toff = byte offset of the tile inside it.  The descriptor's extent
+    // bounds every load to that (slot, head).
+    auto tile_rsrc = [&](int t, int &toff) -> __amdgpu_buffer_rsrc_t {
         const int tok0 = t * kTile;
         const int blk = tok0 >> bshift;
-        const int row0 = tok0 - (blk << bshift);
+        toff = ((tok0 - (blk << bshift)) >> 6) * kTileBytes;
         const int slot = __builtin_amdgcn_readfirstlane(trow[blk]);
         const uint16_t *base = p.pool + (int64_t)slot * p.slot_elems + head_off;
-        const __amdgpu_buffer_rsrc_t rs =
-            __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, head_bytes, 0x00020000);
-
-        // ---- loads: K A-operands [mt][ks], V^T B-operands [nt][ks] ----
-        u32x4 ka[4][4], vb[8][2];
+        return __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, head_bytes, 0x00020000);
+    };
+    const int loff = lane * 16;
+    u32x4 ka[4][4], vb[8][2];
+    auto load_k = [&](int t) {
+        int toff;
+        const __amdgpu_buffer_rsrc_t rs = tile_rsrc(t, toff);
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks)
-                ka[mt][ks] = __builtin_amdgcn_raw_buffer_load_b128(rs, koff[mt] + 64 * ks, row0 * (kHeadDim * 2), 0);
+                ka[mt][ks] = __builtin_amdgcn_raw_buffer_load_b128(rs, loff, toff + (mt * 4 + ks) * 1024, kStreamLoad);
+    };
+    auto load_v = [&](int t) {
+        int toff;
+        const __amdgpu_buffer_rsrc_t rs = tile_rsrc(t, toff);
 #pragma unroll
         for (int nt = 0; nt < 8; ++nt)
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks)
                 vb[nt][ks] = __builtin_amdgcn_raw_buffer_load_b128(
-                    rs, voff + 64 * ks, vt_bytes + row0 * 2 + nt * 16 * bk * 2, 0);
+                    rs, loff, toff + kTileBytes / 2 + (nt * 2 + ks) * 1024, kStreamLoad);
+    };
+
+    int t = tile0 + wave;
+    if (t < tile_end) {
+        load_k(t);
+        load_v(t);
+    }
+    for (; t < tile_end; t += kWaves) {
+        const int tok0 = t * kTile;
+        const int tn = t + kWaves;
 
         // ---- QK on the matrix cores ----
         f32x4 s[4];
@@ -138,6 +156,7 @@ __global__ __launch_bounds__(256, 2) void gqa_attend_kernel(const AttendParams p
             for (int ks = 0; ks < 4; ++ks)
                 s[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka[mt][ks]), qop[ks], s[mt], 0, 0, 0);
         }
+        if (tn < tile_end) load_k(tn);
 
         // ---- online softmax (exp2 domain) for head n over this tile ----
         const bool partial = tok0 < t_start || tok0 + kTile > t_end;
@@ -204,6 +223,7 @@ __global__ __launch_bounds__(256, 2) void gqa_attend_kernel(const AttendParams p
                 o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(phi[ks], as_bf16x8(vb[nt][ks]), o[nt], 0, 0, 0);
                 o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo[ks], as_bf16x8(vb[nt][ks]), o[nt], 0, 0, 0);
             }
+        if (tn < tile_end) load_v(tn);
     }
 
     // ---- merge the four wavefront states through LDS ----

@@ -11,6 +11,30 @@ typedef __attribute__((ext_vector_type(4))) float f32x4;
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
+// Places 16-byte piece k (dims 8k..8k+7) of the K (which = 0) or V row of
+// token `row` of one KV head into the GPU pool's TILED64 format; `head`
+// points at the head's first tile in the slot.  A tile is 1024 K pieces then
+// 1024 V pieces of 8 bf16, in the order the attention kernel's matrix-core
+// lanes read them (see attend_gqa.hip).
+__device__ __forceinline__ void put_tiled(uint16_t *head, int row, int which, int k, u32x4 v) {
+    uint16_t *tile = head + (int64_t)(row >> 6) * (2 * 64 * 128);
+    const int t = row & 63;
+    if (which == 0) {
+        const int mt = 2 * (t >> 5) + ((t & 7) >> 2);
+        const int nk = 4 * ((t & 31) >> 3) + (t & 3);
+        const int piece = (4 * mt + (k >> 2)) * 64 + 16 * (k & 3) + nk;
+        *reinterpret_cast<u32x4 *>(tile + piece * 8) = v;
+    } else {
+        uint16_t *vt = tile + 1024 * 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int d = 8 * k + e;
+            const int piece = (2 * (d >> 4) + (t >> 5)) * 64 + 16 * ((t & 31) >> 3) + (d & 15);
+            vt[piece * 8 + (t & 7)] = (uint16_t)((e & 1) ? (v[e >> 1] >> 16) : (v[e >> 1] & 0xffffu));
+        }
+    }
+}
+
 // fp32 -> bf16, round to nearest even (NaN stays NaN).
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     uint32_t u = __float_as_uint(f);
@@ -114,7 +138,7 @@ __global__ __launch_bounds__(256) void merge_kernel(int32_t rows, int32_t width,
 
 // ---------------------------------------------------------------------------
 // Decode append: one workgroup per appended row (all KV heads, K and V).
-// GPU-pool GQA slot per KV head: K rows [Bk][D], then V transposed [D][Bk].
+// GPU-pool GQA rows go to the TILED64 format (put_tiled).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void append_kernel(const AppendParams p) {
     const int r = blockIdx.x;
@@ -132,17 +156,7 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendParams p) {
             const int k = q - g * row16;
             const uint16_t *src = (which ? p.v_new : p.k_new) + ((int64_t)r * p.n_kv_heads + g) * p.row_elems;
             uint16_t *head = p.pool + slot0 + (int64_t)g * 2 * bk * p.row_elems;
-            const u32x4 v = reinterpret_cast<const u32x4 *>(src)[k];
-            if (which == 0) {
-                reinterpret_cast<u32x4 *>(head + (int64_t)row * p.row_elems)[k] = v;
-            } else {
-                uint16_t *vt = head + (int64_t)bk * p.row_elems + row;   // column `row` of V^T
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    vt[(int64_t)(8 * k + 2 * e) * bk] = (uint16_t)(v[e] & 0xffffu);
-                    vt[(int64_t)(8 * k + 2 * e + 1) * bk] = (uint16_t)(v[e] >> 16);
-                }
-            }
+            put_tiled(head, row, which, k, reinterpret_cast<const u32x4 *>(src)[k]);
         }
     } else {
         const uint16_t *src = p.k_new + (int64_t)r * p.row_elems;
@@ -176,17 +190,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(const ScatterParams p) {
             const int k = q - g * row16;
             const uint16_t *src = (which ? p.src_v : p.src_k) + ((int64_t)j * p.n_kv_heads + g) * p.row_elems;
             uint16_t *head = p.pool + slot * p.slot_elems + (int64_t)g * 2 * bk * p.row_elems;
-            const u32x4 v = reinterpret_cast<const u32x4 *>(src)[k];
-            if (which == 0) {
-                reinterpret_cast<u32x4 *>(head + (int64_t)off * p.row_elems)[k] = v;
-            } else {
-                uint16_t *vt = head + (int64_t)bk * p.row_elems + off;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    vt[(int64_t)(8 * k + 2 * e) * bk] = (uint16_t)(v[e] & 0xffffu);
-                    vt[(int64_t)(8 * k + 2 * e + 1) * bk] = (uint16_t)(v[e] >> 16);
-                }
-            }
+            put_tiled(head, off, which, k, reinterpret_cast<const u32x4 *>(src)[k]);
         } else {
             const uint16_t *src = p.src_k + (int64_t)j * p.row_elems;
             uint16_t *dst = p.pool + slot * p.slot_elems + (int64_t)off * p.row_elems;

@@ -64,6 +64,7 @@ constexpr size_t kStageBytes = 64u << 20;
 struct wsk_cache {
     wsk_partition_spec spec;
     int device = -1;
+    int cu_count = 256;           // compute units of the device (MI355X: 256)
     int32_t max_blocks = 0;       // logical blocks per sequence
     int32_t row_elems = 0;        // bf16 elements of one cached row (one head's K, or one MLA row)
     int32_t rows_per_pos = 0;     // rows one position stores (GQA: 2 * Hkv; MLA: 1)
@@ -166,7 +167,8 @@ void commit(wsk_cache *c, const std::vector<Pending> &pend) {
 
 // Offset (elements) of position pos, KV head g, K (which = 0) or V (1), in
 // its slot of the CPU pool, where every row is token-major.  (The GPU pool
-// stores GQA V transposed; its rows are placed by the append/scatter kernels.)
+// stores GQA rows in 64-token matrix-core tiles, placed by the append/scatter
+// kernels.)
 inline int64_t row_offset(const wsk_cache *c, int32_t pos, int g, int which) {
     const int bk = c->spec.block_tokens;
     const int off = pos % bk;
@@ -175,12 +177,15 @@ inline int64_t row_offset(const wsk_cache *c, int32_t pos, int g, int which) {
 }
 
 // Split-KV chunking of one attend call.  Chunks are whole 64-token tiles of
-// the absolute tile grid; every call with the same arguments yields the same
-// layout, so wsk_attend_workspace and wsk_attend agree.
+// the absolute tile grid.  Each sequence gets a number of chunks in
+// proportion to its tiles, so that all workgroups carry about the same work
+// and the whole grid is about one round of resident workgroups (every CU busy
+// from start to end, no tail).  Every call with the same arguments yields the
+// same layout, so wsk_attend_workspace and wsk_attend agree.
 struct AttendPlan {
-    int32_t tiles_per_chunk = 4;
     int heads_per_wg = 1;
     int head_groups = 1;
+    std::vector<int32_t> tpc;       // tiles per chunk, per sequence
     std::vector<int32_t> nchunks;   // per sequence
     int64_t partials = 0;           // sum of nchunks
     size_t part_o_bytes = 0;
@@ -211,17 +216,23 @@ int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *
         pl.head_groups = G / pl.heads_per_wg;
         units = sp.n_kv_heads * pl.head_groups;
     }
-    // About 2048 workgroups keep every CU busy through several rounds while
-    // each wavefront still streams several tiles; at least 4 tiles per chunk
-    // (one per wavefront), at most 64.
-    int64_t want = (total_tiles * units + 2047) / 2048;
-    int64_t tpc = std::max<int64_t>(4, std::min<int64_t>(64, want));
-    tpc = (tpc + 3) / 4 * 4;
-    pl.tiles_per_chunk = (int32_t)tpc;
+    // workgroups resident at once (2 per CU for the attention kernels); the
+    // chunk budget per (KV head, head group) unit follows from it
+    const int64_t slots = 2 * (int64_t)c->cu_count;
+    const int64_t budget = std::max<int64_t>(1, slots / units);
+    pl.tpc.assign(n, 1);
     pl.nchunks.assign(n, 0);
     pl.partials = 0;
     for (int32_t i = 0; i < n; ++i) {
-        pl.nchunks[i] = (int32_t)((n_tiles(start[i], end[i]) + tpc - 1) / tpc);
+        const int64_t T = n_tiles(start[i], end[i]);
+        if (T == 0) continue;
+        // chunks in proportion to this sequence's tiles, at least one, and at
+        // least 4 tiles (one per wavefront) per chunk when the range allows
+        int64_t want = total_tiles ? (budget * T + total_tiles / 2) / total_tiles : 1;
+        want = std::max<int64_t>(1, std::min<int64_t>(want, (T + 3) / 4));
+        const int64_t tpc = (T + want - 1) / want;
+        pl.tpc[i] = (int32_t)tpc;
+        pl.nchunks[i] = (int32_t)((T + tpc - 1) / tpc);
         pl.partials += pl.nchunks[i];
     }
     const int width = sp.kind == WSK_KIND_GQA ? kHeadDim : kLatent;
@@ -287,7 +298,8 @@ int wsk_init(const wsk_partition_spec *spec, int device, wsk_cache **out) {
             wsk_destroy(c);
             return hip_fail(guard.err, "hipSetDevice");
         }
-        hipError_t e = hipSuccess;
+        hipError_t e = hipDeviceGetAttribute(&c->cu_count, hipDeviceAttributeMultiprocessorCount, device);
+        if (e == hipSuccess && c->cu_count <= 0) c->cu_count = 256;
         const size_t pool_bytes = (size_t)spec->device_pool_blocks * slot_bytes;
         if (pool_bytes) e = hipMalloc((void **)&c->dpool, pool_bytes);
         if (e == hipSuccess && pool_bytes) e = hipMemset(c->dpool, 0, pool_bytes);
@@ -564,10 +576,10 @@ int wsk_views(const wsk_cache *c, int32_t seq, wsk_view *cpu, wsk_view *gpu) {
         if (!v) continue;
         v->slot_bytes = slot_bytes;
         v->head_bytes = gqa ? 2 * c->spec.block_tokens * row_bytes : 0;
-        v->v_bytes = gqa ? c->spec.block_tokens * row_bytes : 0;
+        v->v_bytes = gqa ? (side == 0 ? c->spec.block_tokens * row_bytes : kTile * row_bytes) : 0;
         v->row_bytes = row_bytes;
         v->block_tokens = c->spec.block_tokens;
-        v->v_transposed = (gqa && side == 1) ? 1 : 0;
+        v->layout = (gqa && side == 1) ? WSK_LAYOUT_TILED64 : WSK_LAYOUT_ROWS;
         v->reserved = 0;
         if (side == 0) {
             v->pool = c->hpool;
@@ -635,7 +647,6 @@ int wsk_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start
         ap.group = sp.n_q_heads / ap.n_kv_heads;
         ap.head_groups = gqa ? pl.head_groups : 1;
         ap.block_tokens = sp.block_tokens;
-        ap.tiles_per_chunk = pl.tiles_per_chunk;
         ap.n = m;
         ap.scale_log2 = sp.softmax_scale * 1.4426950408889634f;
         const int units = ap.n_kv_heads * ap.head_groups;
@@ -645,6 +656,7 @@ int wsk_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start
             ap.seq[r] = ids[i0 + r];
             ap.start[r] = start[i0 + r];
             ap.end[r] = end[i0 + r];
+            ap.tpc[r] = pl.tpc[i0 + r];
             const int32_t nc = pl.nchunks[i0 + r];
             ap.wg_begin[r + 1] = ap.wg_begin[r] + nc * units;
             ap.chunk_begin[r + 1] = ap.chunk_begin[r] + nc;

@@ -16,11 +16,15 @@ constexpr int kHeadDim = 128;
 // MLA latent and RoPE widths.
 constexpr int kLatent = 512;
 constexpr int kRope = 64;
+// Cache policy of loads that stream KV rows read once per step: non-temporal
+// (gfx950 "nt"), so they do not displace reusable lines in L2 and the
+// Infinity Cache.
+constexpr int kStreamLoad = 2;
 
 // ---------------------------------------------------------------------------
 // Split-KV attention (pass 1).  One workgroup = (sequence i, KV head g, query
-// head group hg, chunk c); a chunk is tiles_per_chunk consecutive 64-token
-// tiles of [start, end) on the absolute tile grid.  Each workgroup writes a
+// head group hg, chunk c); a chunk is tpc[i] consecutive 64-token tiles of
+// [start, end) on the absolute tile grid.  Each workgroup writes a
 // normalised partial O and its LSE for its heads into part_o / part_lse at
 // partial index chunk_begin[i] + c.
 // ---------------------------------------------------------------------------
@@ -38,10 +42,10 @@ struct AttendParams {
     int32_t group;           // query heads per KV head
     int32_t head_groups;     // workgroups per KV head along the query heads
     int32_t block_tokens;
-    int32_t tiles_per_chunk;
     int32_t n;
     float scale_log2;        // softmax scale * log2(e)
     int32_t seq[kMaxLaunchSeqs];
+    int32_t tpc[kMaxLaunchSeqs];   // tiles per chunk of each sequence
     int32_t start[kMaxLaunchSeqs];
     int32_t end[kMaxLaunchSeqs];
     int32_t wg_begin[kMaxLaunchSeqs + 1];

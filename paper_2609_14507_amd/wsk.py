@@ -21,6 +21,7 @@ ERROR_NAMES = {WSK_EINVAL: "EINVAL", WSK_ENOMEM: "ENOMEM", WSK_ERANGE: "ERANGE",
                WSK_EHIP: "EHIP", WSK_ESTATE: "ESTATE"}
 KIND_GQA, KIND_MLA = 0, 1
 PART_CPU, PART_GPU = 0, 1
+LAYOUT_ROWS, LAYOUT_TILED64 = 0, 1
 
 
 class WskError(RuntimeError):
@@ -48,7 +49,7 @@ class wsk_view(ctypes.Structure):
                 ("slot_bytes", ctypes.c_int64), ("head_bytes", ctypes.c_int64), ("v_bytes", ctypes.c_int64),
                 ("row_bytes", ctypes.c_int64), ("start", ctypes.c_int32), ("end", ctypes.c_int32),
                 ("block_tokens", ctypes.c_int32), ("is_device", ctypes.c_int32),
-                ("v_transposed", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("layout", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 _lib = None

@@ -90,25 +90,32 @@ def _check_routing_and_bytes(sess, model, prefill, ks, vs, full_pool=False):
         for p in range(L):
             r = wsk.wsk_route(sess.h, b, p)
             assert r == model.route(b, p), (b, p, r, model.route(b, p))
-        # bytes of the GPU partition, block by block
+        # bytes of the GPU partition: every position, both K and V, at the
+        # element the TILED64 formula of include/wsk.h names
+        assert gpu_v.layout == wsk.LAYOUT_TILED64
         s = min(sess.splits[b], L)
-        for p0 in range(s, L, sess.spec.block_tokens):
-            part, blk, slot, off = wsk.wsk_route(sess.h, b, p0)
-            p1 = min(L, (blk + 1) * sess.spec.block_tokens)
-            n = p1 - p0
-            bk = sess.spec.block_tokens
-            assert gpu_v.v_transposed == 1
-            for g in range(w.n_kv_heads):
-                head = (slot * slot_bytes + g * gpu_v.head_bytes) // 2
-                a = head + off * w.head_dim                      # K rows, token-major
-                got = pool[a:a + n * w.head_dim].reshape(n, w.head_dim)
-                mism += int(np.count_nonzero(got != k[p0:p1, g]))
-                vt = head + gpu_v.v_bytes // 2                   # V^T [head_dim][bk]
-                idx = vt + np.arange(w.head_dim)[:, None] * bk + np.arange(off, off + n)[None, :]
-                mism += int(np.count_nonzero(pool[idx] != v[p0:p1, g].T))
-                if touched is not None:
-                    touched[a:a + n * w.head_dim] = True
-                    touched[idx] = True
+        pos = np.arange(s, L)
+        if pos.size == 0:
+            continue
+        slots = np.array([wsk.wsk_route(sess.h, b, int(p_))[2] for p_ in pos])
+        off = pos % sess.spec.block_tokens
+        t = off % 64
+        tile_base = slots * (slot_bytes // 2) + (off // 64) * 16384
+        d = np.arange(w.head_dim)
+        mt = 2 * (t // 32) + (t % 8) // 4
+        nk = 4 * ((t % 32) // 8) + t % 4
+        k_el = (4 * mt[:, None] + d[None] // 32) * 64 + 16 * ((d[None] % 32) // 8) + nk[:, None]
+        k_el = k_el * 8 + d[None] % 8
+        v_el = (2 * (d[None] // 16) + t[:, None] // 32) * 64 + 16 * ((t[:, None] % 32) // 8) + d[None] % 16
+        v_el = 8192 + v_el * 8 + (t[:, None] % 8)
+        for g in range(w.n_kv_heads):
+            head = tile_base[:, None] + g * (gpu_v.head_bytes // 2)
+            ka, va = head + k_el, head + v_el
+            mism += int(np.count_nonzero(pool[ka] != k[s:L, g]))
+            mism += int(np.count_nonzero(pool[va] != v[s:L, g]))
+            if touched is not None:
+                touched[ka] = True
+                touched[va] = True
     assert mism == 0, mism
     if touched is not None:
         assert not pool[~touched].any()
