@@ -56,10 +56,13 @@ def cpu_baseline(w, pf, steps_inputs, budget_s: float):
     t_total, nbytes, done = 0.0, 0, 0
     for b in range(len(pf.lengths)):
         k = np.concatenate([pf.k[b], st.k_new[b][None]])
-        v = np.concatenate([pf.v[b], st.v_new[b][None]])
+        v = None if pf.v is None else np.concatenate([pf.v[b], st.v_new[b][None]])
         s, L = min(pf.splits[b], k.shape[0]), k.shape[0]
         t0 = time.perf_counter()
-        oracle.attend(st.q[b], k, v, s, L, w.softmax_scale, w.group)
+        if v is None:   # MLA: one latent row per token, values = its latent part
+            oracle.attend(st.q[b], k, None, s, L, w.softmax_scale, w.n_q_heads, dv=w.latent_dim)
+        else:
+            oracle.attend(st.q[b], k, v, s, L, w.softmax_scale, w.group)
         t_total += time.perf_counter() - t0
         nbytes += (L - s) * w.token_bytes
         done += 1
@@ -97,8 +100,7 @@ def main():
     from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
 
     w = wl.CONFIGS[args.config]
-    if w.kind == wl.MLA:
-        raise SystemExit("MLA bench is not wired yet")
+    mla = w.kind == wl.MLA
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     K, W = args.steps, args.warmup
@@ -112,10 +114,17 @@ def main():
     steps_in = [wl.draw_step(w, pf.gen) for _ in range(W + K)]
     log("bench: routing the prefill into the cache")
     sess = DecodeSession(w, pf, 0, extra_tokens=W + K)
-    B, H, D = sess.B, w.n_q_heads, w.head_dim
+    B, H = sess.B, w.n_q_heads
+    D = sess.out_width                      # attend output width (MLA: the latent)
     qs = [to_device_bf16(s.q, dev) for s in steps_in]
     kn = [to_device_bf16(s.k_new, dev) for s in steps_in]
-    vn = [to_device_bf16(s.v_new, dev) for s in steps_in]
+    vn = [None if mla else to_device_bf16(s.v_new, dev) for s in steps_in]
+    if mla:
+        from paper_2609_14507_amd import wsk
+        w_uk, w_uv = wl.draw_mla_weights(w, pf.gen)
+        w_uk_d, w_uv_d = to_device_bf16(w_uk, dev), to_device_bf16(w_uv, dev)
+        qn = [to_device_bf16(s.q_nope, dev) for s in steps_in]
+        o_out = torch.empty(B, H, w.head_dim, device=dev)
     o_c, l_c = wl.draw_cpu_partial(pf.gen, B * H, D)
     o_cpu = torch.from_numpy(o_c).to(dev).view(B, H, D)
     l_cpu = torch.from_numpy(l_c).to(dev).view(B, H)
@@ -131,11 +140,15 @@ def main():
         if not args.no_flush:
             flush.add_(1)
         ev[0].record(stream)
+        if mla:   # query-side projection into the latent space, in place
+            wsk.wsk_mla_absorb(qn[i], w_uk_d, qs[i], w.row_elems)
         sess.append(kn[i], vn[i])
         ev[1].record(stream)
         sess.attend(qs[i], o=o_g, lse=l_g)
         ev[2].record(stream)
         sess.merge(o_cpu, l_cpu, o_g, l_g, o_m, l_m)
+        if mla:   # output-side expansion of the merged latent output
+            wsk.wsk_mla_expand(o_m, w_uv_d, o_out)
         ev[3].record(stream)
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(W + K)]
@@ -158,7 +171,8 @@ def main():
     nbytes = np.array(nbytes, dtype=np.float64)
     value = float(nbytes.sum() / (step_ms.sum() * 1e-3) / 1e9)
     att_gbs = float(nbytes.sum() / (att_ms.sum() * 1e-3) / 1e9)
-    log("bench: step %.1f us (append %.1f, attend %.1f, merge %.1f); attend %.0f GB/s; wall %.1f ms/step"
+    log("bench: step %.1f us (absorb+append %.1f, attend %.1f, merge(+expand) %.1f); attend %.0f GB/s; "
+        "wall %.1f ms/step"
         % (step_ms.mean() * 1e3, app_ms.mean() * 1e3, att_ms.mean() * 1e3, mrg_ms.mean() * 1e3, att_gbs,
            wall / K * 1e3))
     sess.close()
@@ -182,11 +196,13 @@ def main():
             "q_heads": w.n_q_heads,
             "kv_heads": w.n_kv_heads,
             "head_dim": w.head_dim,
+            **({"latent_dim": w.latent_dim, "rope_dim": w.rope_dim, "nope_dim": w.nope_dim} if mla else {}),
             "context": w.context if w.context else [w.ragged_lo, w.ragged_hi],
             "cpu_share": args.share if args.share is not None else (w.cpu_share or [w.share_lo, w.share_hi]),
             "gpu_tokens_per_step": int(nbytes.mean() / w.token_bytes),
             "kv_bytes_per_step": int(nbytes.mean()),
-            "step": "append + attend (pass 1 + chunk combine) + LSE merge",
+            "step": ("absorb + append + attend (pass 1 + chunk combine) + LSE merge + expand" if mla
+                     else "append + attend (pass 1 + chunk combine) + LSE merge"),
             "cache_flush_between_steps": not args.no_flush,
         },
         "breakdown_us": {
@@ -199,7 +215,7 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "wsk_attend (gqa_attend_kernel + combine_kernel)",
+            "kernel": "wsk_attend (%s_attend_kernel + combine_kernel)" % ("mla" if mla else "gqa"),
             "achieved": round(att_gbs, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",

@@ -201,62 +201,125 @@ __global__ __launch_bounds__(256) void scatter_kernel(const ScatterParams p) {
 
 // ---------------------------------------------------------------------------
 // MLA absorption: q_lat[i][h][l] = sum_k q_nope[i][h][k] * W_UK[h][k][l],
-// fp32 accumulation, one bf16 rounding.  Workgroup = (head, 64 latent
-// columns, 8 tokens); W_UK is read once per workgroup, coalesced over l.
+// fp32 accumulation, one bf16 rounding.  Workgroup = (head, 256 latent
+// columns, 8 tokens), 256 threads = 32 column groups of 8 x 8 slices of the
+// k range; each thread streams its W_UK rows in 16-byte loads and the slices
+// are summed through LDS.
 // ---------------------------------------------------------------------------
 constexpr int kAbsorbTok = 8;
 
-__global__ __launch_bounds__(64) void absorb_kernel(int32_t n, int32_t H, int32_t dn, int32_t dl,
-                                                    const uint16_t *q_nope, const uint16_t *w_uk,
-                                                    uint16_t *out, int64_t out_stride) {
+__global__ __launch_bounds__(256) void absorb_kernel(int32_t n, int32_t H, int32_t dn, int32_t dl,
+                                                     const uint16_t *q_nope, const uint16_t *w_uk,
+                                                     uint16_t *out, int64_t out_stride) {
     __shared__ float sq[kAbsorbTok][256];
+    __shared__ float red[8][kAbsorbTok][256];
     const int h = blockIdx.x;
-    const int l = blockIdx.y * 64 + threadIdx.x;
+    const int cb = blockIdx.y * 256;
     const int i0 = blockIdx.z * kAbsorbTok;
     const int nt = min(kAbsorbTok, n - i0);
-    for (int t = threadIdx.x; t < kAbsorbTok * dn; t += 64) {
+    const int cg = threadIdx.x & 31, sl = threadIdx.x >> 5;
+    for (int t = threadIdx.x; t < kAbsorbTok * dn; t += 256) {
         const int ii = t / dn, k = t - ii * dn;
         sq[ii][k] = ii < nt ? bf16_to_f32(q_nope[((int64_t)(i0 + ii) * H + h) * dn + k]) : 0.f;
     }
     __syncthreads();
-    float acc[kAbsorbTok];
+    float acc[kAbsorbTok][8];
 #pragma unroll
-    for (int ii = 0; ii < kAbsorbTok; ++ii) acc[ii] = 0.f;
-    const uint16_t *w = w_uk + (int64_t)h * dn * dl + l;
-    for (int k = 0; k < dn; ++k) {
-        const float wv = bf16_to_f32(w[(int64_t)k * dl]);
+    for (int ii = 0; ii < kAbsorbTok; ++ii)
 #pragma unroll
-        for (int ii = 0; ii < kAbsorbTok; ++ii) acc[ii] = fmaf(sq[ii][k], wv, acc[ii]);
+        for (int c = 0; c < 8; ++c) acc[ii][c] = 0.f;
+    const int col0 = cb + 8 * cg;
+    const int kper = (dn + 7) / 8;
+    const int k0 = sl * kper, k1 = min(dn, k0 + kper);
+    if (col0 < dl) {
+        const uint16_t *w = w_uk + (int64_t)h * dn * dl + col0;
+#pragma unroll 8
+        for (int k = k0; k < k1; ++k) {
+            const u32x4 wv = *reinterpret_cast<const u32x4 *>(w + (int64_t)k * dl);
+            float wf[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                wf[2 * e] = __uint_as_float(wv[e] << 16);
+                wf[2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
+            }
+#pragma unroll
+            for (int ii = 0; ii < kAbsorbTok; ++ii)
+#pragma unroll
+                for (int c = 0; c < 8; ++c) acc[ii][c] = fmaf(sq[ii][k], wf[c], acc[ii][c]);
+        }
     }
-    for (int ii = 0; ii < nt; ++ii) out[((int64_t)(i0 + ii) * H + h) * out_stride + l] = f32_to_bf16(acc[ii]);
+#pragma unroll
+    for (int ii = 0; ii < kAbsorbTok; ++ii)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) red[sl][ii][8 * cg + c] = acc[ii][c];
+    __syncthreads();
+    for (int t = threadIdx.x; t < kAbsorbTok * 256; t += 256) {
+        const int ii = t >> 8, c = t & 255;
+        if (ii >= nt || cb + c >= dl) continue;
+        float v = 0.f;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v += red[q][ii][c];
+        out[((int64_t)(i0 + ii) * H + h) * out_stride + cb + c] = f32_to_bf16(v);
+    }
 }
 
 // ---------------------------------------------------------------------------
 // MLA expansion: o[i][h][j] = sum_l o_lat[i][h][l] * W_UV[h][l][j], fp32.
-// Workgroup = (head, 64 output columns, 8 tokens).
+// Workgroup = (head, 128 output columns, 8 tokens), 256 threads = 16 column
+// groups of 8 x 16 slices of the l range, summed through LDS.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(64) void expand_kernel(int32_t n, int32_t H, int32_t dl, int32_t dv,
-                                                    const float *o_lat, const uint16_t *w_uv, float *o) {
+__global__ __launch_bounds__(256) void expand_kernel(int32_t n, int32_t H, int32_t dl, int32_t dv,
+                                                     const float *o_lat, const uint16_t *w_uv, float *o) {
     __shared__ float so[kAbsorbTok][1024];
+    __shared__ float red[16][kAbsorbTok][128];
     const int h = blockIdx.x;
-    const int j = blockIdx.y * 64 + threadIdx.x;
+    const int cb = blockIdx.y * 128;
     const int i0 = blockIdx.z * kAbsorbTok;
     const int nt = min(kAbsorbTok, n - i0);
-    for (int t = threadIdx.x; t < kAbsorbTok * dl; t += 64) {
+    const int cg = threadIdx.x & 15, sl = threadIdx.x >> 4;
+    for (int t = threadIdx.x; t < kAbsorbTok * dl; t += 256) {
         const int ii = t / dl, l = t - ii * dl;
         so[ii][l] = ii < nt ? o_lat[((int64_t)(i0 + ii) * H + h) * dl + l] : 0.f;
     }
     __syncthreads();
-    float acc[kAbsorbTok];
+    float acc[kAbsorbTok][8];
 #pragma unroll
-    for (int ii = 0; ii < kAbsorbTok; ++ii) acc[ii] = 0.f;
-    const uint16_t *w = w_uv + (int64_t)h * dl * dv + j;
-    for (int l = 0; l < dl; ++l) {
-        const float wv = bf16_to_f32(w[(int64_t)l * dv]);
+    for (int ii = 0; ii < kAbsorbTok; ++ii)
 #pragma unroll
-        for (int ii = 0; ii < kAbsorbTok; ++ii) acc[ii] = fmaf(so[ii][l], wv, acc[ii]);
+        for (int c = 0; c < 8; ++c) acc[ii][c] = 0.f;
+    const int col0 = cb + 8 * cg;
+    const int lper = (dl + 15) / 16;
+    const int l0 = sl * lper, l1 = min(dl, l0 + lper);
+    if (col0 < dv) {
+        const uint16_t *w = w_uv + (int64_t)h * dl * dv + col0;
+#pragma unroll 8
+        for (int l = l0; l < l1; ++l) {
+            const u32x4 wv = *reinterpret_cast<const u32x4 *>(w + (int64_t)l * dv);
+            float wf[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                wf[2 * e] = __uint_as_float(wv[e] << 16);
+                wf[2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
+            }
+#pragma unroll
+            for (int ii = 0; ii < kAbsorbTok; ++ii)
+#pragma unroll
+                for (int c = 0; c < 8; ++c) acc[ii][c] = fmaf(so[ii][l], wf[c], acc[ii][c]);
+        }
     }
-    for (int ii = 0; ii < nt; ++ii) o[((int64_t)(i0 + ii) * H + h) * dv + j] = acc[ii];
+#pragma unroll
+    for (int ii = 0; ii < kAbsorbTok; ++ii)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) red[sl][ii][8 * cg + c] = acc[ii][c];
+    __syncthreads();
+    for (int t = threadIdx.x; t < kAbsorbTok * 128; t += 256) {
+        const int ii = t >> 7, c = t & 127;
+        if (ii >= nt || cb + c >= dv) continue;
+        float v = 0.f;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) v += red[q][ii][c];
+        o[((int64_t)(i0 + ii) * H + h) * dv + cb + c] = v;
+    }
 }
 
 }  // namespace
@@ -304,16 +367,16 @@ hipError_t launch_scatter(const ScatterParams &p, hipStream_t s) {
 hipError_t launch_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t *q_nope,
                              const uint16_t *w_uk, uint16_t *out, int64_t out_stride, hipStream_t s) {
     if (n <= 0) return hipSuccess;
-    const dim3 grid(H, dl / 64, (n + kAbsorbTok - 1) / kAbsorbTok);
-    hipLaunchKernelGGL(absorb_kernel, grid, dim3(64), 0, s, n, H, dn, dl, q_nope, w_uk, out, out_stride);
+    const dim3 grid(H, (dl + 255) / 256, (n + kAbsorbTok - 1) / kAbsorbTok);
+    hipLaunchKernelGGL(absorb_kernel, grid, dim3(256), 0, s, n, H, dn, dl, q_nope, w_uk, out, out_stride);
     return hipGetLastError();
 }
 
 hipError_t launch_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat,
                              const uint16_t *w_uv, float *o, hipStream_t s) {
     if (n <= 0) return hipSuccess;
-    const dim3 grid(H, dv / 64, (n + kAbsorbTok - 1) / kAbsorbTok);
-    hipLaunchKernelGGL(expand_kernel, grid, dim3(64), 0, s, n, H, dl, dv, o_lat, w_uv, o);
+    const dim3 grid(H, (dv + 127) / 128, (n + kAbsorbTok - 1) / kAbsorbTok);
+    hipLaunchKernelGGL(expand_kernel, grid, dim3(256), 0, s, n, H, dl, dv, o_lat, w_uv, o);
     return hipGetLastError();
 }
 

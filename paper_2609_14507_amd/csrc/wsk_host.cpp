@@ -216,9 +216,10 @@ int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *
         pl.head_groups = G / pl.heads_per_wg;
         units = sp.n_kv_heads * pl.head_groups;
     }
-    // workgroups resident at once (2 per CU for the attention kernels); the
-    // chunk budget per (KV head, head group) unit follows from it
-    const int64_t slots = 2 * (int64_t)c->cu_count;
+    // workgroups resident at once (GQA kernel: 2 per CU; MLA kernel, whose
+    // double-buffered latent tiles fill the LDS: 1 per CU); the chunk budget
+    // per (KV head, head group) unit follows from it
+    const int64_t slots = (sp.kind == WSK_KIND_GQA ? 2 : 1) * (int64_t)c->cu_count;
     const int64_t budget = std::max<int64_t>(1, slots / units);
     pl.tpc.assign(n, 1);
     pl.nchunks.assign(n, 0);

@@ -1,0 +1,179 @@
+"""GPU parity of the MLA (absorbed latent) decode path against the fp64 oracle.
+
+Attend over the latent GPU partition, the LSE merge in latent space, and the
+query absorption / output expansion steps, within max_abs <= 1e-2 and
+L1-ratio <= 1e-3 of the oracle (bf16 inputs, fp32 accumulation).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.route import RouteModel
+from paper_2609_14507_amd import workloads as wl
+from paper_2609_14507_amd import wsk
+from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
+from tests.gpu_util import assert_close, assert_lse, say
+
+pytestmark = pytest.mark.gpu
+DEV = 0
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    torch.cuda.set_device(DEV)
+    yield
+    torch.cuda.synchronize()
+
+
+def _mla_workload(H=16, batch=2, context=1000, seed=7):
+    return wl.Workload("mla-edge", wl.MLA, batch=batch, n_q_heads=H, n_kv_heads=1, head_dim=128,
+                       latent_dim=512, rope_dim=64, nope_dim=128, context=context, kv_std=0.5, seed=seed)
+
+
+def _o_lat(w, q_b, rows, a, e):
+    return oracle.attend(q_b, rows, None, a, e, w.softmax_scale, w.n_q_heads, dv=w.latent_dim)
+
+
+@pytest.mark.parametrize("H,bk", [(16, 64), (16, 128), (8, 256), (5, 64)])
+def test_mla_ranges(H, bk):
+    """Unaligned, single-token, single-tile and empty ranges; fewer than 16 heads."""
+    lengths = [1000, 130, 64, 2100, 1]
+    splits = [0, 65, 64, 700, 0]
+    w = _mla_workload(H=H, batch=len(lengths), context=max(lengths), seed=H + bk)
+    gen = torch.Generator().manual_seed(w.seed)
+    rows = [wl.draw_bf16(gen, (L, w.row_elems), w.kv_std) for L in lengths]
+    pf = wl.Prefill(lengths, splits, rows, None, gen)
+    q_bits = wl.draw_bf16(gen, (len(lengths), H, w.row_elems))
+    dev = torch.device("cuda", DEV)
+    say("case mla ranges H=%d bk=%d" % (H, bk))
+    with DecodeSession(w, pf, DEV, extra_tokens=0, block_tokens=bk) as sess:
+        q = to_device_bf16(q_bits, dev)
+        cases = [
+            [(0, 1000), (65, 130), (64, 64), (700, 2100), (0, 1)],
+            [(999, 1000), (100, 101), (64, 64), (2099, 2100), (1, 1)],
+            [(10, 63), (65, 129), (64, 64), (701, 1400), (0, 0)],
+            [(63, 65), (127, 130), (64, 64), (767, 1985), (0, 1)],
+        ]
+        for ranges in cases:
+            start = [a for a, _ in ranges]
+            end = [e for _, e in ranges]
+            o, l = sess.attend(q, start, end)
+            o, l = o.cpu().numpy(), l.cpu().numpy()
+            for b, (a, e) in enumerate(ranges):
+                if e == a:
+                    assert np.all(o[b] == 0) and np.all(np.isneginf(l[b])), (b, a, e)
+                    continue
+                o_r, l_r = _o_lat(w, q_bits[b], rows[b], a, e)
+                assert_close(o[b], o_r, "mla b%d [%d,%d)" % (b, a, e))
+                assert_lse(l[b], l_r, "mla b%d [%d,%d)" % (b, a, e))
+
+
+def test_mla_garbage_outside_range_is_ignored():
+    w = _mla_workload(batch=1, context=700, seed=3)
+    gen = torch.Generator().manual_seed(3)
+    rows = wl.draw_bf16(gen, (700, w.row_elems), w.kv_std)
+    bad = rows.copy()
+    bad[:80] = 0x7FC0
+    bad[600:] = 0xFF80
+    pf = wl.Prefill([700], [0], [bad], None, gen)
+    q_bits = wl.draw_bf16(gen, (1, w.n_q_heads, w.row_elems))
+    say("case mla garbage rows")
+    with DecodeSession(w, pf, DEV, extra_tokens=0) as sess:
+        o, l = sess.attend(to_device_bf16(q_bits, torch.device("cuda", DEV)), [80], [600])
+        o_r, l_r = _o_lat(w, q_bits[0], rows, 80, 600)
+        assert_close(o.cpu().numpy()[0], o_r, "mla garbage outside")
+        assert_lse(l.cpu().numpy()[0], l_r, "mla garbage outside")
+
+
+def test_mla_absorb_and_expand_kernels():
+    rng_gen = torch.Generator().manual_seed(11)
+    w = wl.C4
+    n, H = 5, w.n_q_heads
+    q_nope = wl.draw_bf16(rng_gen, (n, H, w.nope_dim))
+    w_uk, w_uv = wl.draw_mla_weights(w, rng_gen)
+    dev = torch.device("cuda", DEV)
+    say("case absorb/expand")
+    out = torch.zeros(n, H, w.row_elems, dtype=torch.bfloat16, device=dev)
+    wsk.wsk_mla_absorb(to_device_bf16(q_nope, dev), to_device_bf16(w_uk, dev), out, w.row_elems)
+    got = out.cpu().view(torch.int16).numpy().view(np.uint16)
+    assert not got[:, :, w.latent_dim:].any()            # the rope part is left alone
+    got = got[:, :, :w.latent_dim]
+    mism = 0
+    for i in range(n):
+        ref = oracle.mla_absorb(q_nope[i], w_uk)          # fp64, unrounded
+        ref_bits = oracle.round_bf16(ref)
+        diff = got[i] != ref_bits
+        mism += int(diff.sum())
+        # fp32 accumulation may round differently only where the exact value is
+        # within fp32 error of a bf16 rounding boundary: one bf16 ulp at most
+        g = oracle.bf16_to_f64(got[i][diff])
+        r = ref[diff]
+        ulp = 2.0 ** (np.floor(np.log2(np.abs(r))) - 7)
+        # fp32 sum of dn products: error below dn * 2^-24 * sum |terms|
+        s_abs = np.einsum("hk,hkl->hl", np.abs(oracle.bf16_to_f64(q_nope[i])),
+                          np.abs(oracle.bf16_to_f64(w_uk)))[diff]
+        assert np.all(np.abs(g - r) <= ulp * 0.5 + w.nope_dim * 2.0 ** -24 * s_abs)
+    assert mism <= got.size // 1000, mism
+    # expansion of fp32 latent outputs
+    o_lat = np.random.default_rng(5).standard_normal((n, H, w.latent_dim)).astype(np.float32)
+    o = torch.empty(n, H, w.head_dim, device=dev)
+    wsk.wsk_mla_expand(torch.from_numpy(o_lat).to(dev), to_device_bf16(w_uv, dev), o)
+    ref = np.stack([oracle.mla_expand(o_lat[i].astype(np.float64), w_uv) for i in range(n)])
+    assert_close(o.cpu().numpy(), ref, "expand")
+
+
+def test_c4_deepseek_v2_lite_full_path():
+    """Absorb -> append -> attend the GPU range -> merge with the CPU partial in
+    latent space -> expand, against the oracle doing every step in fp64."""
+    w = wl.C4
+    say("case c4", w.name)
+    pf = wl.make_prefill(w)
+    st = wl.draw_step(w, pf.gen)
+    w_uk, w_uv = wl.draw_mla_weights(w, pf.gen)
+    dev = torch.device("cuda", DEV)
+    B, H = w.batch, w.n_q_heads
+    with DecodeSession(w, pf, DEV) as sess:
+        sess.append(to_device_bf16(st.k_new, dev), None)
+        # (a) attend parity on the drawn absorbed query
+        q = to_device_bf16(st.q, dev)
+        o_g, l_g = sess.attend(q)
+        og, lg = o_g.cpu().numpy(), l_g.cpu().numpy()
+        rows_full = [np.concatenate([pf.k[b], st.k_new[b][None]]) for b in range(B)]
+        ref_o, ref_l = [], []
+        for b in range(B):
+            a, e = sess.gpu_range(b)
+            o_r, l_r = _o_lat(w, st.q[b], rows_full[b], a, e)
+            ref_o.append(o_r)
+            ref_l.append(l_r)
+        assert_close(og, np.stack(ref_o), "c4 gpu partial")
+        assert_lse(lg, np.stack(ref_l), "c4 gpu partial")
+        # (b) the whole step from q_nope, q_rope and the absorption weights
+        q_full = q.clone()
+        wsk.wsk_mla_absorb(to_device_bf16(st.q_nope, dev), to_device_bf16(w_uk, dev), q_full, w.row_elems)
+        o_g2, l_g2 = sess.attend(q_full)
+        cpu_o, cpu_l, ref = [], [], []
+        for b in range(B):
+            q_lat = oracle.round_bf16(oracle.mla_absorb(st.q_nope[b], w_uk))
+            qb = np.concatenate([q_lat, st.q_rope[b]], axis=1)
+            o_c, l_c = _o_lat(w, qb, rows_full[b], 0, pf.splits[b])
+            cpu_o.append(o_c)
+            cpu_l.append(l_c)
+            o_f, _ = _o_lat(w, qb, rows_full[b], 0, rows_full[b].shape[0])
+            ref.append(oracle.mla_expand(o_f, w_uv))
+        o_cd = torch.from_numpy(np.stack(cpu_o).astype(np.float32)).to(dev)
+        l_cd = torch.from_numpy(np.stack(cpu_l).astype(np.float32)).to(dev)
+        o_m, _ = sess.merge(o_cd, l_cd, o_g2, l_g2)
+        o_out = torch.empty(B, H, w.head_dim, device=dev)
+        wsk.wsk_mla_expand(o_m, to_device_bf16(w_uv, dev), o_out)
+        assert_close(o_out.cpu().numpy(), np.stack(ref), "c4 full path")
+        # routing of the appended rows and the split
+        model = RouteModel(sess.spec.block_tokens, sess.spec.host_pool_blocks, sess.spec.device_pool_blocks)
+        for b in range(B):
+            model.open(b, pf.splits[b])
+            model.write(b, 0, pf.lengths[b])
+        model.append(list(range(B)))
+        for b in (0, 3, 7):
+            for p in (0, pf.splits[b] - 1, pf.splits[b], pf.lengths[b] - 1, pf.lengths[b]):
+                assert wsk.wsk_route(sess.h, b, p) == model.route(b, p)
