@@ -88,6 +88,9 @@ def main():
     ap.add_argument("--no-flush", action="store_true", help="skip the Infinity Cache flush between steps")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed steps, run a plain 256 MiB device copy three times (the reference "
+                         "dispatch that scales HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -176,6 +179,15 @@ def main():
         % (step_ms.mean() * 1e3, app_ms.mean() * 1e3, att_ms.mean() * 1e3, mrg_ms.mean() * 1e3, att_gbs,
            wall / K * 1e3))
     sess.close()
+    if args.copy_calibration:
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        for _ in range(3):
+            flush.add_(1)
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("bench: copy calibration: 3 x %d bytes read + written" % src.numel())
 
     out = {
         "metric": METRIC,

@@ -57,6 +57,7 @@ extern "C" {
 
 #define WSK_LAYOUT_ROWS 0    /* token-major rows                               */
 #define WSK_LAYOUT_TILED64 1 /* GQA GPU pool: 64-token tiles in matrix-core order */
+#define WSK_LAYOUT_MLA32 2   /* MLA GPU pool: 32-token tiles in matrix-core order */
 
 /* Largest number of query heads one KV head may serve in a GQA cache.       */
 #define WSK_MAX_GROUP 64
@@ -93,7 +94,11 @@ extern "C" {
  *                       mt = 2*(t/32) + (t%8)/4,  nk = 4*((t%32)/8) + t%4
  *                    V: piece (2*(d/16) + t/32)*64 + 16*((t%32)/8) + d%16,
  *                       elem t%8
- *   MLA, both      slot = [block_tokens][latent_dim + rope_dim]  (latent | rope)
+ *   MLA, CPU pool  slot = [block_tokens][latent_dim + rope_dim]  (latent | rope)
+ *   MLA, GPU pool  slot = [block_tokens / 32 tiles][2304 16-byte pieces]
+ *                  (WSK_LAYOUT_MLA32); piece c (dims 8c..8c+7, c = 0..71) of
+ *                  token u of a tile (0..31) is piece
+ *                    (2*(c/4) + (u/4)%2)*64 + 16*(c%4) + 4*(u/8) + u%4
  */
 typedef struct wsk_partition_spec {
     int32_t kind;
@@ -131,6 +136,8 @@ typedef struct wsk_loc {
  * layout WSK_LAYOUT_TILED64 (GQA GPU pool): tile k = (p % block_tokens) / 64
  *   starts at head + k * 32768; its K pieces follow, then its V pieces at
  *   + 16384, placed as described for the slot layout above.
+ * layout WSK_LAYOUT_MLA32 (MLA GPU pool): tile k = (p % block_tokens) / 32
+ *   starts at head + k * 36864, pieces placed as described above.
  * CPU views hold host addresses; GPU views hold device addresses (the table
  * too).  The pointers are borrowed: they stay valid until wsk_destroy,
  * because placed blocks never move (Sec. 4.2).

@@ -9,25 +9,36 @@
 // so heads x latent form a dense tile and both products run on the matrix
 // cores (v_mfma_f32_16x16x32_bf16, up to 16 heads):
 //
-//   S^T [64 tokens x 16 heads] = C [64 x 576] . Q^T [576 x 16]
-//   O   [16 heads x 512]      += P [16 x 64]  . c [64 x 512]
+//   S^T [32 tokens x 16 heads] = C [32 x 576] . Q^T [576 x 16]     (2 M-tiles)
+//   O   [16 heads x 512]      += P [16 x 32]  . c [32 x 512]       (32 N-tiles)
 //
 // Each latent row is read from HBM once and used by both products (the
-// paper's CPU kernel makes the same point for its cache tiles).  A workgroup
-// of 4 wavefronts walks one chunk of 64-token tiles together:
-//   - wavefront w fetches the rows of its QK M-tile (16 tokens x 576) from
-//     HBM straight into its A-operand registers, one tile ahead, computes
-//     QK there (18 MFMAs in two independent chains), and stores the rows to
-//     the double-buffered LDS tile (72 KB) that all wavefronts' P.V reads;
-//   - the tile max per head is exchanged through LDS; probabilities go to
-//     LDS as bf16 hi + lo parts in the P.V A-operand order;
-//   - P.V: wavefront w computes output dims [128w, 128w + 128) for all 64
-//     tokens; its B-operands (8 consecutive tokens of one dim) come from the
-//     row-major tile through ds_read_b64_tr_b16, which transposes 16 lanes'
-//     4-element rows into 4-token columns.
-// LDS placement: row (token) t, 16-byte chunk c of the tile lives at slot
-// t*72 + (c ^ x(t)); x(t) spreads the rows read together by one instruction
-// over distinct banks for both the QK reads and the transposing reads.
+// paper's CPU kernel makes the same point for its cache tiles).
+//
+// A workgroup of 4 wavefronts walks its chunk one 32-token tile at a time;
+// the tile's 18 K-steps are split over the wavefronts by latent columns:
+// wavefront w holds latent dims [128w, 128w + 128) (K-steps 4w .. 4w+3) and,
+// for w < 2, the rope K-step 16 + w.  It computes a partial S^T over its
+// K-steps and, after one exchange of partial scores through LDS, the P.V
+// product for its own 128 output columns.
+//   - The GPU pool stores each 32-token tile in the order of the QK
+//     A-operand registers (WSK_LAYOUT_MLA32): load (ks, mt) is one fully
+//     coalesced 1 KB read landing in the registers that feed the MFMA.
+//   - P.V contracts over tokens, so its B-operand needs 8 consecutive tokens
+//     of one latent dim per lane: the transpose of what was loaded.  It is
+//     made on the matrix cores: C_mtile [16 tok x 32 dims] . E [32 x 16],
+//     with E a 0/1 selection of 16 dims, gives the 16 x 16 block with each
+//     lane holding 4 consecutive tokens of one dim.  The products are exact
+//     (x * 1 and x * 0 summed in fp32), so the upper halves of the fp32
+//     results are the cached bf16 values bit for bit.
+//   - The token order inside an M-tile makes the QK accumulator of lane
+//     (g, n) hold tokens 8g..8g+7 of head n, which is exactly the P.V
+//     A-operand: probabilities never leave the registers.
+//   - Each wavefront keeps its pieces of three tiles in registers; a
+//     register is refilled with the tile three ahead as soon as it has been
+//     consumed, so about 100 KB per workgroup is always in flight.
+//   - The only synchronisation is the barrier of the score exchange (one
+//     per tile; partial scores are double-buffered).
 // Tokens outside [start, end) are fetched from past the buffer descriptor's
 // extent, which yields zeros, and their scores are masked to -inf.
 
@@ -37,38 +48,30 @@ namespace wsk {
 namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
-typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
-typedef __attribute__((ext_vector_type(4))) short s16x4;
-typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kRow = kLatent + kRope;        // 576 bf16 per cached token
-constexpr int kChunksPerRow = kRow / 8;      // 72 16-byte chunks
-constexpr int kTileSlots = kTile * kChunksPerRow;   // 4608 16-byte slots = 72 KB
-constexpr int kKSteps = kRow / 32;           // 18 QK K-steps
+constexpr int kRow = kLatent + kRope;          // 576 bf16 per cached token
+constexpr int kSub = 32;                       // tokens per tile
+constexpr int kSubBytes = kSub * kRow * 2;     // 36864
+constexpr int kWaveKS = 5;                     // K-steps per wavefront (4 latent + rope for w < 2)
+constexpr int kWaveNT = 8;                     // P.V N-tiles (128 columns) per wavefront
+constexpr int kDepth = 3;                      // tiles held per wavefront
+constexpr int kOOB = 0x40000000;               // offset past any descriptor extent
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-__device__ __forceinline__ int tile_token(int mt, int r) {
-    return 32 * (mt >> 1) + 8 * (r >> 2) + 4 * (mt & 1) + (r & 3);
-}
-// bank spread of row t (0..7): bit 1 of t -> bit 1, bit 3 -> bit 0, bit 4 -> bit 2
-__device__ __forceinline__ int row_xor(int t) {
-    return (((t >> 1) & 1) << 1) | ((t >> 3) & 1) | (((t >> 4) & 1) << 2);
-}
+// token (0..31) held by row r of M-tile mt
+__device__ __forceinline__ int sub_token(int mt, int r) { return 8 * (r >> 2) + 4 * mt + (r & 3); }
 
-__global__ __launch_bounds__(256, 1) void mla_attend_kernel(const AttendParams p) {
-    __shared__ u32x4 s_tile[2][kTileSlots];           // 2 x 72 KB
-    __shared__ u32x4 s_p[2][2][4][16];                // [hi/lo][ks][grp][head] 8 bf16 = 2 KB
-    __shared__ float s_max[4][16];
-    __shared__ float s_sum[4][16];
+__global__ __launch_bounds__(256, 2) void mla_attend_kernel(const AttendParams p) {
+    __shared__ f32x4 s_part[2][4][2][64];          // 16 KB: partial S^T per wavefront, double-buffered
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n = lane & 15;
     const int grp = lane >> 4;
+    const bool rope = wave < 2;
 
     // ---- work item (uniform): sequence i, chunk c ----
     const int wg = blockIdx.x;
@@ -78,9 +81,9 @@ __global__ __launch_bounds__(256, 1) void mla_attend_kernel(const AttendParams p
     const int seq = p.seq[i];
     const int t_start = p.start[i];
     const int t_end = p.end[i];
-    const int tpc = p.tpc[i];
-    const int tile0 = (t_start >> 6) + c * tpc;
-    const int tile_end = min(tile0 + tpc, ((t_end - 1) >> 6) + 1);
+    const int tile0 = (t_start >> 6) + c * p.tpc[i];   // a chunk is tpc 64-token tiles
+    const int sub_begin = max(2 * tile0, t_start >> 5);
+    const int sub_end = min(2 * (tile0 + p.tpc[i]), ((t_end - 1) >> 5) + 1);
     const int H = p.n_q_heads;
     typedef const __attribute__((address_space(4))) int32_t ci32;
     ci32 *trow = (ci32 *)(p.table + (int64_t)seq * p.table_stride);
@@ -88,178 +91,185 @@ __global__ __launch_bounds__(256, 1) void mla_attend_kernel(const AttendParams p
     const int bshift = __builtin_ctz(bk);
     const int slot_bytes = bk * kRow * 2;
 
-    // Q^T operand: lane (grp, n) holds q[n][32ks + 8grp .. +8] for all 18 K-steps
-    bf16x8 qop[kKSteps];
+    // K-step j of this wavefront: latent 4w + j (j < 4), rope 16 + w (j = 4)
+    auto ks_of = [&](int j) { return j < 4 ? 4 * wave + j : 16 + wave; };
+
+    // Q^T operands of those K-steps: lane (grp, n) holds q[n][32ks + 8grp .. +8]
+    bf16x8 qop[kWaveKS];
     {
         const u32x4 *qrow = reinterpret_cast<const u32x4 *>(p.q + (int64_t)i * p.q_row +
                                                             (int64_t)(n < H ? n : 0) * kRow);
 #pragma unroll
-        for (int ks = 0; ks < kKSteps; ++ks) {
-            const u32x4 v = qrow[ks * 4 + grp];
-            qop[ks] = as_bf16x8(n < H ? v : u32x4{0u, 0u, 0u, 0u});
+        for (int j = 0; j < kWaveKS; ++j) {
+            const u32x4 v = qrow[ks_of(j) * 4 + grp];
+            qop[j] = as_bf16x8((n < H && (j < 4 || rope)) ? v : u32x4{0u, 0u, 0u, 0u});
         }
     }
+    // selection operands E_half: lane (grp, j) holds E[8grp .. 8grp+7][j],
+    // E[k][j] = 1 iff k = 16 half + j
+    bf16x8 sel[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sel[h][e] = (8 * grp + e == 16 * h + n) ? (__bf16)1.0f : (__bf16)0.0f;
 
-    // Staging: lane (grp, n) of wavefront w fetches, for each K-step ks, the
-    // 16 bytes its QK A-operand needs -- token tile_token(w, n), chunk
-    // 4ks + grp -- straight into registers, multiplies them there, and also
-    // stores them to the LDS tile (slot token*72 + (chunk ^ row_xor(token)))
-    // for every wavefront's P.V.
-    const int st_tok = tile_token(wave, n);
-    const int st_x = row_xor(st_tok);
-    u32x4 stX[kKSteps], stY[kKSteps];
-    // Tiles past the chunk's end are "loaded" from past the descriptor's
-    // extent (no memory traffic): loads stay unconditional so the compiler
-    // waits for exactly the stage it needs.
-    auto load_tile = [&](int t, u32x4 (&st)[kKSteps]) {
-        const bool valid = t < tile_end;
-        const int tt = valid ? t : tile0;
-        const int tok0 = tt * kTile;
+    // ---- tile addressing ----
+    struct Src {
+        __amdgpu_buffer_rsrc_t rs;
+        int soff;       // byte offset of the tile in its slot
+        int voff[2];    // per M-tile lane offset (kOOB for rows outside the range)
+    };
+    auto tile_src = [&](int sub) {
+        Src s;
+        const bool valid = sub < sub_end;
+        const int su = valid ? sub : sub_begin;
+        const int tok0 = su * kSub;
         const int blk = tok0 >> bshift;
-        const int row0 = tok0 - (blk << bshift);
         const int slot = __builtin_amdgcn_readfirstlane(trow[blk]);
-        const uint16_t *base = p.pool + (int64_t)slot * p.slot_elems;
-        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, slot_bytes, 0x00020000);
-        const int tk = tok0 + st_tok;
-        // rows outside [start, end) are fetched from past the extent: zeros
-        const bool ok = valid && tk >= t_start && tk < t_end;
-        const int off0 = ok ? st_tok * (kRow * 2) + grp * 16 : 0x40000000;
+        s.rs = __builtin_amdgcn_make_buffer_rsrc((void *)(p.pool + (int64_t)slot * p.slot_elems), 0, slot_bytes,
+                                                 0x00020000);
+        s.soff = ((tok0 & (bk - 1)) >> 5) * kSubBytes;
+        const bool partial = tok0 < t_start || tok0 + kSub > t_end;
 #pragma unroll
-        for (int ks = 0; ks < kKSteps; ++ks)
-            st[ks] = __builtin_amdgcn_raw_buffer_load_b128(rs, off0 + (ok ? ks * 64 : 0), row0 * (kRow * 2),
-                                                           kStreamLoad);
+        for (int mt = 0; mt < 2; ++mt) {
+            const int tk = tok0 + sub_token(mt, n);
+            const bool ok = valid && (!partial || (tk >= t_start && tk < t_end));
+            s.voff[mt] = ok ? lane * 16 : kOOB;
+        }
+        return s;
     };
-    auto store_tile = [&](int buf, const u32x4 (&st)[kKSteps]) {
-        u32x4 *dst = s_tile[buf] + st_tok * kChunksPerRow;
+    typedef u32x4 Stage[kWaveKS][2];
+    // (wavefronts 2 and 3 have no rope K-step: their fifth piece is fetched
+    // from past the extent, which costs no memory traffic and keeps every
+    // wavefront's instruction stream, and its load counts, the same)
+    auto load_j = [&](const Src &s, Stage &st, int j) {
 #pragma unroll
-        for (int ks = 0; ks < kKSteps; ++ks) dst[(4 * ks + grp) ^ st_x] = st[ks];
+        for (int mt = 0; mt < 2; ++mt)
+            st[j][mt] = __builtin_amdgcn_raw_buffer_load_b128(s.rs, (j < 4 || rope) ? s.voff[mt] : kOOB,
+                                                              s.soff + (2 * ks_of(j) + mt) * 1024, kStreamLoad);
+    };
+    auto load_tile = [&](int sub, Stage &st) {
+        const Src s = tile_src(sub);
+#pragma unroll
+        for (int j = 4; j >= 0; --j) load_j(s, st, j);
     };
 
-    // P.V transposing reads: lane (grp, i=n) points at token 32ks + 8grp + 4h + n/4,
-    // dims 128*wave + 16nt + 4(n%4) .. +4, i.e. chunk 16*wave + 2nt + (n%4)/2, half (n%4)%2
-    const int tr_tok_lo = 8 * grp + (n >> 2);
-    const int tr_chunk = 16 * wave + ((n & 3) >> 1);
-    const int tr_half = (n & 1) * 8;
-
+    f32x4 o[kWaveNT];
+#pragma unroll
+    for (int nt = 0; nt < kWaveNT; ++nt) o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m_run = -INFINITY;
     float l_lane = 0.f;
-    f32x4 o[8];
-#pragma unroll
-    for (int nt = 0; nt < 8; ++nt) o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // One tile: QK from the registers of `cur` (tile t, already in LDS buffer
-    // buf), refill `cur` with tile t+2, softmax, P.V from LDS, then publish
-    // `nxt` (tile t+1) into the other buffer.
-    auto step = [&](int t, int buf, u32x4 (&cur)[kKSteps], u32x4 (&nxt)[kKSteps]) {
+    // One tile t held in st: partial QK, score exchange, softmax, P.V; each
+    // consumed K-step of st is refilled with tile t + kDepth.
+    auto step = [&](int t, Stage &st) {
+        const Src nx = tile_src(t + kDepth);
+        const int tok0 = t * kSub;
         f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (t < tile_end) {
-            __syncthreads();   // tile t is in LDS for every wavefront; tile t-1 is no longer read
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[4][0]), qop[4], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[4][1]), qop[4], s1, 0, 0, 0);
+        load_j(nx, st, 4);
 #pragma unroll
-            for (int ks = 0; ks < kKSteps; ks += 2) {
-                s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cur[ks]), qop[ks], s0, 0, 0, 0);
-                s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cur[ks + 1]), qop[ks + 1], s1, 0, 0, 0);
+        for (int j = 0; j < 4; ++j) {
+            s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[j][0]), qop[j], s0, 0, 0, 0);
+            s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[j][1]), qop[j], s1, 0, 0, 0);
+        }
+        // ---- exchange partial scores; every wavefront sums them in the same order ----
+        const int b = t & 1;
+        s_part[b][wave][0][lane] = s0;
+        s_part[b][wave][1][lane] = s1;
+        __syncthreads();
+        f32x4 S0 = s_part[b][0][0][lane], S1 = s_part[b][0][1][lane];
+#pragma unroll
+        for (int w = 1; w < 4; ++w) {
+            S0 += s_part[b][w][0][lane];
+            S1 += s_part[b][w][1][lane];
+        }
+
+        // ---- online softmax: lane (grp, n) holds head n, tokens 8grp + e ----
+        const bool partial = tok0 < t_start || tok0 + kSub > t_end;
+        float sv[8];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            sv[r] = S0[r] * p.scale_log2;
+            sv[4 + r] = S1[r] * p.scale_log2;
+        }
+        if (partial) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int tk = tok0 + 8 * grp + e;
+                if (tk < t_start || tk >= t_end) sv[e] = -INFINITY;
             }
         }
-        load_tile(t + 2, cur);
-        if (t < tile_end) {
-            const int tok0 = t * kTile;
-            const u32x4 *tile = s_tile[buf];
-            const f32x4 s = s0 + s1;
-            // ---- softmax over the 64 tokens of the tile, per head n ----
-            const bool partial = tok0 < t_start || tok0 + kTile > t_end;
-            float sv[4];
-            float mloc = -INFINITY;
+        float mloc = sv[0];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int tk = tok0 + tile_token(wave, 4 * grp + r);
-                const bool ok = !partial || (tk >= t_start && tk < t_end);
-                sv[r] = ok ? s[r] * p.scale_log2 : -INFINITY;
-                mloc = fmaxf(mloc, sv[r]);
-            }
-            mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-            mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-            if (grp == 0) s_max[wave][n] = mloc;
-            __syncthreads();
-            const float mt = fmaxf(fmaxf(s_max[0][n], s_max[1][n]), fmaxf(s_max[2][n], s_max[3][n]));
-            const float m_new = fmaxf(m_run, mt);
-            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-            m_run = m_new;
-            float psum = 0.f;
-            bf16x4 phi, plo;
+        for (int e = 1; e < 8; ++e) mloc = fmaxf(mloc, sv[e]);
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+        const float m_new = fmaxf(m_run, mloc);      // finite: every tile holds a token of the range
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        bf16x8 phi, plo;
+        float psum = 0.f;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float pv = __builtin_amdgcn_exp2f(sv[r] - m_new);
-                psum += pv;
-                const __bf16 hi = (__bf16)pv;
-                phi[r] = hi;
-                plo[r] = (__bf16)(pv - (float)hi);
-            }
-            l_lane = fmaf(l_lane, alpha, psum);
-            // tokens 32(w>>1) + 8grp + 4(w&1) + r are elements 4(w&1) + r of the
-            // P.V A-operand of (ks = w>>1, grp, head n)
-            {
-                u32x2 *dh = reinterpret_cast<u32x2 *>(&s_p[0][wave >> 1][grp][n]) + (wave & 1);
-                u32x2 *dl = reinterpret_cast<u32x2 *>(&s_p[1][wave >> 1][grp][n]) + (wave & 1);
-                *dh = __builtin_bit_cast(u32x2, phi);
-                *dl = __builtin_bit_cast(u32x2, plo);
-            }
+        for (int e = 0; e < 8; ++e) {
+            const float pv = __builtin_amdgcn_exp2f(sv[e] - m_new);
+            psum += pv;
+            const __bf16 hi = (__bf16)pv;
+            phi[e] = hi;
+            plo[e] = (__bf16)(pv - (float)hi);
+        }
+        l_lane = fmaf(l_lane, alpha, psum);
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {   // some head's running max moved
             float alpha_r[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) alpha_r[r] = __shfl(alpha, 4 * grp + r);
 #pragma unroll
-            for (int nt = 0; nt < 8; ++nt)
+            for (int nt = 0; nt < kWaveNT; ++nt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) o[nt][r] *= alpha_r[r];
-            __syncthreads();
+        }
 
-            // ---- P.V: output dims [128 wave, 128 wave + 128) ----
+        // ---- O[:, 128w + 16nt ..] += P . c ----
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                const bf16x8 ahi = as_bf16x8(s_p[0][ks][grp][n]);
-                const bf16x8 alo = as_bf16x8(s_p[1][ks][grp][n]);
-                s16x4 half[8][2];
-#pragma unroll
-                for (int nt = 0; nt < 8; ++nt)
-#pragma unroll
-                    for (int h2 = 0; h2 < 2; ++h2) {
-                        const int tk = 32 * ks + tr_tok_lo + 4 * h2;
-                        const int ch = tr_chunk + 2 * nt;
-                        const char *addr = reinterpret_cast<const char *>(tile) +
-                                           (tk * kChunksPerRow + (ch ^ row_xor(tk))) * 16 + tr_half;
-                        half[nt][h2] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                            (__attribute__((address_space(3))) s16x4 *)(addr));
-                    }
-#pragma unroll
-                for (int nt = 0; nt < 8; ++nt) {
-                    const bf16x8 b = __builtin_bit_cast(
-                        bf16x8, __builtin_shufflevector(half[nt][0], half[nt][1], 0, 1, 2, 3, 4, 5, 6, 7));
-                    o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, b, o[nt], 0, 0, 0);
-                    o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, b, o[nt], 0, 0, 0);
-                }
-            }
-            if (t + 1 < tile_end) store_tile(buf ^ 1, nxt);   // nobody reads buf^1 until the next barrier
+        for (int nt = 0; nt < kWaveNT; ++nt) {
+            const int j = nt >> 1;
+            // transpose on the matrix cores: lane (grp, jj) gets tokens
+            // 8grp + 4mt + r (r = 0..3) of dim 128w + 16nt + jj from M-tile mt
+            const f32x4 zero = f32x4{0.f, 0.f, 0.f, 0.f};
+            const f32x4 t0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[j][0]), sel[nt & 1], zero, 0, 0, 0);
+            const f32x4 t1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[j][1]), sel[nt & 1], zero, 0, 0, 0);
+            // exact bf16 values held in fp32: keep the upper halves
+            u32x4 bv;
+            bv[0] = __builtin_amdgcn_perm(__float_as_uint(t0[1]), __float_as_uint(t0[0]), 0x07060302u);
+            bv[1] = __builtin_amdgcn_perm(__float_as_uint(t0[3]), __float_as_uint(t0[2]), 0x07060302u);
+            bv[2] = __builtin_amdgcn_perm(__float_as_uint(t1[1]), __float_as_uint(t1[0]), 0x07060302u);
+            bv[3] = __builtin_amdgcn_perm(__float_as_uint(t1[3]), __float_as_uint(t1[2]), 0x07060302u);
+            o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(phi, as_bf16x8(bv), o[nt], 0, 0, 0);
+            o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo, as_bf16x8(bv), o[nt], 0, 0, 0);
+            if (nt & 1) load_j(nx, st, j);   // K-step j consumed: refill with tile t + kDepth
         }
     };
 
-    if (tile0 < tile_end) {
-        load_tile(tile0, stX);
-        store_tile(0, stX);
-        load_tile(tile0 + 1, stY);
+    Stage st0, st1, st2;
+    load_tile(sub_begin, st0);
+    load_tile(sub_begin + 1, st1);
+    load_tile(sub_begin + 2, st2);
+    int t = sub_begin;
+    for (; t + 2 < sub_end; t += kDepth) {
+        step(t, st0);
+        step(t + 1, st1);
+        step(t + 2, st2);
     }
-    for (int t = tile0; t < tile_end; t += 2) {
-        step(t, 0, stX, stY);
-        step(t + 1, 1, stY, stX);
-    }
+    if (t < sub_end) step(t, st0);
+    if (t + 1 < sub_end) step(t + 1, st1);
 
-    // ---- normalise and write this chunk's partial ----
+    // ---- normalise and write this wavefront's 128 columns of the partial ----
     float l_tot = l_lane + __shfl_xor(l_lane, 16);
-    l_tot += __shfl_xor(l_tot, 32);
-    if (grp == 0) s_sum[wave][n] = l_tot;
-    __syncthreads();
-    const float den = s_sum[0][n] + s_sum[1][n] + s_sum[2][n] + s_sum[3][n];   // head n
+    l_tot += __shfl_xor(l_tot, 32);                  // head n, in every lane of column n
     float inv_r[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) inv_r[r] = 1.f / __shfl(den, 4 * grp + r);
+    for (int r = 0; r < 4; ++r) inv_r[r] = 1.f / __shfl(l_tot, 4 * grp + r);
     const int part = p.chunk_begin[i] + c;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -267,11 +277,11 @@ __global__ __launch_bounds__(256, 1) void mla_attend_kernel(const AttendParams p
         if (h < H) {
             float *dst = p.part_o + ((int64_t)part * H + h) * kLatent + 128 * wave + n;
 #pragma unroll
-            for (int nt = 0; nt < 8; ++nt) dst[16 * nt] = o[nt][r] * inv_r[r];
+            for (int nt = 0; nt < kWaveNT; ++nt) dst[16 * nt] = o[nt][r] * inv_r[r];
         }
     }
     if (wave == 0 && grp == 0 && n < H)
-        p.part_lse[(int64_t)part * H + n] = (m_run + __log2f(den)) * 0.69314718055994530942f;
+        p.part_lse[(int64_t)part * H + n] = (m_run + __log2f(l_tot)) * 0.69314718055994530942f;
 }
 
 }  // namespace

@@ -35,6 +35,17 @@ __device__ __forceinline__ void put_tiled(uint16_t *head, int row, int which, in
     }
 }
 
+// Places 16-byte piece c (dims 8c..8c+7) of the MLA row of token `row` into
+// a GPU-pool slot in the MLA32 format: 32-token tiles of 2304 pieces, piece
+// (ks, mt, lane) being what matrix-core lane (lane / 16, lane % 16) of M-tile
+// mt loads for K-step ks (see attend_mla.hip).
+__device__ __forceinline__ void put_mla32(uint16_t *slot, int row, int c, u32x4 v) {
+    uint16_t *tile = slot + (int64_t)(row >> 5) * (32 * (kLatent + kRope));
+    const int u = row & 31;
+    const int piece = (2 * (c >> 2) + ((u >> 2) & 1)) * 64 + 16 * (c & 3) + 4 * (u >> 3) + (u & 3);
+    *reinterpret_cast<u32x4 *>(tile + piece * 8) = v;
+}
+
 // fp32 -> bf16, round to nearest even (NaN stays NaN).
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     uint32_t u = __float_as_uint(f);
@@ -138,7 +149,7 @@ __global__ __launch_bounds__(256) void merge_kernel(int32_t rows, int32_t width,
 
 // ---------------------------------------------------------------------------
 // Decode append: one workgroup per appended row (all KV heads, K and V).
-// GPU-pool GQA rows go to the TILED64 format (put_tiled).
+// GPU-pool rows go to the TILED64 (GQA) or MLA32 (MLA) format.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void append_kernel(const AppendParams p) {
     const int r = blockIdx.x;
@@ -160,9 +171,8 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendParams p) {
         }
     } else {
         const uint16_t *src = p.k_new + (int64_t)r * p.row_elems;
-        uint16_t *dst = p.pool + slot0 + (int64_t)row * p.row_elems;
         for (int k = threadIdx.x; k < row16; k += blockDim.x)
-            reinterpret_cast<u32x4 *>(dst)[k] = reinterpret_cast<const u32x4 *>(src)[k];
+            put_mla32(p.pool + slot0, row, k, reinterpret_cast<const u32x4 *>(src)[k]);
     }
 }
 
@@ -193,8 +203,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(const ScatterParams p) {
             put_tiled(head, off, which, k, reinterpret_cast<const u32x4 *>(src)[k]);
         } else {
             const uint16_t *src = p.src_k + (int64_t)j * p.row_elems;
-            uint16_t *dst = p.pool + slot * p.slot_elems + (int64_t)off * p.row_elems;
-            reinterpret_cast<u32x4 *>(dst)[q] = reinterpret_cast<const u32x4 *>(src)[q];
+            put_mla32(p.pool + slot * p.slot_elems, off, q, reinterpret_cast<const u32x4 *>(src)[q]);
         }
     }
 }

@@ -167,8 +167,7 @@ void commit(wsk_cache *c, const std::vector<Pending> &pend) {
 
 // Offset (elements) of position pos, KV head g, K (which = 0) or V (1), in
 // its slot of the CPU pool, where every row is token-major.  (The GPU pool
-// stores GQA rows in 64-token matrix-core tiles, placed by the append/scatter
-// kernels.)
+// stores rows in matrix-core tiles, placed by the append/scatter kernels.)
 inline int64_t row_offset(const wsk_cache *c, int32_t pos, int g, int which) {
     const int bk = c->spec.block_tokens;
     const int off = pos % bk;
@@ -216,10 +215,9 @@ int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *
         pl.head_groups = G / pl.heads_per_wg;
         units = sp.n_kv_heads * pl.head_groups;
     }
-    // workgroups resident at once (GQA kernel: 2 per CU; MLA kernel, whose
-    // double-buffered latent tiles fill the LDS: 1 per CU); the chunk budget
+    // workgroups resident at once (both kernels: 2 per CU); the chunk budget
     // per (KV head, head group) unit follows from it
-    const int64_t slots = (sp.kind == WSK_KIND_GQA ? 2 : 1) * (int64_t)c->cu_count;
+    const int64_t slots = 2 * (int64_t)c->cu_count;
     const int64_t budget = std::max<int64_t>(1, slots / units);
     pl.tpc.assign(n, 1);
     pl.nchunks.assign(n, 0);
@@ -580,7 +578,7 @@ int wsk_views(const wsk_cache *c, int32_t seq, wsk_view *cpu, wsk_view *gpu) {
         v->v_bytes = gqa ? (side == 0 ? c->spec.block_tokens * row_bytes : kTile * row_bytes) : 0;
         v->row_bytes = row_bytes;
         v->block_tokens = c->spec.block_tokens;
-        v->layout = (gqa && side == 1) ? WSK_LAYOUT_TILED64 : WSK_LAYOUT_ROWS;
+        v->layout = side == 0 ? WSK_LAYOUT_ROWS : gqa ? WSK_LAYOUT_TILED64 : WSK_LAYOUT_MLA32;
         v->reserved = 0;
         if (side == 0) {
             v->pool = c->hpool;

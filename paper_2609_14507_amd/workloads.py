@@ -4,7 +4,7 @@ This module only draws inputs: it holds none of the method's arithmetic
 (no softmax, no merge, no routing).  Both the HIP path and the oracle consume
 the arrays produced here, so a parity test compares the two on the same bytes.
 
-Shapes follow the models of the evaluation setup (Sec. 6.1): Qwen3-30B-A3B
+Shapes follow the models of the evaluation setup (Sec. 7.1): Qwen3-30B-A3B
 (GQA, 32 query heads, 4 KV heads, head dim 128), Mixtral-8x7B (GQA, 32 query
 heads, 8 KV heads) and DeepSeek-V2-Lite (MLA, 16 heads, a 512-wide compressed
 latent plus a 64-wide decoupled RoPE key).  The paper's prompts come from

@@ -21,7 +21,7 @@ ERROR_NAMES = {WSK_EINVAL: "EINVAL", WSK_ENOMEM: "ENOMEM", WSK_ERANGE: "ERANGE",
                WSK_EHIP: "EHIP", WSK_ESTATE: "ESTATE"}
 KIND_GQA, KIND_MLA = 0, 1
 PART_CPU, PART_GPU = 0, 1
-LAYOUT_ROWS, LAYOUT_TILED64 = 0, 1
+LAYOUT_ROWS, LAYOUT_TILED64, LAYOUT_MLA32 = 0, 1, 2
 
 
 class WskError(RuntimeError):

@@ -13,7 +13,7 @@ from oracle.route import RouteModel
 from paper_2609_14507_amd import workloads as wl
 from paper_2609_14507_amd import wsk
 from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
-from tests.gpu_util import assert_close, assert_lse, say
+from tests.gpu_util import assert_close, assert_lse, d2h, say
 
 pytestmark = pytest.mark.gpu
 DEV = 0
@@ -30,6 +30,35 @@ def _gpu():
 def _mla_workload(H=16, batch=2, context=1000, seed=7):
     return wl.Workload("mla-edge", wl.MLA, batch=batch, n_q_heads=H, n_kv_heads=1, head_dim=128,
                        latent_dim=512, rope_dim=64, nope_dim=128, context=context, kv_std=0.5, seed=seed)
+
+
+def _check_pool_bytes(sess, rows_full):
+    """Every GPU-partition row sits at the element the MLA32 formula of
+    include/wsk.h names for its routed slot, and every other pool byte is 0."""
+    _, gpu_v = wsk.wsk_views(sess.h, 0)
+    assert gpu_v.layout == wsk.LAYOUT_MLA32
+    row = sess.w.row_elems
+    pool = d2h(gpu_v.pool, gpu_v.slot_bytes * sess.spec.device_pool_blocks).view(np.uint16)
+    touched = np.zeros(pool.shape, bool)
+    c = np.arange(row // 8)
+    mism = 0
+    for b in range(sess.B):
+        L = sess.lengths[b]
+        s = min(sess.splits[b], L)
+        pos = np.arange(s, L)
+        if pos.size == 0:
+            continue
+        slots = np.array([wsk.wsk_route(sess.h, b, int(p_))[2] for p_ in pos])
+        off = pos % sess.spec.block_tokens
+        u = off % 32
+        base = slots * (gpu_v.slot_bytes // 2) + (off // 32) * (32 * row)
+        piece = (2 * (c[None] // 4) + (u[:, None] // 4) % 2) * 64 + 16 * (c[None] % 4) + 4 * (u[:, None] // 8) \
+            + u[:, None] % 4
+        el = (base[:, None, None] + piece[:, :, None] * 8 + np.arange(8)[None, None]).reshape(len(pos), row)
+        mism += int(np.count_nonzero(pool[el] != rows_full[b][s:L]))
+        touched[el] = True
+    assert mism == 0, mism
+    assert not pool[~touched].any()
 
 
 def _o_lat(w, q_b, rows, a, e):
@@ -49,6 +78,7 @@ def test_mla_ranges(H, bk):
     dev = torch.device("cuda", DEV)
     say("case mla ranges H=%d bk=%d" % (H, bk))
     with DecodeSession(w, pf, DEV, extra_tokens=0, block_tokens=bk) as sess:
+        _check_pool_bytes(sess, rows)
         q = to_device_bf16(q_bits, dev)
         cases = [
             [(0, 1000), (65, 130), (64, 64), (700, 2100), (0, 1)],
@@ -141,6 +171,7 @@ def test_c4_deepseek_v2_lite_full_path():
         o_g, l_g = sess.attend(q)
         og, lg = o_g.cpu().numpy(), l_g.cpu().numpy()
         rows_full = [np.concatenate([pf.k[b], st.k_new[b][None]]) for b in range(B)]
+        _check_pool_bytes(sess, rows_full)
         ref_o, ref_l = [], []
         for b in range(B):
             a, e = sess.gpu_range(b)

@@ -327,7 +327,7 @@ def test_route_exhaustion_changes_nothing_and_close_reclaims():
 
 
 # ---------------------------------------------------------------------------
-# Workload shapes against the paper's printed byte counts (Tables 1 and 3)
+# Workload shapes against the paper's printed byte counts (Tables 1 and 2)
 # ---------------------------------------------------------------------------
 
 def test_token_bytes_reproduce_paper_tables():
@@ -343,7 +343,7 @@ def test_token_bytes_reproduce_paper_tables():
         layers = g["layers"][model]
         kv_bs4 = tb * layers * 4 * 32768 / 1e9
         assert round(kv_bs4, 1) == g["table1_kv_gb_bs4_seq32k"][model]
-        t3 = g["table3_seq32k_bs32"][model]
+        t3 = g["table2_seq32k_bs32"][model]
         full = tb * layers * 32 * 32768 / 1e9
         assert abs((t3["unpinned_gb"] + t3["pinned_gb"]) - full) < 0.011
         dwin = g["dwindow_tokens"] * 32 * tb * layers / 1e6
