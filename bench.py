@@ -49,23 +49,42 @@ def cpu_model() -> str:
 
 
 def cpu_baseline(w, pf, steps_inputs, budget_s: float):
-    """The fp64 oracle, as it stands, over the GPU range of decode step 0, on the
-    host's cores.  Sequences are taken in order until the time budget is spent."""
+    """The fp64 oracle, as it stands, over the same GPU ranges as the timed
+    decode steps (step k attends [s_b, L_b + k + 1) with the appended rows), on
+    the host's cores: steps are taken in order, sequence by sequence, until the
+    time budget is spent."""
     import oracle
-    st = steps_inputs[0]
+    B = len(pf.lengths)
+    S = len(steps_inputs)
+    ks, vs = [], []
+    for b in range(B):   # cache rows plus every step's appended row, in place
+        L = pf.lengths[b]
+        k = np.empty((L + S,) + pf.k[b].shape[1:], dtype=pf.k[b].dtype)
+        k[:L] = pf.k[b]
+        for j, st in enumerate(steps_inputs):
+            k[L + j] = st.k_new[b]
+        ks.append(k)
+        if pf.v is not None:
+            v = np.empty((L + S,) + pf.v[b].shape[1:], dtype=pf.v[b].dtype)
+            v[:L] = pf.v[b]
+            for j, st in enumerate(steps_inputs):
+                v[L + j] = st.v_new[b]
+            vs.append(v)
     t_total, nbytes, done = 0.0, 0, 0
-    for b in range(len(pf.lengths)):
-        k = np.concatenate([pf.k[b], st.k_new[b][None]])
-        v = None if pf.v is None else np.concatenate([pf.v[b], st.v_new[b][None]])
-        s, L = min(pf.splits[b], k.shape[0]), k.shape[0]
-        t0 = time.perf_counter()
-        if v is None:   # MLA: one latent row per token, values = its latent part
-            oracle.attend(st.q[b], k, None, s, L, w.softmax_scale, w.n_q_heads, dv=w.latent_dim)
-        else:
-            oracle.attend(st.q[b], k, v, s, L, w.softmax_scale, w.group)
-        t_total += time.perf_counter() - t0
-        nbytes += (L - s) * w.token_bytes
-        done += 1
+    for j, st in enumerate(steps_inputs):
+        for b in range(B):
+            L = pf.lengths[b] + j + 1
+            s = min(pf.splits[b], L)
+            t0 = time.perf_counter()
+            if pf.v is None:   # MLA: one latent row per token, values = its latent part
+                oracle.attend(st.q[b], ks[b][:L], None, s, L, w.softmax_scale, w.n_q_heads, dv=w.latent_dim)
+            else:
+                oracle.attend(st.q[b], ks[b][:L], vs[b][:L], s, L, w.softmax_scale, w.group)
+            t_total += time.perf_counter() - t0
+            nbytes += (L - s) * w.token_bytes
+            done += 1
+            if t_total >= budget_s:
+                break
         if t_total >= budget_s:
             break
     return {
@@ -73,9 +92,56 @@ def cpu_baseline(w, pf, steps_inputs, budget_s: float):
         "unit": "GB/s",
         "cores": oracle.max_threads(),
         "kind": "oracle",
-        "sample": "fp64 oracle over the GPU range of decode step 0 for %d of %d sequences "
-                  "(%.2f GB of KV, %.1f s); CPU: %s" % (done, len(pf.lengths), nbytes / 1e9, t_total, cpu_model()),
+        "sample": "fp64 oracle over the GPU ranges of the decode steps in order, %d (sequence, step) ranges "
+                  "of %d sequences x %d steps (%.2f GB of KV, %.1f s); CPU: %s"
+                  % (done, B, S, nbytes / 1e9, t_total, cpu_model()),
     }
+
+
+# HBM bytes per launch of the pass-1 kernel, from two rocprofv3 --pmc runs of
+# this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each scaled by
+# what the same counter reads for the plain 256 MiB copy of --copy-calibration
+# (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  Keyed by workload; valid only for the
+# kernel source they were taken on (sha256), null otherwise.
+TRAFFIC = {
+    "qwen3-30b-a3b-b16-L32768": {
+        "source": "paper_2609_14507_amd/csrc/attend_gqa.hip",
+        "sha256": "cb08cb8d7b9d23c8768f70800b55bc79c92f82d94ad2f6b64817e24c6291c081",
+        "fetch_bytes": 368959.1 * 1024 * 2.0,
+        "write_bytes": 2064.0 * 1024 * 1.0,
+        "kv_bytes": 751714304,
+    },
+    "deepseek-v2-lite-mla-b8-L65536": {
+        "source": "paper_2609_14507_amd/csrc/attend_mla.hip",
+        "sha256": "c76f6b96a5f38f5321dd2ebf70ff6b1c93724cd1724f8e8a488087cb9cd79927",
+        "fetch_bytes": 177756.8 * 1024 * 2.0,
+        "write_bytes": 15903.0 * 1024 * 1.0,
+        "kv_bytes": 362414592,
+    },
+}
+
+
+def roofline(w, kind, achieved_gbs, kv_bytes):
+    """Roofline entry of the pass-1 kernel (the one that streams the KV)."""
+    import hashlib
+    traffic = None
+    t = TRAFFIC.get(w.name)
+    if t is not None:
+        with open(os.path.join(ROOT, t["source"]), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() == t["sha256"]:
+                traffic = t["fetch_bytes"] + t["write_bytes"]
+    out = {
+        "bound": "hbm",
+        "kernel": "%s_attend_kernel (wsk_attend pass 1)" % kind,
+        "achieved": round(achieved_gbs, 1),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved_gbs / HBM_PEAK_GBS, 4),
+        "traffic": None if traffic is None else int(traffic),
+    }
+    if traffic is not None:
+        out["traffic_per_kv_byte"] = round(traffic / t["kv_bytes"], 4)
+    return out
 
 
 def main():
@@ -147,14 +213,18 @@ def main():
             wsk.wsk_mla_absorb(qn[i], w_uk_d, qs[i], w.row_elems)
         sess.append(kn[i], vn[i])
         ev[1].record(stream)
-        sess.attend(qs[i], o=o_g, lse=l_g)
+        # wsk_attend as its two passes, so that pass 1 (the KV-streaming
+        # kernel) is timed on its own
+        sess.attend_pass1(qs[i])
         ev[2].record(stream)
+        sess.attend_pass2(o=o_g, lse=l_g)
+        ev[3].record(stream)
         sess.merge(o_cpu, l_cpu, o_g, l_g, o_m, l_m)
         if mla:   # output-side expansion of the merged latent output
             wsk.wsk_mla_expand(o_m, w_uv_d, o_out)
-        ev[3].record(stream)
+        ev[4].record(stream)
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(W + K)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(W + K)]
     nbytes = []
     log("bench: %d warmup + %d timed steps" % (W, K))
     for i in range(W):
@@ -167,17 +237,17 @@ def main():
         step(i, events[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    step_ms = np.array([events[i][0].elapsed_time(events[i][3]) for i in range(W, W + K)])
-    att_ms = np.array([events[i][1].elapsed_time(events[i][2]) for i in range(W, W + K)])
-    app_ms = np.array([events[i][0].elapsed_time(events[i][1]) for i in range(W, W + K)])
-    mrg_ms = np.array([events[i][2].elapsed_time(events[i][3]) for i in range(W, W + K)])
+    el = lambda a, b: np.array([events[i][a].elapsed_time(events[i][b]) for i in range(W, W + K)])
+    step_ms, app_ms, p1_ms, p2_ms, mrg_ms = el(0, 4), el(0, 1), el(1, 2), el(2, 3), el(3, 4)
+    att_ms = p1_ms + p2_ms
     nbytes = np.array(nbytes, dtype=np.float64)
     value = float(nbytes.sum() / (step_ms.sum() * 1e-3) / 1e9)
     att_gbs = float(nbytes.sum() / (att_ms.sum() * 1e-3) / 1e9)
-    log("bench: step %.1f us (absorb+append %.1f, attend %.1f, merge(+expand) %.1f); attend %.0f GB/s; "
-        "wall %.1f ms/step"
-        % (step_ms.mean() * 1e3, app_ms.mean() * 1e3, att_ms.mean() * 1e3, mrg_ms.mean() * 1e3, att_gbs,
-           wall / K * 1e3))
+    p1_gbs = float(nbytes.sum() / (p1_ms.sum() * 1e-3) / 1e9)
+    log("bench: step %.1f us (absorb+append %.1f, attend pass 1 %.1f + pass 2 %.1f, merge(+expand) %.1f); "
+        "pass 1 %.0f GB/s, attend %.0f GB/s; wall %.1f ms/step"
+        % (step_ms.mean() * 1e3, app_ms.mean() * 1e3, p1_ms.mean() * 1e3, p2_ms.mean() * 1e3, mrg_ms.mean() * 1e3,
+           p1_gbs, att_gbs, wall / K * 1e3))
     sess.close()
     if args.copy_calibration:
         src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
@@ -218,22 +288,16 @@ def main():
             "cache_flush_between_steps": not args.no_flush,
         },
         "breakdown_us": {
-            "append": round(float(app_ms.mean() * 1e3), 2),
-            "attend": round(float(att_ms.mean() * 1e3), 2),
-            "merge": round(float(mrg_ms.mean() * 1e3), 2),
+            ("absorb_append" if mla else "append"): round(float(app_ms.mean() * 1e3), 2),
+            "attend_pass1": round(float(p1_ms.mean() * 1e3), 2),
+            "attend_pass2_combine": round(float(p2_ms.mean() * 1e3), 2),
+            ("merge_expand" if mla else "merge"): round(float(mrg_ms.mean() * 1e3), 2),
+            "attend_gbs": round(att_gbs, 1),
             "step_p10": round(float(np.percentile(step_ms, 10) * 1e3), 2),
             "step_p90": round(float(np.percentile(step_ms, 90) * 1e3), 2),
             "wall_per_step_incl_flush": round(wall / K * 1e6, 1),
         },
-        "roofline": {
-            "bound": "hbm",
-            "kernel": "wsk_attend (%s_attend_kernel + combine_kernel)" % ("mla" if mla else "gqa"),
-            "achieved": round(att_gbs, 1),
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": round(att_gbs / HBM_PEAK_GBS, 4),
-            "traffic": None,
-        },
+        "roofline": roofline(w, "mla" if mla else "gqa", p1_gbs, float(nbytes.mean())),
     }
     if not args.no_cpu_baseline:
         log("bench: timing the oracle on the host (%.0f s budget)" % args.cpu_budget)

@@ -276,6 +276,27 @@ int wsk_attend(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
                float *o, float *lse, void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * The two passes of wsk_attend, for callers that schedule or time them
+ * apart.  Called with the same cache state, seq_ids, start, end and
+ * workspace, wsk_attend_pass1 followed by wsk_attend_pass2 on the stream is
+ * wsk_attend:
+ *   pass 1 attends every chunk of every range (split-KV: each range is cut
+ *          into chunks of whole 64-token tiles spread over the GPU) and
+ *          leaves each chunk's normalised partial O and LSE in ws;
+ *   pass 2 merges the chunks of each (sequence, head) by their LSE into o
+ *          and lse.
+ * The workspace contents between the passes are private to the library.
+ * Arguments, ownership and errors as for wsk_attend (pass 1 takes no o/lse,
+ * pass 2 no q).
+ */
+int wsk_attend_pass1(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
+                     const int32_t *start, const int32_t *end, const void *q,
+                     void *ws, size_t ws_bytes, void *stream);
+int wsk_attend_pass2(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
+                     const int32_t *start, const int32_t *end, float *o,
+                     float *lse, void *ws, size_t ws_bytes, void *stream);
+
+/*
  * LSE merge of two partials over disjoint key sets (Sec. 4.2, Sec. 5.1),
  * row by row, on the GPU:
  *   m = max(lse_a, lse_b);  m = -inf  ->  O = 0, LSE = -inf

@@ -56,42 +56,78 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 
 // ---------------------------------------------------------------------------
 // Chunk combine: O = sum_c w_c O_c / sum_c w_c, w_c = exp(lse_c - max lse),
-// LSE = max + ln sum w_c.  One wavefront per (sequence, head); each lane owns
-// WIDTH/64 consecutive output elements; chunk loads are unrolled so many are
-// in flight at once.  No chunk (empty range): O = 0, LSE = -inf.
+// LSE = max + ln sum w_c.  Workgroup = (sequence, head, 128-column slice);
+// its 256 threads are 8 chunk groups x 32 float4 columns, so a whole
+// sequence's partials are fetched in one or two rounds of loads; the groups
+// are summed through LDS.  No chunk (empty range): O = 0, LSE = -inf.
 // ---------------------------------------------------------------------------
-template <int WIDTH>
-__global__ __launch_bounds__(64) void combine_kernel(const CombineParams p) {
-    constexpr int PER = WIDTH / 64;
-    typedef __attribute__((ext_vector_type(PER))) float fv;
+constexpr int kCombineCols4 = 32;                   // float4 columns per workgroup
+constexpr int kCombineGroups = 256 / kCombineCols4; // chunk groups
+constexpr int kCombineW = 1024;                     // chunk weights kept in LDS
+
+__device__ __forceinline__ float block_reduce(float v, bool is_max, float *s_red) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+        const float u = __shfl_xor(v, d);
+        v = is_max ? fmaxf(v, u) : v + u;
+    }
+    __syncthreads();                                 // s_red free (earlier use finished)
+    if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    float r = s_red[0];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) r = is_max ? fmaxf(r, s_red[w]) : r + s_red[w];
+    return r;
+}
+
+__global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int width) {
+    __shared__ float s_w[kCombineW];
+    __shared__ float s_red[4];
+    __shared__ f32x4 s_acc[kCombineGroups][kCombineCols4];
     const int row = blockIdx.x;                 // i * H + h
-    const int i = row / p.n_q_heads;
-    const int h = row - i * p.n_q_heads;
+    const int H = p.n_q_heads;
+    const int i = row / H;
+    const int h = row - i * H;
     const int c0 = p.chunk_begin[i];
     const int nc = p.chunk_begin[i + 1] - c0;
-    const int lane = threadIdx.x;
-    fv *out = reinterpret_cast<fv *>(p.o + (int64_t)row * WIDTH) + lane;
+    const int tid = threadIdx.x;
+    const int col0 = blockIdx.y * 4 * kCombineCols4;
+    f32x4 *out = reinterpret_cast<f32x4 *>(p.o + (int64_t)row * width + col0);
     if (nc == 0) {
-        *out = fv{};
-        if (lane == 0) p.lse[row] = -INFINITY;
+        if (tid < kCombineCols4) out[tid] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (tid == 0 && blockIdx.y == 0) p.lse[row] = -INFINITY;
         return;
     }
-    const float *pl = p.part_lse + (int64_t)c0 * p.n_q_heads + h;
+    const float *pl = p.part_lse + (int64_t)c0 * H + h;
     float m = -INFINITY;
+    for (int c = tid; c < nc; c += 256) m = fmaxf(m, pl[(int64_t)c * H]);
+    m = block_reduce(m, true, s_red);
+    float dsum = 0.f;
+    for (int c = tid; c < nc; c += 256) {
+        const float w = __expf(pl[(int64_t)c * H] - m);
+        if (c < kCombineW) s_w[c] = w;
+        dsum += w;
+    }
+    const float den = block_reduce(dsum, false, s_red);   // its barriers also publish s_w
+    const int g = tid / kCombineCols4;
+    const int c4 = tid - g * kCombineCols4;
+    const f32x4 *po = reinterpret_cast<const f32x4 *>(p.part_o + ((int64_t)c0 * H + h) * width + col0) + c4;
+    const int64_t cstride = (int64_t)H * width / 4;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 8
-    for (int c = 0; c < nc; ++c) m = fmaxf(m, pl[(int64_t)c * p.n_q_heads]);
-    float den = 0.f;
-    fv acc = fv{};
-    const fv *po = reinterpret_cast<const fv *>(p.part_o + ((int64_t)c0 * p.n_q_heads + h) * WIDTH) + lane;
-    const int64_t cstride = (int64_t)p.n_q_heads * WIDTH / PER;
-#pragma unroll 8
-    for (int c = 0; c < nc; ++c) {
-        const float w = __expf(pl[(int64_t)c * p.n_q_heads] - m);
-        den += w;
+    for (int c = g; c < nc; c += kCombineGroups) {
+        const float w = c < kCombineW ? s_w[c] : __expf(pl[(int64_t)c * H] - m);
         acc += w * po[c * cstride];
     }
-    *out = acc * (1.f / den);
-    if (lane == 0) p.lse[row] = m + __logf(den);
+    s_acc[g][c4] = acc;
+    __syncthreads();
+    if (tid < kCombineCols4) {
+        f32x4 t = s_acc[0][tid];
+#pragma unroll
+        for (int gg = 1; gg < kCombineGroups; ++gg) t += s_acc[gg][tid];
+        out[tid] = t * (1.f / den);
+    }
+    if (tid == 0 && blockIdx.y == 0) p.lse[row] = m + __logf(den);
 }
 
 // ---------------------------------------------------------------------------
@@ -335,12 +371,9 @@ __global__ __launch_bounds__(256) void expand_kernel(int32_t n, int32_t H, int32
 
 hipError_t launch_combine(const CombineParams &p, int width, hipStream_t s) {
     if (p.n <= 0) return hipSuccess;
-    const dim3 grid(p.n * p.n_q_heads), block(64);
-    switch (width) {
-        case 128: hipLaunchKernelGGL(combine_kernel<128>, grid, block, 0, s, p); break;
-        case 512: hipLaunchKernelGGL(combine_kernel<512>, grid, block, 0, s, p); break;
-        default: return hipErrorInvalidValue;
-    }
+    if (width <= 0 || width % (4 * kCombineCols4)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(combine_kernel, dim3(p.n * p.n_q_heads, width / (4 * kCombineCols4)), dim3(256), 0, s, p,
+                       width);
     return hipGetLastError();
 }
 

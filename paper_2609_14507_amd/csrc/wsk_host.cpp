@@ -607,15 +607,23 @@ int wsk_attend_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, cons
     return WSK_OK;
 }
 
-int wsk_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
-               const void *q, float *o, float *lse, void *ws, size_t ws_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// wsk_attend and its two passes: pass 1 writes the chunk partials into ws,
+// pass 2 merges them into o / lse.
+int attend_passes(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
+                  const void *q, float *o, float *lse, void *ws, size_t ws_bytes, void *stream, bool pass1,
+                  bool pass2) {
     if (!c) return fail(WSK_EINVAL, "cache is NULL");
     AttendPlan pl;
     int rc = make_plan(c, n, ids, start, end, pl);
     if (rc) return rc;
     if (n == 0) return WSK_OK;
     if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
-    if (!q || !o || !lse) return fail(WSK_EINVAL, "q/o/lse must not be NULL");
+    if (pass1 && !q) return fail(WSK_EINVAL, "q must not be NULL");
+    if (pass2 && (!o || !lse)) return fail(WSK_EINVAL, "o/lse must not be NULL");
     if (pl.bytes && (!ws || ws_bytes < pl.bytes)) return fail(WSK_EINVAL, "workspace of %zu bytes needed", pl.bytes);
     if (((uintptr_t)ws & 255) != 0) return fail(WSK_EINVAL, "workspace must be 256-byte aligned");
     const wsk_partition_spec &sp = c->spec;
@@ -665,11 +673,15 @@ int wsk_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start
             ap.chunk_begin[r] = ap.chunk_begin[m];
         }
         const int n_wg = ap.wg_begin[m];
-        if (gqa)
-            e = launch_gqa_attend(ap, pl.heads_per_wg, n_wg, st);
-        else
-            e = launch_mla_attend(ap, n_wg, st);
-        if (e != hipSuccess) break;
+        if (pass1) {
+            if (gqa)
+                e = launch_gqa_attend(ap, pl.heads_per_wg, n_wg, st);
+            else
+                e = launch_mla_attend(ap, n_wg, st);
+            if (e != hipSuccess) break;
+        }
+        part_base += ap.chunk_begin[m];
+        if (!pass2) continue;
         cp.part_o = ap.part_o;
         cp.part_lse = ap.part_lse;
         cp.o = o + (int64_t)i0 * sp.n_q_heads * width;
@@ -678,10 +690,28 @@ int wsk_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start
         cp.n_q_heads = sp.n_q_heads;
         for (int32_t r = 0; r <= kMaxLaunchSeqs; ++r) cp.chunk_begin[r] = ap.chunk_begin[r];
         e = launch_combine(cp, width, st);
-        part_base += ap.chunk_begin[m];
     }
     if (e != hipSuccess) return hip_fail(e, "wsk_attend");
     return WSK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int wsk_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
+               const void *q, float *o, float *lse, void *ws, size_t ws_bytes, void *stream) {
+    return attend_passes(c, n, ids, start, end, q, o, lse, ws, ws_bytes, stream, true, true);
+}
+
+int wsk_attend_pass1(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
+                     const void *q, void *ws, size_t ws_bytes, void *stream) {
+    return attend_passes(c, n, ids, start, end, q, nullptr, nullptr, ws, ws_bytes, stream, true, false);
+}
+
+int wsk_attend_pass2(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
+                     float *o, float *lse, void *ws, size_t ws_bytes, void *stream) {
+    return attend_passes(c, n, ids, start, end, nullptr, o, lse, ws, ws_bytes, stream, false, true);
 }
 
 int wsk_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a, const float *o_b,

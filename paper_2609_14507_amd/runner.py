@@ -81,21 +81,41 @@ class DecodeSession:
             self._ws = torch.empty(need + spare, dtype=torch.uint8, device=self.dev)
         return self._ws
 
-    def attend(self, q: torch.Tensor, start: Optional[Sequence[int]] = None, end: Optional[Sequence[int]] = None,
-               ids: Optional[List[int]] = None, o: Optional[torch.Tensor] = None,
-               lse: Optional[torch.Tensor] = None):
+    def _ranges(self, start, end, ids):
         ids = self.ids if ids is None else ids
         if start is None:
             start = [self.gpu_range(b)[0] for b in ids]
         if end is None:
             end = [self.lengths[b] for b in ids]
-        n, H = len(ids), self.w.n_q_heads
+        return ids, start, end
+
+    def _outputs(self, n, o, lse):
+        H = self.w.n_q_heads
         if o is None:
             o = torch.empty(n, H, self.out_width, dtype=torch.float32, device=self.dev)
         if lse is None:
             lse = torch.empty(n, H, dtype=torch.float32, device=self.dev)
+        return o, lse
+
+    def attend(self, q: torch.Tensor, start: Optional[Sequence[int]] = None, end: Optional[Sequence[int]] = None,
+               ids: Optional[List[int]] = None, o: Optional[torch.Tensor] = None,
+               lse: Optional[torch.Tensor] = None):
+        ids, start, end = self._ranges(start, end, ids)
+        o, lse = self._outputs(len(ids), o, lse)
         ws = self.workspace(ids, start, end)
         wsk.wsk_attend(self.h, ids, start, end, q, o, lse, ws)
+        return o, lse
+
+    def attend_pass1(self, q: torch.Tensor, start=None, end=None, ids=None):
+        """Pass 1 only (chunk partials in the session workspace); attend_pass2 with
+        the same ranges completes it."""
+        ids, start, end = self._ranges(start, end, ids)
+        wsk.wsk_attend_pass1(self.h, ids, start, end, q, self.workspace(ids, start, end))
+
+    def attend_pass2(self, start=None, end=None, ids=None, o=None, lse=None):
+        ids, start, end = self._ranges(start, end, ids)
+        o, lse = self._outputs(len(ids), o, lse)
+        wsk.wsk_attend_pass2(self.h, ids, start, end, o, lse, self.workspace(ids, start, end))
         return o, lse
 
     @staticmethod

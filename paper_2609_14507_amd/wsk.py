@@ -70,6 +70,8 @@ _SIGS = {
     "wsk_views": ([_VP, _I32, ctypes.POINTER(wsk_view), ctypes.POINTER(wsk_view)], ctypes.c_int),
     "wsk_attend_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_attend": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
+    "wsk_attend_pass1": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
+    "wsk_attend_pass2": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_merge": ([_I32, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP], ctypes.c_int),
     "wsk_mla_absorb": ([_I32, _I32, _I32, _I32, _VP, _VP, _VP, _I64, _VP], ctypes.c_int),
     "wsk_mla_expand": ([_I32, _I32, _I32, _I32, _VP, _VP, _VP, _VP], ctypes.c_int),
@@ -205,6 +207,20 @@ def wsk_attend(h: int, seq_ids, start, end, q, o, lse, ws, stream=None):
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(lib().wsk_attend(h, len(seq_ids), _i32_array(seq_ids), _i32_array(start), _i32_array(end),
                             _ptr(q), _ptr(o), _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
+
+
+def wsk_attend_pass1(h: int, seq_ids, start, end, q, ws, stream=None):
+    """Pass 1 of wsk_attend: the chunk partials into ws."""
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().wsk_attend_pass1(h, len(seq_ids), _i32_array(seq_ids), _i32_array(start), _i32_array(end),
+                                  _ptr(q), _ptr(ws), nbytes, _stream(stream)))
+
+
+def wsk_attend_pass2(h: int, seq_ids, start, end, o, lse, ws, stream=None):
+    """Pass 2 of wsk_attend: merges the chunk partials in ws into o, lse."""
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().wsk_attend_pass2(h, len(seq_ids), _i32_array(seq_ids), _i32_array(start), _i32_array(end),
+                                  _ptr(o), _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
 
 
 def wsk_merge(o_a, lse_a, o_b, lse_b, o_out, lse_out, o_bf16=None, stream=None):

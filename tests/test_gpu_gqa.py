@@ -368,3 +368,27 @@ def test_c5_ragged_64_steps():
                 ranges = [sess.gpu_range(b) for b in range(sess.B)]
                 _check_step(w, sess, st.q, ks, vs, pf, o_g.cpu().numpy(), l_g.cpu().numpy(), o_m.cpu().numpy(),
                             l_m.cpu().numpy(), ranges, "c5 step %d" % step)
+
+
+@pytest.mark.parametrize("kind", ["gqa", "mla"])
+def test_two_passes_equal_attend(kind):
+    """wsk_attend_pass1 then wsk_attend_pass2 is wsk_attend, bit for bit."""
+    if kind == "gqa":
+        w = wl.Workload("two-pass-gqa", wl.GQA, batch=3, n_q_heads=16, n_kv_heads=2, head_dim=128,
+                        context=3000, cpu_share=0.25, seed=21)
+    else:
+        w = wl.Workload("two-pass-mla", wl.MLA, batch=3, n_q_heads=16, n_kv_heads=1, head_dim=128,
+                        latent_dim=512, rope_dim=64, nope_dim=128, context=3000, cpu_share=0.25, kv_std=0.5,
+                        seed=22)
+    say("case two passes", kind)
+    pf = wl.make_prefill(w)
+    st = wl.draw_step(w, pf.gen)
+    dev = torch.device("cuda", DEV)
+    with DecodeSession(w, pf, DEV, extra_tokens=0) as sess:
+        q = to_device_bf16(st.q, dev)
+        o1, l1 = sess.attend(q)
+        o1, l1 = o1.cpu().numpy(), l1.cpu().numpy()
+        sess.attend_pass1(q)
+        o2, l2 = sess.attend_pass2()
+        assert np.array_equal(o1, o2.cpu().numpy())
+        assert np.array_equal(l1, l2.cpu().numpy())

@@ -22,13 +22,13 @@ GOLDEN = os.path.join(ROOT, "tests", "golden")
 def _declared_symbols():
     with open(os.path.join(ROOT, "include", "wsk.h")) as f:
         text = f.read()
-    return sorted(set(re.findall(r"\b(wsk_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(wsk_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_library_exports_every_declared_symbol():
     L = wsk.lib()
     names = _declared_symbols()
-    assert len(names) == 17
+    assert len(names) == 19
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(wsk._SIGS)
