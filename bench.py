@@ -106,7 +106,7 @@ def cpu_baseline(w, pf, steps_inputs, budget_s: float):
 TRAFFIC = {
     "qwen3-30b-a3b-b16-L32768": {
         "source": "paper_2609_14507_amd/csrc/attend_gqa.hip",
-        "sha256": "cb08cb8d7b9d23c8768f70800b55bc79c92f82d94ad2f6b64817e24c6291c081",
+        "sha256": "e5813847daac21bddd068a7f125084699f8189c717c91099486efc5dc7c2acb6",
         "fetch_bytes": 368959.1 * 1024 * 2.0,
         "write_bytes": 2064.0 * 1024 * 1.0,
         "kv_bytes": 751714304,

@@ -3,7 +3,7 @@
 // For every query head served by one KV head, computes the exact softmax
 // attention over one chunk of the sequence range (the GPU engine of
 // Sec. 5.1) and writes the normalised partial output and its natural-log LSE
-// (the "partial output and normaliser" merged by LSE, Sec. 4.2).
+// (the partial result with its normaliser that Sec. 4.2 merges by LSE).
 //
 // The G query heads of a KV head share every K and V row, so both products
 // are dense contractions and run on the matrix cores
