@@ -9,9 +9,10 @@ depend on its values).
 
 Timing: W untimed warmup steps, then K timed steps.  Before each step a
 512 MB buffer is rewritten so the 256 MB Infinity Cache holds no KV; HIP
-events on the stream the kernels run on bracket each step (and the attend
-call inside it), outside the flush.  The algorithmic bytes of a step are the
-bf16 K and V rows of every attended position, read once.
+events on the stream the kernels run on bracket each step and, inside it,
+the two passes of the attend call, outside the flush.  The algorithmic bytes
+of a step are the bf16 K and V rows (MLA: latent rows) of every attended
+position, read once.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -113,9 +114,9 @@ TRAFFIC = {
     },
     "deepseek-v2-lite-mla-b8-L65536": {
         "source": "paper_2609_14507_amd/csrc/attend_mla.hip",
-        "sha256": "c76f6b96a5f38f5321dd2ebf70ff6b1c93724cd1724f8e8a488087cb9cd79927",
-        "fetch_bytes": 177756.8 * 1024 * 2.0,
-        "write_bytes": 15903.0 * 1024 * 1.0,
+        "sha256": "ae01f652ea0f430a3eb4abe15a9a5220abb73a5e31f7d907432c7c904ed80c47",
+        "fetch_bytes": 177757.9 * 1024 * 2.0,
+        "write_bytes": 7951.5 * 1024 * 1.0,
         "kv_bytes": 362414592,
     },
 }

@@ -226,6 +226,7 @@ int wsk_write(wsk_cache *cache, int32_t seq, int32_t pos0, int32_t n,
  * DEVICE pointers, row i for seq_ids[i]:
  *   GQA  k_new, v_new: bf16 [n][n_kv_heads][head_dim]
  *   MLA  k_new:        bf16 [n][latent_dim + rope_dim], v_new NULL
+ * (16-byte aligned).
  * Routing (slot allocation) happens on the host during the call; the copy
  * runs asynchronously on stream, and the inputs must stay valid until the
  * stream reaches it.  Every appended position must be in the GPU partition
@@ -268,6 +269,7 @@ int wsk_attend_workspace(const wsk_cache *cache, int32_t n, const int32_t *seq_i
  *        (the absorbed query q_lat | q_rope)   (the latent output, before expansion)
  *   lse fp32 [n][n_q_heads] (natural log)
  *   ws   at least wsk_attend_workspace() bytes, 256-byte aligned
+ *   q and o 16-byte aligned
  * Softmax and accumulation are fp32 from bf16 inputs.
  * Errors: EINVAL, ESTATE, ERANGE (range outside the GPU partition), EHIP.
  */
@@ -303,8 +305,9 @@ int wsk_attend_pass2(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
  *   otherwise w_x = exp(lse_x - m),  O = (w_a O_a + w_b O_b) / (w_a + w_b),
  *   LSE = m + ln(w_a + w_b)
  * All pointers are DEVICE pointers: o_* fp32 [rows][width], lse_* fp32
- * [rows].  o_out/lse_out may alias o_b/lse_b (or o_a/lse_a).  o_bf16, if not
- * NULL, also receives O rounded to bf16 (nearest-even), [rows][width].
+ * [rows]; o_a, o_b, o_out 16-byte aligned.  o_out/lse_out may alias o_b/lse_b
+ * (or o_a/lse_a).  o_bf16, if not NULL, also receives O rounded to bf16
+ * (nearest-even), [rows][width].
  * Errors: EINVAL (rows < 0, width <= 0 or width % 4 != 0), EHIP.
  */
 int wsk_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a,
@@ -319,7 +322,8 @@ int wsk_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a,
  *   out: row (i, h) is written at out + (i*H + h) * out_stride elements
  *   (out_stride >= dl; pass latent+rope to fill the first dl elements of an
  *   attend query buffer in place).
- * Supported: dl % 64 == 0, 1 <= dn <= 256.  Errors: EINVAL, EHIP.
+ * Supported: dl % 64 == 0, 1 <= dn <= 256; w_uk 16-byte aligned.
+ * Errors: EINVAL, EHIP.
  */
 int wsk_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t *q_nope,
                    const uint16_t *w_uk, uint16_t *out, int64_t out_stride, void *stream);
@@ -328,7 +332,8 @@ int wsk_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t 
  * MLA output-side expansion (Sec. 6.1): O[i][h] = W_UV[h]^T O_lat[i][h],
  * fp32 accumulation.  DEVICE pointers: o_lat fp32 [n][H][dl],
  * w_uv bf16 [H][dl][dv], o fp32 [n][H][dv].
- * Supported: dv % 64 == 0, 1 <= dl <= 1024.  Errors: EINVAL, EHIP.
+ * Supported: dv % 64 == 0, 1 <= dl <= 1024; w_uv 16-byte aligned.
+ * Errors: EINVAL, EHIP.
  */
 int wsk_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat,
                    const uint16_t *w_uv, float *o, void *stream);

@@ -15,12 +15,14 @@
 // Each latent row is read from HBM once and used by both products (the
 // paper's CPU kernel makes the same point for its cache tiles).
 //
-// A workgroup of 4 wavefronts walks its chunk one 32-token tile at a time;
-// the tile's 18 K-steps are split over the wavefronts by latent columns:
-// wavefront w holds latent dims [128w, 128w + 128) (K-steps 4w .. 4w+3) and,
-// for w < 2, the rope K-step 16 + w.  It computes a partial S^T over its
-// K-steps and, after one exchange of partial scores through LDS, the P.V
-// product for its own 128 output columns.
+// A workgroup is two teams of 4 wavefronts; the teams take alternate 32-token
+// tiles of the workgroup's chunk and merge their results through LDS at the
+// end (one partial per workgroup).  Within a team, the tile's 18 K-steps are
+// split over the wavefronts by latent columns: wavefront w holds latent dims
+// [128w, 128w + 128) (K-steps 4w .. 4w+3) and, for w < 2, the rope K-step
+// 16 + w.  It computes a partial S^T over its K-steps and, after one exchange
+// of partial scores through LDS, the P.V product for its own 128 output
+// columns.
 //   - The GPU pool stores each 32-token tile in the order of the QK
 //     A-operand registers (WSK_LAYOUT_MLA32): load (ks, mt) is one fully
 //     coalesced 1 KB read landing in the registers that feed the MFMA.
@@ -36,9 +38,10 @@
 //     A-operand: probabilities never leave the registers.
 //   - Each wavefront keeps its pieces of three tiles in registers; a
 //     register is refilled with the tile three ahead as soon as it has been
-//     consumed, so about 100 KB per workgroup is always in flight.
+//     consumed, so about 200 KB per workgroup is always in flight.
 //   - The only synchronisation is the barrier of the score exchange (one
-//     per tile; partial scores are double-buffered).
+//     per round of two tiles, shared by both teams; partial scores are
+//     double-buffered).
 // Tokens outside [start, end) are fetched from past the buffer descriptor's
 // extent, which yields zeros, and their scores are masked to -inf.
 
@@ -64,11 +67,14 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 // token (0..31) held by row r of M-tile mt
 __device__ __forceinline__ int sub_token(int mt, int r) { return 8 * (r >> 2) + 4 * mt + (r & 3); }
 
-__global__ __launch_bounds__(256, 2) void mla_attend_kernel(const AttendParams p) {
-    __shared__ f32x4 s_part[2][4][2][64];          // 16 KB: partial S^T per wavefront, double-buffered
+__global__ __launch_bounds__(512, 1) void mla_attend_kernel(const AttendParams p) {
+    __shared__ f32x4 s_part[2][2][4][2][64];       // 32 KB: partial S^T per team and wavefront, double-buffered
+    __shared__ float s_m1[16], s_l1[16];
 
     const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int team = wv >> 2;       // two teams of 4 wavefronts take alternate tiles
+    const int wave = wv & 3;
     const int n = lane & 15;
     const int grp = lane >> 4;
     const bool rope = wave < 2;
@@ -163,7 +169,8 @@ __global__ __launch_bounds__(256, 2) void mla_attend_kernel(const AttendParams p
     // One tile t held in st: partial QK, score exchange, softmax, P.V; each
     // consumed K-step of st is refilled with tile t + kDepth.
     auto step = [&](int t, Stage &st) {
-        const Src nx = tile_src(t + kDepth);
+        const bool valid = t < sub_end;
+        const Src nx = tile_src(t + 2 * kDepth);
         const int tok0 = t * kSub;
         f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = f32x4{0.f, 0.f, 0.f, 0.f};
         s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[4][0]), qop[4], s0, 0, 0, 0);
@@ -175,15 +182,16 @@ __global__ __launch_bounds__(256, 2) void mla_attend_kernel(const AttendParams p
             s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[j][1]), qop[j], s1, 0, 0, 0);
         }
         // ---- exchange partial scores; every wavefront sums them in the same order ----
-        const int b = t & 1;
-        s_part[b][wave][0][lane] = s0;
-        s_part[b][wave][1][lane] = s1;
+        const int b = (t >> 1) & 1;
+        s_part[team][b][wave][0][lane] = s0;
+        s_part[team][b][wave][1][lane] = s1;
         __syncthreads();
-        f32x4 S0 = s_part[b][0][0][lane], S1 = s_part[b][0][1][lane];
+        if (!valid) return;   // this team has no tile in the last round
+        f32x4 S0 = s_part[team][b][0][0][lane], S1 = s_part[team][b][0][1][lane];
 #pragma unroll
         for (int w = 1; w < 4; ++w) {
-            S0 += s_part[b][w][0][lane];
-            S1 += s_part[b][w][1][lane];
+            S0 += s_part[team][b][w][0][lane];
+            S1 += s_part[team][b][w][1][lane];
         }
 
         // ---- online softmax: lane (grp, n) holds head n, tokens 8grp + e ----
@@ -252,43 +260,69 @@ __global__ __launch_bounds__(256, 2) void mla_attend_kernel(const AttendParams p
     };
 
     Stage st0, st1, st2;
-    load_tile(sub_begin, st0);
-    load_tile(sub_begin + 1, st1);
-    load_tile(sub_begin + 2, st2);
-    int t = sub_begin;
-    for (; t + 2 < sub_end; t += kDepth) {
-        step(t, st0);
-        step(t + 1, st1);
-        step(t + 2, st2);
+    const int t0 = sub_begin + team;
+    load_tile(t0, st0);
+    load_tile(t0 + 2, st1);
+    load_tile(t0 + 4, st2);
+    const int rounds = (sub_end - sub_begin + 1) >> 1;   // same for both teams
+    int r = 0;
+    for (; r + 2 < rounds; r += kDepth) {
+        step(t0 + 2 * r, st0);
+        step(t0 + 2 * r + 2, st1);
+        step(t0 + 2 * r + 4, st2);
     }
-    if (t < sub_end) step(t, st0);
-    if (t + 1 < sub_end) step(t + 1, st1);
+    if (r < rounds) step(t0 + 2 * r, st0);
+    if (r + 1 < rounds) step(t0 + 2 * r + 2, st1);
 
-    // ---- normalise and write this wavefront's 128 columns of the partial ----
+    // ---- merge the two teams, normalise, write this wavefront's 128 columns ----
     float l_tot = l_lane + __shfl_xor(l_lane, 16);
     l_tot += __shfl_xor(l_tot, 32);                  // head n, in every lane of column n
-    float inv_r[4];
+    __syncthreads();                                 // s_part is free
+    float *sx = reinterpret_cast<float *>(&s_part[0][0][0][0][0]) + wave * 16 * 128;
+    if (team == 1) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) inv_r[r] = 1.f / __shfl(l_tot, 4 * grp + r);
+        for (int nt = 0; nt < kWaveNT; ++nt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sx[(4 * grp + r) * 128 + 16 * nt + n] = o[nt][r];
+        if (wave == 0 && grp == 0) {
+            s_m1[n] = m_run;
+            s_l1[n] = l_tot;
+        }
+    }
+    __syncthreads();
+    if (team == 1) return;
     const int part = p.chunk_begin[i] + c;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int h = 4 * grp + r;
+        const float m0 = __shfl(m_run, h), l0 = __shfl(l_tot, h);
+        const float m1 = s_m1[h], l1 = s_l1[h];
+        const float M = fmaxf(m0, m1);
+        const float w0 = __builtin_amdgcn_exp2f(m0 - M);
+        const float w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
+        const float den = w0 * l0 + w1 * l1;
+        const float inv = 1.f / den;
         if (h < H) {
             float *dst = p.part_o + ((int64_t)part * H + h) * kLatent + 128 * wave + n;
 #pragma unroll
-            for (int nt = 0; nt < kWaveNT; ++nt) dst[16 * nt] = o[nt][r] * inv_r[r];
+            for (int nt = 0; nt < kWaveNT; ++nt)
+                dst[16 * nt] = (w0 * o[nt][r] + w1 * sx[h * 128 + 16 * nt + n]) * inv;
         }
     }
-    if (wave == 0 && grp == 0 && n < H)
-        p.part_lse[(int64_t)part * H + n] = (m_run + __log2f(l_tot)) * 0.69314718055994530942f;
+    if (wave == 0 && grp == 0 && n < H) {
+        const float m1 = s_m1[n], l1 = s_l1[n];
+        const float M = fmaxf(m_run, m1);
+        const float den = __builtin_amdgcn_exp2f(m_run - M) * l_tot +
+                          (m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M) * l1);
+        p.part_lse[(int64_t)part * H + n] = (M + __log2f(den)) * 0.69314718055994530942f;
+    }
 }
 
 }  // namespace
 
 hipError_t launch_mla_attend(const AttendParams &p, int n_wg, hipStream_t s) {
     if (n_wg <= 0) return hipSuccess;
-    hipLaunchKernelGGL(mla_attend_kernel, dim3(n_wg), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(mla_attend_kernel, dim3(n_wg), dim3(512), 0, s, p);
     return hipGetLastError();
 }
 

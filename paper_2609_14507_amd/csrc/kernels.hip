@@ -245,127 +245,139 @@ __global__ __launch_bounds__(256) void scatter_kernel(const ScatterParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// MLA absorption: q_lat[i][h][l] = sum_k q_nope[i][h][k] * W_UK[h][k][l],
-// fp32 accumulation, one bf16 rounding.  Workgroup = (head, 256 latent
-// columns, 8 tokens), 256 threads = 32 column groups of 8 x 8 slices of the
-// k range; each thread streams its W_UK rows in 16-byte loads and the slices
-// are summed through LDS.
+// MLA absorption and expansion: per head, a batch of up to 8 token rows times
+// a bf16 weight matrix, fp32 accumulation:
+//   absorb  q_lat[i][h][l] = sum_k q_nope[i][h][k] W_UK[h][k][l]  (bf16 out, one rounding)
+//   expand  o[i][h][j]     = sum_l o_lat[i][h][l]  W_UV[h][l][j]  (fp32 out)
+// Workgroup = (head, CB output columns, 8 tokens); its 256 threads are CB/8
+// column groups x (2048/CB) row slices, so each thread fetches its few weight
+// rows (16-byte loads) in one round and the grid has 128-256 workgroups.  The
+// inputs of the 8 tokens are staged in LDS; the row slices are summed through
+// LDS in a fixed order.
 // ---------------------------------------------------------------------------
-constexpr int kAbsorbTok = 8;
+constexpr int kProjTok = 8;
 
-__global__ __launch_bounds__(256) void absorb_kernel(int32_t n, int32_t H, int32_t dn, int32_t dl,
-                                                     const uint16_t *q_nope, const uint16_t *w_uk,
-                                                     uint16_t *out, int64_t out_stride) {
-    __shared__ float sq[kAbsorbTok][256];
-    __shared__ float red[8][kAbsorbTok][256];
+template <int CB, int KMAX, typename Tin, bool kBf16Out>
+__global__ __launch_bounds__(256) void proj_kernel(int32_t n, int32_t H, int32_t K, int32_t C, const Tin *x,
+                                                   const uint16_t *w, void *out, int64_t out_stride) {
+    constexpr int CG = CB / 8;          // column groups of 8
+    constexpr int SL = 256 / CG;        // row slices
+    __shared__ float sx[kProjTok * KMAX];               // [kProjTok][K]
+    __shared__ float red[SL * kProjTok * CB];           // [SL][kProjTok][CB], 64 KB
     const int h = blockIdx.x;
-    const int cb = blockIdx.y * 256;
-    const int i0 = blockIdx.z * kAbsorbTok;
-    const int nt = min(kAbsorbTok, n - i0);
-    const int cg = threadIdx.x & 31, sl = threadIdx.x >> 5;
-    for (int t = threadIdx.x; t < kAbsorbTok * dn; t += 256) {
-        const int ii = t / dn, k = t - ii * dn;
-        sq[ii][k] = ii < nt ? bf16_to_f32(q_nope[((int64_t)(i0 + ii) * H + h) * dn + k]) : 0.f;
+    const int cb = blockIdx.y * CB;
+    const int i0 = blockIdx.z * kProjTok;
+    const int nt = min(kProjTok, n - i0);
+    const int cg = threadIdx.x % CG, sl = threadIdx.x / CG;
+    const int col0 = cb + 8 * cg;
+    const bool col_ok = col0 < C;
+    const uint16_t *wc = w + (int64_t)h * K * C + col0;
+    // this thread's first four weight rows, issued before anything waits
+    u32x4 wv[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int k = sl + q * SL;
+        wv[q] = (col_ok && k < K) ? *reinterpret_cast<const u32x4 *>(wc + (int64_t)k * C) : u32x4{0u, 0u, 0u, 0u};
+    }
+    // the 8 tokens' input rows into LDS as fp32, 16 bytes per load where the width allows
+    constexpr int kVec = 16 / sizeof(Tin);
+    if (K % kVec == 0 && ((uintptr_t)x & 15) == 0) {
+        const int nv = kProjTok * K / kVec;
+        for (int t = threadIdx.x; t < nv; t += 256) {
+            const int e = t * kVec, ii = e / K, k = e - ii * K;
+            float v[kVec];
+            if (ii < nt) {
+                const u32x4 raw = *reinterpret_cast<const u32x4 *>(x + ((int64_t)(i0 + ii) * H + h) * K + k);
+#pragma unroll
+                for (int j = 0; j < kVec; ++j) {
+                    if constexpr (sizeof(Tin) == 2)
+                        v[j] = __uint_as_float((j & 1) ? (raw[j >> 1] & 0xffff0000u) : (raw[j >> 1] << 16));
+                    else
+                        v[j] = __uint_as_float(raw[j]);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < kVec; ++j) v[j] = 0.f;
+            }
+#pragma unroll
+            for (int j = 0; j < kVec; ++j) sx[e + j] = v[j];
+        }
+    } else {
+        for (int t = threadIdx.x; t < kProjTok * K; t += 256) {
+            const int ii = t / K, k = t - ii * K;
+            float v = 0.f;
+            if (ii < nt) {
+                const Tin xv = x[((int64_t)(i0 + ii) * H + h) * K + k];
+                if constexpr (sizeof(Tin) == 2)
+                    v = bf16_to_f32(xv);
+                else
+                    v = xv;
+            }
+            sx[t] = v;
+        }
     }
     __syncthreads();
-    float acc[kAbsorbTok][8];
+    float acc[kProjTok][8];
 #pragma unroll
-    for (int ii = 0; ii < kAbsorbTok; ++ii)
+    for (int ii = 0; ii < kProjTok; ++ii)
 #pragma unroll
         for (int c = 0; c < 8; ++c) acc[ii][c] = 0.f;
-    const int col0 = cb + 8 * cg;
-    const int kper = (dn + 7) / 8;
-    const int k0 = sl * kper, k1 = min(dn, k0 + kper);
-    if (col0 < dl) {
-        const uint16_t *w = w_uk + (int64_t)h * dn * dl + col0;
-#pragma unroll 8
-        for (int k = k0; k < k1; ++k) {
-            const u32x4 wv = *reinterpret_cast<const u32x4 *>(w + (int64_t)k * dl);
+    auto fma_rows = [&](int k0) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int k = k0 + q * SL;
+            if (k >= K) break;
             float wf[8];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                wf[2 * e] = __uint_as_float(wv[e] << 16);
-                wf[2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
+                wf[2 * e] = __uint_as_float(wv[q][e] << 16);
+                wf[2 * e + 1] = __uint_as_float(wv[q][e] & 0xffff0000u);
             }
 #pragma unroll
-            for (int ii = 0; ii < kAbsorbTok; ++ii)
+            for (int ii = 0; ii < kProjTok; ++ii) {
+                const float xv = sx[ii * K + k];
 #pragma unroll
-                for (int c = 0; c < 8; ++c) acc[ii][c] = fmaf(sq[ii][k], wf[c], acc[ii][c]);
+                for (int c = 0; c < 8; ++c) acc[ii][c] = fmaf(xv, wf[c], acc[ii][c]);
+            }
         }
+    };
+    fma_rows(sl);
+    for (int k0 = sl + 4 * SL; k0 < K; k0 += 4 * SL) {   // rows beyond the first four (wide K only)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int k = k0 + q * SL;
+            wv[q] = (col_ok && k < K) ? *reinterpret_cast<const u32x4 *>(wc + (int64_t)k * C)
+                                      : u32x4{0u, 0u, 0u, 0u};
+        }
+        fma_rows(k0);
     }
 #pragma unroll
-    for (int ii = 0; ii < kAbsorbTok; ++ii)
+    for (int ii = 0; ii < kProjTok; ++ii)
 #pragma unroll
-        for (int c = 0; c < 8; ++c) red[sl][ii][8 * cg + c] = acc[ii][c];
+        for (int c = 0; c < 8; ++c) red[(sl * kProjTok + ii) * CB + 8 * cg + c] = acc[ii][c];
     __syncthreads();
-    for (int t = threadIdx.x; t < kAbsorbTok * 256; t += 256) {
-        const int ii = t >> 8, c = t & 255;
-        if (ii >= nt || cb + c >= dl) continue;
-        float v = 0.f;
+    for (int t = threadIdx.x; t < kProjTok * CB; t += 256) {
+        const int ii = t / CB, c = t - ii * CB;
+        if (ii >= nt || cb + c >= C) continue;
+        float part[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};   // 8 loads in flight
 #pragma unroll
-        for (int q = 0; q < 8; ++q) v += red[q][ii][c];
-        out[((int64_t)(i0 + ii) * H + h) * out_stride + cb + c] = f32_to_bf16(v);
+        for (int q = 0; q < SL; q += 8)
+#pragma unroll
+            for (int u = 0; u < 8; ++u) part[u] += red[((q + u) * kProjTok + ii) * CB + c];
+        const float v = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
+        const int64_t o = ((int64_t)(i0 + ii) * H + h) * out_stride + cb + c;
+        if constexpr (kBf16Out)
+            reinterpret_cast<uint16_t *>(out)[o] = f32_to_bf16(v);
+        else
+            reinterpret_cast<float *>(out)[o] = v;
     }
 }
 
-// ---------------------------------------------------------------------------
-// MLA expansion: o[i][h][j] = sum_l o_lat[i][h][l] * W_UV[h][l][j], fp32.
-// Workgroup = (head, 128 output columns, 8 tokens), 256 threads = 16 column
-// groups of 8 x 16 slices of the l range, summed through LDS.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void expand_kernel(int32_t n, int32_t H, int32_t dl, int32_t dv,
-                                                     const float *o_lat, const uint16_t *w_uv, float *o) {
-    __shared__ float so[kAbsorbTok][1024];
-    __shared__ float red[16][kAbsorbTok][128];
-    const int h = blockIdx.x;
-    const int cb = blockIdx.y * 128;
-    const int i0 = blockIdx.z * kAbsorbTok;
-    const int nt = min(kAbsorbTok, n - i0);
-    const int cg = threadIdx.x & 15, sl = threadIdx.x >> 4;
-    for (int t = threadIdx.x; t < kAbsorbTok * dl; t += 256) {
-        const int ii = t / dl, l = t - ii * dl;
-        so[ii][l] = ii < nt ? o_lat[((int64_t)(i0 + ii) * H + h) * dl + l] : 0.f;
-    }
-    __syncthreads();
-    float acc[kAbsorbTok][8];
-#pragma unroll
-    for (int ii = 0; ii < kAbsorbTok; ++ii)
-#pragma unroll
-        for (int c = 0; c < 8; ++c) acc[ii][c] = 0.f;
-    const int col0 = cb + 8 * cg;
-    const int lper = (dl + 15) / 16;
-    const int l0 = sl * lper, l1 = min(dl, l0 + lper);
-    if (col0 < dv) {
-        const uint16_t *w = w_uv + (int64_t)h * dl * dv + col0;
-#pragma unroll 8
-        for (int l = l0; l < l1; ++l) {
-            const u32x4 wv = *reinterpret_cast<const u32x4 *>(w + (int64_t)l * dv);
-            float wf[8];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                wf[2 * e] = __uint_as_float(wv[e] << 16);
-                wf[2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
-            }
-#pragma unroll
-            for (int ii = 0; ii < kAbsorbTok; ++ii)
-#pragma unroll
-                for (int c = 0; c < 8; ++c) acc[ii][c] = fmaf(so[ii][l], wf[c], acc[ii][c]);
-        }
-    }
-#pragma unroll
-    for (int ii = 0; ii < kAbsorbTok; ++ii)
-#pragma unroll
-        for (int c = 0; c < 8; ++c) red[sl][ii][8 * cg + c] = acc[ii][c];
-    __syncthreads();
-    for (int t = threadIdx.x; t < kAbsorbTok * 128; t += 256) {
-        const int ii = t >> 7, c = t & 127;
-        if (ii >= nt || cb + c >= dv) continue;
-        float v = 0.f;
-#pragma unroll
-        for (int q = 0; q < 16; ++q) v += red[q][ii][c];
-        o[((int64_t)(i0 + ii) * H + h) * dv + cb + c] = v;
-    }
-}
+constexpr int kAbsorbCols = 32;   // 16 heads x 512 / 32 = 256 workgroups
+constexpr int kExpandCols = 16;   // 16 heads x 128 / 16 = 128 workgroups
+
+constexpr int kAbsorbMaxK = 256;  // q_nope width limit (wsk_mla_absorb)
+constexpr int kExpandMaxK = 1024; // latent width limit (wsk_mla_expand)
 
 }  // namespace
 
@@ -409,16 +421,18 @@ hipError_t launch_scatter(const ScatterParams &p, hipStream_t s) {
 hipError_t launch_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t *q_nope,
                              const uint16_t *w_uk, uint16_t *out, int64_t out_stride, hipStream_t s) {
     if (n <= 0) return hipSuccess;
-    const dim3 grid(H, (dl + 255) / 256, (n + kAbsorbTok - 1) / kAbsorbTok);
-    hipLaunchKernelGGL(absorb_kernel, grid, dim3(256), 0, s, n, H, dn, dl, q_nope, w_uk, out, out_stride);
+    const dim3 grid(H, (dl + kAbsorbCols - 1) / kAbsorbCols, (n + kProjTok - 1) / kProjTok);
+    hipLaunchKernelGGL((proj_kernel<kAbsorbCols, kAbsorbMaxK, uint16_t, true>), grid, dim3(256), 0, s, n, H, dn, dl,
+                       q_nope, w_uk, (void *)out, out_stride);
     return hipGetLastError();
 }
 
 hipError_t launch_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat,
                              const uint16_t *w_uv, float *o, hipStream_t s) {
     if (n <= 0) return hipSuccess;
-    const dim3 grid(H, (dv + 127) / 128, (n + kAbsorbTok - 1) / kAbsorbTok);
-    hipLaunchKernelGGL(expand_kernel, grid, dim3(256), 0, s, n, H, dl, dv, o_lat, w_uv, o);
+    const dim3 grid(H, (dv + kExpandCols - 1) / kExpandCols, (n + kProjTok - 1) / kProjTok);
+    hipLaunchKernelGGL((proj_kernel<kExpandCols, kExpandMaxK, float, false>), grid, dim3(256), 0, s, n, H, dl, dv,
+                       o_lat, w_uv, (void *)o, (int64_t)dv);
     return hipGetLastError();
 }
 

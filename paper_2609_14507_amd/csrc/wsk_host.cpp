@@ -161,6 +161,10 @@ int plan(wsk_cache *c, int32_t seq, int32_t pos0, int32_t n, std::vector<Pending
     return WSK_OK;
 }
 
+// Device buffers read or written with 16-byte vector accesses must be
+// 16-byte aligned.
+inline bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
+
 void commit(wsk_cache *c, const std::vector<Pending> &pend) {
     for (const Pending &p : pend) tab(c, p.part, p.seq, p.blk) = p.slot;
 }
@@ -215,9 +219,10 @@ int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *
         pl.head_groups = G / pl.heads_per_wg;
         units = sp.n_kv_heads * pl.head_groups;
     }
-    // workgroups resident at once (both kernels: 2 per CU); the chunk budget
-    // per (KV head, head group) unit follows from it
-    const int64_t slots = 2 * (int64_t)c->cu_count;
+    // workgroups resident at once (GQA kernel: 2 per CU; MLA kernel, whose
+    // workgroups are twice as wide: 1 per CU); the chunk budget per (KV head,
+    // head group) unit follows from it
+    const int64_t slots = (sp.kind == WSK_KIND_GQA ? 2 : 1) * (int64_t)c->cu_count;
     const int64_t budget = std::max<int64_t>(1, slots / units);
     pl.tpc.assign(n, 1);
     pl.nchunks.assign(n, 0);
@@ -487,6 +492,7 @@ int wsk_append(wsk_cache *c, int32_t n, const int32_t *ids, const void *k_new, c
     if (!k_new) return fail(WSK_EINVAL, "k_new is NULL");
     if (sp.kind == WSK_KIND_GQA && !v_new) return fail(WSK_EINVAL, "v_new is NULL");
     if (sp.kind == WSK_KIND_MLA && v_new) return fail(WSK_EINVAL, "MLA caches take no v_new");
+    if (!aligned16(k_new) || !aligned16(v_new)) return fail(WSK_EINVAL, "k_new/v_new must be 16-byte aligned");
     if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
     std::vector<int32_t> order(n);
     for (int32_t i = 0; i < n; ++i) {
@@ -624,6 +630,7 @@ int attend_passes(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *st
     if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
     if (pass1 && !q) return fail(WSK_EINVAL, "q must not be NULL");
     if (pass2 && (!o || !lse)) return fail(WSK_EINVAL, "o/lse must not be NULL");
+    if (!aligned16(q) || !aligned16(o)) return fail(WSK_EINVAL, "q and o must be 16-byte aligned");
     if (pl.bytes && (!ws || ws_bytes < pl.bytes)) return fail(WSK_EINVAL, "workspace of %zu bytes needed", pl.bytes);
     if (((uintptr_t)ws & 255) != 0) return fail(WSK_EINVAL, "workspace must be 256-byte aligned");
     const wsk_partition_spec &sp = c->spec;
@@ -719,6 +726,8 @@ int wsk_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a,
     if (rows < 0 || width <= 0 || width % 4) return fail(WSK_EINVAL, "rows %d width %d", rows, width);
     if (rows == 0) return WSK_OK;
     if (!o_a || !lse_a || !o_b || !lse_b || !o_out || !lse_out) return fail(WSK_EINVAL, "NULL pointer");
+    if (!aligned16(o_a) || !aligned16(o_b) || !aligned16(o_out))
+        return fail(WSK_EINVAL, "o_a, o_b and o_out must be 16-byte aligned");
     hipError_t e = launch_merge(rows, width, o_a, lse_a, o_b, lse_b, o_out, lse_out, o_bf16, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "wsk_merge");
     return WSK_OK;
@@ -730,6 +739,7 @@ int wsk_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t 
         return fail(WSK_EINVAL, "absorb sizes n=%d H=%d dn=%d dl=%d stride=%lld", n, H, dn, dl, (long long)out_stride);
     if (n == 0) return WSK_OK;
     if (!q_nope || !w_uk || !out) return fail(WSK_EINVAL, "NULL pointer");
+    if (!aligned16(w_uk)) return fail(WSK_EINVAL, "w_uk must be 16-byte aligned");
     hipError_t e = launch_mla_absorb(n, H, dn, dl, q_nope, w_uk, out, out_stride, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "wsk_mla_absorb");
     return WSK_OK;
@@ -741,6 +751,7 @@ int wsk_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_
         return fail(WSK_EINVAL, "expand sizes n=%d H=%d dl=%d dv=%d", n, H, dl, dv);
     if (n == 0) return WSK_OK;
     if (!o_lat || !w_uv || !o) return fail(WSK_EINVAL, "NULL pointer");
+    if (!aligned16(w_uv)) return fail(WSK_EINVAL, "w_uv must be 16-byte aligned");
     hipError_t e = launch_mla_expand(n, H, dl, dv, o_lat, w_uv, o, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "wsk_mla_expand");
     return WSK_OK;

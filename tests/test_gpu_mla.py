@@ -208,3 +208,44 @@ def test_c4_deepseek_v2_lite_full_path():
         for b in (0, 3, 7):
             for p in (0, pf.splits[b] - 1, pf.splits[b], pf.lengths[b] - 1, pf.lengths[b]):
                 assert wsk.wsk_route(sess.h, b, p) == model.route(b, p)
+
+
+def test_alignment_rules():
+    """Buffers the kernels access 16 bytes at a time must be 16-byte aligned
+    (refused with EINVAL, nothing launched); a q_nope or o_lat that is not
+    aligned is staged element by element and gives the same bits."""
+    gen = torch.Generator().manual_seed(31)
+    w = wl.C4
+    n, H = 3, w.n_q_heads
+    dev = torch.device("cuda", DEV)
+    q_nope = wl.draw_bf16(gen, (n, H, w.nope_dim))
+    w_uk, w_uv = wl.draw_mla_weights(w, gen)
+    say("case alignment")
+    wk = to_device_bf16(w_uk, dev)
+    out_a = torch.zeros(n, H, w.latent_dim, dtype=torch.bfloat16, device=dev)
+    wsk.wsk_mla_absorb(to_device_bf16(q_nope, dev), wk, out_a, w.latent_dim)
+    buf = torch.zeros(q_nope.size + 1, dtype=torch.bfloat16, device=dev)
+    q_mis = buf[1:].view(n, H, w.nope_dim)
+    q_mis.copy_(to_device_bf16(q_nope, dev))
+    out_b = torch.zeros_like(out_a)
+    wsk.wsk_mla_absorb(q_mis, wk, out_b, w.latent_dim)
+    assert torch.equal(out_a.view(torch.int16), out_b.view(torch.int16))
+    wbuf = torch.zeros(w_uk.size + 1, dtype=torch.bfloat16, device=dev)
+    with pytest.raises(wsk.WskError) as ei:
+        wsk.wsk_mla_absorb(q_mis, wbuf[1:].view(w_uk.shape), out_b, w.latent_dim)
+    assert ei.value.code == wsk.WSK_EINVAL
+    o_lat = torch.randn(n, H, w.latent_dim, generator=torch.Generator().manual_seed(3)).to(dev)
+    wv = to_device_bf16(w_uv, dev)
+    o1 = torch.empty(n, H, w.head_dim, device=dev)
+    wsk.wsk_mla_expand(o_lat, wv, o1)
+    lbuf = torch.zeros(o_lat.numel() + 1, device=dev)
+    l_mis = lbuf[1:].view(n, H, w.latent_dim)
+    l_mis.copy_(o_lat)
+    o2 = torch.empty_like(o1)
+    wsk.wsk_mla_expand(l_mis, wv, o2)
+    assert torch.equal(o1, o2)
+    r = torch.zeros(4 * 128 + 1, device=dev)
+    l = torch.zeros(4, device=dev)
+    with pytest.raises(wsk.WskError) as ei:
+        wsk.wsk_merge(r[1:].view(4, 128), l, r[1:].view(4, 128), l, r[1:].view(4, 128), l)
+    assert ei.value.code == wsk.WSK_EINVAL
