@@ -2,10 +2,11 @@
 
 One step = the whole hot path over one batch: append the new token's K/V of
 every sequence into its GPU partition, split-KV attention over the GPU range
-(pass 1 + chunk combine), LSE merge with the CPU-range partial.  Inputs are
-seeded synthetic tensors already resident in HBM; the CPU-range partial fed
-to the merge is a seeded synthetic (O, LSE) pair (the merge's cost does not
-depend on its values).
+(pass 1), then pass 2, which merges the chunk partials and the CPU-range
+partial by their LSE in one launch (MLA adds the query absorption before and
+the output expansion after).  Inputs are seeded synthetic tensors already
+resident in HBM; the CPU-range partial fed to the merge is a seeded
+synthetic (O, LSE) pair (the merge's cost does not depend on its values).
 
 Timing: W untimed warmup steps, then K timed steps.  Before each step a
 512 MB buffer is rewritten so the 256 MB Infinity Cache holds no KV; HIP
@@ -181,9 +182,9 @@ def main():
     if args.share is not None:
         splits = [wl.split_point(args.share, L) for L in pf.lengths]
         pf = wl.Prefill(pf.lengths, splits, pf.k, pf.v, pf.gen)
-    steps_in = [wl.draw_step(w, pf.gen) for _ in range(W + K)]
+    steps_in = [wl.draw_step(w, pf.gen) for _ in range(W + 2 * K)]
     log("bench: routing the prefill into the cache")
-    sess = DecodeSession(w, pf, 0, extra_tokens=W + K)
+    sess = DecodeSession(w, pf, 0, extra_tokens=W + 2 * K)
     B, H = sess.B, w.n_q_heads
     D = sess.out_width                      # attend output width (MLA: the latent)
     qs = [to_device_bf16(s.q, dev) for s in steps_in]
@@ -198,57 +199,72 @@ def main():
     o_c, l_c = wl.draw_cpu_partial(pf.gen, B * H, D)
     o_cpu = torch.from_numpy(o_c).to(dev).view(B, H, D)
     l_cpu = torch.from_numpy(l_c).to(dev).view(B, H)
-    o_g = torch.empty(B, H, D, device=dev)
-    l_g = torch.empty(B, H, device=dev)
     o_m = torch.empty(B, H, D, device=dev)
     l_m = torch.empty(B, H, device=dev)
     sess.workspace(sess.ids, [min(s, L) for s, L in zip(splits, pf.lengths)], list(pf.lengths))
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
-    def step(i, ev):
+    def step(i, ev=None, parts=None):
+        """One decode step.  ev = (start, end) events around the step; parts =
+        5 events around its pieces (diagnostic steps only: every event record
+        costs GPU time of its own)."""
         if not args.no_flush:
             flush.add_(1)
-        ev[0].record(stream)
+        mark = (lambda k: parts[k].record(stream)) if parts else (lambda k: None)
+        if ev:
+            ev[0].record(stream)
+        mark(0)
         if mla:   # query-side projection into the latent space, in place
             wsk.wsk_mla_absorb(qn[i], w_uk_d, qs[i], w.row_elems)
         sess.append(kn[i], vn[i])
-        ev[1].record(stream)
+        mark(1)
         # wsk_attend as its two passes, so that pass 1 (the KV-streaming
-        # kernel) is timed on its own
+        # kernel) is timed on its own; pass 2 also merges the CPU partial
         sess.attend_pass1(qs[i])
-        ev[2].record(stream)
-        sess.attend_pass2(o=o_g, lse=l_g)
-        ev[3].record(stream)
-        sess.merge(o_cpu, l_cpu, o_g, l_g, o_m, l_m)
+        mark(2)
+        sess.attend_pass2(o=o_m, lse=l_m, o_x=o_cpu, lse_x=l_cpu)
+        mark(3)
         if mla:   # output-side expansion of the merged latent output
             wsk.wsk_mla_expand(o_m, w_uv_d, o_out)
-        ev[4].record(stream)
+            mark(4)
+        if ev:
+            ev[1].record(stream)
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(W + K)]
-    nbytes = []
-    log("bench: %d warmup + %d timed steps" % (W, K))
+    def kv_bytes():   # algorithmic bytes of the next step: [s_b, L_b + 1) of every sequence
+        return sum((sess.lengths[b] + 1 - min(splits[b], sess.lengths[b])) * w.token_bytes for b in range(B))
+
+    ev_step = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
+    ev_part = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
+    log("bench: %d warmup + %d timed steps (+ %d diagnostic steps with per-part events)" % (W, K, K))
     for i in range(W):
-        step(i, events[i])
+        step(i)
     torch.cuda.synchronize()
+    nbytes = []
     t0 = time.perf_counter()
-    for i in range(W, W + K):
-        nbytes.append(sum((sess.lengths[b] + 1 - min(splits[b], sess.lengths[b])) * w.token_bytes
-                          for b in range(B)))
-        step(i, events[i])
+    for k in range(K):
+        nbytes.append(kv_bytes())
+        step(W + k, ev=ev_step[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    el = lambda a, b: np.array([events[i][a].elapsed_time(events[i][b]) for i in range(W, W + K)])
-    step_ms, app_ms, p1_ms, p2_ms, mrg_ms = el(0, 4), el(0, 1), el(1, 2), el(2, 3), el(3, 4)
-    att_ms = p1_ms + p2_ms
+    d_bytes = []
+    for k in range(K):
+        d_bytes.append(kv_bytes())
+        step(W + K + k, parts=ev_part[k])
+    torch.cuda.synchronize()
+    step_ms = np.array([e[0].elapsed_time(e[1]) for e in ev_step])
+    el = lambda a, b: np.array([e[a].elapsed_time(e[b]) for e in ev_part])
+    app_ms, p1_ms, p2_ms = el(0, 1), el(1, 2), el(2, 3)
+    exp_ms = el(3, 4) if mla else np.zeros(K)
     nbytes = np.array(nbytes, dtype=np.float64)
+    d_bytes = np.array(d_bytes, dtype=np.float64)
     value = float(nbytes.sum() / (step_ms.sum() * 1e-3) / 1e9)
-    att_gbs = float(nbytes.sum() / (att_ms.sum() * 1e-3) / 1e9)
-    p1_gbs = float(nbytes.sum() / (p1_ms.sum() * 1e-3) / 1e9)
-    log("bench: step %.1f us (absorb+append %.1f, attend pass 1 %.1f + pass 2 %.1f, merge(+expand) %.1f); "
-        "pass 1 %.0f GB/s, attend %.0f GB/s; wall %.1f ms/step"
-        % (step_ms.mean() * 1e3, app_ms.mean() * 1e3, p1_ms.mean() * 1e3, p2_ms.mean() * 1e3, mrg_ms.mean() * 1e3,
-           p1_gbs, att_gbs, wall / K * 1e3))
+    att_gbs = float(d_bytes.sum() / ((p1_ms + p2_ms).sum() * 1e-3) / 1e9)
+    p1_gbs = float(d_bytes.sum() / (p1_ms.sum() * 1e-3) / 1e9)
+    log("bench: step %.1f us; diagnostic steps: absorb+append %.1f, attend pass 1 %.1f, pass 2 with merge %.1f, "
+        "expand %.1f us; pass 1 %.0f GB/s; wall %.1f ms/step"
+        % (step_ms.mean() * 1e3, app_ms.mean() * 1e3, p1_ms.mean() * 1e3, p2_ms.mean() * 1e3, exp_ms.mean() * 1e3,
+           p1_gbs, wall / K * 1e3))
     sess.close()
     if args.copy_calibration:
         src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
@@ -284,19 +300,20 @@ def main():
             "cpu_share": args.share if args.share is not None else (w.cpu_share or [w.share_lo, w.share_hi]),
             "gpu_tokens_per_step": int(nbytes.mean() / w.token_bytes),
             "kv_bytes_per_step": int(nbytes.mean()),
-            "step": ("absorb + append + attend (pass 1 + chunk combine) + LSE merge + expand" if mla
-                     else "append + attend (pass 1 + chunk combine) + LSE merge"),
+            "step": ("absorb + append + attend pass 1 + (chunk combine + LSE merge with the CPU partial) + expand"
+                     if mla else "append + attend pass 1 + (chunk combine + LSE merge with the CPU partial)"),
             "cache_flush_between_steps": not args.no_flush,
         },
         "breakdown_us": {
-            ("absorb_append" if mla else "append"): round(float(app_ms.mean() * 1e3), 2),
-            "attend_pass1": round(float(p1_ms.mean() * 1e3), 2),
-            "attend_pass2_combine": round(float(p2_ms.mean() * 1e3), 2),
-            ("merge_expand" if mla else "merge"): round(float(mrg_ms.mean() * 1e3), 2),
-            "attend_gbs": round(att_gbs, 1),
             "step_p10": round(float(np.percentile(step_ms, 10) * 1e3), 2),
             "step_p90": round(float(np.percentile(step_ms, 90) * 1e3), 2),
             "wall_per_step_incl_flush": round(wall / K * 1e6, 1),
+            "diagnostic_steps": "K more steps with events between the parts (each record adds GPU time)",
+            ("absorb_append" if mla else "append"): round(float(app_ms.mean() * 1e3), 2),
+            "attend_pass1": round(float(p1_ms.mean() * 1e3), 2),
+            "attend_pass2_combine_merge": round(float(p2_ms.mean() * 1e3), 2),
+            **({"expand": round(float(exp_ms.mean() * 1e3), 2)} if mla else {}),
+            "attend_gbs": round(att_gbs, 1),
         },
         "roofline": roofline(w, "mla" if mla else "gqa", p1_gbs, float(nbytes.mean())),
     }

@@ -280,13 +280,19 @@ int wsk_attend(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
 /*
  * The two passes of wsk_attend, for callers that schedule or time them
  * apart.  Called with the same cache state, seq_ids, start, end and
- * workspace, wsk_attend_pass1 followed by wsk_attend_pass2 on the stream is
- * wsk_attend:
+ * workspace, wsk_attend_pass1 followed by wsk_attend_pass2 (o_x, lse_x NULL)
+ * on the stream is wsk_attend:
  *   pass 1 attends every chunk of every range (split-KV: each range is cut
  *          into chunks of whole 64-token tiles spread over the GPU) and
  *          leaves each chunk's normalised partial O and LSE in ws;
  *   pass 2 merges the chunks of each (sequence, head) by their LSE into o
  *          and lse.
+ * o_x, lse_x (DEVICE, both or neither; o_x 16-byte aligned): a partial over
+ * other keys with the layout of o and lse, e.g. the CPU range's (O, LSE)
+ * (Sec. 4.2, Sec. 5.1).  Given, pass 2 merges it in as one more chunk, so o
+ * and lse are the LSE merge of the CPU and GPU partials, as wsk_attend
+ * followed by wsk_merge would give (up to fp32 rounding order), in one
+ * launch.  An empty GPU range then returns the other partial unchanged.
  * The workspace contents between the passes are private to the library.
  * Arguments, ownership and errors as for wsk_attend (pass 1 takes no o/lse,
  * pass 2 no q).
@@ -295,7 +301,8 @@ int wsk_attend_pass1(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
                      const int32_t *start, const int32_t *end, const void *q,
                      void *ws, size_t ws_bytes, void *stream);
 int wsk_attend_pass2(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
-                     const int32_t *start, const int32_t *end, float *o,
+                     const int32_t *start, const int32_t *end,
+                     const float *o_x, const float *lse_x, float *o,
                      float *lse, void *ws, size_t ws_bytes, void *stream);
 
 /*

@@ -59,7 +59,9 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 // LSE = max + ln sum w_c.  Workgroup = (sequence, head, 128-column slice);
 // its 256 threads are 8 chunk groups x 32 float4 columns, so a whole
 // sequence's partials are fetched in one or two rounds of loads; the groups
-// are summed through LDS.  No chunk (empty range): O = 0, LSE = -inf.
+// are summed through LDS.  An optional partial over other keys (o_x, lse_x:
+// the CPU range) enters as one more chunk, which makes this the LSE merge of
+// the CPU and GPU partials too.  Nothing to merge: O = 0, LSE = -inf.
 // ---------------------------------------------------------------------------
 constexpr int kCombineCols4 = 32;                   // float4 columns per workgroup
 constexpr int kCombineGroups = 256 / kCombineCols4; // chunk groups
@@ -93,16 +95,19 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int
     const int tid = threadIdx.x;
     const int col0 = blockIdx.y * 4 * kCombineCols4;
     f32x4 *out = reinterpret_cast<f32x4 *>(p.o + (int64_t)row * width + col0);
-    if (nc == 0) {
+    const float lx = p.lse_x ? p.lse_x[row] : -INFINITY;
+    if (nc == 0 && lx == -INFINITY) {
         if (tid < kCombineCols4) out[tid] = f32x4{0.f, 0.f, 0.f, 0.f};
         if (tid == 0 && blockIdx.y == 0) p.lse[row] = -INFINITY;
         return;
     }
     const float *pl = p.part_lse + (int64_t)c0 * H + h;
-    float m = -INFINITY;
+    float m = lx;
     for (int c = tid; c < nc; c += 256) m = fmaxf(m, pl[(int64_t)c * H]);
     m = block_reduce(m, true, s_red);
-    float dsum = 0.f;
+    // the other partial: weight wx (0 when absent or empty; then it is not read)
+    const float wx = lx == -INFINITY ? 0.f : __expf(lx - m);
+    float dsum = tid == 0 ? wx : 0.f;
     for (int c = tid; c < nc; c += 256) {
         const float w = __expf(pl[(int64_t)c * H] - m);
         if (c < kCombineW) s_w[c] = w;
@@ -114,6 +119,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int
     const f32x4 *po = reinterpret_cast<const f32x4 *>(p.part_o + ((int64_t)c0 * H + h) * width + col0) + c4;
     const int64_t cstride = (int64_t)H * width / 4;
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (g == 0 && wx != 0.f) acc = wx * reinterpret_cast<const f32x4 *>(p.o_x + (int64_t)row * width + col0)[c4];
 #pragma unroll 8
     for (int c = g; c < nc; c += kCombineGroups) {
         const float w = c < kCombineW ? s_w[c] : __expf(pl[(int64_t)c * H] - m);

@@ -621,7 +621,7 @@ namespace {
 // pass 2 merges them into o / lse.
 int attend_passes(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
                   const void *q, float *o, float *lse, void *ws, size_t ws_bytes, void *stream, bool pass1,
-                  bool pass2) {
+                  bool pass2, const float *o_x = nullptr, const float *lse_x = nullptr) {
     if (!c) return fail(WSK_EINVAL, "cache is NULL");
     AttendPlan pl;
     int rc = make_plan(c, n, ids, start, end, pl);
@@ -631,6 +631,8 @@ int attend_passes(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *st
     if (pass1 && !q) return fail(WSK_EINVAL, "q must not be NULL");
     if (pass2 && (!o || !lse)) return fail(WSK_EINVAL, "o/lse must not be NULL");
     if (!aligned16(q) || !aligned16(o)) return fail(WSK_EINVAL, "q and o must be 16-byte aligned");
+    if ((o_x == nullptr) != (lse_x == nullptr)) return fail(WSK_EINVAL, "o_x and lse_x must both be given or both NULL");
+    if (!aligned16(o_x)) return fail(WSK_EINVAL, "o_x must be 16-byte aligned");
     if (pl.bytes && (!ws || ws_bytes < pl.bytes)) return fail(WSK_EINVAL, "workspace of %zu bytes needed", pl.bytes);
     if (((uintptr_t)ws & 255) != 0) return fail(WSK_EINVAL, "workspace must be 256-byte aligned");
     const wsk_partition_spec &sp = c->spec;
@@ -693,6 +695,8 @@ int attend_passes(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *st
         cp.part_lse = ap.part_lse;
         cp.o = o + (int64_t)i0 * sp.n_q_heads * width;
         cp.lse = lse + (int64_t)i0 * sp.n_q_heads;
+        cp.o_x = o_x ? o_x + (int64_t)i0 * sp.n_q_heads * width : nullptr;
+        cp.lse_x = lse_x ? lse_x + (int64_t)i0 * sp.n_q_heads : nullptr;
         cp.n = m;
         cp.n_q_heads = sp.n_q_heads;
         for (int32_t r = 0; r <= kMaxLaunchSeqs; ++r) cp.chunk_begin[r] = ap.chunk_begin[r];
@@ -717,8 +721,9 @@ int wsk_attend_pass1(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t 
 }
 
 int wsk_attend_pass2(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
-                     float *o, float *lse, void *ws, size_t ws_bytes, void *stream) {
-    return attend_passes(c, n, ids, start, end, nullptr, o, lse, ws, ws_bytes, stream, false, true);
+                     const float *o_x, const float *lse_x, float *o, float *lse, void *ws, size_t ws_bytes,
+                     void *stream) {
+    return attend_passes(c, n, ids, start, end, nullptr, o, lse, ws, ws_bytes, stream, false, true, o_x, lse_x);
 }
 
 int wsk_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a, const float *o_b,

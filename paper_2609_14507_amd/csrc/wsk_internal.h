@@ -58,6 +58,8 @@ struct CombineParams {
     const float *part_lse;
     float *o;                // launch-local [n][n_q_heads][width]
     float *lse;              // launch-local [n][n_q_heads]
+    const float *o_x;        // optional partial over other keys (the CPU range), merged in
+    const float *lse_x;      //   as one more chunk: launch-local [n][n_q_heads][width], [n][n_q_heads]
     int32_t n;
     int32_t n_q_heads;
     int32_t chunk_begin[kMaxLaunchSeqs + 1];

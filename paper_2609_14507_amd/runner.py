@@ -112,10 +112,11 @@ class DecodeSession:
         ids, start, end = self._ranges(start, end, ids)
         wsk.wsk_attend_pass1(self.h, ids, start, end, q, self.workspace(ids, start, end))
 
-    def attend_pass2(self, start=None, end=None, ids=None, o=None, lse=None):
+    def attend_pass2(self, start=None, end=None, ids=None, o=None, lse=None, o_x=None, lse_x=None):
+        """Pass 2; with (o_x, lse_x) the CPU-range partial is merged in as well."""
         ids, start, end = self._ranges(start, end, ids)
         o, lse = self._outputs(len(ids), o, lse)
-        wsk.wsk_attend_pass2(self.h, ids, start, end, o, lse, self.workspace(ids, start, end))
+        wsk.wsk_attend_pass2(self.h, ids, start, end, o, lse, self.workspace(ids, start, end), o_x, lse_x)
         return o, lse
 
     @staticmethod

@@ -71,7 +71,8 @@ _SIGS = {
     "wsk_attend_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_attend": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_attend_pass1": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
-    "wsk_attend_pass2": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
+    "wsk_attend_pass2": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP],
+                         ctypes.c_int),
     "wsk_merge": ([_I32, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP], ctypes.c_int),
     "wsk_mla_absorb": ([_I32, _I32, _I32, _I32, _VP, _VP, _VP, _I64, _VP], ctypes.c_int),
     "wsk_mla_expand": ([_I32, _I32, _I32, _I32, _VP, _VP, _VP, _VP], ctypes.c_int),
@@ -216,11 +217,12 @@ def wsk_attend_pass1(h: int, seq_ids, start, end, q, ws, stream=None):
                                   _ptr(q), _ptr(ws), nbytes, _stream(stream)))
 
 
-def wsk_attend_pass2(h: int, seq_ids, start, end, o, lse, ws, stream=None):
-    """Pass 2 of wsk_attend: merges the chunk partials in ws into o, lse."""
+def wsk_attend_pass2(h: int, seq_ids, start, end, o, lse, ws, o_x=None, lse_x=None, stream=None):
+    """Pass 2 of wsk_attend: merges the chunk partials in ws (and, if given,
+    the partial (o_x, lse_x) over other keys) into o, lse."""
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(lib().wsk_attend_pass2(h, len(seq_ids), _i32_array(seq_ids), _i32_array(start), _i32_array(end),
-                                  _ptr(o), _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
+                                  _ptr(o_x), _ptr(lse_x), _ptr(o), _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
 
 
 def wsk_merge(o_a, lse_a, o_b, lse_b, o_out, lse_out, o_bf16=None, stream=None):

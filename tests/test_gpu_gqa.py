@@ -392,3 +392,32 @@ def test_two_passes_equal_attend(kind):
         o2, l2 = sess.attend_pass2()
         assert np.array_equal(o1, o2.cpu().numpy())
         assert np.array_equal(l1, l2.cpu().numpy())
+        # pass 2 with the CPU-range partial merged in (one launch) against
+        # wsk_attend + wsk_merge and against the oracle over the whole context
+        H = w.n_q_heads
+        dv = w.latent_dim if kind == "mla" else w.head_dim
+        cpu_o, cpu_l, full_o, full_l = [], [], [], []
+        for b in range(w.batch):
+            s_b, L = pf.splits[b], pf.lengths[b]
+            v = None if kind == "mla" else pf.v[b]
+            g = w.n_q_heads if kind == "mla" else w.group
+            o_c, l_c = oracle.attend(st.q[b], pf.k[b], v, 0, s_b, w.softmax_scale, g, dv=dv)
+            o_f, l_f = oracle.attend(st.q[b], pf.k[b], v, 0, L, w.softmax_scale, g, dv=dv)
+            cpu_o.append(o_c)
+            cpu_l.append(l_c)
+            full_o.append(o_f)
+            full_l.append(l_f)
+        o_x = torch.from_numpy(np.stack(cpu_o).astype(np.float32)).to(dev)
+        l_x = torch.from_numpy(np.stack(cpu_l).astype(np.float32)).to(dev)
+        sess.attend_pass1(q)
+        o3, l3 = sess.attend_pass2(o_x=o_x, lse_x=l_x)
+        o4, l4 = sess.merge(o_x, l_x, torch.from_numpy(o1).to(dev), torch.from_numpy(l1).to(dev))
+        o3, l3 = o3.cpu().numpy(), l3.cpu().numpy()
+        assert np.allclose(o3, o4.cpu().numpy(), rtol=1e-5, atol=1e-6)
+        assert np.allclose(l3, l4.cpu().numpy(), rtol=0, atol=1e-5)
+        assert_close(o3, np.stack(full_o), "two-pass merged %s" % kind)
+        assert_lse(l3, np.stack(full_l), "two-pass merged %s" % kind)
+        # an empty GPU range returns the other partial unchanged
+        sess.attend_pass1(q, start=[pf.lengths[b] for b in range(w.batch)])
+        o5, l5 = sess.attend_pass2(start=[pf.lengths[b] for b in range(w.batch)], o_x=o_x, lse_x=l_x)
+        assert torch.equal(o5, o_x) and torch.equal(l5, l_x)
