@@ -266,6 +266,25 @@ def main():
         % (step_ms.mean() * 1e3, app_ms.mean() * 1e3, p1_ms.mean() * 1e3, p2_ms.mean() * 1e3, exp_ms.mean() * 1e3,
            p1_gbs, wall / K * 1e3))
     sess.close()
+    # plain streaming read of 2 GiB with the attention kernels' load pattern:
+    # the practical HBM read ceiling the pass-1 rate is compared with
+    from paper_2609_14507_amd import wsk as _wsk
+    probe = torch.empty(2 << 30, dtype=torch.uint8, device=dev)
+    probe.fill_(3)
+    fold = torch.zeros(1, dtype=torch.int32, device=dev)
+    pr_ms = []
+    for it in range(6):
+        flush.add_(1)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        _wsk.wsk_stream_read(probe, fold)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if it:
+            pr_ms.append(e0.elapsed_time(e1))
+    probe_gbs = float(probe.numel() / (np.median(pr_ms) * 1e-3) / 1e9)
+    del probe
+    log("bench: streaming-read probe %.0f GB/s" % probe_gbs)
     if args.copy_calibration:
         src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -316,6 +335,9 @@ def main():
             "attend_gbs": round(att_gbs, 1),
         },
         "roofline": roofline(w, "mla" if mla else "gqa", p1_gbs, float(nbytes.mean())),
+        "stream_read_probe": {"value": round(probe_gbs, 1), "unit": "GB/s", "bytes": 2 << 30,
+                              "what": "wsk_stream_read: one plain read of 2 GiB with the attention kernels' "
+                                      "loads, median of 5, cache flushed before each"},
     }
     if not args.no_cpu_baseline:
         log("bench: timing the oracle on the host (%.0f s budget)" % args.cpu_budget)

@@ -345,6 +345,16 @@ int wsk_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t 
 int wsk_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat,
                    const uint16_t *w_uv, float *o, void *stream);
 
+/*
+ * Measurement aid, not part of the decode path: reads `bytes` of DEVICE
+ * memory at p once with the loads the attention kernels use (16 bytes per
+ * lane, 1 KB per wavefront instruction, non-temporal), spread over the
+ * whole GPU, and XORs a 32-bit fold of the data into *out (DEVICE).  Timing
+ * it gives the plain HBM read rate the attention kernels can be compared
+ * with.  p 16-byte aligned; bytes a multiple of 32768.  Errors: EINVAL, EHIP.
+ */
+int wsk_stream_read(const void *p, size_t bytes, uint32_t *out, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

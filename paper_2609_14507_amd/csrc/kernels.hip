@@ -379,6 +379,31 @@ __global__ __launch_bounds__(256) void proj_kernel(int32_t n, int32_t H, int32_t
     }
 }
 
+// ---------------------------------------------------------------------------
+// Streaming read probe: every wavefront reads 32 KB tiles (32 loads of 1 KB
+// in flight, non-temporal buffer loads like the attention kernels),
+// grid-stride over the buffer, and folds them.
+// ---------------------------------------------------------------------------
+constexpr int kProbeTileBytes = 32768;
+
+__global__ __launch_bounds__(256) void stream_read_kernel(const char *a, int64_t ntiles, uint32_t *out) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t acc = 0;
+    for (int64_t t = (int64_t)blockIdx.x * 4 + wave; t < ntiles; t += (int64_t)gridDim.x * 4) {
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc((void *)(a + t * kProbeTileBytes), 0, kProbeTileBytes, 0x00020000);
+        u32x4 v[kProbeTileBytes / 1024];
+#pragma unroll
+        for (int k = 0; k < kProbeTileBytes / 1024; ++k)
+            v[k] = __builtin_amdgcn_raw_buffer_load_b128(rs, lane * 16, k * 1024, kStreamLoad);
+#pragma unroll
+        for (int k = 0; k < kProbeTileBytes / 1024; ++k) acc ^= v[k][0] ^ v[k][1] ^ v[k][2] ^ v[k][3];
+    }
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) acc ^= __shfl_xor(acc, d);
+    if (lane == 0) atomicXor(out, acc);
+}
+
 constexpr int kAbsorbCols = 32;   // 16 heads x 512 / 32 = 256 workgroups
 constexpr int kExpandCols = 16;   // 16 heads x 128 / 16 = 128 workgroups
 
@@ -421,6 +446,11 @@ hipError_t launch_scatter(const ScatterParams &p, hipStream_t s) {
     int64_t blocks = ((int64_t)p.m * per_pos + 255) / 256;
     if (blocks > 65536) blocks = 65536;
     hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_stream_read(const void *p, int64_t bytes, uint32_t *out, int n_wg, hipStream_t s) {
+    hipLaunchKernelGGL(stream_read_kernel, dim3(n_wg), dim3(256), 0, s, (const char *)p, bytes / kProbeTileBytes, out);
     return hipGetLastError();
 }
 

@@ -762,4 +762,14 @@ int wsk_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_
     return WSK_OK;
 }
 
+int wsk_stream_read(const void *p, size_t bytes, uint32_t *out, void *stream) {
+    if (!p || !out || bytes == 0 || bytes % 32768 || !aligned16(p)) return fail(WSK_EINVAL, "stream_read arguments");
+    int dev = 0, cus = 256;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess) e = launch_stream_read(p, (int64_t)bytes, out, 4 * std::max(cus, 1), (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "wsk_stream_read");
+    return WSK_OK;
+}
+
 }  // extern "C"

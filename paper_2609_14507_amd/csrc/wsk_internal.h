@@ -109,6 +109,7 @@ hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
 hipError_t launch_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a,
                         const float *o_b, const float *lse_b, float *o_out, float *lse_out,
                         uint16_t *o_bf16, hipStream_t s);
+hipError_t launch_stream_read(const void *p, int64_t bytes, uint32_t *out, int n_wg, hipStream_t s);
 hipError_t launch_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t *q_nope,
                              const uint16_t *w_uk, uint16_t *out, int64_t out_stride, hipStream_t s);
 hipError_t launch_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat,

@@ -70,6 +70,7 @@ _SIGS = {
     "wsk_views": ([_VP, _I32, ctypes.POINTER(wsk_view), ctypes.POINTER(wsk_view)], ctypes.c_int),
     "wsk_attend_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_attend": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
+    "wsk_stream_read": ([_VP, ctypes.c_size_t, _VP, _VP], ctypes.c_int),
     "wsk_attend_pass1": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_attend_pass2": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP],
                          ctypes.c_int),
@@ -245,3 +246,8 @@ def wsk_mla_expand(o_lat, w_uv, o, stream=None):
     n, H, dl = o_lat.shape
     dv = w_uv.shape[2]
     _check(lib().wsk_mla_expand(n, H, dl, dv, _ptr(o_lat), _ptr(w_uv), _ptr(o), _stream(stream)))
+
+
+def wsk_stream_read(buf, out, stream=None):
+    """Measurement aid: streams the device tensor buf once; XORs a fold into out (uint32 [1])."""
+    _check(lib().wsk_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(out), _stream(stream)))
