@@ -345,6 +345,57 @@ int wsk_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t 
 int wsk_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat,
                    const uint16_t *w_uv, float *o, void *stream);
 
+/* ---- roofline split policy (Sec. 5.2, Sec. 5.3) ------------------------- */
+
+/*
+ * Per-step latency model of the two engines (Sec. 5.2, Eq. 1):
+ *   T_cpu(r) = r A L + c_cpu,   T_gpu(r) = (1 - r) B L + c_gpu
+ * A, B: cost per KV token of the CPU and the GPU side (seconds, or any one
+ * unit); c_cpu, c_gpu: fixed per-step costs (same unit); r: CPU share of the
+ * L placed tokens.  Requires finite values, A, B, c >= 0 and A + B > 0.
+ */
+typedef struct wsk_roofline {
+    double A;
+    double B;
+    double c_cpu;
+    double c_gpu;
+} wsk_roofline;
+
+/*
+ * The CPU share that balances the two engines at length L >= 1 (Sec. 5.3,
+ * Eq. 2): r = clamp(B/(A+B) + (c_gpu - c_cpu)/((A+B) L), 0, 1).  It is the
+ * share a sequence of length L is opened with (s = floor(r L),
+ * wsk_seq_open).  Errors: EINVAL.
+ */
+int wsk_roofline_share(const wsk_roofline *model, int64_t L, double *r);
+
+/*
+ * Online policy (Sec. 5.3): keeps the model, re-estimates A from the measured
+ * CPU latency of recent steps, and routes decode eviction batches so that the
+ * running fraction of CPU-placed batches follows the marginal share
+ * p = B/(A+B); a sequence opened at share R0 and length L0 then holds
+ * R(L) = p + (R0 - p) L0 / L of its tokens on the CPU.
+ *   create   model0 with A > 0; window >= 1 steps for the A estimate.
+ *   observe  one step's CPU-side latency t_cpu (>= 0, the unit of the model)
+ *            and CPU token count n_cpu (>= 0).  A becomes
+ *            (sum t - w c_cpu) / sum n over the last w <= window steps; it
+ *            is kept when the window has no CPU tokens or the estimate is
+ *            not positive.  *A (may be NULL) receives the current A.
+ *   route_batch  destination of the next eviction batch: WSK_PART_CPU iff
+ *            that leaves the running CPU fraction strictly closer to p (with
+ *            c of k batches on the CPU: c + 1/2 < p (k + 1)), else
+ *            WSK_PART_GPU.
+ *   model    the current model (A estimated; B and the fixed costs as given).
+ * A policy is plain host state: not thread-safe, no GPU work.
+ * Errors: EINVAL, ENOMEM.
+ */
+typedef struct wsk_policy wsk_policy;
+int wsk_policy_create(const wsk_roofline *model0, int32_t window, wsk_policy **out);
+int wsk_policy_destroy(wsk_policy *policy);
+int wsk_policy_observe(wsk_policy *policy, double t_cpu, int64_t n_cpu, double *A);
+int wsk_policy_route_batch(wsk_policy *policy, int32_t *part);
+int wsk_policy_model(const wsk_policy *policy, wsk_roofline *model);
+
 /*
  * Measurement aid, not part of the decode path: reads `bytes` of DEVICE
  * memory at p once with the loads the attention kernels use (16 bytes per

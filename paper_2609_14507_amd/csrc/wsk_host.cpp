@@ -35,6 +35,13 @@ int fail(int code, const char *fmt, ...) {
     return code;
 }
 
+}  // namespace
+
+// Error reporting for the policy functions (policy.cpp).
+int wsk::policy_fail(int code, const char *msg) { return fail(code, "%s", msg); }
+
+namespace {
+
 int hip_fail(hipError_t e, const char *what) {
     return fail(WSK_EHIP, "%s: %s", what, hipGetErrorString(e));
 }

@@ -101,6 +101,9 @@ struct ScatterParams {
     int32_t row_elems;
 };
 
+// Sets the calling thread's last error message; returns code.
+int policy_fail(int code, const char *msg);
+
 hipError_t launch_gqa_attend(const AttendParams &p, int heads_per_wg, int n_wg, hipStream_t s);
 hipError_t launch_mla_attend(const AttendParams &p, int n_wg, hipStream_t s);
 hipError_t launch_combine(const CombineParams &p, int width, hipStream_t s);

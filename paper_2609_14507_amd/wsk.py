@@ -44,6 +44,11 @@ class wsk_loc(ctypes.Structure):
                 ("offset", ctypes.c_int32)]
 
 
+class wsk_roofline(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_double), ("B", ctypes.c_double), ("c_cpu", ctypes.c_double),
+                ("c_gpu", ctypes.c_double)]
+
+
 class wsk_view(ctypes.Structure):
     _fields_ = [("pool", ctypes.c_void_p), ("table", ctypes.POINTER(ctypes.c_int32)),
                 ("slot_bytes", ctypes.c_int64), ("head_bytes", ctypes.c_int64), ("v_bytes", ctypes.c_int64),
@@ -71,6 +76,13 @@ _SIGS = {
     "wsk_attend_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_attend": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_stream_read": ([_VP, ctypes.c_size_t, _VP, _VP], ctypes.c_int),
+    "wsk_roofline_share": ([ctypes.POINTER(wsk_roofline), ctypes.c_int64, ctypes.POINTER(ctypes.c_double)],
+                           ctypes.c_int),
+    "wsk_policy_create": ([ctypes.POINTER(wsk_roofline), _I32, ctypes.POINTER(_VP)], ctypes.c_int),
+    "wsk_policy_destroy": ([_VP], ctypes.c_int),
+    "wsk_policy_observe": ([_VP, ctypes.c_double, ctypes.c_int64, ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
+    "wsk_policy_route_batch": ([_VP, ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
+    "wsk_policy_model": ([_VP, ctypes.POINTER(wsk_roofline)], ctypes.c_int),
     "wsk_attend_pass1": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_attend_pass2": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP],
                          ctypes.c_int),
@@ -251,3 +263,39 @@ def wsk_mla_expand(o_lat, w_uv, o, stream=None):
 def wsk_stream_read(buf, out, stream=None):
     """Measurement aid: streams the device tensor buf once; XORs a fold into out (uint32 [1])."""
     _check(lib().wsk_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(out), _stream(stream)))
+
+
+def wsk_roofline_share(A: float, B: float, c_cpu: float, c_gpu: float, L: int) -> float:
+    """Eq. 2: the CPU share that balances the engines at length L."""
+    r = ctypes.c_double()
+    _check(lib().wsk_roofline_share(ctypes.byref(wsk_roofline(A, B, c_cpu, c_gpu)), L, ctypes.byref(r)))
+    return r.value
+
+
+class Policy:
+    """The online split policy (wsk_policy_*)."""
+
+    def __init__(self, A: float, B: float, c_cpu: float, c_gpu: float, window: int):
+        self.h = _VP()
+        _check(lib().wsk_policy_create(ctypes.byref(wsk_roofline(A, B, c_cpu, c_gpu)), window,
+                                       ctypes.byref(self.h)))
+
+    def observe(self, t_cpu: float, n_cpu: int) -> float:
+        a = ctypes.c_double()
+        _check(lib().wsk_policy_observe(self.h, t_cpu, n_cpu, ctypes.byref(a)))
+        return a.value
+
+    def route(self) -> int:
+        part = ctypes.c_int32()
+        _check(lib().wsk_policy_route_batch(self.h, ctypes.byref(part)))
+        return part.value
+
+    def model(self):
+        m = wsk_roofline()
+        _check(lib().wsk_policy_model(self.h, ctypes.byref(m)))
+        return m.A, m.B, m.c_cpu, m.c_gpu
+
+    def close(self):
+        if self.h:
+            lib().wsk_policy_destroy(self.h)
+            self.h = _VP()
