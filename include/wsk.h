@@ -345,6 +345,26 @@ int wsk_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const uint16_t 
 int wsk_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat,
                    const uint16_t *w_uv, float *o, void *stream);
 
+/*
+ * In-place CPU attention over the CPU partition (the CPU engine of Sec. 5.1;
+ * MLA: the latent variant of Sec. 6.1): for each i < n, every query head of
+ * seq_ids[i] attends positions [start[i], end[i]), which must lie in the CPU
+ * partition: 0 <= start <= end <= min(s, L).  Rows are read where they sit
+ * in the host pool, block by block through the CPU block table (Sec. 4.3
+ * (iii)); nothing is copied.  The result is the same normalised partial O
+ * and natural-log LSE as wsk_attend's (O = 0, LSE = -inf for an empty
+ * range), ready for the LSE merge with the GPU partial.
+ * seq_ids, start, end, q, o, lse: HOST arrays; q, o, lse laid out as for
+ * wsk_attend.  threads: host threads to use (<= 0: every hardware thread).
+ * fp32 arithmetic from bf16 rows.  Synchronous: returns when done.  It
+ * touches host memory only, so GPU work already enqueued keeps running
+ * meanwhile; it must not overlap calls that change the cache.  Works on
+ * host-only caches.  Errors: EINVAL, ESTATE, ERANGE.
+ */
+int wsk_cpu_attend(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
+                   const int32_t *start, const int32_t *end, const void *q,
+                   float *o, float *lse, int32_t threads);
+
 /* ---- roofline split policy (Sec. 5.2, Sec. 5.3) ------------------------- */
 
 /*

@@ -17,6 +17,8 @@
 #include <vector>
 
 #include "../../include/wsk.h"
+#include <thread>
+
 #include "wsk_internal.h"
 
 using namespace wsk;
@@ -766,6 +768,47 @@ int wsk_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_
     if (!aligned16(w_uv)) return fail(WSK_EINVAL, "w_uv must be 16-byte aligned");
     hipError_t e = launch_mla_expand(n, H, dl, dv, o_lat, w_uv, o, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "wsk_mla_expand");
+    return WSK_OK;
+}
+
+int wsk_cpu_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
+                   const void *q, float *o, float *lse, int32_t threads) {
+    if (!c) return fail(WSK_EINVAL, "cache is NULL");
+    if (n < 0) return fail(WSK_EINVAL, "n < 0");
+    if (n == 0) return WSK_OK;
+    if (!ids || !start || !end || !q || !o || !lse) return fail(WSK_EINVAL, "NULL argument");
+    std::vector<const int32_t *> tables(n);
+    for (int32_t i = 0; i < n; ++i) {
+        int rc = check_seq(c, ids[i]);
+        if (rc) return rc;
+        const int32_t s = std::min(c->split[ids[i]], c->length[ids[i]]);
+        if (!(0 <= start[i] && start[i] <= end[i] && end[i] <= s))
+            return fail(WSK_ERANGE, "range [%d, %d) of sequence %d outside its CPU partition [0, %d)", start[i], end[i],
+                        ids[i], s);
+        tables[i] = c->htab[WSK_PART_CPU].data() + (size_t)ids[i] * c->max_blocks;
+    }
+    const wsk_partition_spec &sp = c->spec;
+    const bool mla = sp.kind == WSK_KIND_MLA;
+    CpuAttendArgs x{};
+    x.pool = c->hpool;
+    x.tables = tables.data();
+    x.start = start;
+    x.end = end;
+    x.q = (const uint16_t *)q;
+    x.o = o;
+    x.lse = lse;
+    x.slot_elems = c->slot_elems;
+    x.n = n;
+    x.n_q_heads = sp.n_q_heads;
+    x.group = mla ? sp.n_q_heads : sp.n_q_heads / sp.n_kv_heads;
+    x.row_elems = c->row_elems;
+    x.dv = mla ? sp.latent_dim : sp.head_dim;
+    x.q_row = (int64_t)sp.n_q_heads * c->row_elems;
+    x.block_tokens = sp.block_tokens;
+    x.mla = mla;
+    x.scale_log2 = sp.softmax_scale * 1.4426950408889634f;
+    x.threads = threads > 0 ? threads : (int)std::max(1u, std::thread::hardware_concurrency());
+    cpu_attend(x);
     return WSK_OK;
 }
 

@@ -101,6 +101,24 @@ struct ScatterParams {
     int32_t row_elems;
 };
 
+// In-place CPU attention over host-pool rows (cpu_attend.cpp).
+struct CpuAttendArgs {
+    const uint16_t *pool;          // host pool base
+    const int32_t *const *tables;  // per sequence: its CPU block-table row
+    const int32_t *start, *end;    // per sequence: token range
+    const uint16_t *q;             // [n][n_q_heads][row_elems] bf16
+    float *o;                      // [n][n_q_heads][dv]
+    float *lse;                    // [n][n_q_heads]
+    int64_t slot_elems;
+    int64_t q_row;
+    int n, n_q_heads, group;       // group: query heads per KV head (MLA: n_q_heads)
+    int row_elems, dv, block_tokens;
+    bool mla;
+    float scale_log2;
+    int threads;
+};
+int cpu_attend(const CpuAttendArgs &args);
+
 // Sets the calling thread's last error message; returns code.
 int policy_fail(int code, const char *msg);
 

@@ -76,6 +76,7 @@ _SIGS = {
     "wsk_attend_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_attend": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_stream_read": ([_VP, ctypes.c_size_t, _VP, _VP], ctypes.c_int),
+    "wsk_cpu_attend": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _I32], ctypes.c_int),
     "wsk_roofline_share": ([ctypes.POINTER(wsk_roofline), ctypes.c_int64, ctypes.POINTER(ctypes.c_double)],
                            ctypes.c_int),
     "wsk_policy_create": ([ctypes.POINTER(wsk_roofline), _I32, ctypes.POINTER(_VP)], ctypes.c_int),
@@ -299,3 +300,14 @@ class Policy:
         if self.h:
             lib().wsk_policy_destroy(self.h)
             self.h = _VP()
+
+
+def wsk_cpu_attend(h: int, seq_ids, start, end, q, o, lse, threads: int = 0):
+    """CPU engine over the CPU partition.  q: numpy uint16 (bf16 bits) [n, H, row];
+    o: numpy float32 [n, H, dv]; lse: numpy float32 [n, H] (host arrays)."""
+    import numpy as np
+    for a, dt in ((q, np.uint16), (o, np.float32), (lse, np.float32)):
+        if a.dtype != dt or not a.flags["C_CONTIGUOUS"]:
+            raise ValueError("host arrays must be C-contiguous with the documented dtypes")
+    _check(lib().wsk_cpu_attend(h, len(seq_ids), _i32_array(seq_ids), _i32_array(start), _i32_array(end),
+                                q.ctypes.data, o.ctypes.data, lse.ctypes.data, threads))
