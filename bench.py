@@ -146,6 +146,88 @@ def roofline(w, kind, achieved_gbs, kv_bytes):
     return out
 
 
+def wsk_mod():
+    from paper_2609_14507_amd import wsk
+    return wsk
+
+
+def cpu_gpu_steps(w, sess, wsk, steps_in, i0, F, splits, qs, kn, vn, o_m, l_m, flush, dev, absorb, expand,
+                  gpu_ns_per_token, gpu_fixed_us):
+    """The paper's whole decode step on this machine: the GPU appends and runs pass 1
+    over [s_b, L_b + 1) while the native CPU engine (wsk_cpu_attend) attends
+    [0, s_b) in place in the host pool on every available core; the CPU partial
+    is copied to the device and pass 2 merges it with the GPU chunks.  Timed on
+    the host clock from the first launch to the end of pass 2.  Also fits the
+    roofline split policy (Eq. 2) to the measured per-token costs."""
+    import torch
+    B, H = sess.B, w.n_q_heads
+    D = sess.out_width
+    threads = len(os.sched_getaffinity(0))
+    ids = sess.ids
+    o_c = np.empty((B, H, D), np.float32)
+    l_c = np.empty((B, H), np.float32)
+    o_pin = torch.empty(B, H, D, pin_memory=True)
+    l_pin = torch.empty(B, H, pin_memory=True)
+    o_cd = torch.empty(B, H, D, device=dev)
+    l_cd = torch.empty(B, H, device=dev)
+    cpu_s, full_s, cpu_tok = [], [], []
+    for f in range(F):
+        i = i0 + f
+        ce = [min(splits[b], sess.lengths[b]) for b in range(B)]
+        flush.add_(1)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        if absorb:
+            absorb(i)
+        sess.append(kn[i], vn[i])
+        sess.attend_pass1(qs[i])                         # the GPU works from here on ...
+        t1 = time.perf_counter()
+        wsk.wsk_cpu_attend(sess.h, ids, [0] * B, ce, steps_in[i].q, o_c, l_c, threads)   # ... while the CPU does
+        t2 = time.perf_counter()
+        o_pin.numpy()[:] = o_c
+        l_pin.numpy()[:] = l_c
+        o_cd.copy_(o_pin, non_blocking=True)
+        l_cd.copy_(l_pin, non_blocking=True)
+        sess.attend_pass2(o=o_m, lse=l_m, o_x=o_cd, lse_x=l_cd)
+        if expand:
+            expand()
+        torch.cuda.synchronize()
+        t3 = time.perf_counter()
+        cpu_s.append(t2 - t1)
+        full_s.append(t3 - t0)
+        cpu_tok.append(sum(ce))
+    tok = float(np.mean(cpu_tok))
+    if tok == 0:
+        return None, {"ms": round(float(np.median(full_s)) * 1e3, 3), "cpu_ms": 0.0,
+                      "note": "no CPU range in this workload"}, None
+    # fixed cost of a CPU engine call: one 16-token range per sequence
+    small = []
+    for _ in range(5):
+        t = time.perf_counter()
+        wsk.wsk_cpu_attend(sess.h, ids, [0] * B, [min(16, c) for c in ce], steps_in[i0].q, o_c, l_c, threads)
+        small.append(time.perf_counter() - t)
+    c_cpu = min(small)
+    t_cpu = float(np.median(cpu_s))
+    A = max(t_cpu - c_cpu, 1e-12) / tok
+    Bc = gpu_ns_per_token * 1e-9
+    L = float(np.mean(sess.lengths))
+    r = wsk.wsk_roofline_share(A, Bc, c_cpu, gpu_fixed_us * 1e-6, int(L))
+    cpu_engine = {"value": round(tok * w.token_bytes / t_cpu / 1e9, 2), "unit": "GB/s", "cores": threads,
+                  "kind": "native (wsk_cpu_attend)",
+                  "sample": "the workload's CPU ranges [0, s_b) of %d sequences, %.0f tokens per call, median of %d"
+                            % (B, tok, F)}
+    full = {"ms": round(float(np.median(full_s)) * 1e3, 3), "cpu_ms": round(t_cpu * 1e3, 3),
+            "what": "append + GPU pass 1 over [s_b, L_b] while the CPU engine attends [0, s_b), then pass 2 "
+                    "merging both partials (the workload's split)"}
+    policy = {"A_ns_per_token": round(A * 1e9, 4), "B_ns_per_token": round(Bc * 1e9, 4),
+              "c_cpu_us": round(c_cpu * 1e6, 1), "c_gpu_us": round(gpu_fixed_us, 1), "L": int(L),
+              "balanced_cpu_share": round(r, 5),
+              "what": "Eq. 2 with A from the CPU engine and B from GPU pass 1 measured above"}
+    log("bench: CPU engine %.1f GB/s on %d cores; full CPU+GPU step %.2f ms; balanced CPU share %.4f"
+        % (cpu_engine["value"], threads, full["ms"], r))
+    return cpu_engine, full, policy
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -156,6 +238,8 @@ def main():
     ap.add_argument("--no-flush", action="store_true", help="skip the Infinity Cache flush between steps")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-engine", action="store_true",
+                    help="skip the native CPU engine and the full CPU + GPU steps")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, run a plain 256 MiB device copy three times (the reference "
                          "dispatch that scales HBM byte counters)")
@@ -182,9 +266,10 @@ def main():
     if args.share is not None:
         splits = [wl.split_point(args.share, L) for L in pf.lengths]
         pf = wl.Prefill(pf.lengths, splits, pf.k, pf.v, pf.gen)
-    steps_in = [wl.draw_step(w, pf.gen) for _ in range(W + 2 * K)]
+    F = 5                                    # full CPU + GPU steps after the GPU-only ones
+    steps_in = [wl.draw_step(w, pf.gen) for _ in range(W + 2 * K + F)]
     log("bench: routing the prefill into the cache")
-    sess = DecodeSession(w, pf, 0, extra_tokens=W + 2 * K)
+    sess = DecodeSession(w, pf, 0, extra_tokens=W + 2 * K + F)
     B, H = sess.B, w.n_q_heads
     D = sess.out_width                      # attend output width (MLA: the latent)
     qs = [to_device_bf16(s.q, dev) for s in steps_in]
@@ -265,6 +350,14 @@ def main():
         "expand %.1f us; pass 1 %.0f GB/s; wall %.1f ms/step"
         % (step_ms.mean() * 1e3, app_ms.mean() * 1e3, p1_ms.mean() * 1e3, p2_ms.mean() * 1e3, exp_ms.mean() * 1e3,
            p1_gbs, wall / K * 1e3))
+    cpu_engine, full_step, policy = None, None, None
+    if not args.no_cpu_engine:
+        cpu_engine, full_step, policy = cpu_gpu_steps(
+            w, sess, wsk_mod(), steps_in, W + 2 * K, F, splits, qs, kn, vn, o_m, l_m, flush, dev,
+            None,   # MLA: the drawn absorbed query feeds both engines (no absorb launch)
+            (lambda: wsk_mod().wsk_mla_expand(o_m, w_uv_d, o_out)) if mla else None,
+            gpu_ns_per_token=float(p1_ms.mean() * 1e6 / (d_bytes.mean() / w.token_bytes)),
+            gpu_fixed_us=float((step_ms.mean() - p1_ms.mean()) * 1e3))
     sess.close()
     # plain streaming read of 2 GiB with the attention kernels' load pattern:
     # the practical HBM read ceiling the pass-1 rate is compared with
@@ -339,6 +432,10 @@ def main():
                               "what": "wsk_stream_read: one plain read of 2 GiB with the attention kernels' "
                                       "loads, median of 5, cache flushed before each"},
     }
+    if cpu_engine is not None:
+        out["cpu_engine"] = cpu_engine
+        out["full_step"] = full_step
+        out["split_policy"] = policy
     if not args.no_cpu_baseline:
         log("bench: timing the oracle on the host (%.0f s budget)" % args.cpu_budget)
         out["cpu_baseline"] = cpu_baseline(w, pf, steps_in, args.cpu_budget)

@@ -8,10 +8,10 @@
 // Arithmetic: bf16 rows widened to fp32, fp32 dot products and accumulation,
 // an online softmax over tiles of 16 tokens (one rescale per tile).  Work is
 // cut into (sequence, KV head, chunk of at most kChunk tokens) items spread
-// over host threads; the chunk partials of a (sequence, head) are merged by
-// LSE at the end.  Vector code uses AVX-512 when the CPU has it (16 fp32 per
-// instruction); otherwise (or with WSK_CPU_ENGINE=plain) plain loops compute
-// the same quantities.
+// over a persistent pool of host threads; the chunk partials of a (sequence, head) are merged by
+// LSE at the end.  Vector code uses AVX-512 (with bf16 dot products where the
+// CPU has them); otherwise (or with WSK_CPU_ENGINE=plain / avx512) simpler
+// loops compute the same quantities.
 //
 // Fused multiply-add contraction is off for the scalar code, which therefore
 // follows the written order; the vector code uses explicit FMAs.
@@ -21,6 +21,10 @@
 
 #include <algorithm>
 #include <atomic>
+#include <condition_variable>
+#include <functional>
+#include <mutex>
+#include <memory>
 #include <cmath>
 #include <cstdlib>
 #include <string>
@@ -94,18 +98,21 @@ inline void scale_plain(float *acc, float a, int n) {
     for (int d = 0; d < n; ++d) acc[d] *= a;
 }
 
+enum class Path;
+
 struct Job {
     const CpuAttendArgs *x;
-    bool vec;
+    Path path;
     std::vector<Item> items;
     std::vector<Partial> parts;   // one per item
 };
 
-// Rows of token t of KV head g (K row, V row).
+// Rows of token t of KV head g (K row, V row); block_tokens is a power of two.
 inline void rows_of(const CpuAttendArgs &x, int i, int g, int t, const uint16_t *&k, const uint16_t *&v) {
-    const int32_t slot = x.tables[i][t / x.block_tokens];
+    const int bshift = __builtin_ctz((unsigned)x.block_tokens);
+    const int32_t slot = x.tables[i][t >> bshift];
     const uint16_t *base = x.pool + (int64_t)slot * x.slot_elems;
-    const int off = t % x.block_tokens;
+    const int off = t & (x.block_tokens - 1);
     if (x.mla) {
         k = base + (int64_t)off * x.row_elems;
         v = k;
@@ -162,23 +169,224 @@ void run_item(const CpuAttendArgs &x, const Item &it, Partial &pt, std::vector<f
     }
 }
 
-// The AVX-512 path where the CPU has it, unless WSK_CPU_ENGINE=plain asks for
-// the plain loops (which the tests also check on AVX-512 machines).
-bool use_avx512() {
-    static const bool ok = [] {
-        const char *e = getenv("WSK_CPU_ENGINE");
-        if (e && std::string(e) == "plain") return false;
-        return __builtin_cpu_supports("avx512f") && __builtin_cpu_supports("avx512bw");
-    }();
-    return ok;
+// ---- AVX-512 with bf16 dot products ----------------------------------------
+// A 16-token tile of K is transposed once into dim pairs x tokens, so that
+// vdpbf16ps accumulates the 16 tokens' scores of one head in the 16 lanes of
+// one register (products of bf16 values are exact in fp32; sums are fp32).
+// exp2 over the 16 scores is vectorised: x = n + f with n the nearest integer
+// and |f| <= 1/2, 2^f = e^(f ln 2) from the Taylor series of e^y to the y^7
+// term (remainder below 6e-9 relative for |y| <= ln(2)/2), scaled by 2^n.
+// P.V keeps the accumulators of all heads for a block of columns in
+// registers while the tile's V rows stream through.
+constexpr int kMaxPairs = 288;   // 576 / 2
+
+struct ScratchBf16 {
+    alignas(64) uint32_t kt[kMaxPairs][16];   // K tile, dim pair j of token t at kt[j][t]
+    alignas(64) float p[16][16];              // probabilities [head][token] (up to 16 heads)
+    float alpha[16];
+};
+
+__attribute__((target("avx512f,avx512bw,avx512bf16"))) inline __m512 exp2v(__m512 x) {
+    x = _mm512_max_ps(x, _mm512_set1_ps(-150.f));              // 2^-150 is 0 in fp32; -inf -> 0
+    const __m512 n = _mm512_roundscale_ps(x, _MM_FROUND_TO_NEAREST_INT | _MM_FROUND_NO_EXC);
+    const __m512 y = _mm512_mul_ps(_mm512_sub_ps(x, n), _mm512_set1_ps(0.69314718055994530942f));
+    // 1 + y (1 + y/2 (1 + y/3 (1 + y/4 (1 + y/5 (1 + y/6 (1 + y/7))))))
+    __m512 r = _mm512_fmadd_ps(y, _mm512_set1_ps(1.f / 7.f), _mm512_set1_ps(1.f));
+    r = _mm512_fmadd_ps(_mm512_mul_ps(y, _mm512_set1_ps(1.f / 6.f)), r, _mm512_set1_ps(1.f));
+    r = _mm512_fmadd_ps(_mm512_mul_ps(y, _mm512_set1_ps(1.f / 5.f)), r, _mm512_set1_ps(1.f));
+    r = _mm512_fmadd_ps(_mm512_mul_ps(y, _mm512_set1_ps(1.f / 4.f)), r, _mm512_set1_ps(1.f));
+    r = _mm512_fmadd_ps(_mm512_mul_ps(y, _mm512_set1_ps(1.f / 3.f)), r, _mm512_set1_ps(1.f));
+    r = _mm512_fmadd_ps(_mm512_mul_ps(y, _mm512_set1_ps(0.5f)), r, _mm512_set1_ps(1.f));
+    r = _mm512_fmadd_ps(y, r, _mm512_set1_ps(1.f));
+    return _mm512_scalef_ps(r, n);
 }
+
+// 16 x 16 transpose of 32-bit elements: out[j] holds element j of every in[t]
+__attribute__((target("avx512f,avx512bw,avx512bf16"))) inline void transpose16(__m512i (&r)[16]) {
+    __m512i t[16];
+    for (int i = 0; i < 16; i += 2) {
+        t[i] = _mm512_unpacklo_epi32(r[i], r[i + 1]);
+        t[i + 1] = _mm512_unpackhi_epi32(r[i], r[i + 1]);
+    }
+    for (int i = 0; i < 16; i += 4) {
+        r[i] = _mm512_unpacklo_epi64(t[i], t[i + 2]);
+        r[i + 1] = _mm512_unpackhi_epi64(t[i], t[i + 2]);
+        r[i + 2] = _mm512_unpacklo_epi64(t[i + 1], t[i + 3]);
+        r[i + 3] = _mm512_unpackhi_epi64(t[i + 1], t[i + 3]);
+    }
+    // each 128-bit lane q of r[4b + c] now holds element 4q' + ... : finish with 128-bit shuffles
+    for (int i = 0; i < 4; ++i) {
+        t[i] = _mm512_shuffle_i32x4(r[i], r[i + 4], 0x88);
+        t[i + 4] = _mm512_shuffle_i32x4(r[i], r[i + 4], 0xdd);
+        t[i + 8] = _mm512_shuffle_i32x4(r[i + 8], r[i + 12], 0x88);
+        t[i + 12] = _mm512_shuffle_i32x4(r[i + 8], r[i + 12], 0xdd);
+    }
+    for (int i = 0; i < 4; ++i) {
+        r[i] = _mm512_shuffle_i32x4(t[i], t[i + 8], 0x88);
+        r[i + 8] = _mm512_shuffle_i32x4(t[i], t[i + 8], 0xdd);
+        r[i + 4] = _mm512_shuffle_i32x4(t[i + 4], t[i + 12], 0x88);
+        r[i + 12] = _mm512_shuffle_i32x4(t[i + 4], t[i + 12], 0xdd);
+    }
+}
+
+template <int G>
+__attribute__((target("avx512f,avx512bw,avx512bf16"))) void run_item_bf16(const CpuAttendArgs &x, const Item &it,
+                                                                          Partial &pt, std::vector<float> &qf,
+                                                                          ScratchBf16 &sc) {
+    const int dk = x.row_elems, dv = x.dv, npair = dk / 2;
+    const int h0 = it.g * G;
+    static const uint16_t zero_row[576] = {};
+    // query pairs as raw bf16 bits (qf holds them as 32-bit words)
+    qf.resize((size_t)G * npair);
+    uint32_t *qp = reinterpret_cast<uint32_t *>(qf.data());
+    for (int h = 0; h < G; ++h)
+        __builtin_memcpy(qp + (size_t)h * npair, x.q + (int64_t)it.i * x.q_row + (int64_t)(h0 + h) * dk, dk * 2);
+    pt.m.assign(G, -INFINITY);
+    pt.l.assign(G, 0.f);
+    pt.acc.assign((size_t)G * dv, 0.f);
+    const uint16_t *krow[16], *vrow[16];
+    const __m512 scale = _mm512_set1_ps(x.scale_log2);
+    for (int t0 = it.a; t0 < it.b; t0 += 16) {
+        const int nt = std::min(16, it.b - t0);
+        for (int t = 0; t < 16; ++t) {
+            if (t < nt)
+                rows_of(x, it.i, it.g, t0 + t, krow[t], vrow[t]);
+            else
+                krow[t] = vrow[t] = zero_row;
+        }
+        // K tile -> dim pairs x tokens
+        for (int jb = 0; jb < npair; jb += 16) {
+            __m512i r[16];
+            for (int t = 0; t < 16; ++t) r[t] = _mm512_loadu_si512((const void *)(krow[t] + 2 * jb));
+            transpose16(r);
+            for (int j = 0; j < 16; ++j) _mm512_store_si512((void *)sc.kt[jb + j], r[j]);
+        }
+        const __mmask16 valid = (__mmask16)((1u << nt) - 1u);
+        bool rescale = false;
+        // scores of all G heads at once: one K pair row feeds G independent chains
+        __m512 sacc[G];
+        for (int h = 0; h < G; ++h) sacc[h] = _mm512_setzero_ps();
+        for (int j = 0; j < npair; ++j) {
+            const __m512bh kv = (__m512bh)_mm512_load_si512((const void *)sc.kt[j]);
+            for (int h = 0; h < G; ++h)
+                sacc[h] = _mm512_dpbf16_ps(sacc[h], kv, (__m512bh)_mm512_set1_epi32((int)qp[(size_t)h * npair + j]));
+        }
+        for (int h = 0; h < G; ++h) {
+            __m512 sv = _mm512_mul_ps(sacc[h], scale);
+            sv = _mm512_mask_blend_ps(valid, _mm512_set1_ps(-INFINITY), sv);
+            const float mt = _mm512_reduce_max_ps(sv);
+            const float m_new = std::max(pt.m[h], mt);
+            const float alpha = std::exp2(pt.m[h] - m_new);   // 0 for the first tile
+            sc.alpha[h] = alpha;
+            rescale |= alpha != 1.f;
+            const __m512 pv = exp2v(_mm512_sub_ps(sv, _mm512_set1_ps(m_new)));
+            pt.l[h] = pt.l[h] * alpha + _mm512_reduce_add_ps(pv);
+            pt.m[h] = m_new;
+            _mm512_storeu_ps(sc.p[h], pv);
+        }
+        // O[h][cols] = alpha_h O[h][cols] + sum_t p[h][t] v_t[cols], columns in blocks of 16 x (16 / G)
+        constexpr int cb = G <= 8 ? 32 : 16;   // columns per block: registers hold G x cb / 16 accumulators
+        for (int c0 = 0; c0 < dv; c0 += cb) {
+            __m512 acc[G][cb / 16];
+            for (int h = 0; h < G; ++h)
+                for (int u = 0; u < cb / 16; ++u) {
+                    acc[h][u] = _mm512_loadu_ps(&pt.acc[(size_t)h * dv + c0 + 16 * u]);
+                    if (rescale) acc[h][u] = _mm512_mul_ps(acc[h][u], _mm512_set1_ps(sc.alpha[h]));
+                }
+            for (int t = 0; t < nt; ++t)
+                for (int u = 0; u < cb / 16; ++u) {
+                    const __m512 v = load_bf16x16(vrow[t] + c0 + 16 * u);
+                    for (int h = 0; h < G; ++h) acc[h][u] = _mm512_fmadd_ps(_mm512_set1_ps(sc.p[h][t]), v, acc[h][u]);
+                }
+            for (int h = 0; h < G; ++h)
+                for (int u = 0; u < cb / 16; ++u) _mm512_storeu_ps(&pt.acc[(size_t)h * dv + c0 + 16 * u], acc[h][u]);
+        }
+    }
+}
+
+enum class Path { Plain, Avx512, Avx512Bf16 };
+
+// The fastest path the CPU has; WSK_CPU_ENGINE=plain or =avx512 asks for a
+// slower one (the tests check every path on a CPU that has them all).
+Path cpu_path() {
+    static const Path path = [] {
+        const char *e = getenv("WSK_CPU_ENGINE");
+        const bool f = __builtin_cpu_supports("avx512f") && __builtin_cpu_supports("avx512bw");
+        const bool bf = f && __builtin_cpu_supports("avx512bf16");
+        if (e && std::string(e) == "plain") return Path::Plain;
+        if (e && std::string(e) == "avx512") return f ? Path::Avx512 : Path::Plain;
+        return bf ? Path::Avx512Bf16 : f ? Path::Avx512 : Path::Plain;
+    }();
+    return path;
+}
+
+// Persistent host workers: a call wakes as many as it needs and works
+// alongside them, so a call costs no thread creation.  Calls are serialised.
+// The pool lives until the process ends (its threads block on a condition
+// variable when idle).
+class WorkerPool {
+public:
+    static WorkerPool &get() {
+        static WorkerPool *pool = new WorkerPool;   // never destroyed: idle threads end with the process
+        return *pool;
+    }
+    // runs f on the calling thread and on n_extra pool threads; returns when all are done
+    void run(int n_extra, const std::function<void()> &f) {
+        std::lock_guard<std::mutex> call(call_mu_);
+        std::unique_lock<std::mutex> lk(mu_);
+        try {
+            while ((int)workers_.size() < n_extra) {
+                const int idx = (int)workers_.size();
+                workers_.emplace_back([this, idx] { loop(idx); });
+            }
+        } catch (...) {
+            n_extra = (int)workers_.size();   // fewer threads: the rest of the work is shared by those
+        }
+        job_ = &f;
+        want_ = n_extra;
+        running_ = n_extra;
+        ++epoch_;
+        lk.unlock();
+        wake_.notify_all();
+        f();
+        lk.lock();
+        finished_.wait(lk, [&] { return running_ == 0; });
+        job_ = nullptr;
+    }
+
+private:
+    void loop(int idx) {
+        uint64_t seen = 0;
+        std::unique_lock<std::mutex> lk(mu_);
+        for (;;) {
+            wake_.wait(lk, [&] { return epoch_ != seen; });
+            seen = epoch_;
+            if (idx >= want_) continue;
+            const std::function<void()> *f = job_;
+            lk.unlock();
+            (*f)();
+            lk.lock();
+            if (--running_ == 0) finished_.notify_all();
+        }
+    }
+    std::mutex call_mu_, mu_;
+    std::condition_variable wake_, finished_;
+    std::vector<std::thread> workers_;
+    const std::function<void()> *job_ = nullptr;
+    uint64_t epoch_ = 0;
+    int want_ = 0, running_ = 0;
+};
 
 }  // namespace
 
 int cpu_attend(const CpuAttendArgs &x) {
     Job job;
     job.x = &x;
-    job.vec = use_avx512() && x.row_elems % 16 == 0 && x.dv % 16 == 0;
+    const Path path = cpu_path();
+    const bool shapes16 = x.row_elems % 32 == 0 && x.dv % 32 == 0 && x.row_elems <= 2 * kMaxPairs &&
+                          (x.group == 1 || x.group == 2 || x.group == 4 || x.group == 8 || x.group == 16);
+    job.path = path == Path::Avx512Bf16 && !shapes16 ? Path::Avx512 : path;
+    if (job.path == Path::Avx512 && (x.row_elems % 16 || x.dv % 16)) job.path = Path::Plain;
     const int hkv = x.mla ? 1 : x.n_q_heads / x.group;
     for (int i = 0; i < x.n; ++i)
         for (int g = 0; g < hkv; ++g)
@@ -187,24 +395,27 @@ int cpu_attend(const CpuAttendArgs &x) {
     std::atomic<size_t> next{0};
     auto worker = [&]() {
         std::vector<float> qf;
+        std::unique_ptr<ScratchBf16> sc(job.path == Path::Avx512Bf16 ? new ScratchBf16 : nullptr);
         for (;;) {
             const size_t k = next.fetch_add(1);
             if (k >= job.items.size()) break;
-            if (job.vec)
+            if (job.path == Path::Avx512Bf16) {
+                switch (x.group) {
+                    case 1: run_item_bf16<1>(x, job.items[k], job.parts[k], qf, *sc); break;
+                    case 2: run_item_bf16<2>(x, job.items[k], job.parts[k], qf, *sc); break;
+                    case 4: run_item_bf16<4>(x, job.items[k], job.parts[k], qf, *sc); break;
+                    case 8: run_item_bf16<8>(x, job.items[k], job.parts[k], qf, *sc); break;
+                    default: run_item_bf16<16>(x, job.items[k], job.parts[k], qf, *sc); break;
+                }
+            }
+            else if (job.path == Path::Avx512)
                 run_item<true>(x, job.items[k], job.parts[k], qf);
             else
                 run_item<false>(x, job.items[k], job.parts[k], qf);
         }
     };
     const int nth = std::max(1, std::min<int>(x.threads, (int)job.items.size()));
-    std::vector<std::thread> pool;
-    try {
-        for (int t = 1; t < nth; ++t) pool.emplace_back(worker);
-    } catch (...) {
-        // fewer threads than asked: the ones that started and this one finish the work
-    }
-    worker();
-    for (auto &th : pool) th.join();
+    WorkerPool::get().run(nth - 1, worker);
 
     // merge the chunk partials of every (sequence, head), in chunk order
     const int H = x.n_q_heads, G = x.group, dv = x.dv;

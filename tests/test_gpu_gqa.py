@@ -177,9 +177,10 @@ def _small(Hq, Hkv, lengths, splits, seed, bk=64, std=1.0):
 
 
 @pytest.mark.parametrize("Hq,Hkv,bk", [(8, 2, 64), (32, 4, 64), (4, 4, 64), (32, 2, 128), (24, 4, 256),
-                                        (6, 2, 64)])
+                                        (6, 2, 64), (64, 1, 64), (48, 4, 128)])
 def test_ranges_and_group_sizes(Hq, Hkv, bk):
-    """Unaligned, single-token, single-tile, empty and tail ranges; G = 1, 3, 4, 6, 8, 16."""
+    """Unaligned, single-token, single-tile, empty and tail ranges; G = 1, 3, 4, 6, 8, 12, 16, 64
+    (G = 12 and 64: several query-head groups per KV head)."""
     lengths = [1000, 700, 130, 64, 5000, 1]
     splits = [0, 333, 65, 64, 1234, 0]
     w, pf = _small(Hq, Hkv, lengths, splits, seed=Hq * 7 + bk)
@@ -421,3 +422,36 @@ def test_two_passes_equal_attend(kind):
         sess.attend_pass1(q, start=[pf.lengths[b] for b in range(w.batch)])
         o5, l5 = sess.attend_pass2(start=[pf.lengths[b] for b in range(w.batch)], o_x=o_x, lse_x=l_x)
         assert torch.equal(o5, o_x) and torch.equal(l5, l_x)
+
+
+@pytest.mark.parametrize("kind", ["gqa", "mla"])
+def test_cpu_engine_and_gpu_merge_to_the_whole_context(kind):
+    """The method's whole step: the native CPU engine attends [0, s) in place in
+    the host pool, the GPU attends [s, L), pass 2 merges both: the result is
+    attention over the whole context (fp64 oracle)."""
+    if kind == "gqa":
+        w = wl.Workload("split-gqa", wl.GQA, batch=3, n_q_heads=16, n_kv_heads=2, head_dim=128, context=6000,
+                        cpu_share=0.4, seed=41)
+    else:
+        w = wl.Workload("split-mla", wl.MLA, batch=2, n_q_heads=16, n_kv_heads=1, head_dim=128, latent_dim=512,
+                        rope_dim=64, nope_dim=128, context=4000, cpu_share=0.4, kv_std=0.5, seed=42)
+    say("case cpu+gpu merge", kind)
+    pf = wl.make_prefill(w)
+    st = wl.draw_step(w, pf.gen)
+    dev = torch.device("cuda", DEV)
+    dv = w.latent_dim if kind == "mla" else w.head_dim
+    with DecodeSession(w, pf, DEV, extra_tokens=0) as sess:
+        B, H = sess.B, w.n_q_heads
+        q = to_device_bf16(st.q, dev)
+        sess.attend_pass1(q)
+        o_c = np.empty((B, H, dv), np.float32)
+        l_c = np.empty((B, H), np.float32)
+        wsk.wsk_cpu_attend(sess.h, sess.ids, [0] * B, [pf.splits[b] for b in range(B)], st.q, o_c, l_c, 4)
+        o_m, l_m = sess.attend_pass2(o_x=torch.from_numpy(o_c).to(dev), lse_x=torch.from_numpy(l_c).to(dev))
+        o_m, l_m = o_m.cpu().numpy(), l_m.cpu().numpy()
+    g = w.n_q_heads if kind == "mla" else w.group
+    for b in range(B):
+        v = None if kind == "mla" else pf.v[b]
+        o_r, l_r = oracle.attend(st.q[b], pf.k[b], v, 0, pf.lengths[b], w.softmax_scale, g, dv=dv)
+        assert_close(o_m[b], o_r, "cpu+gpu %s b%d" % (kind, b))
+        assert_lse(l_m[b], l_r, "cpu+gpu %s b%d" % (kind, b))
