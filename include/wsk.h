@@ -346,6 +346,30 @@ int wsk_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_
                    const uint16_t *w_uv, float *o, void *stream);
 
 /*
+ * Block-sparse decode attention over the GPU partition (Sec. 4.4): a
+ * block-level selection (e.g. a top-k over blocks computed by the model)
+ * yields whole blocks, and each query head of seq_ids[i] attends only the
+ * positions of its selected logical blocks
+ *   sel[sel_begin[i] .. sel_begin[i+1])      (sel_begin: n + 1 entries, [0] = 0)
+ * that lie in the GPU partition [s, L) (the block holding s contributes its
+ * positions >= s, the block holding L - 1 those < L).  Blocks must be
+ * distinct GPU blocks of the sequence, in any order; none selected gives
+ * O = 0, LSE = -inf.  The selected blocks are read in place, through a
+ * compacted copy of their table entries kept in ws: nothing is gathered.
+ * o_x, lse_x: optional partial to merge in, as for wsk_attend_pass2.
+ * All of seq_ids, sel_begin, sel are HOST arrays; q, o_x, lse_x, o, lse, ws
+ * DEVICE pointers laid out as for wsk_attend; ws of at least
+ * wsk_attend_blocks_workspace() bytes.  Errors: EINVAL (malformed or
+ * repeated selection), ERANGE (block outside the GPU partition), ESTATE, EHIP.
+ */
+int wsk_attend_blocks_workspace(const wsk_cache *cache, int32_t n, const int32_t *seq_ids,
+                                const int32_t *sel_begin, const int32_t *sel, size_t *bytes);
+int wsk_attend_blocks(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
+                      const int32_t *sel_begin, const int32_t *sel, const void *q,
+                      const float *o_x, const float *lse_x, float *o, float *lse,
+                      void *ws, size_t ws_bytes, void *stream);
+
+/*
  * In-place CPU attention over the CPU partition (the CPU engine of Sec. 5.1;
  * MLA: the latent variant of Sec. 6.1): for each i < n, every query head of
  * seq_ids[i] attends positions [start[i], end[i]), which must lie in the CPU

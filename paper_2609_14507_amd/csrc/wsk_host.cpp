@@ -82,6 +82,9 @@ struct wsk_cache {
     uint16_t *dpool = nullptr;    // GPU partition pool (HBM)
     int32_t *dtab = nullptr;      // device copy of the GPU block table
     uint16_t *dstage = nullptr;   // device staging for wsk_write
+    int32_t *hsel = nullptr;      // pinned host staging of block-selection tables
+    size_t hsel_bytes = 0;
+    hipEvent_t hsel_ev = nullptr; // marks the end of the last selection-table upload
     std::vector<int32_t> htab[2]; // host block tables [part][seq * max_blocks + k]
     std::vector<uint8_t> is_open;
     std::vector<int32_t> split, length;
@@ -206,11 +209,12 @@ struct AttendPlan {
 
 int64_t n_tiles(int32_t a, int32_t e) { return e > a ? (int64_t)((e - 1) / kTile - a / kTile + 1) : 0; }
 
+void plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const int32_t *end, AttendPlan &pl);
+
 int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
               AttendPlan &pl) {
     if (n < 0) return fail(WSK_EINVAL, "n < 0");
     if (n > 0 && (!ids || !start || !end)) return fail(WSK_EINVAL, "seq_ids/start/end must not be NULL");
-    int64_t total_tiles = 0;
     for (int32_t i = 0; i < n; ++i) {
         int rc = check_seq(c, ids[i]);
         if (rc) return rc;
@@ -218,8 +222,16 @@ int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *
         if (!(s <= start[i] && start[i] <= end[i] && end[i] <= L))
             return fail(WSK_ERANGE, "range [%d, %d) of sequence %d outside its GPU partition [%d, %d)", start[i],
                         end[i], ids[i], s, L);
-        total_tiles += n_tiles(start[i], end[i]);
     }
+    plan_chunks(c, n, start, end, pl);
+    return WSK_OK;
+}
+
+// Chunking of valid ranges (positions on the tile grid of the table the
+// kernels will read: the cache's, or a compacted one for block selections).
+void plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const int32_t *end, AttendPlan &pl) {
+    int64_t total_tiles = 0;
+    for (int32_t i = 0; i < n; ++i) total_tiles += n_tiles(start[i], end[i]);
     const wsk_partition_spec &sp = c->spec;
     int units = 1;
     if (sp.kind == WSK_KIND_GQA) {
@@ -251,6 +263,65 @@ int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *
     const int width = sp.kind == WSK_KIND_GQA ? kHeadDim : kLatent;
     pl.part_o_bytes = ((size_t)pl.partials * sp.n_q_heads * width * sizeof(float) + 255) / 256 * 256;
     pl.bytes = pl.part_o_bytes + ((size_t)pl.partials * sp.n_q_heads * sizeof(float) + 255) / 256 * 256;
+}
+
+// A block selection laid out for the kernels (Sec. 4.4): per sequence, the
+// device slots of its selected GPU blocks in a compacted table row, and the
+// virtual range [vstart, vend) over that row.  The block holding s (which may
+// start inside the block) goes first and the block holding L - 1 (which may
+// end inside it) last, so every other selected block is whole.
+struct Selection {
+    std::vector<int32_t> vstart, vend;
+    std::vector<int32_t> tab;   // n x width slots
+    int32_t width = 1;
+};
+
+int make_selection(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin,
+                   const int32_t *sel, Selection &out) {
+    if (n < 0) return fail(WSK_EINVAL, "n < 0");
+    if (n > 0 && (!ids || !sel_begin)) return fail(WSK_EINVAL, "seq_ids/sel_begin must not be NULL");
+    if (n > 0 && sel_begin[0] != 0) return fail(WSK_EINVAL, "sel_begin[0] must be 0");
+    const int bk = c->spec.block_tokens;
+    out.vstart.assign(n, 0);
+    out.vend.assign(n, 0);
+    out.width = 1;
+    for (int32_t i = 0; i < n; ++i) {
+        int rc = check_seq(c, ids[i]);
+        if (rc) return rc;
+        const int32_t k = sel_begin[i + 1] - sel_begin[i];
+        if (k < 0) return fail(WSK_EINVAL, "sel_begin must not decrease");
+        if (k > 0 && !sel) return fail(WSK_EINVAL, "sel must not be NULL");
+        out.width = std::max(out.width, k);
+    }
+    out.tab.assign((size_t)n * out.width, 0);
+    std::vector<uint8_t> seen;
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t sq = ids[i], L = c->length[sq], s = std::min(c->split[sq], L);
+        const int32_t k = sel_begin[i + 1] - sel_begin[i];
+        if (k == 0) continue;
+        const int32_t first = s / bk, last = (L - 1) / bk;   // GPU blocks [first, last]
+        seen.assign(c->max_blocks, 0);
+        bool has_first = false, has_last = false;
+        std::vector<int32_t> mid;
+        for (int32_t j = 0; j < k; ++j) {
+            const int32_t b = sel[sel_begin[i] + j];
+            if (L == s || b < first || b > last)
+                return fail(WSK_ERANGE, "block %d of sequence %d is not in its GPU partition", b, sq);
+            if (seen[b]) return fail(WSK_EINVAL, "block %d of sequence %d selected twice", b, sq);
+            seen[b] = 1;
+            if (b == first) has_first = true;
+            if (b == last) has_last = true;
+            if (b != first && b != last) mid.push_back(b);
+        }
+        std::vector<int32_t> order;
+        if (has_first) order.push_back(first);
+        order.insert(order.end(), mid.begin(), mid.end());
+        if (has_last && last != first) order.push_back(last);
+        for (size_t j = 0; j < order.size(); ++j)
+            out.tab[(size_t)i * out.width + j] = c->htab[WSK_PART_GPU][(size_t)sq * c->max_blocks + order[j]];
+        out.vstart[i] = has_first ? s - first * bk : 0;
+        out.vend[i] = (int32_t)(order.size() - 1) * bk + (has_last ? L - last * bk : bk);
+    }
     return WSK_OK;
 }
 
@@ -338,6 +409,9 @@ int wsk_destroy(wsk_cache *c) {
         if (c->dpool) (void)hipFree(c->dpool);
         if (c->dtab) (void)hipFree(c->dtab);
         if (c->dstage) (void)hipFree(c->dstage);
+        if (c->hsel_ev) (void)hipEventSynchronize(c->hsel_ev);
+        if (c->hsel) (void)hipHostFree(c->hsel);
+        if (c->hsel_ev) (void)hipEventDestroy(c->hsel_ev);
     }
     free(c->hpool);
     delete c;
@@ -628,13 +702,24 @@ namespace {
 
 // wsk_attend and its two passes: pass 1 writes the chunk partials into ws,
 // pass 2 merges them into o / lse.
+// Bytes of the compacted selection table placed after the partials in ws.
+size_t selection_table_bytes(const Selection &sl) { return (sl.tab.size() * sizeof(int32_t) + 255) / 256 * 256; }
+
 int attend_passes(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
                   const void *q, float *o, float *lse, void *ws, size_t ws_bytes, void *stream, bool pass1,
-                  bool pass2, const float *o_x = nullptr, const float *lse_x = nullptr) {
+                  bool pass2, const float *o_x = nullptr, const float *lse_x = nullptr,
+                  const Selection *sel = nullptr) {
     if (!c) return fail(WSK_EINVAL, "cache is NULL");
     AttendPlan pl;
-    int rc = make_plan(c, n, ids, start, end, pl);
-    if (rc) return rc;
+    if (sel) {
+        start = sel->vstart.data();
+        end = sel->vend.data();
+        plan_chunks(c, n, start, end, pl);
+        pl.bytes += selection_table_bytes(*sel);
+    } else {
+        int rc = make_plan(c, n, ids, start, end, pl);
+        if (rc) return rc;
+    }
     if (n == 0) return WSK_OK;
     if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
     if (pass1 && !q) return fail(WSK_EINVAL, "q must not be NULL");
@@ -654,19 +739,41 @@ int attend_passes(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *st
     float *part_o = (float *)ws;
     float *part_lse = (float *)((char *)ws + pl.part_o_bytes);
     hipError_t e = hipSuccess;
+    int32_t *sel_tab = nullptr;
+    if (sel) {   // the compacted table rows, after the partials
+        sel_tab = (int32_t *)((char *)ws + pl.bytes - selection_table_bytes(*sel));
+        if (pass1) {
+            if (!c->hsel_ev) e = hipEventCreateWithFlags(&c->hsel_ev, hipEventDisableTiming);
+            if (e == hipSuccess) e = hipEventSynchronize(c->hsel_ev);   // the previous upload has left the buffer
+            const size_t bytes = sel->tab.size() * sizeof(int32_t);
+            if (e == hipSuccess && c->hsel_bytes < bytes) {
+                if (c->hsel) (void)hipHostFree(c->hsel);
+                c->hsel = nullptr;
+                c->hsel_bytes = 0;
+                e = hipHostMalloc((void **)&c->hsel, bytes, hipHostMallocDefault);
+                if (e == hipSuccess) c->hsel_bytes = bytes;
+            }
+            if (e == hipSuccess) {
+                memcpy(c->hsel, sel->tab.data(), bytes);
+                e = hipMemcpyAsync(sel_tab, c->hsel, bytes, hipMemcpyHostToDevice, st);
+            }
+            if (e == hipSuccess) e = hipEventRecord(c->hsel_ev, st);
+            if (e != hipSuccess) return hip_fail(e, "selection table upload");
+        }
+    }
     int64_t part_base = 0;
     for (int32_t i0 = 0; i0 < n && e == hipSuccess; i0 += kMaxLaunchSeqs) {
         const int32_t m = std::min(kMaxLaunchSeqs, n - i0);
         AttendParams ap{};
         CombineParams cp{};
         ap.pool = c->dpool;
-        ap.table = c->dtab;
+        ap.table = sel ? sel_tab : c->dtab;
         ap.q = (const uint16_t *)q + (int64_t)i0 * sp.n_q_heads * qw;
         ap.part_o = part_o + part_base * sp.n_q_heads * width;
         ap.part_lse = part_lse + part_base * sp.n_q_heads;
         ap.slot_elems = c->slot_elems;
         ap.q_row = (int64_t)sp.n_q_heads * qw;
-        ap.table_stride = c->max_blocks;
+        ap.table_stride = sel ? sel->width : c->max_blocks;
         ap.n_q_heads = sp.n_q_heads;
         ap.n_kv_heads = gqa ? sp.n_kv_heads : 1;
         ap.group = sp.n_q_heads / ap.n_kv_heads;
@@ -678,7 +785,7 @@ int attend_passes(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *st
         ap.wg_begin[0] = 0;
         ap.chunk_begin[0] = 0;
         for (int32_t r = 0; r < m; ++r) {
-            ap.seq[r] = ids[i0 + r];
+            ap.seq[r] = sel ? i0 + r : ids[i0 + r];   // row of the table the kernels read
             ap.start[r] = start[i0 + r];
             ap.end[r] = end[i0 + r];
             ap.tpc[r] = pl.tpc[i0 + r];
@@ -722,6 +829,28 @@ extern "C" {
 int wsk_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
                const void *q, float *o, float *lse, void *ws, size_t ws_bytes, void *stream) {
     return attend_passes(c, n, ids, start, end, q, o, lse, ws, ws_bytes, stream, true, true);
+}
+
+int wsk_attend_blocks_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin,
+                                 const int32_t *sel, size_t *bytes) {
+    if (!c || !bytes) return fail(WSK_EINVAL, "NULL argument");
+    Selection sl;
+    int rc = make_selection(c, n, ids, sel_begin, sel, sl);
+    if (rc) return rc;
+    AttendPlan pl;
+    plan_chunks(c, n, sl.vstart.data(), sl.vend.data(), pl);
+    *bytes = pl.bytes + selection_table_bytes(sl);
+    return WSK_OK;
+}
+
+int wsk_attend_blocks(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin, const int32_t *sel,
+                      const void *q, const float *o_x, const float *lse_x, float *o, float *lse, void *ws,
+                      size_t ws_bytes, void *stream) {
+    if (!c) return fail(WSK_EINVAL, "cache is NULL");
+    Selection sl;
+    int rc = make_selection(c, n, ids, sel_begin, sel, sl);
+    if (rc) return rc;
+    return attend_passes(c, n, ids, nullptr, nullptr, q, o, lse, ws, ws_bytes, stream, true, true, o_x, lse_x, &sl);
 }
 
 int wsk_attend_pass1(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,

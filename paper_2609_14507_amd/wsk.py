@@ -76,6 +76,9 @@ _SIGS = {
     "wsk_attend_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_attend": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_stream_read": ([_VP, ctypes.c_size_t, _VP, _VP], ctypes.c_int),
+    "wsk_attend_blocks_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+    "wsk_attend_blocks": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP],
+                          ctypes.c_int),
     "wsk_cpu_attend": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _I32], ctypes.c_int),
     "wsk_roofline_share": ([ctypes.POINTER(wsk_roofline), ctypes.c_int64, ctypes.POINTER(ctypes.c_double)],
                            ctypes.c_int),
@@ -311,3 +314,29 @@ def wsk_cpu_attend(h: int, seq_ids, start, end, q, o, lse, threads: int = 0):
             raise ValueError("host arrays must be C-contiguous with the documented dtypes")
     _check(lib().wsk_cpu_attend(h, len(seq_ids), _i32_array(seq_ids), _i32_array(start), _i32_array(end),
                                 q.ctypes.data, o.ctypes.data, lse.ctypes.data, threads))
+
+
+def _selection(sel_lists):
+    begin = [0]
+    flat = []
+    for lst in sel_lists:
+        flat.extend(int(b) for b in lst)
+        begin.append(len(flat))
+    return begin, flat
+
+
+def wsk_attend_blocks_workspace(h: int, seq_ids, sel_lists) -> int:
+    begin, flat = _selection(sel_lists)
+    b = ctypes.c_size_t()
+    _check(lib().wsk_attend_blocks_workspace(h, len(seq_ids), _i32_array(seq_ids), _i32_array(begin),
+                                             _i32_array(flat) if flat else None, ctypes.byref(b)))
+    return b.value
+
+
+def wsk_attend_blocks(h: int, seq_ids, sel_lists, q, o, lse, ws, o_x=None, lse_x=None, stream=None):
+    """Block-sparse attention: sel_lists[i] = logical GPU blocks of seq_ids[i] to attend."""
+    begin, flat = _selection(sel_lists)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().wsk_attend_blocks(h, len(seq_ids), _i32_array(seq_ids), _i32_array(begin),
+                                   _i32_array(flat) if flat else None, _ptr(q), _ptr(o_x), _ptr(lse_x), _ptr(o),
+                                   _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
