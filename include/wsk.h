@@ -6,16 +6,22 @@
  * KVCache Format for CPU-GPU Load Balancing in MoE Inference":
  *
  *   - Sec. 3 and Sec. 4.3 (i): every cached byte gets its one physical home
- *     when it is written, and placed data never moves afterwards.  Here a
- *     sequence's CPU partition is the prefix [0, s) and its GPU partition the
- *     suffix [s, L); s is fixed when the sequence is opened.
+ *     when it is written, and placed data never moves afterwards.  A
+ *     sequence's positions [0, s) go to the CPU partition (pageable host
+ *     memory, read in place by the CPU engine), [s, load_end) to the load
+ *     region (pinned host memory in the GPU's slot layout, streamed to the
+ *     GPU through a ping-pong pair of HBM buffers), and later positions to
+ *     the GPU pool in HBM; s and load_end are fixed when the sequence is
+ *     opened.  By default load_end = s and the GPU side is HBM-resident.
+ *   - Sec. 4.2: decode rows are appended to the GPU pool (the D-window);
+ *     wsk_flush evicts whole batches of D rows from it to the CPU partition
+ *     or the load region, where they stay.
  *   - Sec. 4.1: each partition is made of fixed-size blocks of block_tokens
  *     tokens on an absolute grid (block k holds positions [k*Bk, (k+1)*Bk)).
  *     A block straddling s has a slot in both pools, each holding only its
  *     own side's positions.
  *   - Sec. 4.3: the interface is a PartitionSpec plus init / append / views
- *     (and flush, which this library does not implement: it has no D-window
- *     eviction).  The GPU side additionally attends its own range and merges
+ *     / flush.  The GPU side additionally attends its own range and merges
  *     partial results (Sec. 4.2, last paragraph; Sec. 5.1).
  *
  * Conventions for every call:
@@ -53,7 +59,8 @@ extern "C" {
 #define WSK_KIND_MLA 1 /* one compressed latent row per token (MLA)          */
 
 #define WSK_PART_CPU 0
-#define WSK_PART_GPU 1
+#define WSK_PART_GPU 1  /* the GPU pool in HBM                                */
+#define WSK_PART_LOAD 2 /* the pinned load region, streamed to the GPU        */
 
 #define WSK_LAYOUT_ROWS 0    /* token-major rows                               */
 #define WSK_LAYOUT_TILED64 1 /* GQA GPU pool: 64-token tiles in matrix-core order */
@@ -81,6 +88,16 @@ extern "C" {
  *   device_pool_blocks slots in the GPU pool (HBM), >= 0
  *   host_pool_blocks   slots in the CPU pool (pageable host memory), >= 0
  *   softmax_scale      multiplier of q.k before the softmax, finite and > 0
+ *   evict_tokens       D, the eviction batch of wsk_flush (Sec. 4.2): a
+ *                      multiple of block_tokens, or 0 (no eviction)
+ *   load_arena_blocks  load-region slots pinned by one host allocation; the
+ *                      region is pinned arena by arena as it fills, one
+ *                      arena ahead of use (Sec. 4.3 end, Sec. 5)
+ *   pingpong_blocks    slots of each of the two HBM ping-pong buffers that
+ *                      the load region is streamed through (Sec. 4.2)
+ *   load_pool_blocks   slots of the load region, >= 0; 0 = no load region
+ *                      (then load_arena_blocks and pingpong_blocks are 0),
+ *                      else load_arena_blocks > 0 and pingpong_blocks > 0
  *
  * Slot layouts (bf16).  Each partition's layout is fixed by the format for
  * the engine that reads it (Sec. 4.3 (ii)):
@@ -95,6 +112,8 @@ extern "C" {
  *                    V: piece (2*(d/16) + t/32)*64 + 16*((t%32)/8) + d%16,
  *                       elem t%8
  *   MLA, CPU pool  slot = [block_tokens][latent_dim + rope_dim]  (latent | rope)
+ *   (The load region's slots have the GPU pool's layout, so that a DMA
+ *   lands them ready for the GPU kernels.)
  *   MLA, GPU pool  slot = [block_tokens / 32 tiles][2304 16-byte pieces]
  *                  (WSK_LAYOUT_MLA32); piece c (dims 8c..8c+7, c = 0..71) of
  *                  token u of a tile (0..31) is piece
@@ -114,13 +133,17 @@ typedef struct wsk_partition_spec {
     int64_t device_pool_blocks;
     int64_t host_pool_blocks;
     float softmax_scale;
+    int32_t evict_tokens;
+    int32_t load_arena_blocks;
+    int32_t pingpong_blocks;
+    int64_t load_pool_blocks;
 } wsk_partition_spec;
 
 typedef struct wsk_cache wsk_cache;
 
 /* Where one cached position lives (wsk_route). */
 typedef struct wsk_loc {
-    int32_t part;          /* WSK_PART_CPU or WSK_PART_GPU            */
+    int32_t part;          /* WSK_PART_CPU, WSK_PART_GPU or WSK_PART_LOAD */
     int32_t logical_block; /* pos / block_tokens                      */
     int32_t slot;          /* slot index in that partition's pool     */
     int32_t offset;        /* pos % block_tokens: row within the slot */
@@ -149,7 +172,8 @@ typedef struct wsk_view {
     int64_t head_bytes;
     int64_t v_bytes;
     int64_t row_bytes;
-    int32_t start, end;   /* positions held: CPU [0, min(s, L)), GPU [min(s, L), L) */
+    int32_t start, end;   /* CPU: [0, min(s, L)); GPU: the D-window [min(w, L), L);
+                             later CPU segments (wsk_seq_segments) use the same table */
     int32_t block_tokens;
     int32_t is_device;
     int32_t layout;       /* WSK_LAYOUT_ROWS or WSK_LAYOUT_TILED64 */
@@ -184,6 +208,17 @@ int wsk_get_spec(const wsk_cache *cache, wsk_partition_spec *out);
  * range), ESTATE (already open).
  */
 int wsk_seq_open(wsk_cache *cache, int32_t seq, int32_t split);
+
+/*
+ * Open seq with a load range: positions p < split go to the CPU partition,
+ * split <= p < load_end to the load region (the paper's pinned load region,
+ * Sec. 4.2), p >= load_end to the GPU pool (the D-window, where decode rows
+ * are appended).  load_end >= split; a non-empty load range needs a load
+ * region and load_end a multiple of block_tokens (so that every later block
+ * of the GPU pool is whole).  wsk_seq_open(c, seq, s) is
+ * wsk_seq_open_window(c, seq, s, s).  Errors: EINVAL, ESTATE.
+ */
+int wsk_seq_open_window(wsk_cache *cache, int32_t seq, int32_t split, int32_t load_end);
 
 /* Close seq and return all its slots to the free sets (in-place block
  * reclamation at session end, Sec. 4.2).  Work already enqueued that reads
@@ -346,21 +381,26 @@ int wsk_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_
                    const uint16_t *w_uv, float *o, void *stream);
 
 /*
- * Block-sparse decode attention over the GPU partition (Sec. 4.4): a
- * block-level selection (e.g. a top-k over blocks computed by the model)
- * yields whole blocks, and each query head of seq_ids[i] attends only the
- * positions of its selected logical blocks
+ * Block-sparse decode attention over the GPU side (Sec. 4.4): a block-level
+ * selection (e.g. a top-k over blocks computed by the model) yields whole
+ * blocks, and each query head of seq_ids[i] attends only the positions of
+ * its selected logical blocks
  *   sel[sel_begin[i] .. sel_begin[i+1])      (sel_begin: n + 1 entries, [0] = 0)
- * that lie in the GPU partition [s, L) (the block holding s contributes its
- * positions >= s, the block holding L - 1 those < L).  Blocks must be
- * distinct GPU blocks of the sequence, in any order; none selected gives
- * O = 0, LSE = -inf.  The selected blocks are read in place, through a
- * compacted copy of their table entries kept in ws: nothing is gathered.
+ * that lie on the GPU side: in the GPU pool (the D-window [w, L)) or in the
+ * load region.  A block holding s contributes its positions >= s, the block
+ * holding L - 1 those < L.  Blocks must be distinct, in any order, each with
+ * GPU-side positions; none selected gives O = 0, LSE = -inf.  Selected
+ * GPU-pool blocks are read in place, through a compacted copy of their table
+ * entries kept in ws.  Selected load-region blocks are gathered by the host,
+ * one memcpy per block, into pinned staging and sent as one contiguous DMA
+ * per ping-pong buffer (the gather of the next buffer overlaps the DMA of
+ * the current one); the call returns when the last gather is done.
  * o_x, lse_x: optional partial to merge in, as for wsk_attend_pass2.
  * All of seq_ids, sel_begin, sel are HOST arrays; q, o_x, lse_x, o, lse, ws
  * DEVICE pointers laid out as for wsk_attend; ws of at least
  * wsk_attend_blocks_workspace() bytes.  Errors: EINVAL (malformed or
- * repeated selection), ERANGE (block outside the GPU partition), ESTATE, EHIP.
+ * repeated selection), ERANGE (block without GPU-side positions), ESTATE,
+ * EHIP.
  */
 int wsk_attend_blocks_workspace(const wsk_cache *cache, int32_t n, const int32_t *seq_ids,
                                 const int32_t *sel_begin, const int32_t *sel, size_t *bytes);
@@ -372,9 +412,10 @@ int wsk_attend_blocks(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
 /*
  * In-place CPU attention over the CPU partition (the CPU engine of Sec. 5.1;
  * MLA: the latent variant of Sec. 6.1): for each i < n, every query head of
- * seq_ids[i] attends positions [start[i], end[i]), which must lie in the CPU
- * partition: 0 <= start <= end <= min(s, L).  Rows are read where they sit
- * in the host pool, block by block through the CPU block table (Sec. 4.3
+ * seq_ids[i] attends positions [start[i], end[i]), which must all be in the
+ * CPU partition (the prefix [0, min(s, L)) and the batches wsk_flush moved
+ * there).  Rows are read where they sit in the host pool, block by block
+ * through the CPU block table (Sec. 4.3
  * (iii)); nothing is copied.  The result is the same normalised partial O
  * and natural-log LSE as wsk_attend's (O = 0, LSE = -inf for an empty
  * range), ready for the LSE merge with the GPU partial.
@@ -388,6 +429,81 @@ int wsk_attend_blocks(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
 int wsk_cpu_attend(wsk_cache *cache, int32_t n, const int32_t *seq_ids,
                    const int32_t *start, const int32_t *end, const void *q,
                    float *o, float *lse, int32_t threads);
+
+/*
+ * wsk_cpu_attend over every CPU-partition position of each listed sequence
+ * (the prefix [0, min(s, L)) and all batches flushed to the CPU): one
+ * partial (O, LSE) per sequence.  Arguments as for wsk_cpu_attend.
+ */
+int wsk_cpu_attend_all(wsk_cache *cache, int32_t n, const int32_t *seq_ids, const void *q, float *o,
+                       float *lse, int32_t threads);
+
+/*
+ * The GPU side of one decode step (Sec. 4.2): every query head of seq_ids[i]
+ * attends all of the sequence's GPU-side positions -- the D-window [w, L)
+ * in place in HBM, and the load-region positions streamed host -> device
+ * through the two ping-pong buffers (Sec. 4.2: the buffers are allocated
+ * once and overwritten in turn; each is refilled as soon as the kernels
+ * reading it finish, so the DMA of one buffer overlaps the attention over
+ * the other).  Runs of consecutive load slots travel as one DMA each.  The
+ * chunk partials, plus o_x / lse_x when given (the CPU partial), are merged
+ * into o / lse.  q, o_x, lse_x, o, lse, ws: DEVICE pointers laid out as for
+ * wsk_attend; ws of at least wsk_attend_gpu_workspace() bytes, 256-byte
+ * aligned.  The DMA runs on the cache's own copy stream, ordered after the
+ * evictions of earlier wsk_flush calls; the kernels run on stream.
+ * Returns after enqueueing.  Errors: EINVAL, ESTATE, EHIP.
+ */
+int wsk_attend_gpu_workspace(const wsk_cache *cache, int32_t n, const int32_t *seq_ids, size_t *bytes);
+int wsk_attend_gpu(wsk_cache *cache, int32_t n, const int32_t *seq_ids, const void *q, const float *o_x,
+                   const float *lse_x, float *o, float *lse, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * D-window eviction ("flush", Sec. 4.2 and 4.3): for each listed sequence
+ * whose D-window [w, L) holds a whole batch, move the batch [w, w') to
+ * part[i] (WSK_PART_CPU or WSK_PART_LOAD) and set w = w', where
+ * w' = floor((w + D) / block_tokens) * block_tokens (= w + D once w is
+ * block-aligned); a sequence with L < w' is left as it is.  moved[i]
+ * (optional, HOST) receives w' - w or 0.  The batch's GPU-pool slots are
+ * freed.  To the load region the slots travel as device -> host DMA into
+ * pinned memory, enqueued on stream (the layouts match); to the CPU the
+ * rows are copied out on stream, the call waits for them, and the host
+ * writes them token-major into the CPU pool.  The part chosen per batch is
+ * the caller's: wsk_policy_route_batch gives the paper's roofline routing.
+ * Later writes that reuse the freed slots must be ordered after this call on
+ * stream.  seq_ids (distinct, open), part, moved: HOST arrays.  Needs
+ * evict_tokens > 0 and a device; LOAD needs a load region.
+ * All-or-nothing for slot allocation (ENOMEM changes nothing).
+ * Errors: EINVAL, ESTATE, ENOMEM, EHIP.
+ */
+int wsk_flush(wsk_cache *cache, int32_t n, const int32_t *seq_ids, const int32_t *part, int32_t *moved,
+              void *stream);
+
+/* The homes of an open sequence's positions [0, L), in order, as runs of one
+ * home each (adjacent runs differ): run k is [start[k], end[k]) in part[k]
+ * (WSK_PART_*).  count receives the number of runs; at most cap are stored
+ * (the arrays may be NULL when cap = 0).  Errors: EINVAL, ESTATE. */
+int wsk_seq_segments(const wsk_cache *cache, int32_t seq, int32_t cap, int32_t *start, int32_t *end,
+                     int32_t *part, int32_t *count);
+
+/* HOST address of load-region slot `slot` (layout as the GPU pool's slots),
+ * for inspection.  The slot's arena must be allocated.  Errors: EINVAL,
+ * ERANGE. */
+int wsk_load_slot(const wsk_cache *cache, int32_t slot, const void **ptr);
+
+/* Load-region accounting (Sec. 4.3 end): bytes pinned so far, arenas, the
+ * seconds spent pinning them, slots in use, and the bytes sent host ->
+ * device by wsk_attend_gpu / wsk_attend_blocks and device -> host by
+ * wsk_flush since wsk_init. */
+typedef struct wsk_load_info {
+    int64_t pinned_bytes;
+    int64_t slots_used;
+    int64_t h2d_bytes;
+    int64_t d2h_bytes;
+    double pin_seconds;
+    int32_t arenas;
+    int32_t reserved;
+} wsk_load_info;
+int wsk_load_stats(const wsk_cache *cache, wsk_load_info *out);
 
 /* ---- roofline split policy (Sec. 5.2, Sec. 5.3) ------------------------- */
 

@@ -390,7 +390,9 @@ int cpu_attend(const CpuAttendArgs &x) {
     const int hkv = x.mla ? 1 : x.n_q_heads / x.group;
     for (int i = 0; i < x.n; ++i)
         for (int g = 0; g < hkv; ++g)
-            for (int a = x.start[i]; a < x.end[i]; a += kChunk) job.items.push_back({i, g, a, std::min(x.end[i], a + kChunk)});
+            for (int j = x.rbegin ? x.rbegin[i] : i; j < (x.rbegin ? x.rbegin[i + 1] : i + 1); ++j)
+                for (int a = x.start[j]; a < x.end[j]; a += kChunk)
+                    job.items.push_back({i, g, a, std::min(x.end[j], a + kChunk)});
     job.parts.resize(job.items.size());
     std::atomic<size_t> next{0};
     auto worker = [&]() {

@@ -1,0 +1,760 @@
+// The GPU side's host-resident data (Sec. 4.2, 4.3, 4.4): the pinned load
+// region, its streaming through a ping-pong pair of HBM buffers into the
+// pass-1 kernels, D-window eviction (flush), block-sparse selections with the
+// gather into pinned staging, and the CPU engine over every CPU position.
+//
+// The load region stores slots in the GPU pool's layout, so a DMA lands
+// blocks the kernels read unchanged: the host places rows into that layout
+// when it writes them (the paper's layout attribute fixed by the format).
+// A sequence's GPU-side positions are its load-region segments plus the
+// D-window [window, L) in HBM; blocks never mix the two (load_end and every
+// flush boundary after it are block-aligned), and the only partial blocks
+// are the one holding s (positions >= s) and the one holding L - 1.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cstdlib>
+#include <cstring>
+#include <thread>
+#include <vector>
+
+#include "cache.h"
+
+using namespace wsk;
+
+namespace {
+
+// ---- GPU slot layouts, host side -------------------------------------------
+// Pieces are 16 bytes (8 bf16).  GQA (64-token tiles, per KV head): K piece j
+// (dims 8j..8j+7) of token t, and V element (t, d); MLA (32-token tiles):
+// piece c (dims 8c..8c+7) of token u.
+constexpr int kPiece = 8;
+constexpr int kGqaTilePieces = 2048;   // K 1024 + V 1024
+constexpr int kMlaTilePieces = 2304;
+
+inline int gqa_k_piece(int t, int j) {
+    const int mt = 2 * (t / 32) + (t % 8) / 4;
+    const int nk = 4 * ((t % 32) / 8) + t % 4;
+    return (4 * mt + j / 4) * 64 + 16 * (j % 4) + nk;
+}
+inline int64_t gqa_v_elem(int t, int d) {   // element index inside the V half of a tile
+    return (int64_t)((2 * (d / 16) + t / 32) * 64 + 16 * ((t % 32) / 8) + d % 16) * kPiece + t % 8;
+}
+inline int mla_piece(int u, int c) { return (2 * (c / 4) + (u / 4) % 2) * 64 + 16 * (c % 4) + 4 * (u / 8) + u % 4; }
+
+// Places the rows of one position (row offset off in its block) into a slot
+// of GPU layout.  GQA: k[g], v[g] = the head_dim row of KV head g; MLA: k[0].
+void put_position(const wsk_cache *c, uint16_t *slot, int off, const uint16_t *const *k,
+                  const uint16_t *const *v) {
+    const int bk = c->spec.block_tokens;
+    if (c->spec.kind == WSK_KIND_MLA) {
+        uint16_t *tile = slot + (int64_t)(off / 32) * kMlaTilePieces * kPiece;
+        const int u = off % 32;
+        for (int p = 0; p < (kLatent + kRope) / kPiece; ++p)
+            memcpy(tile + (int64_t)mla_piece(u, p) * kPiece, k[0] + p * kPiece, 16);
+        return;
+    }
+    const int t = off % 64;
+    for (int g = 0; g < c->spec.n_kv_heads; ++g) {
+        uint16_t *tile = slot + ((int64_t)g * (bk / 64) + off / 64) * kGqaTilePieces * kPiece;
+        for (int j = 0; j < kHeadDim / kPiece; ++j) memcpy(tile + (int64_t)gqa_k_piece(t, j) * kPiece, k[g] + j * kPiece, 16);
+        uint16_t *vt = tile + 1024 * kPiece;
+        for (int d = 0; d < kHeadDim; ++d) vt[gqa_v_elem(t, d)] = v[g][d];
+    }
+}
+
+// The inverse: reads the rows of one position out of a slot of GPU layout.
+void get_position(const wsk_cache *c, const uint16_t *slot, int off, uint16_t *const *k, uint16_t *const *v) {
+    const int bk = c->spec.block_tokens;
+    if (c->spec.kind == WSK_KIND_MLA) {
+        const uint16_t *tile = slot + (int64_t)(off / 32) * kMlaTilePieces * kPiece;
+        const int u = off % 32;
+        for (int p = 0; p < (kLatent + kRope) / kPiece; ++p)
+            memcpy(k[0] + p * kPiece, tile + (int64_t)mla_piece(u, p) * kPiece, 16);
+        return;
+    }
+    const int t = off % 64;
+    for (int g = 0; g < c->spec.n_kv_heads; ++g) {
+        const uint16_t *tile = slot + ((int64_t)g * (bk / 64) + off / 64) * kGqaTilePieces * kPiece;
+        for (int j = 0; j < kHeadDim / kPiece; ++j) memcpy(k[g] + j * kPiece, tile + (int64_t)gqa_k_piece(t, j) * kPiece, 16);
+        const uint16_t *vt = tile + 1024 * kPiece;
+        for (int d = 0; d < kHeadDim; ++d) v[g][d] = vt[gqa_v_elem(t, d)];
+    }
+}
+
+int32_t arena_blocks(const wsk_cache *c) { return c->spec.load_arena_blocks; }
+
+// Allocates arena k: pinned (hipHostMalloc) on a device cache, plain aligned
+// host memory on a host-only one.  Records the time spent.
+int pin_arena(wsk_cache *c, size_t k) {
+    if (c->arenas[k]) return WSK_OK;
+    const int64_t first = (int64_t)k * arena_blocks(c);
+    const int64_t slots = std::min<int64_t>(arena_blocks(c), c->spec.load_pool_blocks - first);
+    const size_t bytes = (size_t)slots * slot_bytes(c);
+    const auto t0 = std::chrono::steady_clock::now();
+    void *p = nullptr;
+    if (c->device >= 0) {
+        DeviceGuard guard(c->device);
+        if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+        hipError_t e = hipHostMalloc(&p, bytes, hipHostMallocDefault);
+        if (e != hipSuccess) return fail(WSK_ENOMEM, "pinning %zu bytes of the load region: %s", bytes,
+                                         hipGetErrorString(e));
+    } else {
+        p = aligned_alloc(64, (bytes + 63) / 64 * 64);
+        if (!p) return fail(WSK_ENOMEM, "load region arena of %zu bytes", bytes);
+        memset(p, 0, bytes);
+    }
+    c->pin_seconds += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+    c->pinned_bytes += (int64_t)bytes;
+    c->arenas[k] = (uint16_t *)p;
+    return WSK_OK;
+}
+
+// Gathers the rows of positions [a, e) of sequence seq out of bounce (GPU
+// layout, block b at bounce + index_of[b] slots) into the CPU pool.
+void untile_to_cpu(wsk_cache *c, int32_t seq, int32_t a, int32_t e, const uint16_t *bounce, int32_t first_blk) {
+    const int bk = c->spec.block_tokens;
+    const int hkv = c->spec.kind == WSK_KIND_GQA ? c->spec.n_kv_heads : 1;
+    std::vector<uint16_t *> kp(hkv), vp(hkv);
+    for (int32_t p = a; p < e; ++p) {
+        const int32_t blk = p / bk;
+        const uint16_t *src = bounce + (int64_t)(blk - first_blk) * c->slot_elems;
+        uint16_t *dst = c->hpool + (int64_t)tab(c, WSK_PART_CPU, seq, blk) * c->slot_elems;
+        for (int g = 0; g < hkv; ++g) {
+            kp[g] = dst + row_offset(c, p, g, 0);
+            vp[g] = c->spec.kind == WSK_KIND_GQA ? dst + row_offset(c, p, g, 1) : nullptr;
+        }
+        get_position(c, src, p % bk, kp.data(), vp.data());
+    }
+}
+
+}  // namespace
+
+// ---- region management ---------------------------------------------------------
+
+uint16_t *wsk::load_slot_ptr(const wsk_cache *c, int32_t slot) {
+    return c->arenas[slot / arena_blocks(c)] + (int64_t)(slot % arena_blocks(c)) * c->slot_elems;
+}
+
+int wsk::load_ensure(wsk_cache *c, const std::vector<Pending> &pend) {
+    int32_t hi = -1;
+    for (const Pending &p : pend) {
+        if (p.part != WSK_PART_LOAD) continue;
+        int rc = pin_arena(c, (size_t)(p.slot / arena_blocks(c)));
+        if (rc) return rc;
+        hi = std::max(hi, p.slot);
+    }
+    // pin one arena ahead once the current one is half used, so that later
+    // writes and evictions find their memory already pinned
+    if (hi >= 0 && hi % arena_blocks(c) >= arena_blocks(c) / 2) {
+        const size_t next = (size_t)(hi / arena_blocks(c)) + 1;
+        if (next < c->arenas.size()) (void)pin_arena(c, next);   // a failure here is retried when needed
+    }
+    return WSK_OK;
+}
+
+int wsk::load_init(wsk_cache *c) {
+    const int64_t A = arena_blocks(c);
+    c->arenas.assign((size_t)((c->spec.load_pool_blocks + A - 1) / A), nullptr);
+    if (c->device < 0) return WSK_OK;
+    DeviceGuard guard(c->device);
+    if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+    const int32_t P = c->spec.pingpong_blocks;
+    const size_t buf = (size_t)P * slot_bytes(c);
+    hipError_t e = hipSuccess;
+    for (int b = 0; b < 2 && e == hipSuccess; ++b) e = hipMalloc((void **)&c->pingpong[b], buf);
+    for (int b = 0; b < 2 && e == hipSuccess; ++b) e = hipHostMalloc((void **)&c->hgather[b], buf, hipHostMallocDefault);
+    if (e == hipSuccess) e = hipMalloc((void **)&c->dident, (size_t)P * sizeof(int32_t));
+    if (e == hipSuccess) {
+        std::vector<int32_t> ident(P);
+        for (int32_t i = 0; i < P; ++i) ident[i] = i;
+        e = hipMemcpy(c->dident, ident.data(), (size_t)P * sizeof(int32_t), hipMemcpyHostToDevice);
+    }
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->copy_stream, hipStreamNonBlocking);
+    hipEvent_t *evs[] = {&c->filled[0], &c->filled[1], &c->consumed[0], &c->consumed[1],
+                         &c->staged[0], &c->staged[1], &c->flush_ev};
+    for (hipEvent_t *ev : evs)
+        if (e == hipSuccess) e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+    // every wait on these events is valid from the start
+    for (hipEvent_t *ev : evs)
+        if (e == hipSuccess) e = hipEventRecord(*ev, c->copy_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->copy_stream);
+    if (e != hipSuccess) return hip_fail(e, "load region set-up");
+    return WSK_OK;
+}
+
+void wsk::load_destroy(wsk_cache *c) {
+    if (c->device >= 0) {
+        DeviceGuard guard(c->device);
+        if (c->copy_stream) (void)hipStreamSynchronize(c->copy_stream);
+        if (c->flush_ev) (void)hipEventSynchronize(c->flush_ev);
+        for (int b = 0; b < 2; ++b) {
+            if (c->consumed[b]) (void)hipEventSynchronize(c->consumed[b]);
+            if (c->pingpong[b]) (void)hipFree(c->pingpong[b]);
+            if (c->hgather[b]) (void)hipHostFree(c->hgather[b]);
+        }
+        if (c->dident) (void)hipFree(c->dident);
+        if (c->hbounce) (void)hipHostFree(c->hbounce);
+        hipEvent_t evs[] = {c->filled[0], c->filled[1], c->consumed[0], c->consumed[1],
+                            c->staged[0], c->staged[1], c->flush_ev};
+        for (hipEvent_t ev : evs)
+            if (ev) (void)hipEventDestroy(ev);
+        if (c->copy_stream) (void)hipStreamDestroy(c->copy_stream);
+        for (uint16_t *a : c->arenas)
+            if (a) (void)hipHostFree(a);
+    } else {
+        for (uint16_t *a : c->arenas) free(a);
+    }
+    c->arenas.clear();
+}
+
+void wsk::load_write_rows(wsk_cache *c, int32_t seq, int32_t pos0, int32_t p0, int32_t p1, const uint16_t *k,
+                          const uint16_t *v) {
+    const int bk = c->spec.block_tokens;
+    const bool gqa = c->spec.kind == WSK_KIND_GQA;
+    const int hkv = gqa ? c->spec.n_kv_heads : 1;
+    std::vector<const uint16_t *> kp(hkv), vp(hkv);
+    for (int32_t p = p0; p < p1; ++p) {
+        uint16_t *slot = load_slot_ptr(c, tab(c, WSK_PART_LOAD, seq, p / bk));
+        for (int g = 0; g < hkv; ++g) {
+            kp[g] = k + ((int64_t)(p - pos0) * hkv + g) * c->row_elems;
+            vp[g] = gqa ? v + ((int64_t)(p - pos0) * hkv + g) * c->row_elems : nullptr;
+        }
+        put_position(c, slot, p % bk, kp.data(), vp.data());
+    }
+}
+
+// ---- the GPU side of a step: plan ---------------------------------------------
+namespace {
+
+// One load-region block to stream: call row i, load slot, the positions
+// [lo, hi) of the block that are attended.
+struct LoadPiece {
+    int32_t i, slot, lo, hi;
+};
+
+// The work of one wsk_attend_gpu / wsk_attend_blocks call.
+struct GpuPlan {
+    RowLaunch hbm;                   // GPU-pool rows, read in place
+    std::vector<int32_t> sel_tab;    // compacted table rows (selections only)
+    int32_t sel_width = 0;
+    std::vector<LoadPiece> pieces;   // in call-row order; a row's partial pieces at its ends
+    std::vector<size_t> chunk_first; // first piece of each ping-pong chunk, then pieces.size()
+    std::vector<RowLaunch> chunks;
+    std::vector<int64_t> pb;         // partials of row i: [pb[i], pb[i + 1])
+    size_t part_o_bytes = 0, part_lse_bytes = 0, sel_off = 0, bytes = 0;
+};
+
+inline size_t up256(size_t x) { return (x + 255) / 256 * 256; }
+
+// Rows of the ping-pong chunks and the partial layout, once hbm and pieces
+// are set.
+void finish_plan(const wsk_cache *c, int32_t n, GpuPlan &g) {
+    const int32_t P = std::max(c->spec.pingpong_blocks, 1);
+    const int bk = c->spec.block_tokens;
+    g.chunk_first.clear();
+    for (size_t j = 0; j < g.pieces.size(); j += (size_t)P) g.chunk_first.push_back(j);
+    g.chunk_first.push_back(g.pieces.size());
+    const size_t nch = g.chunk_first.size() - 1;
+    g.chunks.assign(nch, RowLaunch());
+    for (size_t k = 0; k < nch; ++k) {
+        RowLaunch &rl = g.chunks[k];
+        rl.trow.assign(n, 0);
+        rl.start.assign(n, 0);
+        rl.end.assign(n, 0);
+        const size_t j0 = g.chunk_first[k], j1 = g.chunk_first[k + 1];
+        for (size_t j = j0; j < j1;) {
+            const int32_t i = g.pieces[j].i;
+            size_t e = j;
+            while (e < j1 && g.pieces[e].i == i) ++e;
+            rl.trow[i] = (int32_t)(j - j0);   // staged slots of row i: j - j0 .. e - j0 - 1
+            rl.start[i] = g.pieces[j].lo;
+            rl.end[i] = (int32_t)(e - j - 1) * bk + g.pieces[e - 1].hi;
+            j = e;
+        }
+        plan_chunks(c, n, rl.start.data(), rl.end.data(), rl.plan);
+    }
+    g.pb.assign(n + 1, 0);
+    for (int32_t i = 0; i < n; ++i) {
+        int64_t cnt = g.hbm.plan.nchunks[i];
+        for (const RowLaunch &rl : g.chunks) cnt += rl.plan.nchunks[i];
+        g.pb[i + 1] = g.pb[i] + cnt;
+    }
+    g.hbm.pbase.assign(n, 0);
+    for (RowLaunch &rl : g.chunks) rl.pbase.assign(n, 0);
+    for (int32_t i = 0; i < n; ++i) {
+        int64_t p = g.pb[i];
+        g.hbm.pbase[i] = p;
+        p += g.hbm.plan.nchunks[i];
+        for (RowLaunch &rl : g.chunks) {
+            rl.pbase[i] = p;
+            p += rl.plan.nchunks[i];
+        }
+    }
+    const int width = c->spec.kind == WSK_KIND_GQA ? kHeadDim : kLatent;
+    const int64_t partials = g.pb[n];
+    g.part_o_bytes = up256((size_t)partials * c->spec.n_q_heads * width * sizeof(float));
+    g.part_lse_bytes = up256((size_t)partials * c->spec.n_q_heads * sizeof(float));
+    g.sel_off = g.part_o_bytes + g.part_lse_bytes;
+    g.bytes = g.sel_off + up256(g.sel_tab.size() * sizeof(int32_t));
+}
+
+int check_ids(const wsk_cache *c, int32_t n, const int32_t *ids) {
+    if (!c) return fail(WSK_EINVAL, "cache is NULL");
+    if (n < 0) return fail(WSK_EINVAL, "n < 0");
+    if (n > 0 && !ids) return fail(WSK_EINVAL, "seq_ids is NULL");
+    for (int32_t i = 0; i < n; ++i) {
+        int rc = check_seq(c, ids[i]);
+        if (rc) return rc;
+    }
+    return WSK_OK;
+}
+
+// Every GPU-side position of each sequence: the D-window in place, every
+// load-region block streamed.
+int plan_dense(const wsk_cache *c, int32_t n, const int32_t *ids, GpuPlan &g) {
+    int rc = check_ids(c, n, ids);
+    if (rc) return rc;
+    const int bk = c->spec.block_tokens;
+    g.hbm.trow.assign(ids, ids + n);
+    g.hbm.start.resize(n);
+    g.hbm.end.resize(n);
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t sq = ids[i], L = c->length[sq];
+        g.hbm.start[i] = std::min(c->window[sq], L);
+        g.hbm.end[i] = L;
+        for (const Seg &s : c->segs[sq]) {
+            if (s.part != WSK_PART_LOAD) continue;
+            const int32_t e = std::min(s.e, L);
+            for (int32_t blk = s.a / bk; blk * bk < e; ++blk) {
+                const int32_t lo = std::max(s.a - blk * bk, 0), hi = std::min(e - blk * bk, bk);
+                g.pieces.push_back({i, tab(c, WSK_PART_LOAD, sq, blk), lo, hi});
+            }
+        }
+    }
+    plan_chunks(c, n, g.hbm.start.data(), g.hbm.end.data(), g.hbm.plan);
+    finish_plan(c, n, g);
+    return WSK_OK;
+}
+
+// A block selection: selected GPU-pool blocks through a compacted table row
+// (the window's first block first, the block holding L - 1 last), selected
+// load-region blocks streamed (a partial first block first).
+int plan_selection(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin, const int32_t *sel,
+                   GpuPlan &g) {
+    int rc = check_ids(c, n, ids);
+    if (rc) return rc;
+    if (n > 0 && !sel_begin) return fail(WSK_EINVAL, "sel_begin is NULL");
+    if (n > 0 && sel_begin[0] != 0) return fail(WSK_EINVAL, "sel_begin[0] must be 0");
+    const int bk = c->spec.block_tokens;
+    int32_t width = 1;
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t k = sel_begin[i + 1] - sel_begin[i];
+        if (k < 0) return fail(WSK_EINVAL, "sel_begin must not decrease");
+        if (k > 0 && !sel) return fail(WSK_EINVAL, "sel is NULL");
+        width = std::max(width, k);
+    }
+    g.sel_width = width;
+    g.sel_tab.assign((size_t)n * width, 0);
+    g.hbm.trow.resize(n);
+    g.hbm.start.assign(n, 0);
+    g.hbm.end.assign(n, 0);
+    std::vector<uint8_t> seen;
+    for (int32_t i = 0; i < n; ++i) {
+        g.hbm.trow[i] = i;
+        const int32_t sq = ids[i], L = c->length[sq];
+        const int32_t k = sel_begin[i + 1] - sel_begin[i];
+        if (k == 0) continue;
+        const int32_t w = std::min(c->window[sq], L);
+        const int32_t first = w / bk, last = (L - 1) / bk;   // GPU-pool blocks [first, last] when w < L
+        seen.assign(c->max_blocks, 0);
+        bool has_first = false, has_last = false;
+        std::vector<int32_t> mid;
+        std::vector<LoadPiece> lhead, lmid, ltail;
+        for (int32_t j = 0; j < k; ++j) {
+            const int32_t b = sel[sel_begin[i] + j];
+            if (b < 0 || b >= c->max_blocks || b * bk >= L)
+                return fail(WSK_ERANGE, "block %d of sequence %d is not written", b, sq);
+            if (seen[b]) return fail(WSK_EINVAL, "block %d of sequence %d selected twice", b, sq);
+            seen[b] = 1;
+            if (w < L && b >= first) {
+                if (b == first) has_first = true;
+                if (b == last) has_last = true;
+                if (b != first && b != last) mid.push_back(b);
+                continue;
+            }
+            // a load-region block: its load positions are one run [lo, hi)
+            int32_t lo = -1, hi = -1;
+            for (const Seg &s : c->segs[sq]) {
+                if (s.part != WSK_PART_LOAD) continue;
+                const int32_t a = std::max(s.a, b * bk), e = std::min({s.e, (b + 1) * bk, L});
+                if (a < e) {
+                    lo = a - b * bk;
+                    hi = e - b * bk;
+                }
+            }
+            if (lo < 0) return fail(WSK_ERANGE, "block %d of sequence %d has no GPU-side positions", b, sq);
+            const LoadPiece pc{i, tab(c, WSK_PART_LOAD, sq, b), lo, hi};
+            (lo > 0 ? lhead : hi < bk ? ltail : lmid).push_back(pc);
+        }
+        std::vector<int32_t> order;
+        if (has_first) order.push_back(first);
+        order.insert(order.end(), mid.begin(), mid.end());
+        if (has_last && last != first) order.push_back(last);
+        for (size_t j = 0; j < order.size(); ++j)
+            g.sel_tab[(size_t)i * width + j] = tab(c, WSK_PART_GPU, sq, order[j]);
+        if (!order.empty()) {
+            g.hbm.start[i] = has_first ? w - first * bk : 0;
+            g.hbm.end[i] = (int32_t)(order.size() - 1) * bk + (has_last ? L - last * bk : bk);
+        }
+        g.pieces.insert(g.pieces.end(), lhead.begin(), lhead.end());
+        g.pieces.insert(g.pieces.end(), lmid.begin(), lmid.end());
+        g.pieces.insert(g.pieces.end(), ltail.begin(), ltail.end());
+    }
+    plan_chunks(c, n, g.hbm.start.data(), g.hbm.end.data(), g.hbm.plan);
+    finish_plan(c, n, g);
+    return WSK_OK;
+}
+
+// ---- the GPU side of a step: execution --------------------------------------------
+int run_plan(wsk_cache *c, int32_t n, GpuPlan &g, bool gather, const void *q, const float *o_x, const float *lse_x,
+             float *o, float *lse, void *ws, size_t ws_bytes, void *stream) {
+    if (n == 0) return WSK_OK;
+    if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
+    int rc = check_outputs(q, o, lse, o_x, lse_x, true, true);
+    if (rc) return rc;
+    if (!ws || ws_bytes < g.bytes) return fail(WSK_EINVAL, "workspace of %zu bytes needed", g.bytes);
+    if (((uintptr_t)ws & 255) != 0) return fail(WSK_EINVAL, "workspace must be 256-byte aligned");
+    if (!g.chunks.empty() && !c->copy_stream) return fail(WSK_ESTATE, "the cache has no load region");
+    DeviceGuard guard(c->device);
+    if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+    hipStream_t st = (hipStream_t)stream, cs = c->copy_stream;
+    float *part_o = (float *)ws;
+    float *part_lse = (float *)((char *)ws + g.part_o_bytes);
+    hipError_t e = hipSuccess;
+
+    // GPU-pool rows, in place
+    g.hbm.pool = c->dpool;
+    if (!g.sel_tab.empty()) {
+        int32_t *dsel = (int32_t *)((char *)ws + g.sel_off);
+        const size_t bytes = g.sel_tab.size() * sizeof(int32_t);
+        if (!c->hsel_ev) e = hipEventCreateWithFlags(&c->hsel_ev, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventSynchronize(c->hsel_ev);   // the previous upload has left the buffer
+        if (e == hipSuccess && c->hsel_bytes < bytes) {
+            if (c->hsel) (void)hipHostFree(c->hsel);
+            c->hsel = nullptr;
+            c->hsel_bytes = 0;
+            e = hipHostMalloc((void **)&c->hsel, bytes, hipHostMallocDefault);
+            if (e == hipSuccess) c->hsel_bytes = bytes;
+        }
+        if (e == hipSuccess) {
+            memcpy(c->hsel, g.sel_tab.data(), bytes);
+            e = hipMemcpyAsync(dsel, c->hsel, bytes, hipMemcpyHostToDevice, st);
+        }
+        if (e == hipSuccess) e = hipEventRecord(c->hsel_ev, st);
+        g.hbm.table = dsel;
+        g.hbm.table_stride = g.sel_width;
+    } else {
+        g.hbm.table = c->dtab;
+        g.hbm.table_stride = c->max_blocks;
+    }
+    if (e == hipSuccess) e = launch_rows(c, g.hbm, n, q, part_o, part_lse, st);
+
+    // load-region blocks through the ping-pong pair
+    const size_t nch = g.chunks.size();
+    const size_t sb = slot_bytes(c);
+    if (nch && e == hipSuccess) {
+        if (gather) e = hipEventSynchronize(c->flush_ev);   // evicted blocks are in place before the host reads them
+        else e = hipStreamWaitEvent(cs, c->flush_ev, 0);     // ... before the DMA reads them
+    }
+    for (size_t k = 0; k < nch && e == hipSuccess; ++k) {
+        const int b = (int)(k & 1);
+        const size_t j0 = g.chunk_first[k], j1 = g.chunk_first[k + 1];
+        e = hipStreamWaitEvent(cs, c->consumed[b], 0);   // the kernels that read buffer b are done
+        if (e != hipSuccess) break;
+        if (gather) {
+            // gather the selected blocks into staging b (one memcpy each),
+            // then one DMA; the next gather overlaps this DMA
+            e = hipEventSynchronize(c->staged[b]);
+            if (e != hipSuccess) break;
+            for (size_t j = j0; j < j1; ++j)
+                memcpy(c->hgather[b] + (int64_t)(j - j0) * c->slot_elems, load_slot_ptr(c, g.pieces[j].slot), sb);
+            e = hipMemcpyAsync(c->pingpong[b], c->hgather[b], (j1 - j0) * sb, hipMemcpyHostToDevice, cs);
+            if (e == hipSuccess) e = hipEventRecord(c->staged[b], cs);
+        } else {
+            // one DMA per run of consecutive slots of one arena
+            for (size_t j = j0; j < j1 && e == hipSuccess;) {
+                size_t r = j + 1;
+                while (r < j1 && g.pieces[r].slot == g.pieces[r - 1].slot + 1 &&
+                       g.pieces[r].slot % arena_blocks(c) != 0)
+                    ++r;
+                e = hipMemcpyAsync(c->pingpong[b] + (int64_t)(j - j0) * c->slot_elems,
+                                   load_slot_ptr(c, g.pieces[j].slot), (r - j) * sb, hipMemcpyHostToDevice, cs);
+                j = r;
+            }
+        }
+        c->h2d_bytes += (int64_t)((j1 - j0) * sb);
+        if (e == hipSuccess) e = hipEventRecord(c->filled[b], cs);
+        if (e == hipSuccess) e = hipStreamWaitEvent(st, c->filled[b], 0);
+        if (e != hipSuccess) break;
+        RowLaunch &rl = g.chunks[k];
+        rl.pool = c->pingpong[b];
+        rl.table = c->dident;
+        rl.table_stride = 1;
+        e = launch_rows(c, rl, n, q, part_o, part_lse, st);
+        if (e == hipSuccess) e = hipEventRecord(c->consumed[b], st);
+    }
+    if (e == hipSuccess) e = launch_combine_all(c, n, g.pb, part_o, part_lse, o_x, lse_x, o, lse, st);
+    if (e != hipSuccess) return hip_fail(e, "GPU-side attention");
+    return WSK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int wsk_attend_gpu_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, size_t *bytes) {
+    if (!bytes) return fail(WSK_EINVAL, "bytes is NULL");
+    GpuPlan g;
+    int rc = plan_dense(c, n, ids, g);
+    if (rc) return rc;
+    *bytes = g.bytes;
+    return WSK_OK;
+}
+
+int wsk_attend_gpu(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, const float *o_x, const float *lse_x,
+                   float *o, float *lse, void *ws, size_t ws_bytes, void *stream) {
+    GpuPlan g;
+    int rc = plan_dense(c, n, ids, g);
+    if (rc) return rc;
+    return run_plan(c, n, g, false, q, o_x, lse_x, o, lse, ws, ws_bytes, stream);
+}
+
+int wsk_attend_blocks_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin,
+                                const int32_t *sel, size_t *bytes) {
+    if (!bytes) return fail(WSK_EINVAL, "bytes is NULL");
+    GpuPlan g;
+    int rc = plan_selection(c, n, ids, sel_begin, sel, g);
+    if (rc) return rc;
+    *bytes = g.bytes;
+    return WSK_OK;
+}
+
+int wsk_attend_blocks(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin, const int32_t *sel,
+                      const void *q, const float *o_x, const float *lse_x, float *o, float *lse, void *ws,
+                      size_t ws_bytes, void *stream) {
+    GpuPlan g;
+    int rc = plan_selection(c, n, ids, sel_begin, sel, g);
+    if (rc) return rc;
+    return run_plan(c, n, g, true, q, o_x, lse_x, o, lse, ws, ws_bytes, stream);
+}
+
+int wsk_flush(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *part, int32_t *moved, void *stream) {
+    int rc = check_ids(c, n, ids);
+    if (rc) return rc;
+    if (n > 0 && !part) return fail(WSK_EINVAL, "part is NULL");
+    const int32_t D = c->spec.evict_tokens;
+    if (D <= 0) return fail(WSK_ESTATE, "the cache has no eviction batch (evict_tokens = 0)");
+    if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
+    std::vector<int32_t> sorted(ids, ids + n);
+    std::sort(sorted.begin(), sorted.end());
+    for (int32_t j = 1; j < n; ++j)
+        if (sorted[j] == sorted[j - 1]) return fail(WSK_EINVAL, "sequence %d listed twice", sorted[j]);
+    for (int32_t i = 0; i < n; ++i) {
+        if (part[i] != WSK_PART_CPU && part[i] != WSK_PART_LOAD) return fail(WSK_EINVAL, "part[%d] = %d", i, part[i]);
+        if (part[i] == WSK_PART_LOAD && !has_load_region(c)) return fail(WSK_ESTATE, "the cache has no load region");
+    }
+    const int bk = c->spec.block_tokens;
+    // batches and their destination slots (all-or-nothing)
+    std::vector<int32_t> w0(n), w1(n);
+    std::vector<Pending> pend;
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t sq = ids[i];
+        w0[i] = c->window[sq];
+        w1[i] = (w0[i] + D) / bk * bk;
+        if (w1[i] > c->length[sq]) {
+            w1[i] = w0[i];
+            continue;
+        }
+        for (int32_t blk = w0[i] / bk; blk < w1[i] / bk; ++blk) {
+            if (tab(c, part[i], sq, blk) >= 0) continue;   // the CPU slot of the block holding s
+            if (c->free_slots[part[i]].empty()) {
+                undo(c, pend);
+                return fail(WSK_ENOMEM, "%s pool exhausted", part[i] == WSK_PART_CPU ? "CPU" : "load");
+            }
+            pend.push_back({part[i], sq, blk, c->free_slots[part[i]].top()});
+            c->free_slots[part[i]].pop();
+        }
+    }
+    rc = load_ensure(c, pend);
+    if (rc) {
+        undo(c, pend);
+        return rc;
+    }
+    DeviceGuard guard(c->device);
+    if (guard.err != hipSuccess) {
+        undo(c, pend);
+        return hip_fail(guard.err, "hipSetDevice");
+    }
+    commit(c, pend);
+    hipStream_t st = (hipStream_t)stream;
+    const size_t sb = slot_bytes(c);
+    hipError_t e = hipSuccess;
+    // to the load region: device -> host DMA straight into the pinned slots
+    bool any_load = false;
+    for (int32_t i = 0; i < n && e == hipSuccess; ++i) {
+        if (part[i] != WSK_PART_LOAD || w1[i] == w0[i]) continue;
+        any_load = true;
+        const int32_t sq = ids[i];
+        for (int32_t blk = w0[i] / bk; blk < w1[i] / bk && e == hipSuccess; ++blk) {
+            e = hipMemcpyAsync(load_slot_ptr(c, tab(c, WSK_PART_LOAD, sq, blk)),
+                               c->dpool + (int64_t)tab(c, WSK_PART_GPU, sq, blk) * c->slot_elems, sb,
+                               hipMemcpyDeviceToHost, st);
+            c->d2h_bytes += (int64_t)sb;
+        }
+    }
+    if (any_load && e == hipSuccess) e = hipEventRecord(c->flush_ev, st);
+    // to the CPU pool: device -> host into the pinned bounce, then the host
+    // writes the rows token-major
+    size_t cpu_blocks = 0;
+    for (int32_t i = 0; i < n; ++i)
+        if (part[i] == WSK_PART_CPU) cpu_blocks += (size_t)(w1[i] / bk - w0[i] / bk);
+    if (cpu_blocks && e == hipSuccess) {
+        const size_t bytes = cpu_blocks * sb;
+        if (c->hbounce_bytes < bytes) {
+            if (c->hbounce) (void)hipHostFree(c->hbounce);
+            c->hbounce = nullptr;
+            c->hbounce_bytes = 0;
+            e = hipHostMalloc((void **)&c->hbounce, bytes, hipHostMallocDefault);
+            if (e == hipSuccess) c->hbounce_bytes = bytes;
+        }
+        size_t at = 0;
+        for (int32_t i = 0; i < n && e == hipSuccess; ++i) {
+            if (part[i] != WSK_PART_CPU) continue;
+            for (int32_t blk = w0[i] / bk; blk < w1[i] / bk && e == hipSuccess; ++blk, ++at) {
+                e = hipMemcpyAsync(c->hbounce + (int64_t)at * c->slot_elems,
+                                   c->dpool + (int64_t)tab(c, WSK_PART_GPU, ids[i], blk) * c->slot_elems, sb,
+                                   hipMemcpyDeviceToHost, st);
+                c->d2h_bytes += (int64_t)sb;
+            }
+        }
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        at = 0;
+        for (int32_t i = 0; i < n && e == hipSuccess; ++i) {
+            if (part[i] != WSK_PART_CPU || w1[i] == w0[i]) continue;
+            untile_to_cpu(c, ids[i], w0[i], w1[i], c->hbounce + (int64_t)at * c->slot_elems, w0[i] / bk);
+            at += (size_t)(w1[i] / bk - w0[i] / bk);
+        }
+    }
+    // the batch now lives in its new home: free the GPU-pool slots, extend
+    // the segments, move the window
+    for (int32_t i = 0; i < n; ++i) {
+        if (moved) moved[i] = w1[i] - w0[i];
+        if (w1[i] == w0[i]) continue;
+        const int32_t sq = ids[i];
+        for (int32_t blk = w0[i] / bk; blk < w1[i] / bk; ++blk) {
+            int32_t &t = tab(c, WSK_PART_GPU, sq, blk);
+            c->free_slots[WSK_PART_GPU].push(t);
+            t = -1;
+        }
+        std::vector<Seg> &sg = c->segs[sq];
+        if (!sg.empty() && sg.back().part == part[i] && sg.back().e == w0[i])
+            sg.back().e = w1[i];
+        else
+            sg.push_back({w0[i], w1[i], part[i]});
+        c->window[sq] = w1[i];
+    }
+    if (e != hipSuccess) return hip_fail(e, "wsk_flush");
+    return WSK_OK;
+}
+
+int wsk_cpu_attend_all(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, float *o, float *lse,
+                       int32_t threads) {
+    int rc = check_ids(c, n, ids);
+    if (rc) return rc;
+    if (n == 0) return WSK_OK;
+    if (!q || !o || !lse) return fail(WSK_EINVAL, "NULL argument");
+    std::vector<const int32_t *> tables(n);
+    std::vector<int32_t> rbegin(n + 1, 0), ra, re;
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t sq = ids[i], L = c->length[sq];
+        for (const Seg &s : c->segs[sq])
+            if (s.part == WSK_PART_CPU && s.a < L) {
+                ra.push_back(s.a);
+                re.push_back(std::min(s.e, L));
+            }
+        rbegin[i + 1] = (int32_t)ra.size();
+        tables[i] = c->htab[WSK_PART_CPU].data() + (size_t)sq * c->max_blocks;
+    }
+    const wsk_partition_spec &sp = c->spec;
+    const bool mla = sp.kind == WSK_KIND_MLA;
+    CpuAttendArgs x{};
+    x.pool = c->hpool;
+    x.tables = tables.data();
+    x.start = ra.data();
+    x.end = re.data();
+    x.rbegin = rbegin.data();
+    x.q = (const uint16_t *)q;
+    x.o = o;
+    x.lse = lse;
+    x.slot_elems = c->slot_elems;
+    x.n = n;
+    x.n_q_heads = sp.n_q_heads;
+    x.group = mla ? sp.n_q_heads : sp.n_q_heads / sp.n_kv_heads;
+    x.row_elems = c->row_elems;
+    x.dv = mla ? sp.latent_dim : sp.head_dim;
+    x.q_row = (int64_t)sp.n_q_heads * c->row_elems;
+    x.block_tokens = sp.block_tokens;
+    x.mla = mla;
+    x.scale_log2 = sp.softmax_scale * 1.4426950408889634f;
+    x.threads = threads > 0 ? threads : (int)std::max(1u, std::thread::hardware_concurrency());
+    cpu_attend(x);
+    return WSK_OK;
+}
+
+int wsk_seq_segments(const wsk_cache *c, int32_t seq, int32_t cap, int32_t *start, int32_t *end, int32_t *part,
+                     int32_t *count) {
+    int rc = check_seq(c, seq);
+    if (rc) return rc;
+    if (!count || cap < 0 || (cap > 0 && (!start || !end || !part))) return fail(WSK_EINVAL, "output arrays");
+    const int32_t L = c->length[seq];
+    int32_t k = 0;
+    auto emit = [&](int32_t a, int32_t e, int32_t p) {
+        if (a >= e) return;
+        if (k < cap) {
+            start[k] = a;
+            end[k] = e;
+            part[k] = p;
+        }
+        ++k;
+    };
+    for (const Seg &s : c->segs[seq]) emit(s.a, std::min(s.e, L), s.part);
+    emit(std::min(c->window[seq], L), L, WSK_PART_GPU);
+    *count = k;
+    return WSK_OK;
+}
+
+int wsk_load_slot(const wsk_cache *c, int32_t slot, const void **ptr) {
+    if (!c || !ptr) return fail(WSK_EINVAL, "NULL argument");
+    if (!has_load_region(c) || slot < 0 || slot >= c->spec.load_pool_blocks)
+        return fail(WSK_ERANGE, "load slot %d", slot);
+    if (!c->arenas[slot / arena_blocks(c)]) return fail(WSK_ERANGE, "load slot %d is not allocated", slot);
+    *ptr = load_slot_ptr(c, slot);
+    return WSK_OK;
+}
+
+int wsk_load_stats(const wsk_cache *c, wsk_load_info *out) {
+    if (!c || !out) return fail(WSK_EINVAL, "NULL argument");
+    memset(out, 0, sizeof *out);
+    out->pinned_bytes = c->pinned_bytes;
+    out->pin_seconds = c->pin_seconds;
+    out->slots_used = has_load_region(c) ? c->spec.load_pool_blocks - (int64_t)c->free_slots[WSK_PART_LOAD].size() : 0;
+    out->h2d_bytes = c->h2d_bytes;
+    out->d2h_bytes = c->d2h_bytes;
+    for (uint16_t *a : c->arenas) out->arenas += a != nullptr;
+    return WSK_OK;
+}
+
+}  // extern "C"

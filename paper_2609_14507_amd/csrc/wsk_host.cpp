@@ -10,24 +10,20 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
-#include <functional>
 #include <new>
-#include <queue>
 #include <string>
+#include <thread>
 #include <vector>
 
-#include "../../include/wsk.h"
-#include <thread>
-
-#include "wsk_internal.h"
+#include "cache.h"
 
 using namespace wsk;
 
 namespace {
-
 thread_local std::string g_err;
+}  // namespace
 
-int fail(int code, const char *fmt, ...) {
+int wsk::fail(int code, const char *fmt, ...) {
     char buf[512];
     va_list ap;
     va_start(ap, fmt);
@@ -37,68 +33,14 @@ int fail(int code, const char *fmt, ...) {
     return code;
 }
 
-}  // namespace
+int wsk::hip_fail(hipError_t e, const char *what) {
+    return fail(WSK_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
 
 // Error reporting for the policy functions (policy.cpp).
 int wsk::policy_fail(int code, const char *msg) { return fail(code, "%s", msg); }
 
 namespace {
-
-int hip_fail(hipError_t e, const char *what) {
-    return fail(WSK_EHIP, "%s: %s", what, hipGetErrorString(e));
-}
-
-// Makes the cache's device current for the duration of a call and restores
-// the caller's device afterwards.
-struct DeviceGuard {
-    int prev = -1;
-    hipError_t err = hipSuccess;
-    explicit DeviceGuard(int dev) {
-        if (dev < 0) return;
-        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
-        if (prev != dev) err = hipSetDevice(dev);
-    }
-    ~DeviceGuard() {
-        if (prev >= 0) (void)hipSetDevice(prev);
-    }
-};
-
-typedef std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> MinHeap;
-
-// Bytes of device staging used by wsk_write for the GPU partition's rows.
-constexpr size_t kStageBytes = 64u << 20;
-
-}  // namespace
-
-struct wsk_cache {
-    wsk_partition_spec spec;
-    int device = -1;
-    int cu_count = 256;           // compute units of the device (MI355X: 256)
-    int32_t max_blocks = 0;       // logical blocks per sequence
-    int32_t row_elems = 0;        // bf16 elements of one cached row (one head's K, or one MLA row)
-    int32_t rows_per_pos = 0;     // rows one position stores (GQA: 2 * Hkv; MLA: 1)
-    int64_t slot_elems = 0;       // bf16 elements per slot
-    uint16_t *hpool = nullptr;    // CPU partition pool (pageable, 64-byte aligned)
-    uint16_t *dpool = nullptr;    // GPU partition pool (HBM)
-    int32_t *dtab = nullptr;      // device copy of the GPU block table
-    uint16_t *dstage = nullptr;   // device staging for wsk_write
-    int32_t *hsel = nullptr;      // pinned host staging of block-selection tables
-    size_t hsel_bytes = 0;
-    hipEvent_t hsel_ev = nullptr; // marks the end of the last selection-table upload
-    std::vector<int32_t> htab[2]; // host block tables [part][seq * max_blocks + k]
-    std::vector<uint8_t> is_open;
-    std::vector<int32_t> split, length;
-    MinHeap free_slots[2];
-};
-
-namespace {
-
-struct Pending {
-    int part;
-    int32_t seq;
-    int32_t blk;
-    int32_t slot;
-};
 
 int validate_spec(const wsk_partition_spec *s) {
     if (!s) return fail(WSK_EINVAL, "spec is NULL");
@@ -115,6 +57,15 @@ int validate_spec(const wsk_partition_spec *s) {
         return fail(WSK_EINVAL, "softmax_scale must be finite and positive");
     if ((int64_t)s->max_seqs * ((s->max_seq_len + s->block_tokens - 1) / s->block_tokens) > INT32_MAX)
         return fail(WSK_EINVAL, "block table too large");
+    if (s->evict_tokens < 0 || s->evict_tokens % s->block_tokens)
+        return fail(WSK_EINVAL, "evict_tokens must be a non-negative multiple of block_tokens");
+    if (s->load_pool_blocks < 0 || s->load_pool_blocks > INT32_MAX)
+        return fail(WSK_EINVAL, "load_pool_blocks must be in [0, 2^31)");
+    if (s->load_pool_blocks > 0 && (s->load_arena_blocks <= 0 || s->pingpong_blocks <= 0))
+        return fail(WSK_EINVAL, "a load region needs load_arena_blocks > 0 and pingpong_blocks > 0");
+    if (s->load_pool_blocks == 0 && (s->load_arena_blocks != 0 || s->pingpong_blocks != 0))
+        return fail(WSK_EINVAL, "load_arena_blocks and pingpong_blocks must be 0 without a load region");
+    if (s->pingpong_blocks < 0 || s->load_arena_blocks < 0) return fail(WSK_EINVAL, "negative load-region size");
     if (s->kind == WSK_KIND_GQA) {
         if (s->n_q_heads % s->n_kv_heads) return fail(WSK_EINVAL, "n_q_heads must be a multiple of n_kv_heads");
         if (s->n_q_heads / s->n_kv_heads > WSK_MAX_GROUP) return fail(WSK_EINVAL, "group size above %d", WSK_MAX_GROUP);
@@ -129,33 +80,39 @@ int validate_spec(const wsk_partition_spec *s) {
     return WSK_OK;
 }
 
-int check_seq(const wsk_cache *c, int32_t seq) {
+}  // namespace
+
+int wsk::check_seq(const wsk_cache *c, int32_t seq) {
     if (!c) return fail(WSK_EINVAL, "cache is NULL");
     if (seq < 0 || seq >= c->spec.max_seqs) return fail(WSK_EINVAL, "sequence id %d out of range", seq);
     if (!c->is_open[seq]) return fail(WSK_ESTATE, "sequence %d is not open", seq);
     return WSK_OK;
 }
 
-inline int32_t &tab(wsk_cache *c, int part, int32_t seq, int32_t blk) {
-    return c->htab[part][(size_t)seq * c->max_blocks + blk];
-}
-
-void undo(wsk_cache *c, const std::vector<Pending> &pend) {
+void wsk::undo(wsk_cache *c, const std::vector<Pending> &pend) {
     for (const Pending &p : pend) c->free_slots[p.part].push(p.slot);
 }
 
-// Routing decision for positions [pos0, pos0+n) of seq: every (partition,
-// logical block) touched for the first time takes the lowest free slot of its
-// pool, blocks in ascending order (CPU side of a straddling block first).
-int plan(wsk_cache *c, int32_t seq, int32_t pos0, int32_t n, std::vector<Pending> &pend) {
+namespace {
+const char *const kPartName[3] = {"CPU", "GPU", "load"};
+}
+
+// Routing decision for positions [pos0, pos0+n) of seq (Sec. 4.2): position
+// p goes to the CPU pool if p < s, to the load region if s <= p < load_end,
+// else to the GPU pool.  Every (pool, logical block) touched for the first
+// time takes the lowest free slot of its pool, blocks in ascending order and,
+// within a block, pools in the order CPU, GPU, load.
+int wsk::plan(wsk_cache *c, int32_t seq, int32_t pos0, int32_t n, std::vector<Pending> &pend) {
     if (n <= 0) return WSK_OK;
     const int bk = c->spec.block_tokens;
-    const int32_t s = c->split[seq];
+    const int32_t s = c->split[seq], w0 = std::max(c->load_end[seq], s);
     const int32_t end = pos0 + n;
     for (int32_t blk = pos0 / bk; blk <= (end - 1) / bk; ++blk) {
         const int32_t lo = std::max(pos0, blk * bk), hi = std::min(end, (blk + 1) * bk);
-        for (int part = WSK_PART_CPU; part <= WSK_PART_GPU; ++part) {
-            const bool touched = part == WSK_PART_CPU ? lo < s : hi > s;
+        for (int part : {WSK_PART_CPU, WSK_PART_GPU, WSK_PART_LOAD}) {
+            const bool touched = part == WSK_PART_CPU   ? lo < s
+                                 : part == WSK_PART_GPU ? hi > w0
+                                                        : std::max(lo, s) < std::min(hi, w0);
             if (!touched || tab(c, part, seq, blk) >= 0) continue;
             bool pending_already = false;
             for (const Pending &p : pend)
@@ -164,7 +121,7 @@ int plan(wsk_cache *c, int32_t seq, int32_t pos0, int32_t n, std::vector<Pending
             if (c->free_slots[part].empty()) {
                 undo(c, pend);
                 pend.clear();
-                return fail(WSK_ENOMEM, "%s pool exhausted", part == WSK_PART_CPU ? "CPU" : "GPU");
+                return fail(WSK_ENOMEM, "%s pool exhausted", kPartName[part]);
             }
             pend.push_back({part, seq, blk, c->free_slots[part].top()});
             c->free_slots[part].pop();
@@ -173,44 +130,33 @@ int plan(wsk_cache *c, int32_t seq, int32_t pos0, int32_t n, std::vector<Pending
     return WSK_OK;
 }
 
-// Device buffers read or written with 16-byte vector accesses must be
-// 16-byte aligned.
-inline bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
+int wsk::home_of(const wsk_cache *c, int32_t seq, int32_t pos) {
+    if (pos >= c->window[seq]) return WSK_PART_GPU;
+    for (const Seg &g : c->segs[seq])
+        if (pos >= g.a && pos < g.e) return g.part;
+    return WSK_PART_CPU;   // not reached: the segments cover [0, window)
+}
 
-void commit(wsk_cache *c, const std::vector<Pending> &pend) {
+bool wsk::range_in(const wsk_cache *c, int32_t seq, int32_t a, int32_t e, int part) {
+    const int32_t L = c->length[seq];
+    if (a < 0 || a > e || e > L) return false;
+    if (a == e) return true;
+    const int32_t w = std::min(c->window[seq], L);
+    if (part == WSK_PART_GPU) return a >= w;
+    int32_t p = a;   // walk the segments in order, extending the covered prefix [a, p)
+    for (const Seg &g : c->segs[seq])
+        if (g.part == part && g.a <= p && g.e > p) p = std::min(g.e, w);
+    return p >= e;
+}
+
+void wsk::commit(wsk_cache *c, const std::vector<Pending> &pend) {
     for (const Pending &p : pend) tab(c, p.part, p.seq, p.blk) = p.slot;
 }
 
-// Offset (elements) of position pos, KV head g, K (which = 0) or V (1), in
-// its slot of the CPU pool, where every row is token-major.  (The GPU pool
-// stores rows in matrix-core tiles, placed by the append/scatter kernels.)
-inline int64_t row_offset(const wsk_cache *c, int32_t pos, int g, int which) {
-    const int bk = c->spec.block_tokens;
-    const int off = pos % bk;
-    if (c->spec.kind == WSK_KIND_MLA) return (int64_t)off * c->row_elems;
-    return ((int64_t)(g * 2 + which) * bk + off) * c->row_elems;
-}
+namespace {
 
-// Split-KV chunking of one attend call.  Chunks are whole 64-token tiles of
-// the absolute tile grid.  Each sequence gets a number of chunks in
-// proportion to its tiles, so that all workgroups carry about the same work
-// and the whole grid is about one round of resident workgroups (every CU busy
-// from start to end, no tail).  Every call with the same arguments yields the
-// same layout, so wsk_attend_workspace and wsk_attend agree.
-struct AttendPlan {
-    int heads_per_wg = 1;
-    int head_groups = 1;
-    std::vector<int32_t> tpc;       // tiles per chunk, per sequence
-    std::vector<int32_t> nchunks;   // per sequence
-    int64_t partials = 0;           // sum of nchunks
-    size_t part_o_bytes = 0;
-    size_t bytes = 0;
-};
-
-int64_t n_tiles(int32_t a, int32_t e) { return e > a ? (int64_t)((e - 1) / kTile - a / kTile + 1) : 0; }
-
-void plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const int32_t *end, AttendPlan &pl);
-
+// Validates ranges of the GPU pool (the D-window [window, L) of each
+// sequence) and plans their chunking.
 int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
               AttendPlan &pl) {
     if (n < 0) return fail(WSK_EINVAL, "n < 0");
@@ -218,18 +164,20 @@ int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *
     for (int32_t i = 0; i < n; ++i) {
         int rc = check_seq(c, ids[i]);
         if (rc) return rc;
-        const int32_t L = c->length[ids[i]], s = std::min(c->split[ids[i]], L);
-        if (!(s <= start[i] && start[i] <= end[i] && end[i] <= L))
+        const int32_t L = c->length[ids[i]], w = std::min(c->window[ids[i]], L);
+        if (!(w <= start[i] && start[i] <= end[i] && end[i] <= L))
             return fail(WSK_ERANGE, "range [%d, %d) of sequence %d outside its GPU partition [%d, %d)", start[i],
-                        end[i], ids[i], s, L);
+                        end[i], ids[i], w, L);
     }
     plan_chunks(c, n, start, end, pl);
     return WSK_OK;
 }
 
+}  // namespace
+
 // Chunking of valid ranges (positions on the tile grid of the table the
 // kernels will read: the cache's, or a compacted one for block selections).
-void plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const int32_t *end, AttendPlan &pl) {
+void wsk::plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const int32_t *end, AttendPlan &pl) {
     int64_t total_tiles = 0;
     for (int32_t i = 0; i < n; ++i) total_tiles += n_tiles(start[i], end[i]);
     const wsk_partition_spec &sp = c->spec;
@@ -265,68 +213,6 @@ void plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const int3
     pl.bytes = pl.part_o_bytes + ((size_t)pl.partials * sp.n_q_heads * sizeof(float) + 255) / 256 * 256;
 }
 
-// A block selection laid out for the kernels (Sec. 4.4): per sequence, the
-// device slots of its selected GPU blocks in a compacted table row, and the
-// virtual range [vstart, vend) over that row.  The block holding s (which may
-// start inside the block) goes first and the block holding L - 1 (which may
-// end inside it) last, so every other selected block is whole.
-struct Selection {
-    std::vector<int32_t> vstart, vend;
-    std::vector<int32_t> tab;   // n x width slots
-    int32_t width = 1;
-};
-
-int make_selection(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin,
-                   const int32_t *sel, Selection &out) {
-    if (n < 0) return fail(WSK_EINVAL, "n < 0");
-    if (n > 0 && (!ids || !sel_begin)) return fail(WSK_EINVAL, "seq_ids/sel_begin must not be NULL");
-    if (n > 0 && sel_begin[0] != 0) return fail(WSK_EINVAL, "sel_begin[0] must be 0");
-    const int bk = c->spec.block_tokens;
-    out.vstart.assign(n, 0);
-    out.vend.assign(n, 0);
-    out.width = 1;
-    for (int32_t i = 0; i < n; ++i) {
-        int rc = check_seq(c, ids[i]);
-        if (rc) return rc;
-        const int32_t k = sel_begin[i + 1] - sel_begin[i];
-        if (k < 0) return fail(WSK_EINVAL, "sel_begin must not decrease");
-        if (k > 0 && !sel) return fail(WSK_EINVAL, "sel must not be NULL");
-        out.width = std::max(out.width, k);
-    }
-    out.tab.assign((size_t)n * out.width, 0);
-    std::vector<uint8_t> seen;
-    for (int32_t i = 0; i < n; ++i) {
-        const int32_t sq = ids[i], L = c->length[sq], s = std::min(c->split[sq], L);
-        const int32_t k = sel_begin[i + 1] - sel_begin[i];
-        if (k == 0) continue;
-        const int32_t first = s / bk, last = (L - 1) / bk;   // GPU blocks [first, last]
-        seen.assign(c->max_blocks, 0);
-        bool has_first = false, has_last = false;
-        std::vector<int32_t> mid;
-        for (int32_t j = 0; j < k; ++j) {
-            const int32_t b = sel[sel_begin[i] + j];
-            if (L == s || b < first || b > last)
-                return fail(WSK_ERANGE, "block %d of sequence %d is not in its GPU partition", b, sq);
-            if (seen[b]) return fail(WSK_EINVAL, "block %d of sequence %d selected twice", b, sq);
-            seen[b] = 1;
-            if (b == first) has_first = true;
-            if (b == last) has_last = true;
-            if (b != first && b != last) mid.push_back(b);
-        }
-        std::vector<int32_t> order;
-        if (has_first) order.push_back(first);
-        order.insert(order.end(), mid.begin(), mid.end());
-        if (has_last && last != first) order.push_back(last);
-        for (size_t j = 0; j < order.size(); ++j)
-            out.tab[(size_t)i * out.width + j] = c->htab[WSK_PART_GPU][(size_t)sq * c->max_blocks + order[j]];
-        out.vstart[i] = has_first ? s - first * bk : 0;
-        out.vend[i] = (int32_t)(order.size() - 1) * bk + (has_last ? L - last * bk : bk);
-    }
-    return WSK_OK;
-}
-
-}  // namespace
-
 extern "C" {
 
 const char *wsk_last_error(void) { return g_err.c_str(); }
@@ -354,14 +240,19 @@ int wsk_init(const wsk_partition_spec *spec, int device, wsk_cache **out) {
         const size_t tab_n = (size_t)spec->max_seqs * c->max_blocks;
         c->htab[0].assign(tab_n, -1);
         c->htab[1].assign(tab_n, -1);
+        if (spec->load_pool_blocks > 0) c->htab[2].assign(tab_n, -1);
         c->is_open.assign(spec->max_seqs, 0);
         c->split.assign(spec->max_seqs, 0);
+        c->load_end.assign(spec->max_seqs, 0);
+        c->window.assign(spec->max_seqs, 0);
         c->length.assign(spec->max_seqs, 0);
-        std::vector<int32_t> h(spec->host_pool_blocks), d(spec->device_pool_blocks);
-        for (int32_t i = 0; i < (int32_t)h.size(); ++i) h[i] = i;
-        for (int32_t i = 0; i < (int32_t)d.size(); ++i) d[i] = i;
-        c->free_slots[0] = MinHeap(std::greater<int32_t>(), std::move(h));
-        c->free_slots[1] = MinHeap(std::greater<int32_t>(), std::move(d));
+        c->segs.resize(spec->max_seqs);
+        const int64_t sizes[3] = {spec->host_pool_blocks, spec->device_pool_blocks, spec->load_pool_blocks};
+        for (int part = 0; part < 3; ++part) {
+            std::vector<int32_t> v(sizes[part]);
+            for (int32_t i = 0; i < (int32_t)v.size(); ++i) v[i] = i;
+            c->free_slots[part] = MinHeap(std::greater<int32_t>(), std::move(v));
+        }
     } catch (const std::bad_alloc &) {
         delete c;
         return fail(WSK_ENOMEM, "host allocation failed");
@@ -398,6 +289,15 @@ int wsk_init(const wsk_partition_spec *spec, int device, wsk_cache **out) {
             return r;
         }
     }
+    if (spec->load_pool_blocks > 0) {
+        rc = load_init(c);
+        if (rc) {
+            const std::string msg = g_err;
+            wsk_destroy(c);
+            g_err = msg;
+            return rc;
+        }
+    }
     *out = c;
     return WSK_OK;
 }
@@ -413,6 +313,7 @@ int wsk_destroy(wsk_cache *c) {
         if (c->hsel) (void)hipHostFree(c->hsel);
         if (c->hsel_ev) (void)hipEventDestroy(c->hsel_ev);
     }
+    load_destroy(c);
     free(c->hpool);
     delete c;
     return WSK_OK;
@@ -424,31 +325,60 @@ int wsk_get_spec(const wsk_cache *c, wsk_partition_spec *out) {
     return WSK_OK;
 }
 
-int wsk_seq_open(wsk_cache *c, int32_t seq, int32_t split) {
+int wsk_seq_open_window(wsk_cache *c, int32_t seq, int32_t split, int32_t load_end) {
     if (!c) return fail(WSK_EINVAL, "cache is NULL");
     if (seq < 0 || seq >= c->spec.max_seqs) return fail(WSK_EINVAL, "sequence id %d out of range", seq);
     if (split < 0) return fail(WSK_EINVAL, "split %d < 0", split);
+    if (load_end < split) return fail(WSK_EINVAL, "load_end %d below split %d", load_end, split);
+    if (load_end > c->spec.max_seq_len) return fail(WSK_EINVAL, "load_end %d past max_seq_len", load_end);
+    if (load_end > split) {
+        if (!has_load_region(c)) return fail(WSK_ESTATE, "the cache has no load region");
+        if (load_end % c->spec.block_tokens)
+            return fail(WSK_EINVAL, "load_end %d must be a multiple of block_tokens", load_end);
+    }
     if (c->is_open[seq]) return fail(WSK_ESTATE, "sequence %d already open", seq);
+    std::vector<Seg> segs;
+    if (split > 0) segs.push_back({0, split, WSK_PART_CPU});
+    if (load_end > split) segs.push_back({split, load_end, WSK_PART_LOAD});
+    c->segs[seq].swap(segs);
     c->is_open[seq] = 1;
     c->split[seq] = split;
+    c->load_end[seq] = load_end;
+    c->window[seq] = load_end;
     c->length[seq] = 0;
     return WSK_OK;
 }
 
+int wsk_seq_open(wsk_cache *c, int32_t seq, int32_t split) { return wsk_seq_open_window(c, seq, split, split); }
+
 int wsk_seq_close(wsk_cache *c, int32_t seq) {
     int rc = check_seq(c, seq);
     if (rc) return rc;
-    for (int part = 0; part < 2; ++part)
+    bool load_freed = false;
+    for (int part = 0; part < 3; ++part) {
+        if (c->htab[part].empty()) continue;
         for (int32_t k = 0; k < c->max_blocks; ++k) {
             int32_t &t = tab(c, part, seq, k);
             if (t >= 0) {
                 c->free_slots[part].push(t);
                 t = -1;
+                load_freed |= part == WSK_PART_LOAD;
             }
         }
+    }
+    // a freed load slot may be rewritten by the host as soon as it is reused:
+    // transfers still reading or writing it must end first
+    if (load_freed && c->device >= 0) {
+        DeviceGuard guard(c->device);
+        if (c->copy_stream) (void)hipStreamSynchronize(c->copy_stream);
+        if (c->flush_ev) (void)hipEventSynchronize(c->flush_ev);
+    }
+    c->segs[seq].clear();
     c->is_open[seq] = 0;
     c->length[seq] = 0;
     c->split[seq] = 0;
+    c->load_end[seq] = 0;
+    c->window[seq] = 0;
     return WSK_OK;
 }
 
@@ -468,6 +398,11 @@ int wsk_reserve(wsk_cache *c, int32_t seq, int32_t n) {
     std::vector<Pending> pend;
     rc = plan(c, seq, c->length[seq], n, pend);
     if (rc) return rc;
+    rc = load_ensure(c, pend);
+    if (rc) {
+        undo(c, pend);
+        return rc;
+    }
     // the device table must follow for GPU blocks
     if (c->device >= 0) {
         bool any_gpu = false;
@@ -502,14 +437,19 @@ int wsk_write(wsk_cache *c, int32_t seq, int32_t pos0, int32_t n, const void *k,
     if (!k) return fail(WSK_EINVAL, "k is NULL");
     if (sp.kind == WSK_KIND_GQA && !v) return fail(WSK_EINVAL, "v is NULL");
     if (sp.kind == WSK_KIND_MLA && v) return fail(WSK_EINVAL, "MLA caches take no v");
-    const int32_t s = c->split[seq];
+    const int32_t s = c->split[seq], w0 = std::max(c->load_end[seq], s);
     const int32_t end = pos0 + n;
-    const bool has_gpu = end > s;
+    const bool has_gpu = end > w0;
     if (has_gpu && c->device < 0) return fail(WSK_ESTATE, "host-only cache cannot hold GPU-partition rows");
 
     std::vector<Pending> pend;
     rc = plan(c, seq, pos0, n, pend);
     if (rc) return rc;
+    rc = load_ensure(c, pend);
+    if (rc) {
+        undo(c, pend);
+        return rc;
+    }
     commit(c, pend);
 
     const int hkv = sp.kind == WSK_KIND_GQA ? sp.n_kv_heads : 1;
@@ -527,6 +467,9 @@ int wsk_write(wsk_cache *c, int32_t seq, int32_t pos0, int32_t n, const void *k,
                 memcpy(base + row_offset(c, p, g, w), src[w] + ((int64_t)(p - pos0) * hkv + g) * c->row_elems,
                        row_bytes);
     }
+    // load-region rows: placed by the host in the GPU slot layout
+    if (pos0 < w0 && end > s)
+        load_write_rows(c, seq, pos0, std::max(pos0, s), std::min(end, w0), (const uint16_t *)k, (const uint16_t *)v);
     if (!has_gpu) {
         c->length[seq] = end;
         return WSK_OK;
@@ -536,7 +479,7 @@ int wsk_write(wsk_cache *c, int32_t seq, int32_t pos0, int32_t n, const void *k,
     DeviceGuard guard(c->device);
     if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
     hipStream_t st = (hipStream_t)stream;
-    const int32_t g0 = std::max(pos0, s);
+    const int32_t g0 = std::max(pos0, w0);
     const int32_t b0 = g0 / sp.block_tokens, b1 = (end - 1) / sp.block_tokens;
     hipError_t e = hipMemcpyAsync(c->dtab + (size_t)seq * c->max_blocks + b0, &tab(c, WSK_PART_GPU, seq, b0),
                                   (size_t)(b1 - b0 + 1) * sizeof(int32_t), hipMemcpyHostToDevice, st);
@@ -589,8 +532,10 @@ int wsk_append(wsk_cache *c, int32_t n, const int32_t *ids, const void *k_new, c
     for (int32_t i = 0; i < n; ++i) {
         const int32_t sq = ids[i];
         if (c->length[sq] >= sp.max_seq_len) return fail(WSK_ERANGE, "sequence %d is full", sq);
-        if (c->length[sq] < c->split[sq])
-            return fail(WSK_ERANGE, "position %d of sequence %d is below its split %d", c->length[sq], sq, c->split[sq]);
+        const int32_t w0 = std::max(c->split[sq], c->load_end[sq]);
+        if (c->length[sq] < w0)
+            return fail(WSK_ERANGE, "position %d of sequence %d is below the start %d of its GPU pool range",
+                        c->length[sq], sq, w0);
     }
     std::vector<Pending> pend;
     for (int32_t j = 0; j < n; ++j) {
@@ -643,7 +588,7 @@ int wsk_route(const wsk_cache *c, int32_t seq, int32_t pos, wsk_loc *out) {
     if (rc) return rc;
     if (!out) return fail(WSK_EINVAL, "out is NULL");
     if (pos < 0 || pos >= c->length[seq]) return fail(WSK_ERANGE, "position %d outside [0, %d)", pos, c->length[seq]);
-    const int part = pos < c->split[seq] ? WSK_PART_CPU : WSK_PART_GPU;
+    const int part = home_of(c, seq, pos);
     const int32_t blk = pos / c->spec.block_tokens;
     out->part = part;
     out->logical_block = blk;
@@ -678,7 +623,7 @@ int wsk_views(const wsk_cache *c, int32_t seq, wsk_view *cpu, wsk_view *gpu) {
         } else {
             v->pool = c->dpool;
             v->table = c->dtab ? c->dtab + (size_t)seq * c->max_blocks : nullptr;
-            v->start = std::min(s, L);
+            v->start = std::min(c->window[seq], L);
             v->end = L;
             v->is_device = 1;
         }
@@ -698,126 +643,124 @@ int wsk_attend_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, cons
 
 }  // extern "C"
 
-namespace {
-
-// wsk_attend and its two passes: pass 1 writes the chunk partials into ws,
-// pass 2 merges them into o / lse.
-// Bytes of the compacted selection table placed after the partials in ws.
-size_t selection_table_bytes(const Selection &sl) { return (sl.tab.size() * sizeof(int32_t) + 255) / 256 * 256; }
-
-int attend_passes(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
-                  const void *q, float *o, float *lse, void *ws, size_t ws_bytes, void *stream, bool pass1,
-                  bool pass2, const float *o_x = nullptr, const float *lse_x = nullptr,
-                  const Selection *sel = nullptr) {
-    if (!c) return fail(WSK_EINVAL, "cache is NULL");
-    AttendPlan pl;
-    if (sel) {
-        start = sel->vstart.data();
-        end = sel->vend.data();
-        plan_chunks(c, n, start, end, pl);
-        pl.bytes += selection_table_bytes(*sel);
-    } else {
-        int rc = make_plan(c, n, ids, start, end, pl);
-        if (rc) return rc;
-    }
-    if (n == 0) return WSK_OK;
-    if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
-    if (pass1 && !q) return fail(WSK_EINVAL, "q must not be NULL");
-    if (pass2 && (!o || !lse)) return fail(WSK_EINVAL, "o/lse must not be NULL");
-    if (!aligned16(q) || !aligned16(o)) return fail(WSK_EINVAL, "q and o must be 16-byte aligned");
-    if ((o_x == nullptr) != (lse_x == nullptr)) return fail(WSK_EINVAL, "o_x and lse_x must both be given or both NULL");
-    if (!aligned16(o_x)) return fail(WSK_EINVAL, "o_x must be 16-byte aligned");
-    if (pl.bytes && (!ws || ws_bytes < pl.bytes)) return fail(WSK_EINVAL, "workspace of %zu bytes needed", pl.bytes);
-    if (((uintptr_t)ws & 255) != 0) return fail(WSK_EINVAL, "workspace must be 256-byte aligned");
+void wsk::attend_params(const wsk_cache *c, const AttendPlan &pl, AttendParams &ap) {
     const wsk_partition_spec &sp = c->spec;
     const bool gqa = sp.kind == WSK_KIND_GQA;
-    const int width = gqa ? kHeadDim : kLatent;
     const int qw = gqa ? kHeadDim : kLatent + kRope;
-    DeviceGuard guard(c->device);
-    if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
-    hipStream_t st = (hipStream_t)stream;
-    float *part_o = (float *)ws;
-    float *part_lse = (float *)((char *)ws + pl.part_o_bytes);
+    ap.slot_elems = c->slot_elems;
+    ap.q_row = (int64_t)sp.n_q_heads * qw;
+    ap.n_q_heads = sp.n_q_heads;
+    ap.n_kv_heads = gqa ? sp.n_kv_heads : 1;
+    ap.group = sp.n_q_heads / ap.n_kv_heads;
+    ap.head_groups = gqa ? pl.head_groups : 1;
+    ap.block_tokens = sp.block_tokens;
+    ap.scale_log2 = sp.softmax_scale * 1.4426950408889634f;
+}
+
+hipError_t wsk::launch_rows(const wsk_cache *c, const RowLaunch &rl, int32_t n, const void *q, float *part_o,
+                            float *part_lse, hipStream_t st) {
     hipError_t e = hipSuccess;
-    int32_t *sel_tab = nullptr;
-    if (sel) {   // the compacted table rows, after the partials
-        sel_tab = (int32_t *)((char *)ws + pl.bytes - selection_table_bytes(*sel));
-        if (pass1) {
-            if (!c->hsel_ev) e = hipEventCreateWithFlags(&c->hsel_ev, hipEventDisableTiming);
-            if (e == hipSuccess) e = hipEventSynchronize(c->hsel_ev);   // the previous upload has left the buffer
-            const size_t bytes = sel->tab.size() * sizeof(int32_t);
-            if (e == hipSuccess && c->hsel_bytes < bytes) {
-                if (c->hsel) (void)hipHostFree(c->hsel);
-                c->hsel = nullptr;
-                c->hsel_bytes = 0;
-                e = hipHostMalloc((void **)&c->hsel, bytes, hipHostMallocDefault);
-                if (e == hipSuccess) c->hsel_bytes = bytes;
-            }
-            if (e == hipSuccess) {
-                memcpy(c->hsel, sel->tab.data(), bytes);
-                e = hipMemcpyAsync(sel_tab, c->hsel, bytes, hipMemcpyHostToDevice, st);
-            }
-            if (e == hipSuccess) e = hipEventRecord(c->hsel_ev, st);
-            if (e != hipSuccess) return hip_fail(e, "selection table upload");
-        }
-    }
-    int64_t part_base = 0;
     for (int32_t i0 = 0; i0 < n && e == hipSuccess; i0 += kMaxLaunchSeqs) {
         const int32_t m = std::min(kMaxLaunchSeqs, n - i0);
         AttendParams ap{};
-        CombineParams cp{};
-        ap.pool = c->dpool;
-        ap.table = sel ? sel_tab : c->dtab;
-        ap.q = (const uint16_t *)q + (int64_t)i0 * sp.n_q_heads * qw;
-        ap.part_o = part_o + part_base * sp.n_q_heads * width;
-        ap.part_lse = part_lse + part_base * sp.n_q_heads;
-        ap.slot_elems = c->slot_elems;
-        ap.q_row = (int64_t)sp.n_q_heads * qw;
-        ap.table_stride = sel ? sel->width : c->max_blocks;
-        ap.n_q_heads = sp.n_q_heads;
-        ap.n_kv_heads = gqa ? sp.n_kv_heads : 1;
-        ap.group = sp.n_q_heads / ap.n_kv_heads;
-        ap.head_groups = gqa ? pl.head_groups : 1;
-        ap.block_tokens = sp.block_tokens;
+        attend_params(c, rl.plan, ap);
+        ap.pool = rl.pool;
+        ap.table = rl.table;
+        ap.table_stride = rl.table_stride;
+        ap.q = (const uint16_t *)q + (int64_t)i0 * ap.q_row;
+        ap.part_o = part_o;
+        ap.part_lse = part_lse;
         ap.n = m;
-        ap.scale_log2 = sp.softmax_scale * 1.4426950408889634f;
         const int units = ap.n_kv_heads * ap.head_groups;
         ap.wg_begin[0] = 0;
-        ap.chunk_begin[0] = 0;
         for (int32_t r = 0; r < m; ++r) {
-            ap.seq[r] = sel ? i0 + r : ids[i0 + r];   // row of the table the kernels read
-            ap.start[r] = start[i0 + r];
-            ap.end[r] = end[i0 + r];
-            ap.tpc[r] = pl.tpc[i0 + r];
-            const int32_t nc = pl.nchunks[i0 + r];
+            const int32_t i = i0 + r;
+            const int32_t nc = rl.plan.nchunks[i];
+            ap.seq[r] = nc ? rl.trow[i] : 0;
+            ap.start[r] = nc ? rl.start[i] : 0;
+            ap.end[r] = nc ? rl.end[i] : 0;
+            ap.tpc[r] = rl.plan.tpc[i];
+            ap.chunk_begin[r] = (int32_t)rl.pbase[i];
             ap.wg_begin[r + 1] = ap.wg_begin[r] + nc * units;
-            ap.chunk_begin[r + 1] = ap.chunk_begin[r] + nc;
         }
-        for (int32_t r = m + 1; r <= kMaxLaunchSeqs; ++r) {
-            ap.wg_begin[r] = ap.wg_begin[m];
-            ap.chunk_begin[r] = ap.chunk_begin[m];
-        }
+        for (int32_t r = m + 1; r <= kMaxLaunchSeqs; ++r) ap.wg_begin[r] = ap.wg_begin[m];
         const int n_wg = ap.wg_begin[m];
-        if (pass1) {
-            if (gqa)
-                e = launch_gqa_attend(ap, pl.heads_per_wg, n_wg, st);
-            else
-                e = launch_mla_attend(ap, n_wg, st);
-            if (e != hipSuccess) break;
-        }
-        part_base += ap.chunk_begin[m];
-        if (!pass2) continue;
-        cp.part_o = ap.part_o;
-        cp.part_lse = ap.part_lse;
+        if (n_wg == 0) continue;
+        if (c->spec.kind == WSK_KIND_GQA)
+            e = launch_gqa_attend(ap, rl.plan.heads_per_wg, n_wg, st);
+        else
+            e = launch_mla_attend(ap, n_wg, st);
+    }
+    return e;
+}
+
+hipError_t wsk::launch_combine_all(const wsk_cache *c, int32_t n, const std::vector<int64_t> &pb,
+                                   const float *part_o, const float *part_lse, const float *o_x,
+                                   const float *lse_x, float *o, float *lse, hipStream_t st) {
+    const wsk_partition_spec &sp = c->spec;
+    const int width = sp.kind == WSK_KIND_GQA ? kHeadDim : kLatent;
+    hipError_t e = hipSuccess;
+    for (int32_t i0 = 0; i0 < n && e == hipSuccess; i0 += kMaxLaunchSeqs) {
+        const int32_t m = std::min(kMaxLaunchSeqs, n - i0);
+        CombineParams cp{};
+        cp.part_o = part_o + pb[i0] * sp.n_q_heads * width;
+        cp.part_lse = part_lse + pb[i0] * sp.n_q_heads;
         cp.o = o + (int64_t)i0 * sp.n_q_heads * width;
         cp.lse = lse + (int64_t)i0 * sp.n_q_heads;
         cp.o_x = o_x ? o_x + (int64_t)i0 * sp.n_q_heads * width : nullptr;
         cp.lse_x = lse_x ? lse_x + (int64_t)i0 * sp.n_q_heads : nullptr;
         cp.n = m;
         cp.n_q_heads = sp.n_q_heads;
-        for (int32_t r = 0; r <= kMaxLaunchSeqs; ++r) cp.chunk_begin[r] = ap.chunk_begin[r];
+        for (int32_t r = 0; r <= kMaxLaunchSeqs; ++r) cp.chunk_begin[r] = (int32_t)(pb[i0 + std::min(r, m)] - pb[i0]);
         e = launch_combine(cp, width, st);
     }
+    return e;
+}
+
+int wsk::check_outputs(const void *q, const float *o, const float *lse, const float *o_x, const float *lse_x,
+                       bool pass1, bool pass2) {
+    if (pass1 && !q) return fail(WSK_EINVAL, "q must not be NULL");
+    if (pass2 && (!o || !lse)) return fail(WSK_EINVAL, "o/lse must not be NULL");
+    if (!aligned16(q) || !aligned16(o)) return fail(WSK_EINVAL, "q and o must be 16-byte aligned");
+    if ((o_x == nullptr) != (lse_x == nullptr)) return fail(WSK_EINVAL, "o_x and lse_x must both be given or both NULL");
+    if (!aligned16(o_x)) return fail(WSK_EINVAL, "o_x must be 16-byte aligned");
+    return WSK_OK;
+}
+
+namespace {
+
+// wsk_attend and its two passes over ranges of the GPU pool: pass 1 writes
+// the chunk partials into ws, pass 2 merges them (and o_x) into o / lse.
+int attend_passes(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
+                  const void *q, float *o, float *lse, void *ws, size_t ws_bytes, void *stream, bool pass1,
+                  bool pass2, const float *o_x = nullptr, const float *lse_x = nullptr) {
+    if (!c) return fail(WSK_EINVAL, "cache is NULL");
+    RowLaunch rl;
+    int rc = make_plan(c, n, ids, start, end, rl.plan);
+    if (rc) return rc;
+    if (n == 0) return WSK_OK;
+    if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
+    rc = check_outputs(q, o, lse, o_x, lse_x, pass1, pass2);
+    if (rc) return rc;
+    const AttendPlan &pl = rl.plan;
+    if (pl.bytes && (!ws || ws_bytes < pl.bytes)) return fail(WSK_EINVAL, "workspace of %zu bytes needed", pl.bytes);
+    if (((uintptr_t)ws & 255) != 0) return fail(WSK_EINVAL, "workspace must be 256-byte aligned");
+    DeviceGuard guard(c->device);
+    if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+    hipStream_t st = (hipStream_t)stream;
+    float *part_o = (float *)ws;
+    float *part_lse = (float *)((char *)ws + pl.part_o_bytes);
+    rl.pool = c->dpool;
+    rl.table = c->dtab;
+    rl.table_stride = c->max_blocks;
+    rl.trow.assign(ids, ids + n);
+    rl.start.assign(start, start + n);
+    rl.end.assign(end, end + n);
+    rl.pbase.assign(n + 1, 0);
+    for (int32_t i = 0; i < n; ++i) rl.pbase[i + 1] = rl.pbase[i] + pl.nchunks[i];
+    hipError_t e = hipSuccess;
+    if (pass1) e = launch_rows(c, rl, n, q, part_o, part_lse, st);
+    if (e == hipSuccess && pass2) e = launch_combine_all(c, n, rl.pbase, part_o, part_lse, o_x, lse_x, o, lse, st);
     if (e != hipSuccess) return hip_fail(e, "wsk_attend");
     return WSK_OK;
 }
@@ -829,28 +772,6 @@ extern "C" {
 int wsk_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
                const void *q, float *o, float *lse, void *ws, size_t ws_bytes, void *stream) {
     return attend_passes(c, n, ids, start, end, q, o, lse, ws, ws_bytes, stream, true, true);
-}
-
-int wsk_attend_blocks_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin,
-                                 const int32_t *sel, size_t *bytes) {
-    if (!c || !bytes) return fail(WSK_EINVAL, "NULL argument");
-    Selection sl;
-    int rc = make_selection(c, n, ids, sel_begin, sel, sl);
-    if (rc) return rc;
-    AttendPlan pl;
-    plan_chunks(c, n, sl.vstart.data(), sl.vend.data(), pl);
-    *bytes = pl.bytes + selection_table_bytes(sl);
-    return WSK_OK;
-}
-
-int wsk_attend_blocks(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin, const int32_t *sel,
-                      const void *q, const float *o_x, const float *lse_x, float *o, float *lse, void *ws,
-                      size_t ws_bytes, void *stream) {
-    if (!c) return fail(WSK_EINVAL, "cache is NULL");
-    Selection sl;
-    int rc = make_selection(c, n, ids, sel_begin, sel, sl);
-    if (rc) return rc;
-    return attend_passes(c, n, ids, nullptr, nullptr, q, o, lse, ws, ws_bytes, stream, true, true, o_x, lse_x, &sl);
 }
 
 int wsk_attend_pass1(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *start, const int32_t *end,
@@ -910,10 +831,9 @@ int wsk_cpu_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *s
     for (int32_t i = 0; i < n; ++i) {
         int rc = check_seq(c, ids[i]);
         if (rc) return rc;
-        const int32_t s = std::min(c->split[ids[i]], c->length[ids[i]]);
-        if (!(0 <= start[i] && start[i] <= end[i] && end[i] <= s))
-            return fail(WSK_ERANGE, "range [%d, %d) of sequence %d outside its CPU partition [0, %d)", start[i], end[i],
-                        ids[i], s);
+        if (!range_in(c, ids[i], start[i], end[i], WSK_PART_CPU))
+            return fail(WSK_ERANGE, "range [%d, %d) of sequence %d is not all in its CPU partition", start[i], end[i],
+                        ids[i]);
         tables[i] = c->htab[WSK_PART_CPU].data() + (size_t)ids[i] * c->max_blocks;
     }
     const wsk_partition_spec &sp = c->spec;

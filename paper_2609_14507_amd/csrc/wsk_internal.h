@@ -105,7 +105,8 @@ struct ScatterParams {
 struct CpuAttendArgs {
     const uint16_t *pool;          // host pool base
     const int32_t *const *tables;  // per sequence: its CPU block-table row
-    const int32_t *start, *end;    // per sequence: token range
+    const int32_t *start, *end;    // token ranges: per sequence, or per range when rbegin is set
+    const int32_t *rbegin;         // optional [n + 1]: sequence i attends ranges rbegin[i] .. rbegin[i+1]-1
     const uint16_t *q;             // [n][n_q_heads][row_elems] bf16
     float *o;                      // [n][n_q_heads][dv]
     float *lse;                    // [n][n_q_heads]

@@ -24,30 +24,50 @@ def _cdiv(a: int, b: int) -> int:
 
 class DecodeSession:
     def __init__(self, w: Workload, prefill: Prefill, device: int = 0, extra_tokens: Optional[int] = None,
-                 block_tokens: int = 64, splits: Optional[Sequence[int]] = None, pool_slack: int = 0):
+                 block_tokens: int = 64, splits: Optional[Sequence[int]] = None, pool_slack: int = 0,
+                 load_ends: Optional[Sequence[int]] = None, evict_tokens: int = 0, pingpong_blocks: int = 0,
+                 arena_blocks: int = 0):
+        """load_ends: per sequence, the end of its load-region range [s, load_end)
+        (default: no load range); evict_tokens: the eviction batch D, which
+        also sizes the CPU and load pools for every batch the extra tokens can
+        evict."""
         self.w = w
         self.device = device
         self.dev = torch.device("cuda", device)
         self.B = len(prefill.lengths)
         extra = w.steps if extra_tokens is None else extra_tokens
         self.splits = list(prefill.splits if splits is None else splits)
+        self.load_ends = list(self.splits if load_ends is None else load_ends)
         bk = block_tokens
-        dev_blocks = sum(_cdiv(L + extra, bk) - min(s, L + extra) // bk
-                         for L, s in zip(prefill.lengths, self.splits)) + pool_slack
-        host_blocks = sum(_cdiv(min(s, L), bk) for L, s in zip(prefill.lengths, self.splits)) + pool_slack
-        self.max_len = max(prefill.lengths) + extra
+        Ls = prefill.lengths
+        evict_blocks = _cdiv(extra, bk) + 1 if evict_tokens else 0
+        dev_blocks = sum(_cdiv(L + extra, bk) - min(e, L + extra) // bk
+                         for L, e in zip(Ls, self.load_ends)) + pool_slack
+        host_blocks = sum(_cdiv(min(s, L), bk) + evict_blocks for L, s in zip(Ls, self.splits)) + pool_slack
+        load_blocks = sum((_cdiv(e, bk) - s // bk if e > s else 0) + evict_blocks
+                          for s, e in zip(self.splits, self.load_ends)) if load_ends is not None else 0
+        if load_blocks:
+            load_blocks += pool_slack
+            arena_blocks = arena_blocks or max(1, min(load_blocks, 1024))
+            pingpong_blocks = pingpong_blocks or 512
+        else:
+            arena_blocks = pingpong_blocks = 0
+        self.max_len = max(max(Ls) + extra, max(self.load_ends))
+        common = dict(evict_tokens=evict_tokens, load_pool_blocks=load_blocks, load_arena_blocks=arena_blocks,
+                      pingpong_blocks=pingpong_blocks)
         if w.kind == MLA:
             spec = wsk.make_spec(wsk.KIND_MLA, w.n_q_heads, 1, w.head_dim, bk, self.B, self.max_len, dev_blocks,
-                                 host_blocks, w.softmax_scale, latent_dim=w.latent_dim, rope_dim=w.rope_dim)
+                                 host_blocks, w.softmax_scale, latent_dim=w.latent_dim, rope_dim=w.rope_dim,
+                                 **common)
         else:
             spec = wsk.make_spec(wsk.KIND_GQA, w.n_q_heads, w.n_kv_heads, w.head_dim, bk, self.B, self.max_len,
-                                 dev_blocks, host_blocks, w.softmax_scale)
+                                 dev_blocks, host_blocks, w.softmax_scale, **common)
         self.spec = spec
         torch.cuda.set_device(device)
         self.h = wsk.wsk_init(spec, device)
-        self.lengths = list(prefill.lengths)
+        self.lengths = list(Ls)
         for b in range(self.B):
-            wsk.wsk_seq_open(self.h, b, self.splits[b])
+            wsk.wsk_seq_open_window(self.h, b, self.splits[b], self.load_ends[b])
             wsk.wsk_write(self.h, b, 0, prefill.k[b], None if prefill.v is None else prefill.v[b])
         self.ids = list(range(self.B))
         self._ws = torch.empty(0, dtype=torch.uint8, device=self.dev)
@@ -63,7 +83,25 @@ class DecodeSession:
 
     # -- operations ---------------------------------------------------------------
     def gpu_range(self, b: int):
-        return min(self.splits[b], self.lengths[b]), self.lengths[b]
+        """The D-window [w, L): the GPU-pool range of sequence b."""
+        segs = wsk.wsk_seq_segments(self.h, b)
+        w = segs[-1][0] if segs and segs[-1][2] == wsk.PART_GPU else self.lengths[b]
+        return w, self.lengths[b]
+
+    def attend_gpu(self, q: torch.Tensor, ids: Optional[List[int]] = None, o_x=None, lse_x=None, o=None, lse=None):
+        """Every GPU-side position (D-window in place, load region streamed), merged
+        with (o_x, lse_x) when given."""
+        ids = self.ids if ids is None else ids
+        o, lse = self._outputs(len(ids), o, lse)
+        need = wsk.wsk_attend_gpu_workspace(self.h, ids)
+        if self._ws.numel() < need:
+            self._ws = torch.empty(need + 4096, dtype=torch.uint8, device=self.dev)
+        wsk.wsk_attend_gpu(self.h, ids, q, o, lse, self._ws, o_x, lse_x)
+        return o, lse
+
+    def flush(self, parts: Sequence[int], ids: Optional[List[int]] = None):
+        ids = self.ids if ids is None else ids
+        return wsk.wsk_flush(self.h, ids, parts)
 
     def append(self, k_new: torch.Tensor, v_new: Optional[torch.Tensor], ids: Optional[List[int]] = None):
         ids = self.ids if ids is None else ids

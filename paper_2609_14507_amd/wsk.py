@@ -20,7 +20,7 @@ WSK_OK, WSK_EINVAL, WSK_ENOMEM, WSK_ERANGE, WSK_EHIP, WSK_ESTATE = 0, -1, -2, -3
 ERROR_NAMES = {WSK_EINVAL: "EINVAL", WSK_ENOMEM: "ENOMEM", WSK_ERANGE: "ERANGE",
                WSK_EHIP: "EHIP", WSK_ESTATE: "ESTATE"}
 KIND_GQA, KIND_MLA = 0, 1
-PART_CPU, PART_GPU = 0, 1
+PART_CPU, PART_GPU, PART_LOAD = 0, 1, 2
 LAYOUT_ROWS, LAYOUT_TILED64, LAYOUT_MLA32 = 0, 1, 2
 
 
@@ -36,7 +36,15 @@ class wsk_partition_spec(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("latent_dim", ctypes.c_int32), ("rope_dim", ctypes.c_int32),
                 ("block_tokens", ctypes.c_int32), ("max_seqs", ctypes.c_int32), ("max_seq_len", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("device_pool_blocks", ctypes.c_int64),
-                ("host_pool_blocks", ctypes.c_int64), ("softmax_scale", ctypes.c_float)]
+                ("host_pool_blocks", ctypes.c_int64), ("softmax_scale", ctypes.c_float),
+                ("evict_tokens", ctypes.c_int32), ("load_arena_blocks", ctypes.c_int32),
+                ("pingpong_blocks", ctypes.c_int32), ("load_pool_blocks", ctypes.c_int64)]
+
+
+class wsk_load_info(ctypes.Structure):
+    _fields_ = [("pinned_bytes", ctypes.c_int64), ("slots_used", ctypes.c_int64), ("h2d_bytes", ctypes.c_int64),
+                ("d2h_bytes", ctypes.c_int64), ("pin_seconds", ctypes.c_double), ("arenas", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class wsk_loc(ctypes.Structure):
@@ -66,6 +74,14 @@ _SIGS = {
     "wsk_destroy": ([_VP], ctypes.c_int),
     "wsk_get_spec": ([_VP, ctypes.POINTER(wsk_partition_spec)], ctypes.c_int),
     "wsk_seq_open": ([_VP, _I32, _I32], ctypes.c_int),
+    "wsk_seq_open_window": ([_VP, _I32, _I32, _I32], ctypes.c_int),
+    "wsk_seq_segments": ([_VP, _I32, _I32, _PI32, _PI32, _PI32, _PI32], ctypes.c_int),
+    "wsk_flush": ([_VP, _I32, _PI32, _PI32, _PI32, _VP], ctypes.c_int),
+    "wsk_attend_gpu_workspace": ([_VP, _I32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+    "wsk_attend_gpu": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
+    "wsk_cpu_attend_all": ([_VP, _I32, _PI32, _VP, _VP, _VP, _I32], ctypes.c_int),
+    "wsk_load_slot": ([_VP, _I32, ctypes.POINTER(_VP)], ctypes.c_int),
+    "wsk_load_stats": ([_VP, ctypes.POINTER(wsk_load_info)], ctypes.c_int),
     "wsk_seq_close": ([_VP, _I32], ctypes.c_int),
     "wsk_seq_info": ([_VP, _I32, _PI32, _PI32], ctypes.c_int),
     "wsk_reserve": ([_VP, _I32, _I32], ctypes.c_int),
@@ -147,9 +163,11 @@ def wsk_last_error() -> str:
 
 def make_spec(kind: int, n_q_heads: int, n_kv_heads: int, head_dim: int, block_tokens: int, max_seqs: int,
               max_seq_len: int, device_pool_blocks: int, host_pool_blocks: int, softmax_scale: float,
-              latent_dim: int = 0, rope_dim: int = 0) -> wsk_partition_spec:
+              latent_dim: int = 0, rope_dim: int = 0, evict_tokens: int = 0, load_pool_blocks: int = 0,
+              load_arena_blocks: int = 0, pingpong_blocks: int = 0) -> wsk_partition_spec:
     return wsk_partition_spec(kind, n_q_heads, n_kv_heads, head_dim, latent_dim, rope_dim, block_tokens,
-                              max_seqs, max_seq_len, 0, device_pool_blocks, host_pool_blocks, softmax_scale)
+                              max_seqs, max_seq_len, 0, device_pool_blocks, host_pool_blocks, softmax_scale,
+                              evict_tokens, load_arena_blocks, pingpong_blocks, load_pool_blocks)
 
 
 def wsk_init(spec: wsk_partition_spec, device: int) -> int:
@@ -170,6 +188,60 @@ def wsk_get_spec(h: int) -> wsk_partition_spec:
 
 def wsk_seq_open(h: int, seq: int, split: int):
     _check(lib().wsk_seq_open(h, seq, split))
+
+
+def wsk_seq_open_window(h: int, seq: int, split: int, load_end: int):
+    _check(lib().wsk_seq_open_window(h, seq, split, load_end))
+
+
+def wsk_seq_segments(h: int, seq: int):
+    """[(start, end, part), ...] covering [0, L)."""
+    n = ctypes.c_int32()
+    _check(lib().wsk_seq_segments(h, seq, 0, None, None, None, ctypes.byref(n)))
+    cap = max(1, n.value)
+    a, e, p = (ctypes.c_int32 * cap)(), (ctypes.c_int32 * cap)(), (ctypes.c_int32 * cap)()
+    _check(lib().wsk_seq_segments(h, seq, cap, a, e, p, ctypes.byref(n)))
+    return [(a[k], e[k], p[k]) for k in range(n.value)]
+
+
+def wsk_flush(h: int, seq_ids, parts, stream=None):
+    """Evict one D-batch per listed sequence; returns the positions moved per sequence."""
+    moved = (ctypes.c_int32 * max(1, len(seq_ids)))()
+    _check(lib().wsk_flush(h, len(seq_ids), _i32_array(seq_ids), _i32_array(parts), moved, _stream(stream)))
+    return [moved[i] for i in range(len(seq_ids))]
+
+
+def wsk_attend_gpu_workspace(h: int, seq_ids) -> int:
+    b = ctypes.c_size_t()
+    _check(lib().wsk_attend_gpu_workspace(h, len(seq_ids), _i32_array(seq_ids), ctypes.byref(b)))
+    return b.value
+
+
+def wsk_attend_gpu(h: int, seq_ids, q, o, lse, ws, o_x=None, lse_x=None, stream=None):
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().wsk_attend_gpu(h, len(seq_ids), _i32_array(seq_ids), _ptr(q), _ptr(o_x), _ptr(lse_x), _ptr(o),
+                                _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
+
+
+def wsk_cpu_attend_all(h: int, seq_ids, q, o, lse, threads: int = 0):
+    """CPU engine over every CPU-partition position; host numpy arrays as for wsk_cpu_attend."""
+    for a, dt in ((q, np.uint16), (o, np.float32), (lse, np.float32)):
+        if a.dtype != dt or not a.flags["C_CONTIGUOUS"]:
+            raise ValueError("host arrays must be C-contiguous with the documented dtypes")
+    _check(lib().wsk_cpu_attend_all(h, len(seq_ids), _i32_array(seq_ids), q.ctypes.data, o.ctypes.data,
+                                    lse.ctypes.data, threads))
+
+
+def wsk_load_slot(h: int, slot: int) -> int:
+    p = _VP()
+    _check(lib().wsk_load_slot(h, slot, ctypes.byref(p)))
+    return p.value
+
+
+def wsk_load_stats(h: int) -> wsk_load_info:
+    info = wsk_load_info()
+    _check(lib().wsk_load_stats(h, ctypes.byref(info)))
+    return info
 
 
 def wsk_seq_close(h: int, seq: int):
