@@ -228,6 +228,148 @@ def cpu_gpu_steps(w, sess, wsk, steps_in, i0, F, splits, qs, kn, vn, o_m, l_m, f
     return cpu_engine, full, policy
 
 
+PCIE_PEAK_GBS = 63.0   # PCIe 5.0 x16, one direction: 32 GT/s x 16 lanes x 128/130 / 8
+
+
+def load_region_section(w, pf, steps_in, dev, flush, n_steps=5):
+    """The paper's GPU side with the GPU share in the pinned load region
+    (Sec. 4.2): the prefill's GPU positions below the last 256 go to the load
+    region, the rest is the D-window in HBM; a step streams the load region
+    through the ping-pong pair (wsk_attend_gpu) and merges a CPU partial.
+    Also the block-sparse variant (gather + one DMA per buffer), D-window
+    eviction to both homes, the pinning cost, and plain host<->device copies
+    (pinned vs pageable, transfer size, one DMA vs one per block) as the
+    ceilings the streamed rate is compared with.  Timed on the host clock."""
+    import torch
+    from paper_2609_14507_amd import wsk
+    from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
+    from paper_2609_14507_amd import workloads as wl
+    D, bk = 256, 64
+    B, H = len(pf.lengths), w.n_q_heads
+    load_ends = [max(s, (L - D) // bk * bk) for s, L in zip(pf.splits, pf.lengths)]
+    log("load region: routing the prefill (GPU share below the last %d positions pinned)" % D)
+    sess = DecodeSession(w, pf, 0, extra_tokens=D + 2, load_ends=load_ends, evict_tokens=D, pingpong_blocks=512,
+                         arena_blocks=1024)
+    info0 = wsk.wsk_load_stats(sess.h)
+    q = to_device_bf16(steps_in[0].q, dev)
+    width = sess.out_width
+    o = torch.empty(B, H, width, device=dev)
+    lse = torch.empty(B, H, device=dev)
+    o_c, l_c = wl.draw_cpu_partial(pf.gen, B * H, width)
+    o_x = torch.from_numpy(o_c).to(dev).view(B, H, width)
+    l_x = torch.from_numpy(l_c).to(dev).view(B, H)
+
+    def timed(fn, reps):
+        ts = []
+        for _ in range(reps):
+            flush.add_(1)
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            ts.append(time.perf_counter() - t)
+        return float(np.median(ts))
+
+    # dense streamed step
+    sess.attend_gpu(q, o_x=o_x, lse_x=l_x, o=o, lse=lse)
+    torch.cuda.synchronize()
+    h0 = wsk.wsk_load_stats(sess.h).h2d_bytes
+    t_step = timed(lambda: sess.attend_gpu(q, o_x=o_x, lse_x=l_x, o=o, lse=lse), n_steps)
+    h2d = (wsk.wsk_load_stats(sess.h).h2d_bytes - h0) / n_steps
+    win = sum(L - e for L, e in zip(sess.lengths, load_ends)) * w.token_bytes
+    # block-sparse: every 4th load-region block of each sequence plus its D-window blocks
+    sels = []
+    for b in range(B):
+        segs = wsk.wsk_seq_segments(sess.h, b)
+        lb = [blk for a, e, part in segs if part == wsk.PART_LOAD for blk in range(a // bk, -(-e // bk))]
+        gb = [blk for a, e, part in segs if part == wsk.PART_GPU for blk in range(a // bk, -(-e // bk))]
+        sels.append(lb[::4] + gb)
+    need = wsk.wsk_attend_blocks_workspace(sess.h, sess.ids, sels)
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    run_sparse = lambda: wsk.wsk_attend_blocks(sess.h, sess.ids, sels, q, o, lse, ws, o_x, l_x)
+    run_sparse()
+    torch.cuda.synchronize()
+    h0 = wsk.wsk_load_stats(sess.h).h2d_bytes
+    t_sparse = timed(run_sparse, n_steps)
+    h2d_sparse = (wsk.wsk_load_stats(sess.h).h2d_bytes - h0) / n_steps
+    # D-window eviction: one batch of D per sequence to the load region, then
+    # (after D more appends) one to the CPU partition
+    d0 = wsk.wsk_load_stats(sess.h).d2h_bytes
+    t_fl = timed(lambda: sess.flush([wsk.PART_LOAD] * B), 1)
+    d_fl = wsk.wsk_load_stats(sess.h).d2h_bytes - d0
+    if w.kind == wl.MLA:
+        kn, vn = torch.zeros(B, w.row_elems, dtype=torch.bfloat16, device=dev), None
+    else:
+        kn = torch.zeros(B, w.n_kv_heads, w.head_dim, dtype=torch.bfloat16, device=dev)
+        vn = torch.zeros_like(kn)
+    for _ in range(D):
+        sess.append(kn, vn)
+    d0 = wsk.wsk_load_stats(sess.h).d2h_bytes
+    t_fc = timed(lambda: sess.flush([wsk.PART_CPU] * B), 1)
+    d_fc = wsk.wsk_load_stats(sess.h).d2h_bytes - d0
+    info = wsk.wsk_load_stats(sess.h)
+    sess.close()
+
+    # plain copies through the same link
+    def h2d_gbs(nbytes, pinned=True, reps=3):
+        src = torch.empty(nbytes, dtype=torch.uint8, pin_memory=pinned)
+        src.fill_(1)
+        dst = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        dst.copy_(src, non_blocking=pinned)
+        torch.cuda.synchronize()
+        t = timed(lambda: dst.copy_(src, non_blocking=pinned), reps)
+        return nbytes / t / 1e9
+    ceiling = h2d_gbs(256 << 20)
+    micro = {"pinned_256MiB": round(ceiling, 2), "pageable_256MiB": round(h2d_gbs(256 << 20, pinned=False), 2)}
+    for label, n in (("192KiB", 192 << 10), ("1MiB", 1 << 20), ("8MiB", 8 << 20), ("64MiB", 64 << 20)):
+        micro["pinned_" + label] = round(h2d_gbs(n, reps=5), 2)
+    # 64 MiB as one DMA versus one DMA per 128 KiB block from scattered offsets
+    blk = 128 << 10
+    src = torch.empty(128 << 20, dtype=torch.uint8, pin_memory=True)
+    src.fill_(2)
+    dst = torch.empty(64 << 20, dtype=torch.uint8, device=dev)
+    order = np.random.default_rng(0).permutation(1024)[:512]
+    def per_block():
+        for j, k in enumerate(order):
+            dst[j * blk:(j + 1) * blk].copy_(src[int(k) * blk:(int(k) + 1) * blk], non_blocking=True)
+    per_block()
+    torch.cuda.synchronize()
+    micro["per_block_dmas_64MiB"] = round((64 << 20) / timed(per_block, 3) / 1e9, 2)
+    sect = {
+        "workload": w.name,
+        "what": "GPU side of a step with the GPU share in the pinned load region: load-region blocks streamed "
+                "host->device through two HBM ping-pong buffers of 512 blocks while pass 1 attends the other "
+                "buffer, the D-window attended in place, all merged with a CPU partial (wsk_attend_gpu); host "
+                "clock, median of %d, Infinity Cache flushed before each" % n_steps,
+        "bound": "pcie",
+        "streamed_step_ms": round(t_step * 1e3, 3),
+        "h2d_bytes_per_step": int(h2d),
+        "window_bytes_per_step": int(win),
+        "achieved": round(h2d / t_step / 1e9, 2),
+        "peak": PCIE_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(h2d / t_step / 1e9 / PCIE_PEAK_GBS, 4),
+        "copy_ceiling_gbs": round(ceiling, 2),
+        "frac_of_copy_ceiling": round(h2d / t_step / 1e9 / ceiling, 4),
+        "sparse_gather": {"ms": round(t_sparse * 1e3, 3), "h2d_bytes": int(h2d_sparse),
+                          "gbs": round(h2d_sparse / t_sparse / 1e9, 2),
+                          "what": "wsk_attend_blocks: every 4th load-region block (gathered by the host, one memcpy "
+                                  "per block, one DMA per buffer) plus the D-window blocks in place"},
+        "flush": {"to_load": {"ms": round(t_fl * 1e3, 3), "bytes": int(d_fl), "gbs": round(d_fl / t_fl / 1e9, 2)},
+                  "to_cpu": {"ms": round(t_fc * 1e3, 3), "bytes": int(d_fc), "gbs": round(d_fc / t_fc / 1e9, 2)},
+                  "what": "wsk_flush of one D = %d batch of every sequence; to the CPU includes the host's "
+                          "token-major rewrite" % D},
+        "pinning": {"pinned_bytes": int(info0.pinned_bytes), "arenas": int(info0.arenas),
+                    "ms_per_MiB": round(info0.pin_seconds * 1e3 / max(info0.pinned_bytes / 2 ** 20, 1e-9), 4)},
+        "transfer_micro_gbs": micro,
+    }
+    log("load region: streamed step %.2f ms, %.1f GB/s host->device (copy ceiling %.1f, pageable %.1f); sparse %.2f "
+        "ms; flush to load %.2f ms, to CPU %.2f ms; pinning %.3f ms/MiB"
+        % (t_step * 1e3, sect["achieved"], ceiling, micro["pageable_256MiB"], t_sparse * 1e3, t_fl * 1e3, t_fc * 1e3,
+           sect["pinning"]["ms_per_MiB"]))
+    return sect
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -240,6 +382,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cpu-engine", action="store_true",
                     help="skip the native CPU engine and the full CPU + GPU steps")
+    ap.add_argument("--no-load-region", action="store_true",
+                    help="skip the streamed load-region step, eviction and transfer measurements")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, run a plain 256 MiB device copy three times (the reference "
                          "dispatch that scales HBM byte counters)")
@@ -359,6 +503,7 @@ def main():
             gpu_ns_per_token=float(p1_ms.mean() * 1e6 / (d_bytes.mean() / w.token_bytes)),
             gpu_fixed_us=float((step_ms.mean() - p1_ms.mean()) * 1e3))
     sess.close()
+    load_region = None if args.no_load_region else load_region_section(w, pf, steps_in, dev, flush)
     # plain streaming read of 2 GiB with the attention kernels' load pattern:
     # the practical HBM read ceiling the pass-1 rate is compared with
     from paper_2609_14507_amd import wsk as _wsk
@@ -432,6 +577,8 @@ def main():
                               "what": "wsk_stream_read: one plain read of 2 GiB with the attention kernels' "
                                       "loads, median of 5, cache flushed before each"},
     }
+    if load_region is not None:
+        out["load_region"] = load_region
     if cpu_engine is not None:
         out["cpu_engine"] = cpu_engine
         out["full_step"] = full_step

@@ -379,6 +379,15 @@ private:
 
 }  // namespace
 
+void parallel_tasks(int n_tasks, int threads, const std::function<void(int)> &task) {
+    if (n_tasks <= 0) return;
+    std::atomic<int> next{0};
+    const std::function<void()> worker = [&]() {
+        for (int k; (k = next.fetch_add(1)) < n_tasks;) task(k);
+    };
+    WorkerPool::get().run(std::max(0, std::min(threads, n_tasks) - 1), worker);
+}
+
 int cpu_attend(const CpuAttendArgs &x) {
     Job job;
     job.x = &x;

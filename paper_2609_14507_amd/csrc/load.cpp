@@ -86,6 +86,11 @@ void get_position(const wsk_cache *c, const uint16_t *slot, int off, uint16_t *c
 
 int32_t arena_blocks(const wsk_cache *c) { return c->spec.load_arena_blocks; }
 
+// Host threads for the block gathers and row rewrites: one thread copies
+// ~20 GB/s, the host-to-device link takes ~57, so a few threads keep the
+// link busy.
+int gather_threads() { return (int)std::min(8u, std::max(1u, std::thread::hardware_concurrency())); }
+
 // Allocates arena k: pinned (hipHostMalloc) on a device cache, plain aligned
 // host memory on a host-only one.  Records the time spent.
 int pin_arena(wsk_cache *c, size_t k) {
@@ -112,8 +117,9 @@ int pin_arena(wsk_cache *c, size_t k) {
     return WSK_OK;
 }
 
-// Gathers the rows of positions [a, e) of sequence seq out of bounce (GPU
-// layout, block b at bounce + index_of[b] slots) into the CPU pool.
+// Writes the rows of positions [a, e) of sequence seq, read out of bounce
+// (GPU layout; block first_blk + j at slot j of bounce), token-major into
+// the CPU pool.
 void untile_to_cpu(wsk_cache *c, int32_t seq, int32_t a, int32_t e, const uint16_t *bounce, int32_t first_blk) {
     const int bk = c->spec.block_tokens;
     const int hkv = c->spec.kind == WSK_KIND_GQA ? c->spec.n_kv_heads : 1;
@@ -475,13 +481,21 @@ int run_plan(wsk_cache *c, int32_t n, GpuPlan &g, bool gather, const void *q, co
         e = hipStreamWaitEvent(cs, c->consumed[b], 0);   // the kernels that read buffer b are done
         if (e != hipSuccess) break;
         if (gather) {
-            // gather the selected blocks into staging b (one memcpy each),
-            // then one DMA; the next gather overlaps this DMA
+            // gather the selected blocks into staging b (one memcpy each, on
+            // several threads) and send them as one contiguous DMA per ~8 MB
+            // piece, so that the gather of the next piece overlaps this DMA
             e = hipEventSynchronize(c->staged[b]);
-            if (e != hipSuccess) break;
-            for (size_t j = j0; j < j1; ++j)
-                memcpy(c->hgather[b] + (int64_t)(j - j0) * c->slot_elems, load_slot_ptr(c, g.pieces[j].slot), sb);
-            e = hipMemcpyAsync(c->pingpong[b], c->hgather[b], (j1 - j0) * sb, hipMemcpyHostToDevice, cs);
+            const size_t piece = std::max<size_t>(1, (8u << 20) / sb);
+            for (size_t p0 = j0; p0 < j1 && e == hipSuccess; p0 += piece) {
+                const size_t p1 = std::min(j1, p0 + piece);
+                parallel_tasks((int)(p1 - p0), gather_threads(), [&](int t) {
+                    memcpy(c->hgather[b] + (int64_t)(p0 - j0 + t) * c->slot_elems,
+                           load_slot_ptr(c, g.pieces[p0 + t].slot), sb);
+                });
+                e = hipMemcpyAsync(c->pingpong[b] + (int64_t)(p0 - j0) * c->slot_elems,
+                                   c->hgather[b] + (int64_t)(p0 - j0) * c->slot_elems, (p1 - p0) * sb,
+                                   hipMemcpyHostToDevice, cs);
+            }
             if (e == hipSuccess) e = hipEventRecord(c->staged[b], cs);
         } else {
             // one DMA per run of consecutive slots of one arena
@@ -608,11 +622,17 @@ int wsk_flush(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *part, 
         if (part[i] != WSK_PART_LOAD || w1[i] == w0[i]) continue;
         any_load = true;
         const int32_t sq = ids[i];
-        for (int32_t blk = w0[i] / bk; blk < w1[i] / bk && e == hipSuccess; ++blk) {
-            e = hipMemcpyAsync(load_slot_ptr(c, tab(c, WSK_PART_LOAD, sq, blk)),
-                               c->dpool + (int64_t)tab(c, WSK_PART_GPU, sq, blk) * c->slot_elems, sb,
+        // one DMA per run of blocks consecutive in both pools (and in one arena)
+        for (int32_t blk = w0[i] / bk; blk < w1[i] / bk && e == hipSuccess;) {
+            const int32_t ls = tab(c, WSK_PART_LOAD, sq, blk), gs = tab(c, WSK_PART_GPU, sq, blk);
+            int32_t r = 1;
+            while (blk + r < w1[i] / bk && tab(c, WSK_PART_LOAD, sq, blk + r) == ls + r &&
+                   tab(c, WSK_PART_GPU, sq, blk + r) == gs + r && (ls + r) % arena_blocks(c) != 0)
+                ++r;
+            e = hipMemcpyAsync(load_slot_ptr(c, ls), c->dpool + (int64_t)gs * c->slot_elems, r * sb,
                                hipMemcpyDeviceToHost, st);
-            c->d2h_bytes += (int64_t)sb;
+            c->d2h_bytes += (int64_t)(r * sb);
+            blk += r;
         }
     }
     if (any_load && e == hipSuccess) e = hipEventRecord(c->flush_ev, st);
@@ -641,12 +661,23 @@ int wsk_flush(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *part, 
             }
         }
         if (e == hipSuccess) e = hipStreamSynchronize(st);
+        // one task per evicted block: rows [max(w0, blk Bk), (blk + 1) Bk)
+        struct Task {
+            int32_t seq, a, e;
+            size_t at;
+        };
+        std::vector<Task> tasks;
         at = 0;
-        for (int32_t i = 0; i < n && e == hipSuccess; ++i) {
-            if (part[i] != WSK_PART_CPU || w1[i] == w0[i]) continue;
-            untile_to_cpu(c, ids[i], w0[i], w1[i], c->hbounce + (int64_t)at * c->slot_elems, w0[i] / bk);
-            at += (size_t)(w1[i] / bk - w0[i] / bk);
+        for (int32_t i = 0; i < n; ++i) {
+            if (part[i] != WSK_PART_CPU) continue;
+            for (int32_t blk = w0[i] / bk; blk < w1[i] / bk; ++blk, ++at)
+                tasks.push_back({ids[i], std::max(w0[i], blk * bk), (blk + 1) * bk, at});
         }
+        if (e == hipSuccess)
+            parallel_tasks((int)tasks.size(), gather_threads(), [&](int t) {
+                const Task &k = tasks[t];
+                untile_to_cpu(c, k.seq, k.a, k.e, c->hbounce + (int64_t)k.at * c->slot_elems, k.a / bk);
+            });
     }
     // the batch now lives in its new home: free the GPU-pool slots, extend
     // the segments, move the window

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <functional>
+
 namespace wsk {
 
 // Sequences handled by one kernel launch; a call with more is split.
@@ -119,6 +121,9 @@ struct CpuAttendArgs {
     int threads;
 };
 int cpu_attend(const CpuAttendArgs &args);
+// Runs task(0 .. n_tasks-1) on up to `threads` host threads (the calling one
+// and the CPU engine's persistent pool); returns when all are done.
+void parallel_tasks(int n_tasks, int threads, const std::function<void(int)> &task);
 
 // Sets the calling thread's last error message; returns code.
 int policy_fail(int code, const char *msg);
