@@ -370,6 +370,78 @@ def load_region_section(w, pf, steps_in, dev, flush, n_steps=5):
     return sect
 
 
+def offload_section(w, pf, steps_in, dev, flush, A_s, c_cpu_s, B_s, n_steps=5):
+    """The paper's step when the KV does not stay in HBM (Sec. 4.2, 5.1): each
+    sequence's CPU share [0, s) is attended in place by the CPU engine while
+    the GPU streams its share from the pinned load region (plus the D-window)
+    and attends it; one LSE join.  Timed on the host clock for the all-GPU
+    split (s = 0) and for the split Eq. 2 gives with A (CPU engine) and B
+    (streamed GPU side) measured on this machine."""
+    import torch
+    from paper_2609_14507_amd import wsk
+    from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
+    from paper_2609_14507_amd import workloads as wl
+    D, bk = 256, 64
+    B, H = len(pf.lengths), w.n_q_heads
+    threads = len(os.sched_getaffinity(0))
+    L_mean = float(np.mean(pf.lengths))
+    r_star = wsk.wsk_roofline_share(A_s, B_s, c_cpu_s, 0.0, int(L_mean))
+    q_bits = np.ascontiguousarray(steps_in[0].q)
+    q = to_device_bf16(q_bits, dev)
+    rows = []
+    for label, r in (("all_gpu", 0.0), ("balanced", r_star)):
+        splits = [wl.split_point(r, L) for L in pf.lengths]
+        load_ends = [max(s, (L - D) // bk * bk) for s, L in zip(splits, pf.lengths)]
+        p2 = wl.Prefill(pf.lengths, splits, pf.k, pf.v, pf.gen)
+        log("offload: routing the prefill with CPU share %.3f" % r)
+        sess = DecodeSession(w, p2, 0, extra_tokens=0, load_ends=load_ends, evict_tokens=D, pingpong_blocks=512,
+                             arena_blocks=1024)
+        width = sess.out_width
+        o_c = np.empty((B, H, width), np.float32)
+        l_c = np.empty((B, H), np.float32)
+        o_pin = torch.empty(B, H, width, pin_memory=True)
+        l_pin = torch.empty(B, H, pin_memory=True)
+        o_x = torch.empty(B, H, width, device=dev)
+        l_x = torch.empty(B, H, device=dev)
+        o = torch.empty(B, H, width, device=dev)
+        lse = torch.empty(B, H, device=dev)
+
+        def full_step():
+            sess.attend_gpu_pass1(q)                              # transfers + kernels in flight ...
+            wsk.wsk_cpu_attend_all(sess.h, sess.ids, q_bits, o_c, l_c, threads)   # ... while the CPU attends
+            o_pin.numpy()[:] = o_c
+            l_pin.numpy()[:] = l_c
+            o_x.copy_(o_pin, non_blocking=True)
+            l_x.copy_(l_pin, non_blocking=True)
+            sess.attend_gpu_pass2(o_x=o_x, lse_x=l_x, o=o, lse=lse)
+
+        ts = []
+        for it in range(n_steps + 1):
+            flush.add_(1)
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            full_step()
+            torch.cuda.synchronize()
+            if it:
+                ts.append(time.perf_counter() - t)
+        cpu_tok = sum(min(s, L) for s, L in zip(splits, pf.lengths))
+        rows.append((label, r, float(np.median(ts)), cpu_tok))
+        sess.close()
+    base = rows[0][2]
+    out = {"what": "full decode step with the GPU share offloaded: GPU side streamed from the pinned load region "
+                   "(wsk_attend_gpu_pass1) while the CPU engine attends [0, s) in place (wsk_cpu_attend_all, %d "
+                   "threads), CPU partial copied over, one LSE join (wsk_attend_gpu_pass2); host clock, median of "
+                   "%d" % (threads, n_steps),
+           "A_ns_per_token": round(A_s * 1e9, 3), "B_ns_per_token": round(B_s * 1e9, 3),
+           "c_cpu_us": round(c_cpu_s * 1e6, 1), "eq2_share": round(r_star, 4)}
+    for label, r, t, tok in rows:
+        out[label] = {"cpu_share": round(r, 4), "ms": round(t * 1e3, 3), "cpu_tokens": int(tok),
+                      "speedup_vs_all_gpu": round(base / t, 3)}
+    log("offload: all-GPU streamed step %.2f ms; Eq. 2 share %.3f step %.2f ms (%.2fx)"
+        % (rows[0][2] * 1e3, r_star, rows[1][2] * 1e3, base / rows[1][2]))
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -504,6 +576,10 @@ def main():
             gpu_fixed_us=float((step_ms.mean() - p1_ms.mean()) * 1e3))
     sess.close()
     load_region = None if args.no_load_region else load_region_section(w, pf, steps_in, dev, flush)
+    offload = None
+    if load_region is not None and policy is not None:
+        offload = offload_section(w, pf, steps_in, dev, flush, policy["A_ns_per_token"] * 1e-9,
+                                  policy["c_cpu_us"] * 1e-6, w.token_bytes / (load_region["achieved"] * 1e9))
     # plain streaming read of 2 GiB with the attention kernels' load pattern:
     # the practical HBM read ceiling the pass-1 rate is compared with
     from paper_2609_14507_amd import wsk as _wsk
@@ -579,6 +655,8 @@ def main():
     }
     if load_region is not None:
         out["load_region"] = load_region
+    if offload is not None:
+        out["offload_step"] = offload
     if cpu_engine is not None:
         out["cpu_engine"] = cpu_engine
         out["full_step"] = full_step

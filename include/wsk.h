@@ -457,6 +457,17 @@ int wsk_attend_gpu_workspace(const wsk_cache *cache, int32_t n, const int32_t *s
 int wsk_attend_gpu(wsk_cache *cache, int32_t n, const int32_t *seq_ids, const void *q, const float *o_x,
                    const float *lse_x, float *o, float *lse, void *ws, size_t ws_bytes, void *stream);
 
+/* wsk_attend_gpu as its two passes, so that the CPU engine can compute the
+ * CPU partial while the load region streams (Sec. 4.2: the CPU and the GPU
+ * attend at the same time, one join per step): pass 1 enqueues the
+ * transfers and the attention kernels and leaves the partials in ws; pass 2,
+ * called with the same sequences and no cache change in between, merges
+ * them and o_x / lse_x into o / lse.  Arguments as for wsk_attend_gpu. */
+int wsk_attend_gpu_pass1(wsk_cache *cache, int32_t n, const int32_t *seq_ids, const void *q, void *ws,
+                         size_t ws_bytes, void *stream);
+int wsk_attend_gpu_pass2(wsk_cache *cache, int32_t n, const int32_t *seq_ids, const float *o_x,
+                         const float *lse_x, float *o, float *lse, void *ws, size_t ws_bytes, void *stream);
+
 /*
  * D-window eviction ("flush", Sec. 4.2 and 4.3): for each listed sequence
  * whose D-window [w, L) holds a whole batch, move the batch [w, w') to

@@ -426,10 +426,10 @@ int plan_selection(const wsk_cache *c, int32_t n, const int32_t *ids, const int3
 
 // ---- the GPU side of a step: execution --------------------------------------------
 int run_plan(wsk_cache *c, int32_t n, GpuPlan &g, bool gather, const void *q, const float *o_x, const float *lse_x,
-             float *o, float *lse, void *ws, size_t ws_bytes, void *stream) {
+             float *o, float *lse, void *ws, size_t ws_bytes, void *stream, bool pass1 = true, bool pass2 = true) {
     if (n == 0) return WSK_OK;
     if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
-    int rc = check_outputs(q, o, lse, o_x, lse_x, true, true);
+    int rc = check_outputs(q, o, lse, o_x, lse_x, pass1, pass2);
     if (rc) return rc;
     if (!ws || ws_bytes < g.bytes) return fail(WSK_EINVAL, "workspace of %zu bytes needed", g.bytes);
     if (((uintptr_t)ws & 255) != 0) return fail(WSK_EINVAL, "workspace must be 256-byte aligned");
@@ -440,6 +440,11 @@ int run_plan(wsk_cache *c, int32_t n, GpuPlan &g, bool gather, const void *q, co
     float *part_o = (float *)ws;
     float *part_lse = (float *)((char *)ws + g.part_o_bytes);
     hipError_t e = hipSuccess;
+    if (!pass1) {
+        e = launch_combine_all(c, n, g.pb, part_o, part_lse, o_x, lse_x, o, lse, st);
+        if (e != hipSuccess) return hip_fail(e, "GPU-side attention, pass 2");
+        return WSK_OK;
+    }
 
     // GPU-pool rows, in place
     g.hbm.pool = c->dpool;
@@ -520,7 +525,7 @@ int run_plan(wsk_cache *c, int32_t n, GpuPlan &g, bool gather, const void *q, co
         e = launch_rows(c, rl, n, q, part_o, part_lse, st);
         if (e == hipSuccess) e = hipEventRecord(c->consumed[b], st);
     }
-    if (e == hipSuccess) e = launch_combine_all(c, n, g.pb, part_o, part_lse, o_x, lse_x, o, lse, st);
+    if (e == hipSuccess && pass2) e = launch_combine_all(c, n, g.pb, part_o, part_lse, o_x, lse_x, o, lse, st);
     if (e != hipSuccess) return hip_fail(e, "GPU-side attention");
     return WSK_OK;
 }
@@ -544,6 +549,22 @@ int wsk_attend_gpu(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, c
     int rc = plan_dense(c, n, ids, g);
     if (rc) return rc;
     return run_plan(c, n, g, false, q, o_x, lse_x, o, lse, ws, ws_bytes, stream);
+}
+
+int wsk_attend_gpu_pass1(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, void *ws, size_t ws_bytes,
+                         void *stream) {
+    GpuPlan g;
+    int rc = plan_dense(c, n, ids, g);
+    if (rc) return rc;
+    return run_plan(c, n, g, false, q, nullptr, nullptr, nullptr, nullptr, ws, ws_bytes, stream, true, false);
+}
+
+int wsk_attend_gpu_pass2(wsk_cache *c, int32_t n, const int32_t *ids, const float *o_x, const float *lse_x, float *o,
+                         float *lse, void *ws, size_t ws_bytes, void *stream) {
+    GpuPlan g;
+    int rc = plan_dense(c, n, ids, g);
+    if (rc) return rc;
+    return run_plan(c, n, g, false, nullptr, o_x, lse_x, o, lse, ws, ws_bytes, stream, false, true);
 }
 
 int wsk_attend_blocks_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin,

@@ -99,6 +99,21 @@ class DecodeSession:
         wsk.wsk_attend_gpu(self.h, ids, q, o, lse, self._ws, o_x, lse_x)
         return o, lse
 
+    def attend_gpu_pass1(self, q: torch.Tensor, ids: Optional[List[int]] = None):
+        """Pass 1 of attend_gpu (transfers and kernels enqueued, partials in the
+        session workspace); attend_gpu_pass2 with the same ids completes it."""
+        ids = self.ids if ids is None else ids
+        need = wsk.wsk_attend_gpu_workspace(self.h, ids)
+        if self._ws.numel() < need:
+            self._ws = torch.empty(need + 4096, dtype=torch.uint8, device=self.dev)
+        wsk.wsk_attend_gpu_pass1(self.h, ids, q, self._ws)
+
+    def attend_gpu_pass2(self, ids: Optional[List[int]] = None, o_x=None, lse_x=None, o=None, lse=None):
+        ids = self.ids if ids is None else ids
+        o, lse = self._outputs(len(ids), o, lse)
+        wsk.wsk_attend_gpu_pass2(self.h, ids, o, lse, self._ws, o_x, lse_x)
+        return o, lse
+
     def flush(self, parts: Sequence[int], ids: Optional[List[int]] = None):
         ids = self.ids if ids is None else ids
         return wsk.wsk_flush(self.h, ids, parts)

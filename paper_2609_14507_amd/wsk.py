@@ -79,6 +79,8 @@ _SIGS = {
     "wsk_flush": ([_VP, _I32, _PI32, _PI32, _PI32, _VP], ctypes.c_int),
     "wsk_attend_gpu_workspace": ([_VP, _I32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_attend_gpu": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
+    "wsk_attend_gpu_pass1": ([_VP, _I32, _PI32, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
+    "wsk_attend_gpu_pass2": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_cpu_attend_all": ([_VP, _I32, _PI32, _VP, _VP, _VP, _I32], ctypes.c_int),
     "wsk_load_slot": ([_VP, _I32, ctypes.POINTER(_VP)], ctypes.c_int),
     "wsk_load_stats": ([_VP, ctypes.POINTER(wsk_load_info)], ctypes.c_int),
@@ -221,6 +223,18 @@ def wsk_attend_gpu(h: int, seq_ids, q, o, lse, ws, o_x=None, lse_x=None, stream=
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(lib().wsk_attend_gpu(h, len(seq_ids), _i32_array(seq_ids), _ptr(q), _ptr(o_x), _ptr(lse_x), _ptr(o),
                                 _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
+
+
+def wsk_attend_gpu_pass1(h: int, seq_ids, q, ws, stream=None):
+    nbytes = ws.numel() * ws.element_size()
+    _check(lib().wsk_attend_gpu_pass1(h, len(seq_ids), _i32_array(seq_ids), _ptr(q), _ptr(ws), nbytes,
+                                      _stream(stream)))
+
+
+def wsk_attend_gpu_pass2(h: int, seq_ids, o, lse, ws, o_x=None, lse_x=None, stream=None):
+    nbytes = ws.numel() * ws.element_size()
+    _check(lib().wsk_attend_gpu_pass2(h, len(seq_ids), _i32_array(seq_ids), _ptr(o_x), _ptr(lse_x), _ptr(o),
+                                      _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
 
 
 def wsk_cpu_attend_all(h: int, seq_ids, q, o, lse, threads: int = 0):

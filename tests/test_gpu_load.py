@@ -107,9 +107,15 @@ def test_streamed_attend(kind, bk, pp):
         o, lse = sess.attend_gpu(q, o_x=o_x, lse_x=l_x)
         _check(w, q_bits, pf.k, pf.v, [np.arange(L) for L in lengths], o.cpu().numpy(), lse.cpu().numpy(),
                "whole step")
+        # the two-pass form with the CPU engine running between the passes
+        # (while the transfers and kernels of pass 1 are in flight)
+        sess.attend_gpu_pass1(q)
+        o_x2, l_x2 = _cpu_partial(sess, q_bits)
+        o2, lse2 = sess.attend_gpu_pass2(o_x=o_x2, lse_x=l_x2)
+        assert torch.equal(o2, o) and torch.equal(lse2, lse)
         st = wsk.wsk_load_stats(sess.h)
         load_blocks = sum(-(-min(e, L) // bk) - s // bk for s, e, L in zip(splits, load_ends, lengths) if min(e, L) > s)
-        assert st.h2d_bytes == 3 * load_blocks * w.token_bytes * bk   # three calls
+        assert st.h2d_bytes == 4 * load_blocks * w.token_bytes * bk   # four calls
 
 
 def test_streamed_attend_many_sequences():
