@@ -109,14 +109,14 @@ TRAFFIC = {
     "qwen3-30b-a3b-b16-L32768": {
         "source": "paper_2609_14507_amd/csrc/attend_gqa.hip",
         "sha256": "e5813847daac21bddd068a7f125084699f8189c717c91099486efc5dc7c2acb6",
-        "fetch_bytes": 368959.1 * 1024 * 2.0,
+        "fetch_bytes": 368957.2 * 1024 * 2.0,
         "write_bytes": 2064.0 * 1024 * 1.0,
         "kv_bytes": 751714304,
     },
     "deepseek-v2-lite-mla-b8-L65536": {
         "source": "paper_2609_14507_amd/csrc/attend_mla.hip",
         "sha256": "ae01f652ea0f430a3eb4abe15a9a5220abb73a5e31f7d907432c7c904ed80c47",
-        "fetch_bytes": 177757.9 * 1024 * 2.0,
+        "fetch_bytes": 177772.1 * 1024 * 2.0,
         "write_bytes": 7951.5 * 1024 * 1.0,
         "kv_bytes": 362414592,
     },
