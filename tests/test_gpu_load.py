@@ -270,3 +270,63 @@ def test_sparse_selection_with_load_blocks(kind, bk):
         with pytest.raises(wsk.WskError) as ei:           # past L
             wsk.wsk_attend_blocks_workspace(sess.h, [2], [[5]])
         assert ei.value.code == wsk.WSK_ERANGE
+
+
+def test_policy_routed_eviction_follows_R_of_L():
+    """The split policy drives eviction (Sec. 5.3 with Sec. 4.2): every D-batch
+    goes where wsk_policy_route_batch sends it (the GPU side is the load region
+    here), so after k batches the CPU share of the placed positions is
+    R(L) = p + (R0 - p) L0 / L within D / (2L), and the full step still equals
+    attention over the whole context."""
+    from oracle import policy as P
+    bk, D, batches = 64, 128, 12
+    L0s, s0s = [1000, 700], [200, 420]
+    load_ends = [896, 640]
+    w = _workload("gqa", 2, H=8, seed=9)
+    gen = torch.Generator().manual_seed(21)
+    pf = _prefill(w, L0s, s0s, gen)
+    k_all, v_all = list(pf.k), list(pf.v)
+    A, Bc = 2e-9, 3e-9                      # p = 0.6
+    pols = [wsk.Policy(A, Bc, 1e-5, 1e-5, 4) for _ in range(2)]
+    say("case policy eviction")
+    try:
+        with DecodeSession(w, pf, DEV, extra_tokens=batches * D + D, load_ends=load_ends, evict_tokens=D,
+                           pingpong_blocks=4, arena_blocks=8) as sess:
+            placed0 = list(load_ends)
+            cpu = list(s0s)
+            done = [0, 0]
+            while min(done) < batches:
+                kn = wl.draw_bf16(gen, (2, w.n_kv_heads, w.head_dim))
+                vn = wl.draw_bf16(gen, (2, w.n_kv_heads, w.head_dim))
+                sess.append(to_device_bf16(kn, sess.dev), to_device_bf16(vn, sess.dev))
+                for b in range(2):
+                    k_all[b] = np.concatenate([k_all[b], kn[b:b + 1]])
+                    v_all[b] = np.concatenate([v_all[b], vn[b:b + 1]])
+                for b in range(2):
+                    if done[b] >= batches or sess.gpu_range(b)[1] - sess.gpu_range(b)[0] < D:
+                        continue
+                    part = pols[b].route()
+                    dest = CPU if part == wsk.PART_CPU else LOAD
+                    moved = wsk.wsk_flush(sess.h, [b], [dest])
+                    assert moved == [D]
+                    done[b] += 1
+                    if dest == CPU:
+                        cpu[b] += D
+                    L = placed0[b] + done[b] * D
+                    R0 = s0s[b] / placed0[b]
+                    R = P.cumulative_share(L, placed0[b], R0, P.marginal_share(A, Bc))
+                    assert abs(cpu[b] / L - R) <= D / (2 * L) + 1e-12, (b, done[b], cpu[b] / L, R)
+            # the library's segments agree with the count of CPU positions
+            for b in range(2):
+                segs = wsk.wsk_seq_segments(sess.h, b)
+                w_start = sess.gpu_range(b)[0]
+                assert sum(e - a for a, e, p_ in segs if p_ == CPU) == cpu[b]
+                assert w_start == placed0[b] + batches * D
+            q_bits = wl.draw_bf16(gen, (2, w.n_q_heads, w.row_elems))
+            o_x, l_x = _cpu_partial(sess, q_bits)
+            o, lse = sess.attend_gpu(to_device_bf16(q_bits, sess.dev), o_x=o_x, lse_x=l_x)
+            _check(w, q_bits, k_all, v_all, [np.arange(L) for L in sess.lengths], o.cpu().numpy(),
+                   lse.cpu().numpy(), "policy-routed")
+    finally:
+        for p_ in pols:
+            p_.close()
