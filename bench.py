@@ -1,10 +1,11 @@
 """Benchmark of the GPU-partition decode step on one MI355X.
 
-One step = the whole hot path over one batch: append the new token's K/V of
-every sequence into its GPU partition, split-KV attention over the GPU range
-(pass 1), then pass 2, which merges the chunk partials and the CPU-range
-partial by their LSE in one launch (MLA adds the query absorption before and
-the output expansion after).  Inputs are seeded synthetic tensors already
+One step = the whole hot path over one batch (wsk_decode_step): the new
+token's K/V of every sequence is routed to its GPU partition, split-KV
+attention covers the GPU range written so far (pass 1), then one pass 2
+scores and merges the new token, stores it into the pool, and merges the
+chunk partials and the CPU-range partial by their LSE (MLA adds the query
+absorption before and the output expansion after).  Inputs are seeded synthetic tensors already
 resident in HBM; the CPU-range partial fed to the merge is a seeded
 synthetic (O, LSE) pair (the merge's cost does not depend on its values).
 
@@ -507,9 +508,13 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step(i, ev=None, parts=None):
-        """One decode step.  ev = (start, end) events around the step; parts =
-        5 events around its pieces (diagnostic steps only: every event record
-        costs GPU time of its own)."""
+        """One decode step.  ev = (start, end) events around the step: the timed
+        steps run it as wsk_decode_step (pass 1 over the positions written so
+        far, then one pass 2 that folds in the appended row, stores it and
+        merges the CPU partial).  parts = 5 events around its pieces
+        (diagnostic steps only, every event record costs GPU time of its own):
+        those run the same work as separate calls -- append, pass 1 over
+        [s, L + 1), pass 2 -- so that pass 1 is timed on its own."""
         if not args.no_flush:
             flush.add_(1)
         mark = (lambda k: parts[k].record(stream)) if parts else (lambda k: None)
@@ -518,14 +523,15 @@ def main():
         mark(0)
         if mla:   # query-side projection into the latent space, in place
             wsk.wsk_mla_absorb(qn[i], w_uk_d, qs[i], w.row_elems)
-        sess.append(kn[i], vn[i])
-        mark(1)
-        # wsk_attend as its two passes, so that pass 1 (the KV-streaming
-        # kernel) is timed on its own; pass 2 also merges the CPU partial
-        sess.attend_pass1(qs[i])
-        mark(2)
-        sess.attend_pass2(o=o_m, lse=l_m, o_x=o_cpu, lse_x=l_cpu)
-        mark(3)
+        if parts:
+            sess.append(kn[i], vn[i])
+            mark(1)
+            sess.attend_pass1(qs[i])
+            mark(2)
+            sess.attend_pass2(o=o_m, lse=l_m, o_x=o_cpu, lse_x=l_cpu)
+            mark(3)
+        else:
+            sess.decode_step(qs[i], kn[i], vn[i], o_x=o_cpu, lse_x=l_cpu, o=o_m, lse=l_m)
         if mla:   # output-side expansion of the merged latent output
             wsk.wsk_mla_expand(o_m, w_uv_d, o_out)
             mark(4)
@@ -633,8 +639,10 @@ def main():
             "cpu_share": args.share if args.share is not None else (w.cpu_share or [w.share_lo, w.share_hi]),
             "gpu_tokens_per_step": int(nbytes.mean() / w.token_bytes),
             "kv_bytes_per_step": int(nbytes.mean()),
-            "step": ("absorb + append + attend pass 1 + (chunk combine + LSE merge with the CPU partial) + expand"
-                     if mla else "append + attend pass 1 + (chunk combine + LSE merge with the CPU partial)"),
+            "step": ("absorb + wsk_decode_step (attend pass 1 over [s, L), then one pass 2: the appended row "
+                     "scored, merged and stored, chunk combine, LSE merge with the CPU partial) + expand"
+                     if mla else "wsk_decode_step: attend pass 1 over [s, L), then one pass 2: the appended row "
+                     "scored, merged and stored, chunk combine, LSE merge with the CPU partial"),
             "cache_flush_between_steps": not args.no_flush,
         },
         "breakdown_us": {

@@ -469,6 +469,28 @@ int wsk_attend_gpu_pass2(wsk_cache *cache, int32_t n, const int32_t *seq_ids, co
                          const float *lse_x, float *o, float *lse, void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * One decode step of the GPU side (Sec. 4.2): the append of each listed
+ * sequence's new row at position L (as wsk_append), then every query head
+ * attends all its GPU-side positions [.., L] -- the new row included -- and
+ * the result is merged with o_x / lse_x when given (as wsk_attend_gpu).
+ * Same result as wsk_append followed by wsk_attend_gpu, in one launch less:
+ * pass 1 covers the positions written before the call, and pass 2 scores the
+ * new row straight from k_new (q . k_new), merges it as one more partial and
+ * stores it into the GPU pool.  seq_ids: HOST array of n > 0 distinct open
+ * sequences; q, k_new, v_new, o_x, lse_x, o, lse, ws: DEVICE pointers laid out
+ * as for wsk_append and wsk_attend_gpu; ws of at least
+ * wsk_decode_step_workspace() bytes, queried before the call (it does not
+ * depend on the new rows).  All checks happen before the routing, so a
+ * failed call (other than EHIP) changes nothing.
+ * Errors: EINVAL, ESTATE, ERANGE (a full sequence, or L below load_end),
+ * ENOMEM, EHIP.
+ */
+int wsk_decode_step_workspace(const wsk_cache *cache, int32_t n, const int32_t *seq_ids, size_t *bytes);
+int wsk_decode_step(wsk_cache *cache, int32_t n, const int32_t *seq_ids, const void *q, const void *k_new,
+                    const void *v_new, const float *o_x, const float *lse_x, float *o, float *lse, void *ws,
+                    size_t ws_bytes, void *stream);
+
+/*
  * D-window eviction ("flush", Sec. 4.2 and 4.3): for each listed sequence
  * whose D-window [w, L) holds a whole batch, move the batch [w, w') to
  * part[i] (WSK_PART_CPU or WSK_PART_LOAD) and set w = w', where

@@ -82,10 +82,12 @@ __device__ __forceinline__ float block_reduce(float v, bool is_max, float *s_red
     return r;
 }
 
-__global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int width) {
-    __shared__ float s_w[kCombineW];
-    __shared__ float s_red[4];
-    __shared__ f32x4 s_acc[kCombineGroups][kCombineCols4];
+// One workgroup's part of the combine.  s_new / v_new: an optional partial
+// made of a single token (score s_new in the natural-log domain, value row
+// v_new, bf16, starting at this workgroup's first column); -INFINITY / NULL
+// when absent.
+__device__ __forceinline__ void combine_row(const CombineParams &p, int width, float s_new, const uint16_t *v_new,
+                                            float *s_w, float *s_red, f32x4 (*s_acc)[kCombineCols4]) {
     const int row = blockIdx.x;                 // i * H + h
     const int H = p.n_q_heads;
     const int i = row / H;
@@ -96,18 +98,19 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int
     const int col0 = blockIdx.y * 4 * kCombineCols4;
     f32x4 *out = reinterpret_cast<f32x4 *>(p.o + (int64_t)row * width + col0);
     const float lx = p.lse_x ? p.lse_x[row] : -INFINITY;
-    if (nc == 0 && lx == -INFINITY) {
+    if (nc == 0 && lx == -INFINITY && s_new == -INFINITY) {
         if (tid < kCombineCols4) out[tid] = f32x4{0.f, 0.f, 0.f, 0.f};
         if (tid == 0 && blockIdx.y == 0) p.lse[row] = -INFINITY;
         return;
     }
     const float *pl = p.part_lse + (int64_t)c0 * H + h;
-    float m = lx;
+    float m = fmaxf(lx, s_new);
     for (int c = tid; c < nc; c += 256) m = fmaxf(m, pl[(int64_t)c * H]);
     m = block_reduce(m, true, s_red);
-    // the other partial: weight wx (0 when absent or empty; then it is not read)
+    // the other partials: weights wx, wn (0 when absent or empty; then they are not read)
     const float wx = lx == -INFINITY ? 0.f : __expf(lx - m);
-    float dsum = tid == 0 ? wx : 0.f;
+    const float wn = s_new == -INFINITY ? 0.f : __expf(s_new - m);
+    float dsum = tid == 0 ? wx + wn : 0.f;
     for (int c = tid; c < nc; c += 256) {
         const float w = __expf(pl[(int64_t)c * H] - m);
         if (c < kCombineW) s_w[c] = w;
@@ -120,6 +123,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int
     const int64_t cstride = (int64_t)H * width / 4;
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
     if (g == 0 && wx != 0.f) acc = wx * reinterpret_cast<const f32x4 *>(p.o_x + (int64_t)row * width + col0)[c4];
+    if (g == 0 && wn != 0.f) {
+        const uint2 v2 = reinterpret_cast<const uint2 *>(v_new)[c4];
+        acc += wn * f32x4{__uint_as_float(v2.x << 16), __uint_as_float(v2.x & 0xffff0000u),
+                          __uint_as_float(v2.y << 16), __uint_as_float(v2.y & 0xffff0000u)};
+    }
 #pragma unroll 8
     for (int c = g; c < nc; c += kCombineGroups) {
         const float w = c < kCombineW ? s_w[c] : __expf(pl[(int64_t)c * H] - m);
@@ -134,6 +142,60 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int
         out[tid] = t * (1.f / den);
     }
     if (tid == 0 && blockIdx.y == 0) p.lse[row] = m + __logf(den);
+}
+
+__global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int width) {
+    __shared__ float s_w[kCombineW];
+    __shared__ float s_red[4];
+    __shared__ f32x4 s_acc[kCombineGroups][kCombineCols4];
+    combine_row(p, width, -INFINITY, nullptr, s_w, s_red, s_acc);
+}
+
+// ---------------------------------------------------------------------------
+// Pass 2 of a decode step.  Workgroup (sequence i, head h, column slice) as
+// in combine_kernel; it first scores the step's new token against its query
+// row (q . k_new, fp32 from bf16, the whole row), merges that token as one
+// more partial, and -- in the workgroup of the first query head of each KV
+// head and the first column slice -- stores the new row into the GPU pool
+// (the decode append; the pass-1 kernels of this step did not read it).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void step_combine_kernel(const StepCombineParams sp, int width) {
+    __shared__ float s_w[kCombineW];
+    __shared__ float s_red[4];
+    __shared__ f32x4 s_acc[kCombineGroups][kCombineCols4];
+    const int H = sp.cp.n_q_heads;
+    const int i = blockIdx.x / H;
+    const int h = blockIdx.x - i * H;
+    const int g = h / sp.group;
+    const int tid = threadIdx.x;
+    const int re = sp.row_elems;
+    const bool gqa = sp.kind == 0;
+    const uint16_t *kr = sp.k_new + (gqa ? ((int64_t)i * sp.n_kv_heads + g) * re : (int64_t)i * re);
+    const uint16_t *qr = sp.q + (int64_t)i * sp.q_row + (int64_t)h * re;
+    float d = 0.f;
+    for (int e = tid; e < re; e += 256) d = fmaf(bf16_to_f32(qr[e]), bf16_to_f32(kr[e]), d);
+    d = block_reduce(d, false, s_red);
+    // the append of the new row
+    if (blockIdx.y == 0 && h % sp.group == 0) {
+        const int64_t slot0 = sp.slot_elem0[i];
+        const int row = sp.row[i];
+        if (tid == 0 && h == 0 && sp.tab_index[i] >= 0) sp.table[sp.tab_index[i]] = sp.tab_slot[i];
+        const int row16 = re / 8;
+        if (gqa) {
+            const uint16_t *vr = sp.v_new + ((int64_t)i * sp.n_kv_heads + g) * re;
+            uint16_t *head = sp.pool + slot0 + (int64_t)g * 2 * sp.block_tokens * re;
+            for (int t = tid; t < 2 * row16; t += 256) {
+                const int which = t / row16;
+                const int k = t - which * row16;
+                put_tiled(head, row, which, k, reinterpret_cast<const u32x4 *>(which ? vr : kr)[k]);
+            }
+        } else {
+            for (int k = tid; k < row16; k += 256)
+                put_mla32(sp.pool + slot0, row, k, reinterpret_cast<const u32x4 *>(kr)[k]);
+        }
+    }
+    const uint16_t *vrow = (gqa ? sp.v_new + ((int64_t)i * sp.n_kv_heads + g) * re : kr) + blockIdx.y * 4 * kCombineCols4;
+    combine_row(sp.cp, width, d * sp.scale, vrow, s_w, s_red, s_acc);
 }
 
 // ---------------------------------------------------------------------------
@@ -430,6 +492,13 @@ hipError_t launch_merge(int32_t rows, int32_t width, const float *o_a, const flo
     const int blocks = (rows + rpw - 1) / rpw;
     hipLaunchKernelGGL(merge_kernel, dim3(blocks), dim3(256), 0, s, rows, width, rpw, o_a, lse_a, o_b, lse_b,
                        o_out, lse_out, o_bf16);
+    return hipGetLastError();
+}
+
+hipError_t launch_step_combine(const StepCombineParams &p, int width, hipStream_t s) {
+    if (p.cp.n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(step_combine_kernel, dim3(p.cp.n * p.cp.n_q_heads, width / (4 * kCombineCols4)), dim3(256),
+                       0, s, p, width);
     return hipGetLastError();
 }
 

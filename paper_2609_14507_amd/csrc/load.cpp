@@ -425,15 +425,24 @@ int plan_selection(const wsk_cache *c, int32_t n, const int32_t *ids, const int3
 }
 
 // ---- the GPU side of a step: execution --------------------------------------------
-int run_plan(wsk_cache *c, int32_t n, GpuPlan &g, bool gather, const void *q, const float *o_x, const float *lse_x,
-             float *o, float *lse, void *ws, size_t ws_bytes, void *stream, bool pass1 = true, bool pass2 = true) {
-    if (n == 0) return WSK_OK;
+int check_run(const wsk_cache *c, const GpuPlan &g, const void *q, const float *o_x, const float *lse_x, float *o,
+              float *lse, void *ws, size_t ws_bytes, bool pass1, bool pass2) {
     if (c->device < 0) return fail(WSK_ESTATE, "host-only cache");
     int rc = check_outputs(q, o, lse, o_x, lse_x, pass1, pass2);
     if (rc) return rc;
     if (!ws || ws_bytes < g.bytes) return fail(WSK_EINVAL, "workspace of %zu bytes needed", g.bytes);
     if (((uintptr_t)ws & 255) != 0) return fail(WSK_EINVAL, "workspace must be 256-byte aligned");
     if (!g.chunks.empty() && !c->copy_stream) return fail(WSK_ESTATE, "the cache has no load region");
+    return WSK_OK;
+}
+
+// Pass 1 of a plan (pass1) and its combine (pass2).  The combine is skipped
+// when step is set: the caller launches its own pass 2.
+int run_plan(wsk_cache *c, int32_t n, GpuPlan &g, bool gather, const void *q, const float *o_x, const float *lse_x,
+             float *o, float *lse, void *ws, size_t ws_bytes, void *stream, bool pass1 = true, bool pass2 = true) {
+    if (n == 0) return WSK_OK;
+    int rc = check_run(c, g, q, o_x, lse_x, o, lse, ws, ws_bytes, pass1, pass2);
+    if (rc) return rc;
     DeviceGuard guard(c->device);
     if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
     hipStream_t st = (hipStream_t)stream, cs = c->copy_stream;
@@ -565,6 +574,98 @@ int wsk_attend_gpu_pass2(wsk_cache *c, int32_t n, const int32_t *ids, const floa
     int rc = plan_dense(c, n, ids, g);
     if (rc) return rc;
     return run_plan(c, n, g, false, nullptr, o_x, lse_x, o, lse, ws, ws_bytes, stream, false, true);
+}
+
+int wsk_decode_step_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, size_t *bytes) {
+    return wsk_attend_gpu_workspace(c, n, ids, bytes);
+}
+
+int wsk_decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, const void *k_new, const void *v_new,
+                    const float *o_x, const float *lse_x, float *o, float *lse, void *ws, size_t ws_bytes,
+                    void *stream) {
+    int rc = check_ids(c, n, ids);
+    if (rc) return rc;
+    if (n == 0) return fail(WSK_EINVAL, "n must be positive");
+    const wsk_partition_spec &sp = c->spec;
+    const bool gqa = sp.kind == WSK_KIND_GQA;
+    if (!k_new || (gqa && !v_new) || (!gqa && v_new)) return fail(WSK_EINVAL, "k_new / v_new");
+    if (!aligned16(k_new) || !aligned16(v_new)) return fail(WSK_EINVAL, "k_new/v_new must be 16-byte aligned");
+    std::vector<int32_t> sorted(ids, ids + n);
+    std::sort(sorted.begin(), sorted.end());
+    for (int32_t j = 1; j < n; ++j)
+        if (sorted[j] == sorted[j - 1]) return fail(WSK_EINVAL, "sequence %d listed twice", sorted[j]);
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t sq = ids[i];
+        if (c->length[sq] >= sp.max_seq_len) return fail(WSK_ERANGE, "sequence %d is full", sq);
+        if (c->length[sq] < std::max(c->split[sq], c->load_end[sq]))
+            return fail(WSK_ERANGE, "position %d of sequence %d is below the start of its GPU pool range",
+                        c->length[sq], sq);
+    }
+    // pass 1 covers the positions written so far; the new row joins in pass 2
+    GpuPlan g;
+    rc = plan_dense(c, n, ids, g);
+    if (rc) return rc;
+    rc = check_run(c, g, q, o_x, lse_x, o, lse, ws, ws_bytes, true, true);
+    if (rc) return rc;
+    // routing of the new rows (as wsk_append)
+    std::vector<Pending> pend;
+    for (int32_t j = 0; j < n; ++j) {
+        rc = plan(c, sorted[j], c->length[sorted[j]], 1, pend);
+        if (rc) return rc;
+    }
+    commit(c, pend);
+    rc = run_plan(c, n, g, false, q, nullptr, nullptr, nullptr, nullptr, ws, ws_bytes, stream, true, false);
+    DeviceGuard guard(c->device);
+    hipError_t e = guard.err;
+    const int hkv = gqa ? sp.n_kv_heads : 1;
+    const int width = gqa ? kHeadDim : kLatent;
+    const int re = c->row_elems;
+    float *part_o = (float *)ws;
+    float *part_lse = (float *)((char *)ws + g.part_o_bytes);
+    for (int32_t i0 = 0; i0 < n && !rc && e == hipSuccess; i0 += kMaxLaunchSeqs) {
+        const int32_t m = std::min(kMaxLaunchSeqs, n - i0);
+        StepCombineParams p{};
+        CombineParams &cp = p.cp;
+        cp.part_o = part_o + g.pb[i0] * sp.n_q_heads * width;
+        cp.part_lse = part_lse + g.pb[i0] * sp.n_q_heads;
+        cp.o = o + (int64_t)i0 * sp.n_q_heads * width;
+        cp.lse = lse + (int64_t)i0 * sp.n_q_heads;
+        cp.o_x = o_x ? o_x + (int64_t)i0 * sp.n_q_heads * width : nullptr;
+        cp.lse_x = lse_x ? lse_x + (int64_t)i0 * sp.n_q_heads : nullptr;
+        cp.n = m;
+        cp.n_q_heads = sp.n_q_heads;
+        for (int32_t r = 0; r <= kMaxLaunchSeqs; ++r) cp.chunk_begin[r] = (int32_t)(g.pb[i0 + std::min(r, m)] - g.pb[i0]);
+        p.q_row = (int64_t)sp.n_q_heads * re;
+        p.q = (const uint16_t *)q + (int64_t)i0 * p.q_row;
+        p.k_new = (const uint16_t *)k_new + (int64_t)i0 * hkv * re;
+        p.v_new = v_new ? (const uint16_t *)v_new + (int64_t)i0 * hkv * re : nullptr;
+        p.pool = c->dpool;
+        p.table = c->dtab;
+        p.kind = sp.kind;
+        p.n_kv_heads = hkv;
+        p.group = sp.n_q_heads / hkv;
+        p.row_elems = re;
+        p.block_tokens = sp.block_tokens;
+        p.scale = sp.softmax_scale;
+        for (int32_t r = 0; r < m; ++r) {
+            const int32_t sq = ids[i0 + r];
+            const int32_t pos = c->length[sq];
+            const int32_t blk = pos / sp.block_tokens;
+            p.slot_elem0[r] = (int64_t)tab(c, WSK_PART_GPU, sq, blk) * c->slot_elems;
+            p.row[r] = pos % sp.block_tokens;
+            p.tab_index[r] = -1;
+            for (const Pending &pd : pend)
+                if (pd.seq == sq && pd.part == WSK_PART_GPU && pd.blk == blk) {
+                    p.tab_index[r] = (int32_t)((size_t)sq * c->max_blocks + blk);
+                    p.tab_slot[r] = pd.slot;
+                }
+        }
+        e = launch_step_combine(p, width, (hipStream_t)stream);
+    }
+    for (int32_t i = 0; i < n; ++i) c->length[ids[i]] += 1;
+    if (rc) return rc;
+    if (e != hipSuccess) return hip_fail(e, "wsk_decode_step");
+    return WSK_OK;
 }
 
 int wsk_attend_blocks_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin,

@@ -67,6 +67,30 @@ struct CombineParams {
     int32_t chunk_begin[kMaxLaunchSeqs + 1];
 };
 
+// Pass 2 of a decode step: the chunk combine, plus the step's new token of
+// every sequence taken straight from its input row (its score q.k_new and its
+// value row enter as one more partial), plus the append of that row into the
+// GPU pool (as AppendParams describes it).
+struct StepCombineParams {
+    CombineParams cp;
+    const uint16_t *q;       // launch-local query rows, q_row elements per sequence
+    const uint16_t *k_new;   // launch-local new rows (GQA [n][n_kv_heads][128]; MLA [n][576])
+    const uint16_t *v_new;   // GQA only
+    uint16_t *pool;
+    int32_t *table;
+    int64_t q_row;
+    int32_t kind;
+    int32_t n_kv_heads;
+    int32_t group;           // query heads per KV head (MLA: n_q_heads)
+    int32_t row_elems;       // GQA: 128; MLA: 576
+    int32_t block_tokens;
+    float scale;             // softmax scale (natural-log domain)
+    int64_t slot_elem0[kMaxLaunchSeqs];
+    int32_t row[kMaxLaunchSeqs];
+    int32_t tab_index[kMaxLaunchSeqs];
+    int32_t tab_slot[kMaxLaunchSeqs];
+};
+
 // Decode append: row r of the source goes to row row[r] of the slot whose
 // first element is slot_elem0[r]; GQA rows carry K and V for every KV head
 // (V stored transposed in the GPU pool).  tab_index[r] >= 0 also stores
@@ -131,6 +155,7 @@ int policy_fail(int code, const char *msg);
 hipError_t launch_gqa_attend(const AttendParams &p, int heads_per_wg, int n_wg, hipStream_t s);
 hipError_t launch_mla_attend(const AttendParams &p, int n_wg, hipStream_t s);
 hipError_t launch_combine(const CombineParams &p, int width, hipStream_t s);
+hipError_t launch_step_combine(const StepCombineParams &p, int width, hipStream_t s);
 hipError_t launch_append(const AppendParams &p, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
 hipError_t launch_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a,

@@ -99,6 +99,22 @@ class DecodeSession:
         wsk.wsk_attend_gpu(self.h, ids, q, o, lse, self._ws, o_x, lse_x)
         return o, lse
 
+    def decode_step(self, q: torch.Tensor, k_new: torch.Tensor, v_new: Optional[torch.Tensor], o_x=None, lse_x=None,
+                    o=None, lse=None, ids: Optional[List[int]] = None):
+        """Append + attend every GPU-side position (the new row included) + merge,
+        in one call (wsk_decode_step); the workspace keeps room for one more
+        chunk partial per sequence, so that steps do not allocate."""
+        ids = self.ids if ids is None else ids
+        o, lse = self._outputs(len(ids), o, lse)
+        need = wsk.wsk_decode_step_workspace(self.h, ids)
+        if self._ws.numel() < need:
+            spare = len(ids) * self.w.n_q_heads * (self.out_width + 1) * 4 + 512
+            self._ws = torch.empty(need + spare, dtype=torch.uint8, device=self.dev)
+        wsk.wsk_decode_step(self.h, ids, q, k_new, v_new, o, lse, self._ws, o_x, lse_x)
+        for b in ids:
+            self.lengths[b] += 1
+        return o, lse
+
     def attend_gpu_pass1(self, q: torch.Tensor, ids: Optional[List[int]] = None):
         """Pass 1 of attend_gpu (transfers and kernels enqueued, partials in the
         session workspace); attend_gpu_pass2 with the same ids completes it."""

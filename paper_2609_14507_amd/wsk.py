@@ -81,6 +81,9 @@ _SIGS = {
     "wsk_attend_gpu": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_attend_gpu_pass1": ([_VP, _I32, _PI32, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_attend_gpu_pass2": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
+    "wsk_decode_step_workspace": ([_VP, _I32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+    "wsk_decode_step": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP],
+                        ctypes.c_int),
     "wsk_cpu_attend_all": ([_VP, _I32, _PI32, _VP, _VP, _VP, _I32], ctypes.c_int),
     "wsk_load_slot": ([_VP, _I32, ctypes.POINTER(_VP)], ctypes.c_int),
     "wsk_load_stats": ([_VP, ctypes.POINTER(wsk_load_info)], ctypes.c_int),
@@ -235,6 +238,19 @@ def wsk_attend_gpu_pass2(h: int, seq_ids, o, lse, ws, o_x=None, lse_x=None, stre
     nbytes = ws.numel() * ws.element_size()
     _check(lib().wsk_attend_gpu_pass2(h, len(seq_ids), _i32_array(seq_ids), _ptr(o_x), _ptr(lse_x), _ptr(o),
                                       _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
+
+
+def wsk_decode_step_workspace(h: int, seq_ids) -> int:
+    b = ctypes.c_size_t()
+    _check(lib().wsk_decode_step_workspace(h, len(seq_ids), _i32_array(seq_ids), ctypes.byref(b)))
+    return b.value
+
+
+def wsk_decode_step(h: int, seq_ids, q, k_new, v_new, o, lse, ws, o_x=None, lse_x=None, stream=None):
+    """Append + attend every GPU-side position (the new row included) + merge, in one call."""
+    nbytes = ws.numel() * ws.element_size()
+    _check(lib().wsk_decode_step(h, len(seq_ids), _i32_array(seq_ids), _ptr(q), _ptr(k_new), _ptr(v_new),
+                                 _ptr(o_x), _ptr(lse_x), _ptr(o), _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
 
 
 def wsk_cpu_attend_all(h: int, seq_ids, q, o, lse, threads: int = 0):

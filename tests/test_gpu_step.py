@@ -1,0 +1,163 @@
+"""wsk_decode_step (append + GPU-side attention + merge in one call) against
+the fp64 oracle over the whole context, step after step across block
+boundaries, GQA and MLA, HBM-resident and with a load region; the pool it
+leaves behind is byte-identical to the one wsk_append leaves; and its
+refusals change nothing."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_14507_amd import workloads as wl
+from paper_2609_14507_amd import wsk
+from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
+from tests.gpu_util import assert_close, assert_lse, d2h, say
+
+pytestmark = pytest.mark.gpu
+DEV = 0
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    torch.cuda.set_device(DEV)
+    yield
+    torch.cuda.synchronize()
+
+
+def _workload(kind, B, H, seed):
+    if kind == "gqa":
+        return wl.Workload("step-gqa", wl.GQA, batch=B, n_q_heads=H, n_kv_heads=2, head_dim=128, context=1,
+                           seed=seed)
+    return wl.Workload("step-mla", wl.MLA, batch=B, n_q_heads=H, n_kv_heads=1, head_dim=128, latent_dim=512,
+                       rope_dim=64, nope_dim=128, context=1, kv_std=0.5, seed=seed)
+
+
+def _prefill(w, lengths, splits, gen):
+    if w.kind == wl.MLA:
+        return wl.Prefill(list(lengths), list(splits), [wl.draw_bf16(gen, (L, w.row_elems), w.kv_std) for L in lengths],
+                          None, gen)
+    return wl.Prefill(list(lengths), list(splits),
+                      [wl.draw_bf16(gen, (L, w.n_kv_heads, w.head_dim)) for L in lengths],
+                      [wl.draw_bf16(gen, (L, w.n_kv_heads, w.head_dim)) for L in lengths], gen)
+
+
+def _new_rows(w, B, gen):
+    if w.kind == wl.MLA:
+        return wl.draw_bf16(gen, (B, w.row_elems), w.kv_std), None
+    return wl.draw_bf16(gen, (B, w.n_kv_heads, w.head_dim)), wl.draw_bf16(gen, (B, w.n_kv_heads, w.head_dim))
+
+
+def _dims(w):
+    return (w.latent_dim if w.kind == wl.MLA else w.head_dim), (w.n_q_heads if w.kind == wl.MLA else w.group)
+
+
+def _cpu_partial(sess, q_bits):
+    w = sess.w
+    dv, _ = _dims(w)
+    o = np.empty((sess.B, w.n_q_heads, dv), np.float32)
+    lse = np.empty((sess.B, w.n_q_heads), np.float32)
+    wsk.wsk_cpu_attend_all(sess.h, sess.ids, np.ascontiguousarray(q_bits), o, lse, 8)
+    return torch.from_numpy(o).to(sess.dev), torch.from_numpy(lse).to(sess.dev)
+
+
+def _step(sess, q, kn, vn, o_x, l_x):
+    need = wsk.wsk_decode_step_workspace(sess.h, sess.ids)
+    ws = torch.empty(need, dtype=torch.uint8, device=sess.dev)
+    dv, _ = _dims(sess.w)
+    o = torch.empty(sess.B, sess.w.n_q_heads, dv, device=sess.dev)
+    lse = torch.empty(sess.B, sess.w.n_q_heads, device=sess.dev)
+    wsk.wsk_decode_step(sess.h, sess.ids, q, kn, vn, o, lse, ws, o_x, l_x)
+    for b in sess.ids:
+        sess.lengths[b] += 1
+    return o, lse
+
+
+def _gpu_pool(sess):
+    _, gv = wsk.wsk_views(sess.h, 0)
+    return d2h(gv.pool, gv.slot_bytes * sess.spec.device_pool_blocks)
+
+
+@pytest.mark.parametrize("kind,bk,load", [("gqa", 64, False), ("gqa", 128, True), ("mla", 64, False),
+                                          ("mla", 256, True)])
+def test_decode_steps(kind, bk, load):
+    """Six steps from prefills that end 3 positions before a block boundary
+    (so that a step opens a new block), a sequence with no CPU part, a D-window
+    that starts inside a block and (with a load region) one that starts
+    empty; each step's output against the oracle over [0, L]; a twin cache
+    driven by wsk_append + wsk_attend_gpu ends with a byte-identical GPU pool
+    and close outputs."""
+    lengths = [4 * bk - 3, 2 * bk - 3, 3 * bk]
+    splits = [bk + 11, 0, 2 * bk + 5]
+    load_ends = [3 * bk, bk, 3 * bk] if load else None
+    w = _workload(kind, len(lengths), 8, seed=bk)
+    gen = torch.Generator().manual_seed(w.seed + 3)
+    pf = _prefill(w, lengths, splits, gen)
+    k_all = list(pf.k)
+    v_all = None if pf.v is None else list(pf.v)
+    dv, g = _dims(w)
+    say("case decode step", kind, bk, load)
+    kw = dict(extra_tokens=8, block_tokens=bk, load_ends=load_ends, pingpong_blocks=2, arena_blocks=3)
+    with DecodeSession(w, pf, DEV, **kw) as sess, DecodeSession(w, pf, DEV, **kw) as twin:
+        for step in range(6):
+            q_bits = wl.draw_bf16(gen, (sess.B, w.n_q_heads, w.row_elems))
+            kn, vn = _new_rows(w, sess.B, gen)
+            q = to_device_bf16(q_bits, sess.dev)
+            knd = to_device_bf16(kn, sess.dev)
+            vnd = None if vn is None else to_device_bf16(vn, sess.dev)
+            o_x, l_x = _cpu_partial(sess, q_bits)
+            o, lse = _step(sess, q, knd, vnd, o_x, l_x)
+            twin.append(knd, vnd)
+            o2, lse2 = twin.attend_gpu(q, o_x=o_x, lse_x=l_x)
+            for b in range(sess.B):
+                k_all[b] = np.concatenate([k_all[b], kn[b:b + 1]])
+                if v_all is not None:
+                    v_all[b] = np.concatenate([v_all[b], vn[b:b + 1]])
+            o, lse, o2, lse2 = (t.cpu().numpy() for t in (o, lse, o2, lse2))
+            for b in range(sess.B):
+                L = sess.lengths[b]
+                o_r, l_r = oracle.attend(q_bits[b], k_all[b], None if v_all is None else v_all[b], 0, L,
+                                         w.softmax_scale, g, dv=dv)
+                assert_close(o[b], o_r, "step %d b%d" % (step, b))
+                assert_lse(lse[b], l_r, "step %d b%d" % (step, b))
+                assert np.abs(o[b] - o2[b]).max() <= 1e-5 and np.abs(lse[b] - lse2[b]).max() <= 1e-5
+        torch.cuda.synchronize()
+        assert np.array_equal(_gpu_pool(sess), _gpu_pool(twin))
+        for b in range(sess.B):
+            for p in range(0, sess.lengths[b], 7):
+                assert wsk.wsk_route(sess.h, b, p) == wsk.wsk_route(twin.h, b, p)
+
+
+def test_decode_step_many_sequences_and_refusals():
+    B = 70
+    w = _workload("gqa", B, 8, seed=4)
+    gen = torch.Generator().manual_seed(6)
+    lengths = [int(x) for x in torch.randint(60, 300, (B,), generator=gen)]
+    splits = [L // 3 for L in lengths]
+    pf = _prefill(w, lengths, splits, gen)
+    k_all, v_all = list(pf.k), list(pf.v)
+    dv, g = _dims(w)
+    say("case decode step many")
+    with DecodeSession(w, pf, DEV, extra_tokens=2) as sess:
+        q_bits = wl.draw_bf16(gen, (B, w.n_q_heads, w.row_elems))
+        kn, vn = _new_rows(w, B, gen)
+        q, knd, vnd = (to_device_bf16(x, sess.dev) for x in (q_bits, kn, vn))
+        o, lse = _step(sess, q, knd, vnd, None, None)
+        o, lse = o.cpu().numpy(), lse.cpu().numpy()
+        for b in range(B):
+            k = np.concatenate([k_all[b], kn[b:b + 1]])
+            v = np.concatenate([v_all[b], vn[b:b + 1]])
+            o_r, l_r = oracle.attend(q_bits[b], k, v, splits[b], lengths[b] + 1, w.softmax_scale, g, dv=dv)
+            assert_close(o[b], o_r, "many b%d" % b)
+            assert_lse(lse[b], l_r, "many b%d" % b)
+        ws = torch.empty(wsk.wsk_decode_step_workspace(sess.h, sess.ids), dtype=torch.uint8, device=sess.dev)
+        o_t = torch.empty(2, w.n_q_heads, dv, device=sess.dev)
+        l_t = torch.empty(2, w.n_q_heads, device=sess.dev)
+        before = [wsk.wsk_seq_info(sess.h, b)[0] for b in range(2)]
+        with pytest.raises(wsk.WskError) as ei:                    # a sequence listed twice
+            wsk.wsk_decode_step(sess.h, [1, 1], q[:2], knd[:2], vnd[:2], o_t, l_t, ws)
+        assert ei.value.code == wsk.WSK_EINVAL
+        with pytest.raises(wsk.WskError) as ei:                    # workspace too small
+            wsk.wsk_decode_step(sess.h, [0, 1], q[:2], knd[:2], vnd[:2], o_t, l_t, ws[:256])
+        assert ei.value.code == wsk.WSK_EINVAL
+        assert [wsk.wsk_seq_info(sess.h, b)[0] for b in range(2)] == before
