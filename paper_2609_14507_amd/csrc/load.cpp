@@ -92,7 +92,11 @@ int32_t arena_blocks(const wsk_cache *c) { return c->spec.load_arena_blocks; }
 int gather_threads() { return (int)std::min(8u, std::max(1u, std::thread::hardware_concurrency())); }
 
 // Allocates arena k: pinned (hipHostMalloc) on a device cache, plain aligned
-// host memory on a host-only one.  Records the time spent.
+// host memory on a host-only one, and writes zeros over it.  The first write
+// is where the pages are really faulted in and locked (measured on an MI355X
+// system: the allocation call ~0.003 ms/MiB, the first touch by one thread
+// ~0.37 ms/MiB), so it is done here, off the critical path, in 2 MiB pieces
+// on several threads.  Records the time spent.
 int pin_arena(wsk_cache *c, size_t k) {
     if (c->arenas[k]) return WSK_OK;
     const int64_t first = (int64_t)k * arena_blocks(c);
@@ -109,8 +113,12 @@ int pin_arena(wsk_cache *c, size_t k) {
     } else {
         p = aligned_alloc(64, (bytes + 63) / 64 * 64);
         if (!p) return fail(WSK_ENOMEM, "load region arena of %zu bytes", bytes);
-        memset(p, 0, bytes);
     }
+    const size_t piece = 2u << 20;
+    parallel_tasks((int)((bytes + piece - 1) / piece), gather_threads(), [&](int t) {
+        const size_t a = (size_t)t * piece;
+        memset((char *)p + a, 0, std::min(piece, bytes - a));
+    });
     c->pin_seconds += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
     c->pinned_bytes += (int64_t)bytes;
     c->arenas[k] = (uint16_t *)p;
