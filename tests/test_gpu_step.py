@@ -161,3 +161,59 @@ def test_decode_step_many_sequences_and_refusals():
             wsk.wsk_decode_step(sess.h, [0, 1], q[:2], knd[:2], vnd[:2], o_t, l_t, ws[:256])
         assert ei.value.code == wsk.WSK_EINVAL
         assert [wsk.wsk_seq_info(sess.h, b)[0] for b in range(2)] == before
+
+
+@pytest.mark.parametrize("kind", ["gqa", "mla"])
+def test_decode_loop_with_policy_eviction(kind):
+    """300 decode steps through wsk_decode_step on a cache whose GPU share
+    starts in the load region; whenever a D-window holds a whole batch it is
+    evicted where the split policy routes it (CPU partition or load region);
+    every 50 steps the whole step -- CPU engine over every CPU position,
+    GPU side streamed and in place, the new row -- is checked against the
+    oracle over [0, L]."""
+    from oracle import policy as P
+    bk, D, steps = 64, 128, 300
+    lengths, splits, load_ends = [1500, 900], [300, 0], [1408, 768]
+    w = _workload(kind, 2, 8, seed=13)
+    gen = torch.Generator().manual_seed(17)
+    pf = _prefill(w, lengths, splits, gen)
+    k_all = list(pf.k)
+    v_all = None if pf.v is None else list(pf.v)
+    dv, g = _dims(w)
+    A, Bc = 3e-9, 2e-9                                   # p = 0.4
+    pol = wsk.Policy(A, Bc, 1e-5, 1e-5, 4)
+    say("case decode loop", kind)
+    try:
+        with DecodeSession(w, pf, DEV, extra_tokens=steps, block_tokens=bk, load_ends=load_ends, evict_tokens=D,
+                           pingpong_blocks=5, arena_blocks=6) as sess:
+            flushed = {wsk.PART_CPU: 0, wsk.PART_LOAD: 0}
+            for step in range(steps):
+                q_bits = wl.draw_bf16(gen, (2, w.n_q_heads, w.row_elems))
+                kn, vn = _new_rows(w, 2, gen)
+                q = to_device_bf16(q_bits, sess.dev)
+                o_x, l_x = _cpu_partial(sess, q_bits)
+                o, lse = sess.decode_step(q, to_device_bf16(kn, sess.dev),
+                                          None if vn is None else to_device_bf16(vn, sess.dev), o_x=o_x, lse_x=l_x)
+                for b in range(2):
+                    k_all[b] = np.concatenate([k_all[b], kn[b:b + 1]])
+                    if v_all is not None:
+                        v_all[b] = np.concatenate([v_all[b], vn[b:b + 1]])
+                if step % 50 == 49:
+                    o, lse = o.cpu().numpy(), lse.cpu().numpy()
+                    for b in range(2):
+                        o_r, l_r = oracle.attend(q_bits[b], k_all[b], None if v_all is None else v_all[b], 0,
+                                                 sess.lengths[b], w.softmax_scale, g, dv=dv)
+                        assert_close(o[b], o_r, "loop step %d b%d" % (step, b))
+                        assert_lse(lse[b], l_r, "loop step %d b%d" % (step, b))
+                for b in range(2):
+                    a, e = sess.gpu_range(b)
+                    if e - a >= D + (-a) % bk:
+                        dest = wsk.PART_CPU if pol.route() == wsk.PART_CPU else wsk.PART_LOAD
+                        assert sess.flush([dest], ids=[b]) == [(a + D) // bk * bk - a]
+                        flushed[dest] += 1
+            assert flushed[wsk.PART_CPU] > 0 and flushed[wsk.PART_LOAD] > 0
+            p = P.marginal_share(A, Bc)
+            n = sum(flushed.values())
+            assert abs(flushed[wsk.PART_CPU] / n - p) <= 0.5 / n + 1e-12
+    finally:
+        pol.close()
