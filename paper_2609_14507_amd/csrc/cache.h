@@ -73,7 +73,7 @@ struct wsk_cache {
     hipEvent_t consumed[2] = {nullptr, nullptr};   // the kernels reading buffer b are done
     hipEvent_t staged[2] = {nullptr, nullptr};     // the DMA out of gather staging b is done
     hipEvent_t flush_ev = nullptr;        // end of the last eviction into the load region
-    uint16_t *hgather[2] = {nullptr, nullptr};     // pinned gather staging (sparse selections)
+    uint16_t *hgather[2] = {nullptr, nullptr};     // pinned gather staging (sparse selections), on first use
     uint16_t *hbounce = nullptr;          // pinned bounce of evictions into the CPU pool
     size_t hbounce_bytes = 0;
     int64_t h2d_bytes = 0, d2h_bytes = 0; // load-region traffic since init

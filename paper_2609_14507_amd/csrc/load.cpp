@@ -85,6 +85,7 @@ void get_position(const wsk_cache *c, const uint16_t *slot, int off, uint16_t *c
 }
 
 int32_t arena_blocks(const wsk_cache *c) { return c->spec.load_arena_blocks; }
+int32_t sp_pingpong(const wsk_cache *c) { return c->spec.pingpong_blocks; }
 
 // Host threads for the block gathers and row rewrites: one thread copies
 // ~20 GB/s, the host-to-device link takes ~57, so a few threads keep the
@@ -179,7 +180,6 @@ int wsk::load_init(wsk_cache *c) {
     const size_t buf = (size_t)P * slot_bytes(c);
     hipError_t e = hipSuccess;
     for (int b = 0; b < 2 && e == hipSuccess; ++b) e = hipMalloc((void **)&c->pingpong[b], buf);
-    for (int b = 0; b < 2 && e == hipSuccess; ++b) e = hipHostMalloc((void **)&c->hgather[b], buf, hipHostMallocDefault);
     if (e == hipSuccess) e = hipMalloc((void **)&c->dident, (size_t)P * sizeof(int32_t));
     if (e == hipSuccess) {
         std::vector<int32_t> ident(P);
@@ -507,6 +507,8 @@ int run_plan(wsk_cache *c, int32_t n, GpuPlan &g, bool gather, const void *q, co
             // several threads) and send them as one contiguous DMA per ~8 MB
             // piece, so that the gather of the next piece overlaps this DMA
             e = hipEventSynchronize(c->staged[b]);
+            if (e == hipSuccess && !c->hgather[b])   // pinned on first use
+                e = hipHostMalloc((void **)&c->hgather[b], (size_t)sp_pingpong(c) * sb, hipHostMallocDefault);
             const size_t piece = std::max<size_t>(1, (8u << 20) / sb);
             for (size_t p0 = j0; p0 < j1 && e == hipSuccess; p0 += piece) {
                 const size_t p1 = std::min(j1, p0 + piece);
@@ -871,8 +873,7 @@ int wsk_cpu_attend_all(wsk_cache *c, int32_t n, const int32_t *ids, const void *
     x.mla = mla;
     x.scale_log2 = sp.softmax_scale * 1.4426950408889634f;
     x.threads = threads > 0 ? threads : (int)std::max(1u, std::thread::hardware_concurrency());
-    cpu_attend(x);
-    return WSK_OK;
+    return cpu_attend(x);
 }
 
 int wsk_seq_segments(const wsk_cache *c, int32_t seq, int32_t cap, int32_t *start, int32_t *end, int32_t *part,

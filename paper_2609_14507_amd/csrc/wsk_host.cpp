@@ -857,8 +857,7 @@ int wsk_cpu_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *s
     x.mla = mla;
     x.scale_log2 = sp.softmax_scale * 1.4426950408889634f;
     x.threads = threads > 0 ? threads : (int)std::max(1u, std::thread::hardware_concurrency());
-    cpu_attend(x);
-    return WSK_OK;
+    return cpu_attend(x);
 }
 
 int wsk_stream_read(const void *p, size_t bytes, uint32_t *out, void *stream) {
