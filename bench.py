@@ -592,19 +592,24 @@ def main():
     probe = torch.empty(2 << 30, dtype=torch.uint8, device=dev)
     probe.fill_(3)
     fold = torch.zeros(1, dtype=torch.int32, device=dev)
-    pr_ms = []
-    for it in range(6):
-        flush.add_(1)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        _wsk.wsk_stream_read(probe, fold)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        if it:
-            pr_ms.append(e0.elapsed_time(e1))
-    probe_gbs = float(probe.numel() / (np.median(pr_ms) * 1e-3) / 1e9)
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+
+    def read_gbs(workgroups):
+        ms = []
+        for it in range(6):
+            flush.add_(1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            _wsk.wsk_stream_read(probe, fold, workgroups)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if it:
+                ms.append(e0.elapsed_time(e1))
+        return float(probe.numel() / (np.median(ms) * 1e-3) / 1e9)
+    probe_gbs = read_gbs(0)
+    probe_sweep = {str(n): round(read_gbs(n), 1) for n in (cus // 2, cus * 3 // 4, cus, 2 * cus, 4 * cus)}
     del probe
-    log("bench: streaming-read probe %.0f GB/s" % probe_gbs)
+    log("bench: streaming-read probe %.0f GB/s; by workgroups %s" % (probe_gbs, probe_sweep))
     if args.copy_calibration:
         src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -658,8 +663,10 @@ def main():
         },
         "roofline": roofline(w, "mla" if mla else "gqa", p1_gbs, float(nbytes.mean())),
         "stream_read_probe": {"value": round(probe_gbs, 1), "unit": "GB/s", "bytes": 2 << 30,
+                              "by_workgroups": probe_sweep,
                               "what": "wsk_stream_read: one plain read of 2 GiB with the attention kernels' "
-                                      "loads, median of 5, cache flushed before each"},
+                                      "loads by 4-wavefront workgroups (value: 3/4 of the CUs, the GQA grid's "
+                                      "aim), median of 5, cache flushed before each"},
     }
     if load_region is not None:
         out["load_region"] = load_region

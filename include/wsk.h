@@ -592,12 +592,15 @@ int wsk_policy_model(const wsk_policy *policy, wsk_roofline *model);
 /*
  * Measurement aid, not part of the decode path: reads `bytes` of DEVICE
  * memory at p once with the loads the attention kernels use (16 bytes per
- * lane, 1 KB per wavefront instruction, non-temporal), spread over the
- * whole GPU, and XORs a 32-bit fold of the data into *out (DEVICE).  Timing
- * it gives the plain HBM read rate the attention kernels can be compared
- * with.  p 16-byte aligned; bytes a multiple of 32768.  Errors: EINVAL, EHIP.
+ * lane, 1 KB per wavefront instruction, non-temporal, 32 KB tiles per
+ * wavefront), with `workgroups` workgroups of 4 wavefronts taking the tiles
+ * in turn (<= 0: 3/4 of the compute units, the count the GQA attention
+ * planner aims at), and XORs a 32-bit fold of the data into *out (DEVICE).
+ * Timing it gives the plain HBM read rate the attention kernels can be
+ * compared with.  p 16-byte aligned; bytes a multiple of 32768.
+ * Errors: EINVAL, EHIP.
  */
-int wsk_stream_read(const void *p, size_t bytes, uint32_t *out, void *stream);
+int wsk_stream_read(const void *p, size_t bytes, int32_t workgroups, uint32_t *out, void *stream);
 
 #ifdef __cplusplus
 }

@@ -188,10 +188,10 @@ void wsk::plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const
         pl.head_groups = G / pl.heads_per_wg;
         units = sp.n_kv_heads * pl.head_groups;
     }
-    // workgroups resident at once (GQA kernel: 2 per CU; MLA kernel, whose
-    // workgroups are twice as wide: 1 per CU); the chunk budget per (KV head,
-    // head group) unit follows from it
-    const int64_t slots = (sp.kind == WSK_KIND_GQA ? 2 : 1) * (int64_t)c->cu_count;
+    // workgroups the grid aims at (GQA: 3/4 per CU; MLA, whose workgroups
+    // are twice as wide: 1 per CU); the chunk budget per (KV head, head
+    // group) unit follows from it
+    const int64_t slots = sp.kind == WSK_KIND_GQA ? gqa_resident_slots(c->cu_count) : (int64_t)c->cu_count;
     const int64_t budget = std::max<int64_t>(1, slots / units);
     pl.tpc.assign(n, 1);
     pl.nchunks.assign(n, 0);
@@ -860,12 +860,13 @@ int wsk_cpu_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *s
     return cpu_attend(x);
 }
 
-int wsk_stream_read(const void *p, size_t bytes, uint32_t *out, void *stream) {
+int wsk_stream_read(const void *p, size_t bytes, int32_t workgroups, uint32_t *out, void *stream) {
     if (!p || !out || bytes == 0 || bytes % 32768 || !aligned16(p)) return fail(WSK_EINVAL, "stream_read arguments");
     int dev = 0, cus = 256;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e == hipSuccess) e = launch_stream_read(p, (int64_t)bytes, out, 4 * std::max(cus, 1), (hipStream_t)stream);
+    const int n_wg = workgroups > 0 ? workgroups : std::max(1, gqa_resident_slots(cus));
+    if (e == hipSuccess) e = launch_stream_read(p, (int64_t)bytes, out, n_wg, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "wsk_stream_read");
     return WSK_OK;
 }

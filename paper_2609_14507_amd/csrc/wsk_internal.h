@@ -167,6 +167,12 @@ hipError_t launch_mla_absorb(int32_t n, int32_t H, int32_t dn, int32_t dl, const
 hipError_t launch_mla_expand(int32_t n, int32_t H, int32_t dl, int32_t dv, const float *o_lat,
                              const uint16_t *w_uv, float *o, hipStream_t s);
 
+// Workgroups a GQA pass-1 grid aims at on a GPU with `cus` compute units:
+// 3/4 per CU.  HBM reads with these 16-byte non-temporal loads peak with
+// about that many 4-wavefront streams (MI355X, 2 GiB read: 192 workgroups
+// 7.24 TB/s, 256 6.99, 512 6.81, 1024 6.33); more in flight lowers the rate.
+inline int gqa_resident_slots(int cus) { return cus * 3 / 4; }
+
 // Heads per workgroup used by the GQA kernel for a group size G: the largest
 // power of two dividing G, at most 16 (the matrix-core tile height).
 inline int gqa_heads_per_wg(int G) {

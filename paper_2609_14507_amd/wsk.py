@@ -96,7 +96,7 @@ _SIGS = {
     "wsk_views": ([_VP, _I32, ctypes.POINTER(wsk_view), ctypes.POINTER(wsk_view)], ctypes.c_int),
     "wsk_attend_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_attend": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
-    "wsk_stream_read": ([_VP, ctypes.c_size_t, _VP, _VP], ctypes.c_int),
+    "wsk_stream_read": ([_VP, ctypes.c_size_t, _I32, _VP, _VP], ctypes.c_int),
     "wsk_attend_blocks_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_attend_blocks": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP],
                           ctypes.c_int),
@@ -366,9 +366,9 @@ def wsk_mla_expand(o_lat, w_uv, o, stream=None):
     _check(lib().wsk_mla_expand(n, H, dl, dv, _ptr(o_lat), _ptr(w_uv), _ptr(o), _stream(stream)))
 
 
-def wsk_stream_read(buf, out, stream=None):
-    """Measurement aid: streams the device tensor buf once; XORs a fold into out (uint32 [1])."""
-    _check(lib().wsk_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(out), _stream(stream)))
+def wsk_stream_read(buf, out, workgroups: int = 0, stream=None):
+    """Measurement aid: one plain read of buf with the attention kernels' loads."""
+    _check(lib().wsk_stream_read(_ptr(buf), buf.numel() * buf.element_size(), workgroups, _ptr(out), _stream(stream)))
 
 
 def wsk_roofline_share(A: float, B: float, c_cpu: float, c_gpu: float, L: int) -> float:
