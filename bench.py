@@ -109,15 +109,15 @@ def cpu_baseline(w, pf, steps_inputs, budget_s: float):
 TRAFFIC = {
     "qwen3-30b-a3b-b16-L32768": {
         "source": "paper_2609_14507_amd/csrc/attend_gqa.hip",
-        "sha256": "e5813847daac21bddd068a7f125084699f8189c717c91099486efc5dc7c2acb6",
-        "fetch_bytes": 368957.2 * 1024 * 2.0,
-        "write_bytes": 2064.0 * 1024 * 1.0,
+        "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
+        "fetch_bytes": 368787.1 * 1024 * 2.0,
+        "write_bytes": 774.0 * 1024 * 1.0,
         "kv_bytes": 751714304,
     },
     "deepseek-v2-lite-mla-b8-L65536": {
         "source": "paper_2609_14507_amd/csrc/attend_mla.hip",
-        "sha256": "ae01f652ea0f430a3eb4abe15a9a5220abb73a5e31f7d907432c7c904ed80c47",
-        "fetch_bytes": 177772.1 * 1024 * 2.0,
+        "sha256": "0775ea2a9899f326fce97beb3ec006a7c5deef08bcb37ee803b7eecbe7c63cdd",
+        "fetch_bytes": 177768.0 * 1024 * 2.0,
         "write_bytes": 7951.5 * 1024 * 1.0,
         "kv_bytes": 362414592,
     },

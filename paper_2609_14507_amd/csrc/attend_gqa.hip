@@ -113,8 +113,10 @@ __global__ __launch_bounds__(256, 2) void gqa_attend_kernel(const AttendParams p
         const int blk = tok0 >> bshift;
         toff = ((tok0 - (blk << bshift)) >> 6) * kTileBytes;
         const int slot = __builtin_amdgcn_readfirstlane(trow[blk]);
-        const uint16_t *base = p.pool + (int64_t)slot * p.slot_elems + head_off;
-        return __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, head_bytes, 0x00020000);
+        // a missing table entry (< 0) gets an empty extent: its loads read
+        // zeros instead of memory outside the pool
+        const uint16_t *base = p.pool + (slot < 0 ? 0 : (int64_t)slot * p.slot_elems) + head_off;
+        return __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, slot < 0 ? 0 : head_bytes, 0x00020000);
     };
     const int loff = lane * 16;
     u32x4 ka[4][4], vb[8][2];

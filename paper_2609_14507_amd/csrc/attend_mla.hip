@@ -132,8 +132,10 @@ __global__ __launch_bounds__(512, 1) void mla_attend_kernel(const AttendParams p
         const int tok0 = su * kSub;
         const int blk = tok0 >> bshift;
         const int slot = __builtin_amdgcn_readfirstlane(trow[blk]);
-        s.rs = __builtin_amdgcn_make_buffer_rsrc((void *)(p.pool + (int64_t)slot * p.slot_elems), 0, slot_bytes,
-                                                 0x00020000);
+        // a missing table entry (< 0) gets an empty extent: its loads read
+        // zeros instead of memory outside the pool
+        s.rs = __builtin_amdgcn_make_buffer_rsrc((void *)(p.pool + (slot < 0 ? 0 : (int64_t)slot * p.slot_elems)), 0,
+                                                 slot < 0 ? 0 : slot_bytes, 0x00020000);
         s.soff = ((tok0 & (bk - 1)) >> 5) * kSubBytes;
         const bool partial = tok0 < t_start || tok0 + kSub > t_end;
 #pragma unroll

@@ -154,7 +154,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int
 // ---------------------------------------------------------------------------
 // Pass 2 of a decode step.  Workgroup (sequence i, head h, column slice) as
 // in combine_kernel; it first scores the step's new token against its query
-// row (q . k_new, fp32 from bf16, the whole row), merges that token as one
+// row (q . k_new, fp32 from bf16, the whole row, formed by each wavefront
+// with shuffles), merges that token as one
 // more partial, and -- in the workgroup of the first query head of each KV
 // head and the first column slice -- stores the new row into the GPU pool
 // (the decode append; the pass-1 kernels of this step did not read it).
@@ -172,9 +173,12 @@ __global__ __launch_bounds__(256) void step_combine_kernel(const StepCombinePara
     const bool gqa = sp.kind == 0;
     const uint16_t *kr = sp.k_new + (gqa ? ((int64_t)i * sp.n_kv_heads + g) * re : (int64_t)i * re);
     const uint16_t *qr = sp.q + (int64_t)i * sp.q_row + (int64_t)h * re;
+    // every wavefront forms the whole dot product (no barrier on this path)
+    const int lane = tid & 63;
     float d = 0.f;
-    for (int e = tid; e < re; e += 256) d = fmaf(bf16_to_f32(qr[e]), bf16_to_f32(kr[e]), d);
-    d = block_reduce(d, false, s_red);
+    for (int e = lane; e < re; e += 64) d = fmaf(bf16_to_f32(qr[e]), bf16_to_f32(kr[e]), d);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) d += __shfl_xor(d, o);
     // the append of the new row
     if (blockIdx.y == 0 && h % sp.group == 0) {
         const int64_t slot0 = sp.slot_elem0[i];
