@@ -155,8 +155,14 @@ def test_flush_then_full_step(kind, bk):
     k_all = [k for k in pf.k]
     v_all = None if pf.v is None else [v for v in pf.v]
     say("case flush", kind, bk)
+    from oracle.route import RouteModel
     with DecodeSession(w, pf, DEV, extra_tokens=steps, block_tokens=bk, load_ends=load_ends, evict_tokens=D,
                        pingpong_blocks=3, arena_blocks=4) as sess:
+        # the oracle's routing model replays every operation; routes must agree bit for bit
+        model = RouteModel(bk, sess.spec.host_pool_blocks, sess.spec.device_pool_blocks, sess.spec.load_pool_blocks, D)
+        for b in range(sess.B):
+            model.open(b, splits[b], load_ends[b])
+            model.write(b, 0, lengths[b])
         parts_cycle = [LOAD, CPU, CPU, LOAD]
         flushes = 0
         for step in range(steps):
@@ -167,6 +173,7 @@ def test_flush_then_full_step(kind, bk):
                 kn = wl.draw_bf16(gen, (sess.B, hkv, w.head_dim))
                 vn = wl.draw_bf16(gen, (sess.B, hkv, w.head_dim))
             sess.append(to_device_bf16(kn, sess.dev), None if vn is None else to_device_bf16(vn, sess.dev))
+            model.append(list(range(sess.B)))
             for b in range(sess.B):
                 k_all[b] = np.concatenate([k_all[b], kn[b:b + 1]])
                 if v_all is not None:
@@ -176,6 +183,10 @@ def test_flush_then_full_step(kind, bk):
             parts = [parts_cycle[(flushes + b) % 4] for b in range(sess.B)]
             before = [sess.gpu_range(b)[0] for b in range(sess.B)]
             moved = sess.flush(parts)
+            assert moved == model.flush(list(range(sess.B)), parts)
+            for b in range(sess.B):
+                assert [wsk.wsk_route(sess.h, b, p) for p in range(sess.lengths[b])] == \
+                    [model.route(b, p) for p in range(sess.lengths[b])], (flushes, b)
             flushes += 1
             for b in range(sess.B):
                 w0, L = before[b], sess.lengths[b]

@@ -274,3 +274,70 @@ def test_workspace_grows_with_range_and_is_aligned():
         assert sizes == sorted(sizes)
     finally:
         wsk.wsk_destroy(h)
+
+
+def _segments_of(model, seq):
+    """Runs of one home over [0, L) from the model's per-position homes."""
+    out, homes = [], model.homes[seq]
+    for p, part in enumerate(homes):
+        if out and out[-1][2] == part and out[-1][1] == p:
+            out[-1] = (out[-1][0], p + 1, part)
+        else:
+            out.append((p, p + 1, part))
+    return out
+
+
+def test_routing_with_load_region_matches_oracle_model():
+    """Random open / open-with-load-range / reserve / close on a host-only cache
+    with a load region: every route (part, block, slot, offset), the segment
+    list and every refusal equal the oracle model's, bit for bit."""
+    rng = np.random.default_rng(11)
+    bk, host_blocks, dev_blocks, load_blocks, max_seqs = 64, 30, 30, 30, 5
+    spec = _spec(max_seqs=max_seqs, max_seq_len=4096, device_pool_blocks=dev_blocks, host_pool_blocks=host_blocks)
+    spec.load_pool_blocks, spec.load_arena_blocks, spec.pingpong_blocks = load_blocks, 7, 4
+    h = wsk.wsk_init(spec, -1)
+    model = RouteModel(bk, host_blocks, dev_blocks, load_blocks)
+    try:
+        for step in range(400):
+            sq = int(rng.integers(max_seqs))
+            if sq not in model.split:
+                split = int(rng.integers(0, 600))
+                load_end = split if rng.random() < 0.3 else int(rng.integers(split // bk, 14)) * bk
+                if rng.random() < 0.1:
+                    load_end = split + 1 + int(rng.integers(0, 60))       # unaligned: refused
+                try:
+                    model.open(sq, split, load_end)
+                    expect = None
+                except RouteError as ex:
+                    expect = ex.code
+                try:
+                    wsk.wsk_seq_open_window(h, sq, split, load_end)
+                    got = None
+                except wsk.WskError as ex:
+                    got = ex.name
+                assert got == expect, (step, split, load_end)
+            elif rng.random() < 0.1:
+                model.close(sq)
+                wsk.wsk_seq_close(h, sq)
+            else:
+                n = int(rng.integers(0, 300))
+                try:
+                    model.write(sq, model.length[sq], n)
+                    expect = None
+                except RouteError as ex:
+                    expect = ex.code
+                try:
+                    wsk.wsk_reserve(h, sq, n)
+                    got = None
+                except wsk.WskError as ex:
+                    got = ex.name
+                assert got == expect, step
+            for s2 in model.split:
+                L = model.length[s2]
+                assert wsk.wsk_seq_info(h, s2) == (L, model.split[s2])
+                assert wsk.wsk_seq_segments(h, s2) == _segments_of(model, s2), (step, s2)
+                for p in range(0, L, 5):
+                    assert wsk.wsk_route(h, s2, p) == model.route(s2, p), (step, s2, p)
+        assert wsk.wsk_load_stats(h).slots_used == load_blocks - len(model.free[2])
+    finally:
+        wsk.wsk_destroy(h)
