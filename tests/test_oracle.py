@@ -17,7 +17,7 @@ import scipy.special
 import torch
 
 import oracle
-from oracle.route import CPU, GPU, RouteError, RouteModel
+from oracle.route import CPU, GPU, LOAD, RouteError, RouteModel
 from paper_2609_14507_amd import workloads as wl
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -324,6 +324,65 @@ def test_route_exhaustion_changes_nothing_and_close_reclaims():
     assert m.table(GPU, 1, 4) == [1, 2, 0, -1]
     with pytest.raises(RouteError):
         m.write(1, 12, 1)                # block 3 would need a fourth device slot
+
+
+@pytest.mark.parametrize("bk,D,s,e,L0", [(4, 8, 5, 12, 14), (4, 4, 3, 3, 9), (2, 4, 0, 6, 7), (4, 8, 0, 0, 2),
+                                          (8, 16, 20, 24, 30)])
+def test_route_load_region_and_eviction_invariants(bk, D, s, e, L0):
+    """Brute force over appends and every choice of flush destinations: homes at
+    write time follow [0, s) CPU, [s, load_end) load region, then the D-window;
+    a flush moves exactly the batch [w, floor((w + D)/Bk)*Bk) when it is whole,
+    to its destination, once: a position that left the window never moves again;
+    slots stay unique per pool and none is lost; a batch that is not whole
+    changes nothing."""
+    import itertools
+    for dests in itertools.product((CPU, LOAD), repeat=4):
+        m = RouteModel(bk, 64, 64, 64, D)
+        m.open(0, s, e)
+        m.write(0, 0, L0)
+        for p in range(L0):
+            assert m.route(0, p)[0] == (CPU if p < s else LOAD if p < e else GPU)
+        placed, k = {}, 0
+        for step in range(4 * D):
+            m.append([0])
+            w = m.window[0]
+            w1 = (w + D) // bk * bk
+            before = (dict(m.slot), list(m.homes[0]), m.window[0])
+            moved = m.flush([0], [dests[k % 4]])[0]
+            if w1 > m.length[0]:
+                assert moved == 0 and (dict(m.slot), list(m.homes[0]), m.window[0]) == before
+                continue
+            assert moved == w1 - w and m.window[0] == w1
+            for p in range(w, w1):
+                assert m.route(0, p)[0] == dests[k % 4]
+                assert p not in placed
+            k += 1
+            for p in range(m.length[0]):
+                r = m.route(0, p)
+                if p < m.window[0]:
+                    assert r[0] != GPU
+                    placed.setdefault(p, r)
+                    assert placed[p] == r            # placed data never moves again
+                else:
+                    assert r[0] == GPU
+            for part in (CPU, GPU, LOAD):            # slots unique per pool, none lost
+                used = [v for (pp, _, _), v in m.slot.items() if pp == part]
+                assert len(used) == len(set(used)) and len(used) + len(m.free[part]) == 64
+            addrs = [(m.route(0, p)[0], m.route(0, p)[2], m.route(0, p)[3]) for p in range(m.length[0])]
+            assert len(addrs) == len(set(addrs))
+
+
+def test_route_eviction_exhaustion_changes_nothing():
+    m = RouteModel(4, 1, 8, 1, 8)
+    m.open(0, 0, 0)
+    m.write(0, 0, 8)                     # GPU blocks 0, 1
+    with pytest.raises(RouteError) as ex:
+        m.flush([0], [LOAD])             # two load slots needed, one exists
+    assert ex.value.code == "ENOMEM"
+    assert m.window[0] == 0 and sorted(m.free[LOAD]) == [0] and len(m.free[GPU]) == 6
+    with pytest.raises(RouteError) as ex:
+        m.flush([0, 0], [CPU, CPU])
+    assert ex.value.code == "EINVAL"
 
 
 # ---------------------------------------------------------------------------
