@@ -371,13 +371,15 @@ def load_region_section(w, pf, steps_in, dev, flush, n_steps=5):
     return sect
 
 
-def offload_section(w, pf, steps_in, dev, flush, A_s, c_cpu_s, B_s, n_steps=5):
+def offload_section(w, pf, steps_in, dev, flush, A_s, c_cpu_s, B_s, n_steps=3):
     """The paper's step when the KV does not stay in HBM (Sec. 4.2, 5.1): each
     sequence's CPU share [0, s) is attended in place by the CPU engine while
     the GPU streams its share from the pinned load region (plus the D-window)
-    and attends it; one LSE join.  Timed on the host clock for the all-GPU
-    split (s = 0) and for the split Eq. 2 gives with A (CPU engine) and B
-    (streamed GPU side) measured on this machine."""
+    and attends it; one LSE join.  Timed on the host clock at the all-GPU
+    split (s = 0) and at CPU shares around the one Eq. 2 gives with A (CPU
+    engine) and B (streamed GPU side) measured on this machine, next to Eq. 1's
+    prediction max(r A L, (1 - r) B L) + C for each share (the paper's Fig. 7
+    comparison of the model with measured optima)."""
     import torch
     from paper_2609_14507_amd import wsk
     from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
@@ -386,11 +388,13 @@ def offload_section(w, pf, steps_in, dev, flush, A_s, c_cpu_s, B_s, n_steps=5):
     B, H = len(pf.lengths), w.n_q_heads
     threads = len(os.sched_getaffinity(0))
     L_mean = float(np.mean(pf.lengths))
+    tokens = float(sum(pf.lengths))
     r_star = wsk.wsk_roofline_share(A_s, B_s, c_cpu_s, 0.0, int(L_mean))
+    shares = sorted({0.0} | {round(min(1.0, max(0.0, r_star + d)), 4) for d in (-0.2, -0.1, 0.0, 0.1, 0.2)})
     q_bits = np.ascontiguousarray(steps_in[0].q)
     q = to_device_bf16(q_bits, dev)
     rows = []
-    for label, r in (("all_gpu", 0.0), ("balanced", r_star)):
+    for r in shares:
         splits = [wl.split_point(r, L) for L in pf.lengths]
         load_ends = [max(s, (L - D) // bk * bk) for s, L in zip(splits, pf.lengths)]
         p2 = wl.Prefill(pf.lengths, splits, pf.k, pf.v, pf.gen)
@@ -426,20 +430,28 @@ def offload_section(w, pf, steps_in, dev, flush, A_s, c_cpu_s, B_s, n_steps=5):
             if it:
                 ts.append(time.perf_counter() - t)
         cpu_tok = sum(min(s, L) for s, L in zip(splits, pf.lengths))
-        rows.append((label, r, float(np.median(ts)), cpu_tok))
+        rr = cpu_tok / tokens
+        model = max(rr * A_s * tokens + c_cpu_s, (1 - rr) * B_s * tokens)
+        rows.append((r, float(np.median(ts)), cpu_tok, model))
         sess.close()
-    base = rows[0][2]
+    base = rows[0][1]
+    best = min(rows, key=lambda x: x[1])
+    at_star = [x for x in rows if x[0] == round(r_star, 4)][0]
     out = {"what": "full decode step with the GPU share offloaded: GPU side streamed from the pinned load region "
                    "(wsk_attend_gpu_pass1) while the CPU engine attends [0, s) in place (wsk_cpu_attend_all, %d "
                    "threads), CPU partial copied over, one LSE join (wsk_attend_gpu_pass2); host clock, median of "
-                   "%d" % (threads, n_steps),
+                   "%d, at CPU shares around Eq. 2's, with Eq. 1's prediction" % (threads, n_steps),
            "A_ns_per_token": round(A_s * 1e9, 3), "B_ns_per_token": round(B_s * 1e9, 3),
-           "c_cpu_us": round(c_cpu_s * 1e6, 1), "eq2_share": round(r_star, 4)}
-    for label, r, t, tok in rows:
-        out[label] = {"cpu_share": round(r, 4), "ms": round(t * 1e3, 3), "cpu_tokens": int(tok),
-                      "speedup_vs_all_gpu": round(base / t, 3)}
-    log("offload: all-GPU streamed step %.2f ms; Eq. 2 share %.3f step %.2f ms (%.2fx)"
-        % (rows[0][2] * 1e3, r_star, rows[1][2] * 1e3, base / rows[1][2]))
+           "c_cpu_us": round(c_cpu_s * 1e6, 1), "eq2_share": round(r_star, 4),
+           "sweep": [{"cpu_share": r, "ms": round(t * 1e3, 3), "model_ms": round(mdl * 1e3, 3)}
+                     for r, t, _, mdl in rows],
+           "measured_best_share": best[0],
+           "all_gpu": {"cpu_share": 0.0, "ms": round(base * 1e3, 3)},
+           "balanced": {"cpu_share": at_star[0], "ms": round(at_star[1] * 1e3, 3), "cpu_tokens": int(at_star[2]),
+                        "speedup_vs_all_gpu": round(base / at_star[1], 3)}}
+    log("offload: all-GPU streamed step %.2f ms; Eq. 2 share %.3f step %.2f ms (%.2fx); measured best share %.3f "
+        "(%.2f ms); sweep %s" % (base * 1e3, r_star, at_star[1] * 1e3, base / at_star[1], best[0], best[1] * 1e3,
+                                 [(r, round(t * 1e3, 2)) for r, t, _, _ in rows]))
     return out
 
 

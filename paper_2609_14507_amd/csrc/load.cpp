@@ -229,15 +229,21 @@ void wsk::load_write_rows(wsk_cache *c, int32_t seq, int32_t pos0, int32_t p0, i
     const int bk = c->spec.block_tokens;
     const bool gqa = c->spec.kind == WSK_KIND_GQA;
     const int hkv = gqa ? c->spec.n_kv_heads : 1;
-    std::vector<const uint16_t *> kp(hkv), vp(hkv);
-    for (int32_t p = p0; p < p1; ++p) {
-        uint16_t *slot = load_slot_ptr(c, tab(c, WSK_PART_LOAD, seq, p / bk));
-        for (int g = 0; g < hkv; ++g) {
-            kp[g] = k + ((int64_t)(p - pos0) * hkv + g) * c->row_elems;
-            vp[g] = gqa ? v + ((int64_t)(p - pos0) * hkv + g) * c->row_elems : nullptr;
+    if (p1 <= p0) return;
+    // one task per block: each writes its own slot
+    const int32_t b0 = p0 / bk, b1 = (p1 - 1) / bk;
+    parallel_tasks(b1 - b0 + 1, gather_threads(), [&](int t) {
+        const int32_t blk = b0 + t;
+        uint16_t *slot = load_slot_ptr(c, tab(c, WSK_PART_LOAD, seq, blk));
+        std::vector<const uint16_t *> kp(hkv), vp(hkv);
+        for (int32_t p = std::max(p0, blk * bk); p < std::min(p1, (blk + 1) * bk); ++p) {
+            for (int g = 0; g < hkv; ++g) {
+                kp[g] = k + ((int64_t)(p - pos0) * hkv + g) * c->row_elems;
+                vp[g] = gqa ? v + ((int64_t)(p - pos0) * hkv + g) * c->row_elems : nullptr;
+            }
+            put_position(c, slot, p % bk, kp.data(), vp.data());
         }
-        put_position(c, slot, p % bk, kp.data(), vp.data());
-    }
+    });
 }
 
 // ---- the GPU side of a step: plan ---------------------------------------------
