@@ -211,7 +211,9 @@ def cpu_gpu_steps(w, sess, wsk, steps_in, i0, F, splits, qs, kn, vn, o_m, l_m, f
     t_cpu = float(np.median(cpu_s))
     A = max(t_cpu - c_cpu, 1e-12) / tok
     Bc = gpu_ns_per_token * 1e-9
-    L = float(np.mean(sess.lengths))
+    # A and B are per token of the whole batch and the fixed costs are per
+    # call, so Eq. 2 takes the step's token count
+    L = float(np.sum(sess.lengths))
     r = wsk.wsk_roofline_share(A, Bc, c_cpu, gpu_fixed_us * 1e-6, int(L))
     cpu_engine = {"value": round(tok * w.token_bytes / t_cpu / 1e9, 2), "unit": "GB/s", "cores": threads,
                   "kind": "native (wsk_cpu_attend)",
@@ -221,7 +223,7 @@ def cpu_gpu_steps(w, sess, wsk, steps_in, i0, F, splits, qs, kn, vn, o_m, l_m, f
             "what": "append + GPU pass 1 over [s_b, L_b] while the CPU engine attends [0, s_b), then pass 2 "
                     "merging both partials (the workload's split)"}
     policy = {"A_ns_per_token": round(A * 1e9, 4), "B_ns_per_token": round(Bc * 1e9, 4),
-              "c_cpu_us": round(c_cpu * 1e6, 1), "c_gpu_us": round(gpu_fixed_us, 1), "L": int(L),
+              "c_cpu_us": round(c_cpu * 1e6, 1), "c_gpu_us": round(gpu_fixed_us, 1), "step_tokens": int(L),
               "balanced_cpu_share": round(r, 5),
               "what": "Eq. 2 with A from the CPU engine and B from GPU pass 1 measured above"}
     log("bench: CPU engine %.1f GB/s on %d cores; full CPU+GPU step %.2f ms; balanced CPU share %.4f"
@@ -387,10 +389,12 @@ def offload_section(w, pf, steps_in, dev, flush, A_s, c_cpu_s, B_s, n_steps=3):
     D, bk = 256, 64
     B, H = len(pf.lengths), w.n_q_heads
     threads = len(os.sched_getaffinity(0))
-    L_mean = float(np.mean(pf.lengths))
     tokens = float(sum(pf.lengths))
-    r_star = wsk.wsk_roofline_share(A_s, B_s, c_cpu_s, 0.0, int(L_mean))
-    shares = sorted({0.0} | {round(min(1.0, max(0.0, r_star + d)), 4) for d in (-0.2, -0.1, 0.0, 0.1, 0.2)})
+    # A and B are per token of the whole batch and the CPU engine's fixed cost
+    # is per call, so Eq. 2 takes the step's token count
+    r_star = wsk.wsk_roofline_share(A_s, B_s, c_cpu_s, 0.0, int(tokens))
+    shares = sorted({0.0} | {round(min(1.0, max(0.0, r_star + d)), 4)
+                             for d in (-0.2, -0.1, -0.05, 0.0, 0.05, 0.1, 0.2)})
     q_bits = np.ascontiguousarray(steps_in[0].q)
     q = to_device_bf16(q_bits, dev)
     rows = []
