@@ -215,9 +215,22 @@ def cpu_gpu_steps(w, sess, wsk, steps_in, i0, F, splits, qs, kn, vn, o_m, l_m, f
     # call, so Eq. 2 takes the step's token count
     L = float(np.sum(sess.lengths))
     r = wsk.wsk_roofline_share(A, Bc, c_cpu, gpu_fixed_us * 1e-6, int(L))
-    cpu_engine = {"value": round(tok * w.token_bytes / t_cpu / 1e9, 2), "unit": "GB/s", "cores": threads,
+    # the plain host read rate on the same threads: the CPU engine's ceiling
+    probe = np.ones((1 << 30) // 8, dtype=np.uint64)
+    wsk.wsk_host_read(probe, threads)
+    rd = []
+    for _ in range(3):
+        t = time.perf_counter()
+        wsk.wsk_host_read(probe, threads)
+        rd.append(time.perf_counter() - t)
+    host_gbs = probe.nbytes / float(np.median(rd)) / 1e9
+    del probe
+    engine_gbs = tok * w.token_bytes / t_cpu / 1e9
+    cpu_engine = {"value": round(engine_gbs, 2), "unit": "GB/s", "cores": threads,
                   "kind": "native (wsk_cpu_attend)",
-                  "sample": "the workload's CPU ranges [0, s_b) of %d sequences, %.0f tokens per call, median of %d"
+                  "host_read_gbs": round(host_gbs, 2), "frac_of_host_read": round(engine_gbs / host_gbs, 4),
+                  "sample": "the workload's CPU ranges [0, s_b) of %d sequences, %.0f tokens per call, median of %d; "
+                            "host_read_gbs: wsk_host_read of 1 GiB on the same threads, median of 3"
                             % (B, tok, F)}
     full = {"ms": round(float(np.median(full_s)) * 1e3, 3), "cpu_ms": round(t_cpu * 1e3, 3),
             "what": "append + GPU pass 1 over [s_b, L_b] while the CPU engine attends [0, s_b), then pass 2 "
@@ -226,8 +239,8 @@ def cpu_gpu_steps(w, sess, wsk, steps_in, i0, F, splits, qs, kn, vn, o_m, l_m, f
               "c_cpu_us": round(c_cpu * 1e6, 1), "c_gpu_us": round(gpu_fixed_us, 1), "step_tokens": int(L),
               "balanced_cpu_share": round(r, 5),
               "what": "Eq. 2 with A from the CPU engine and B from GPU pass 1 measured above"}
-    log("bench: CPU engine %.1f GB/s on %d cores; full CPU+GPU step %.2f ms; balanced CPU share %.4f"
-        % (cpu_engine["value"], threads, full["ms"], r))
+    log("bench: CPU engine %.1f GB/s on %d cores (plain host read %.1f GB/s); full CPU+GPU step %.2f ms; "
+        "balanced CPU share %.4f" % (cpu_engine["value"], threads, host_gbs, full["ms"], r))
     return cpu_engine, full, policy
 
 

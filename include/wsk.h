@@ -602,6 +602,16 @@ int wsk_policy_model(const wsk_policy *policy, wsk_roofline *model);
  */
 int wsk_stream_read(const void *p, size_t bytes, int32_t workgroups, uint32_t *out, void *stream);
 
+/*
+ * Measurement aid, not part of the decode path: reads `bytes` of HOST memory
+ * at p once on `threads` threads of the CPU engine's pool (<= 0: every
+ * hardware thread), 64-byte vector loads in 4 MiB pieces, and stores the XOR
+ * of its 64-bit words in *out (HOST).  Timing it gives the plain host read
+ * rate the CPU engine (wsk_cpu_attend) can be compared with.  bytes a
+ * multiple of 8.  Synchronous.  Errors: EINVAL.
+ */
+int wsk_host_read(const void *p, size_t bytes, int32_t threads, uint64_t *out);
+
 #ifdef __cplusplus
 }
 #endif

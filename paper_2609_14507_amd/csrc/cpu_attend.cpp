@@ -379,6 +379,47 @@ private:
 
 }  // namespace
 
+namespace {
+// XOR of the 64-bit words of [p, p + n), read with 64-byte vector loads where
+// the CPU has them.
+__attribute__((target("avx512f"))) uint64_t fold_avx512(const uint64_t *p, size_t n) {
+    __m512i a0 = _mm512_setzero_si512(), a1 = a0, a2 = a0, a3 = a0;
+    size_t i = 0;
+    for (; i + 32 <= n; i += 32) {
+        a0 = _mm512_xor_si512(a0, _mm512_loadu_si512(p + i));
+        a1 = _mm512_xor_si512(a1, _mm512_loadu_si512(p + i + 8));
+        a2 = _mm512_xor_si512(a2, _mm512_loadu_si512(p + i + 16));
+        a3 = _mm512_xor_si512(a3, _mm512_loadu_si512(p + i + 24));
+    }
+    alignas(64) uint64_t t[8];
+    _mm512_store_si512(t, _mm512_xor_si512(_mm512_xor_si512(a0, a1), _mm512_xor_si512(a2, a3)));
+    uint64_t r = 0;
+    for (int k = 0; k < 8; ++k) r ^= t[k];
+    for (; i < n; ++i) r ^= p[i];
+    return r;
+}
+uint64_t fold_plain(const uint64_t *p, size_t n) {
+    uint64_t r = 0;
+    for (size_t i = 0; i < n; ++i) r ^= p[i];
+    return r;
+}
+}  // namespace
+
+uint64_t host_read(const void *p, size_t bytes, int threads) {
+    const size_t piece = 4u << 20;   // 4 MiB per task
+    const size_t n = (bytes + piece - 1) / piece;
+    std::vector<uint64_t> part(n, 0);
+    const bool vec = __builtin_cpu_supports("avx512f");
+    parallel_tasks((int)n, threads, [&](int t) {
+        const size_t a = (size_t)t * piece, len = std::min(piece, bytes - a) / 8;
+        const uint64_t *w = reinterpret_cast<const uint64_t *>((const char *)p + a);
+        part[t] = vec ? fold_avx512(w, len) : fold_plain(w, len);
+    });
+    uint64_t r = 0;
+    for (uint64_t x : part) r ^= x;
+    return r;
+}
+
 void parallel_tasks(int n_tasks, int threads, const std::function<void(int)> &task) {
     if (n_tasks <= 0) return;
     std::atomic<int> next{0};

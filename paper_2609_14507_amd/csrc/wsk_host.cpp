@@ -860,6 +860,12 @@ int wsk_cpu_attend(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *s
     return cpu_attend(x);
 }
 
+int wsk_host_read(const void *p, size_t bytes, int32_t threads, uint64_t *out) {
+    if (!p || !out || bytes == 0 || bytes % 8) return fail(WSK_EINVAL, "host_read arguments");
+    *out = host_read(p, bytes, threads > 0 ? threads : (int)std::max(1u, std::thread::hardware_concurrency()));
+    return WSK_OK;
+}
+
 int wsk_stream_read(const void *p, size_t bytes, int32_t workgroups, uint32_t *out, void *stream) {
     if (!p || !out || bytes == 0 || bytes % 32768 || !aligned16(p)) return fail(WSK_EINVAL, "stream_read arguments");
     int dev = 0, cus = 256;

@@ -148,6 +148,9 @@ int cpu_attend(const CpuAttendArgs &args);
 // Runs task(0 .. n_tasks-1) on up to `threads` host threads (the calling one
 // and the CPU engine's persistent pool); returns when all are done.
 void parallel_tasks(int n_tasks, int threads, const std::function<void(int)> &task);
+// Reads host memory [p, p + bytes) once on `threads` threads of that pool
+// (bytes a multiple of 8) and returns the XOR of its 64-bit words.
+uint64_t host_read(const void *p, size_t bytes, int threads);
 
 // Sets the calling thread's last error message; returns code.
 int policy_fail(int code, const char *msg);

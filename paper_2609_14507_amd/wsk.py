@@ -97,6 +97,7 @@ _SIGS = {
     "wsk_attend_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_attend": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_stream_read": ([_VP, ctypes.c_size_t, _I32, _VP, _VP], ctypes.c_int),
+    "wsk_host_read": ([_VP, ctypes.c_size_t, _I32, ctypes.POINTER(ctypes.c_uint64)], ctypes.c_int),
     "wsk_attend_blocks_workspace": ([_VP, _I32, _PI32, _PI32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_attend_blocks": ([_VP, _I32, _PI32, _PI32, _PI32, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP],
                           ctypes.c_int),
@@ -364,6 +365,15 @@ def wsk_mla_expand(o_lat, w_uv, o, stream=None):
     n, H, dl = o_lat.shape
     dv = w_uv.shape[2]
     _check(lib().wsk_mla_expand(n, H, dl, dv, _ptr(o_lat), _ptr(w_uv), _ptr(o), _stream(stream)))
+
+
+def wsk_host_read(arr: np.ndarray, threads: int = 0) -> int:
+    """Measurement aid: one plain read of a host array on the CPU engine's threads."""
+    if not arr.flags["C_CONTIGUOUS"]:
+        raise ValueError("array must be C-contiguous")
+    out = ctypes.c_uint64()
+    _check(lib().wsk_host_read(arr.ctypes.data, arr.nbytes, threads, ctypes.byref(out)))
+    return out.value
 
 
 def wsk_stream_read(buf, out, workgroups: int = 0, stream=None):

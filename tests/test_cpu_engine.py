@@ -95,3 +95,15 @@ def test_cpu_engine_errors():
         assert ei.value.code in (wsk.WSK_EINVAL, wsk.WSK_ESTATE)
     finally:
         wsk.wsk_destroy(h)
+
+
+@pytest.mark.parametrize("nbytes", [8, 8000, (5 << 20) + 8, 3 << 22])
+def test_host_read_probe_folds_every_word(nbytes):
+    """wsk_host_read reads every 64-bit word once (its XOR equals numpy's),
+    whole 4 MiB pieces and ragged tails alike, on any thread count."""
+    a = np.random.default_rng(nbytes).integers(0, 2 ** 63, size=nbytes // 8, dtype=np.uint64)
+    want = int(np.bitwise_xor.reduce(a))
+    for threads in (1, 3, 0):
+        assert wsk.wsk_host_read(a, threads) == want
+    with pytest.raises(wsk.WskError):
+        wsk.wsk_host_read(np.zeros(3, np.uint8))
