@@ -10,11 +10,16 @@ resident in HBM; the CPU-range partial fed to the merge is a seeded
 synthetic (O, LSE) pair (the merge's cost does not depend on its values).
 
 Timing: W untimed warmup steps, then K timed steps.  Before each step a
-512 MB buffer is rewritten so the 256 MB Infinity Cache holds no KV; HIP
-events on the stream the kernels run on bracket each step and, inside it,
-the two passes of the attend call, outside the flush.  The algorithmic bytes
-of a step are the bf16 K and V rows (MLA: latent rows) of every attended
-position, read once.
+512 MB buffer is rewritten so the 256 MB Infinity Cache holds no KV.  One
+pair of HIP events on the stream the kernels run on brackets the K
+(flush + step) pairs, and another the same K flushes alone, run right after;
+a step's time is the difference over K.  Events are not recorded between
+the steps: each record leaves the GPU idle for ~5 us, which a per-step pair
+would count as step time.  The pass-1 kernel alone (the roofline's kernel)
+is timed the same way, K (flush + pass 1) pairs less K flushes.  K more
+diagnostic steps run the pieces as separate calls with events between
+them, for the breakdown.  The algorithmic bytes of a step are the bf16 K
+and V rows (MLA: latent rows) of every attended position, read once.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -570,45 +575,75 @@ def main():
     def kv_bytes():   # algorithmic bytes of the next step: [s_b, L_b + 1) of every sequence
         return sum((sess.lengths[b] + 1 - min(splits[b], sess.lengths[b])) * w.token_bytes for b in range(B))
 
-    ev_step = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
+    def bracket(fn):   # ms of fn() on the stream, one event pair around it
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
+    def flushes():
+        if not args.no_flush:
+            for _ in range(K):
+                flush.add_(1)
+
     ev_part = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
     log("bench: %d warmup + %d timed steps (+ %d diagnostic steps with per-part events)" % (W, K, K))
     for i in range(W):
         step(i)
     torch.cuda.synchronize()
     nbytes = []
+
+    def timed_steps():
+        for k in range(K):
+            nbytes.append(kv_bytes())
+            step(W + k)
     t0 = time.perf_counter()
-    for k in range(K):
-        nbytes.append(kv_bytes())
-        step(W + k, ev=ev_step[k])
-    torch.cuda.synchronize()
+    t_steps = bracket(timed_steps)
     wall = time.perf_counter() - t0
+    t_flush = bracket(flushes)
+    step_ms = (t_steps - t_flush) / K
+
+    # the pass-1 kernel alone, K launches over the current GPU ranges
+    p1_bytes = float(sum((sess.lengths[b] - min(splits[b], sess.lengths[b])) * w.token_bytes for b in range(B)))
+
+    def pass1s():
+        for k in range(K):
+            if not args.no_flush:
+                flush.add_(1)
+            sess.attend_pass1(qs[W + k])
+    t_p1 = bracket(pass1s)
+    t_flush2 = bracket(flushes)
+    p1_kernel_ms = (t_p1 - t_flush2) / K
+
     d_bytes = []
     for k in range(K):
         d_bytes.append(kv_bytes())
         step(W + K + k, parts=ev_part[k])
     torch.cuda.synchronize()
-    step_ms = np.array([e[0].elapsed_time(e[1]) for e in ev_step])
     el = lambda a, b: np.array([e[a].elapsed_time(e[b]) for e in ev_part])
     app_ms, p1_ms, p2_ms = el(0, 1), el(1, 2), el(2, 3)
     exp_ms = el(3, 4) if mla else np.zeros(K)
     nbytes = np.array(nbytes, dtype=np.float64)
     d_bytes = np.array(d_bytes, dtype=np.float64)
-    value = float(nbytes.sum() / (step_ms.sum() * 1e-3) / 1e9)
+    value = float(nbytes.mean() / (step_ms * 1e-3) / 1e9)
     att_gbs = float(d_bytes.sum() / ((p1_ms + p2_ms).sum() * 1e-3) / 1e9)
-    p1_gbs = float(d_bytes.sum() / (p1_ms.sum() * 1e-3) / 1e9)
-    log("bench: step %.1f us; diagnostic steps: absorb+append %.1f, attend pass 1 %.1f, pass 2 with merge %.1f, "
-        "expand %.1f us; pass 1 %.0f GB/s; wall %.1f ms/step"
-        % (step_ms.mean() * 1e3, app_ms.mean() * 1e3, p1_ms.mean() * 1e3, p2_ms.mean() * 1e3, exp_ms.mean() * 1e3,
-           p1_gbs, wall / K * 1e3))
+    p1_gbs = float(p1_bytes / (p1_kernel_ms * 1e-3) / 1e9)
+    log("bench: step %.1f us (%.1f us per flush + step less %.1f us per flush); pass 1 alone %.1f us, %.0f GB/s; "
+        "diagnostic steps (events between parts): absorb+append %.1f, attend pass 1 %.1f, pass 2 with merge %.1f, "
+        "expand %.1f us; wall %.1f ms/step"
+        % (step_ms * 1e3, t_steps / K * 1e3, t_flush / K * 1e3, p1_kernel_ms * 1e3, p1_gbs, app_ms.mean() * 1e3,
+           p1_ms.mean() * 1e3, p2_ms.mean() * 1e3, exp_ms.mean() * 1e3, wall / K * 1e3))
     cpu_engine, full_step, policy = None, None, None
     if not args.no_cpu_engine:
         cpu_engine, full_step, policy = cpu_gpu_steps(
             w, sess, wsk_mod(), steps_in, W + 2 * K, F, splits, qs, kn, vn, o_m, l_m, flush, dev,
             None,   # MLA: the drawn absorbed query feeds both engines (no absorb launch)
             (lambda: wsk_mod().wsk_mla_expand(o_m, w_uv_d, o_out)) if mla else None,
-            gpu_ns_per_token=float(p1_ms.mean() * 1e6 / (d_bytes.mean() / w.token_bytes)),
-            gpu_fixed_us=float((step_ms.mean() - p1_ms.mean()) * 1e3))
+            gpu_ns_per_token=float(p1_kernel_ms * 1e6 / (p1_bytes / w.token_bytes)),
+            gpu_fixed_us=float((step_ms - p1_kernel_ms) * 1e3))
     sess.close()
     load_region = None if args.no_load_region else load_region_section(w, pf, steps_in, dev, flush)
     offload = None
@@ -656,7 +691,7 @@ def main():
         "n_gpus": 1,
         "steps": K,
         "warmup": W,
-        "ms_per_step": round(float(step_ms.mean()), 4),
+        "ms_per_step": round(float(step_ms), 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -680,17 +715,20 @@ def main():
             "cache_flush_between_steps": not args.no_flush,
         },
         "breakdown_us": {
-            "step_p10": round(float(np.percentile(step_ms, 10) * 1e3), 2),
-            "step_p90": round(float(np.percentile(step_ms, 90) * 1e3), 2),
+            "step": round(step_ms * 1e3, 2),
+            "flush_plus_step": round(t_steps / K * 1e3, 2),
+            "flush": round(t_flush / K * 1e3, 2),
+            "pass1_kernel": round(p1_kernel_ms * 1e3, 2),
             "wall_per_step_incl_flush": round(wall / K * 1e6, 1),
-            "diagnostic_steps": "K more steps with events between the parts (each record adds GPU time)",
+            "diagnostic_steps": "K more steps with events between the parts (each record adds ~5 us of GPU "
+                                "idle time to the part it closes)",
             ("absorb_append" if mla else "append"): round(float(app_ms.mean() * 1e3), 2),
             "attend_pass1": round(float(p1_ms.mean() * 1e3), 2),
             "attend_pass2_combine_merge": round(float(p2_ms.mean() * 1e3), 2),
             **({"expand": round(float(exp_ms.mean() * 1e3), 2)} if mla else {}),
             "attend_gbs": round(att_gbs, 1),
         },
-        "roofline": roofline(w, "mla" if mla else "gqa", p1_gbs, float(nbytes.mean())),
+        "roofline": roofline(w, "mla" if mla else "gqa", p1_gbs, p1_bytes),
         "stream_read_probe": {"value": round(probe_gbs, 1), "unit": "GB/s", "bytes": 2 << 30,
                               "by_workgroups": probe_sweep,
                               "what": "wsk_stream_read: one plain read of 2 GiB with the attention kernels' "

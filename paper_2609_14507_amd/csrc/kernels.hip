@@ -1,50 +1,11 @@
 // Small kernels of the decode path, gfx950: chunk combine, LSE merge,
 // decode append, bulk scatter, MLA query absorption and output expansion.
 
+#include "device_rows.h"
 #include "wsk_internal.h"
 
 namespace wsk {
 namespace {
-
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
-typedef __attribute__((ext_vector_type(4))) float f32x4;
-
-__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
-
-// Places 16-byte piece k (dims 8k..8k+7) of the K (which = 0) or V row of
-// token `row` of one KV head into the GPU pool's TILED64 format; `head`
-// points at the head's first tile in the slot.  A tile is 1024 K pieces then
-// 1024 V pieces of 8 bf16, in the order the attention kernel's matrix-core
-// lanes read them (see attend_gqa.hip).
-__device__ __forceinline__ void put_tiled(uint16_t *head, int row, int which, int k, u32x4 v) {
-    uint16_t *tile = head + (int64_t)(row >> 6) * (2 * 64 * 128);
-    const int t = row & 63;
-    if (which == 0) {
-        const int mt = 2 * (t >> 5) + ((t & 7) >> 2);
-        const int nk = 4 * ((t & 31) >> 3) + (t & 3);
-        const int piece = (4 * mt + (k >> 2)) * 64 + 16 * (k & 3) + nk;
-        *reinterpret_cast<u32x4 *>(tile + piece * 8) = v;
-    } else {
-        uint16_t *vt = tile + 1024 * 8;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int d = 8 * k + e;
-            const int piece = (2 * (d >> 4) + (t >> 5)) * 64 + 16 * ((t & 31) >> 3) + (d & 15);
-            vt[piece * 8 + (t & 7)] = (uint16_t)((e & 1) ? (v[e >> 1] >> 16) : (v[e >> 1] & 0xffffu));
-        }
-    }
-}
-
-// Places 16-byte piece c (dims 8c..8c+7) of the MLA row of token `row` into
-// a GPU-pool slot in the MLA32 format: 32-token tiles of 2304 pieces, piece
-// (ks, mt, lane) being what matrix-core lane (lane / 16, lane % 16) of M-tile
-// mt loads for K-step ks (see attend_mla.hip).
-__device__ __forceinline__ void put_mla32(uint16_t *slot, int row, int c, u32x4 v) {
-    uint16_t *tile = slot + (int64_t)(row >> 5) * (32 * (kLatent + kRope));
-    const int u = row & 31;
-    const int piece = (2 * (c >> 2) + ((u >> 2) & 1)) * 64 + 16 * (c & 3) + 4 * (u >> 3) + (u & 3);
-    *reinterpret_cast<u32x4 *>(tile + piece * 8) = v;
-}
 
 // fp32 -> bf16, round to nearest even (NaN stays NaN).
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
@@ -57,15 +18,17 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 // ---------------------------------------------------------------------------
 // Chunk combine: O = sum_c w_c O_c / sum_c w_c, w_c = exp(lse_c - max lse),
 // LSE = max + ln sum w_c.  Workgroup = (sequence, head, 128-column slice);
-// its 256 threads are 8 chunk groups x 32 float4 columns, so a whole
-// sequence's partials are fetched in one or two rounds of loads; the groups
-// are summed through LDS.  An optional partial over other keys (o_x, lse_x:
+// its 256 threads are 8 chunk groups x 32 float4 columns; the partials of
+// the first 32 chunks are loaded together with every LSE before any is used,
+// so up to 32 chunks cost one wait for memory; the groups are summed through
+// LDS.  An optional partial over other keys (o_x, lse_x:
 // the CPU range) enters as one more chunk, which makes this the LSE merge of
 // the CPU and GPU partials too.  Nothing to merge: O = 0, LSE = -inf.
 // ---------------------------------------------------------------------------
 constexpr int kCombineCols4 = 32;                   // float4 columns per workgroup
 constexpr int kCombineGroups = 256 / kCombineCols4; // chunk groups
 constexpr int kCombineW = 1024;                     // chunk weights kept in LDS
+constexpr int kCombineRegs = 4;                     // chunk partials per thread loaded up front
 
 __device__ __forceinline__ float block_reduce(float v, bool is_max, float *s_red) {
 #pragma unroll
@@ -82,36 +45,86 @@ __device__ __forceinline__ float block_reduce(float v, bool is_max, float *s_red
     return r;
 }
 
-// One workgroup's part of the combine.  s_new / v_new: an optional partial
-// made of a single token (score s_new in the natural-log domain, value row
-// v_new, bf16, starting at this workgroup's first column); -INFINITY / NULL
-// when absent.
-__device__ __forceinline__ void combine_row(const CombineParams &p, int width, float s_new, const uint16_t *v_new,
-                                            float *s_w, float *s_red, f32x4 (*s_acc)[kCombineCols4]) {
+// What one thread of a combine workgroup reads.  combine_load issues all of
+// it at once -- the partials of the first kCombineGroups x kCombineRegs
+// chunks, their LSEs, the other partial and the new token's value columns --
+// so that the combine waits for memory once, not once per dependent step.
+struct CombineIn {
+    f32x4 po[kCombineRegs];   // chunk g + kCombineGroups j, this thread's float4 column
+    f32x4 ox;                 // other partial's columns (chunk group 0)
+    f32x4 vn;                 // new token's value columns (chunk group 0)
+    float lse_c;              // LSE of chunk tid (tid < nc), else -inf
+    float lx;                 // other partial's LSE
+    int nc;
+};
+
+// v_new: the new token's value row (bf16) from this workgroup's first column,
+// or NULL when there is none.
+__device__ __forceinline__ CombineIn combine_load(const CombineParams &p, int width, const uint16_t *v_new) {
     const int row = blockIdx.x;                 // i * H + h
     const int H = p.n_q_heads;
     const int i = row / H;
     const int h = row - i * H;
     const int c0 = p.chunk_begin[i];
-    const int nc = p.chunk_begin[i + 1] - c0;
+    const int tid = threadIdx.x;
+    const int g = tid / kCombineCols4;
+    const int c4 = tid - g * kCombineCols4;
+    const int col0 = blockIdx.y * 4 * kCombineCols4;
+    CombineIn in;
+    in.nc = p.chunk_begin[i + 1] - c0;
+    const f32x4 *po = reinterpret_cast<const f32x4 *>(p.part_o + ((int64_t)c0 * H + h) * width + col0) + c4;
+    const int64_t cstride = (int64_t)H * width / 4;
+#pragma unroll
+    for (int j = 0; j < kCombineRegs; ++j) {
+        const int c = g + kCombineGroups * j;
+        in.po[j] = c < in.nc ? po[c * cstride] : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    in.lse_c = tid < in.nc ? p.part_lse[(int64_t)(c0 + tid) * H + h] : -INFINITY;
+    in.lx = p.lse_x ? p.lse_x[row] : -INFINITY;
+    in.ox = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (p.o_x && g == 0) in.ox = reinterpret_cast<const f32x4 *>(p.o_x + (int64_t)row * width + col0)[c4];
+    in.vn = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (v_new && g == 0) {
+        const uint2 v2 = reinterpret_cast<const uint2 *>(v_new)[c4];
+        in.vn = f32x4{__uint_as_float(v2.x << 16), __uint_as_float(v2.x & 0xffff0000u),
+                      __uint_as_float(v2.y << 16), __uint_as_float(v2.y & 0xffff0000u)};
+    }
+    return in;
+}
+
+// One workgroup's part of the combine, from what combine_load read.  s_new:
+// the score of an optional partial made of the single token whose value row
+// combine_load was given (natural-log domain), -INFINITY when absent.
+__device__ __forceinline__ void combine_finish(const CombineParams &p, int width, const CombineIn &in, float s_new,
+                                               float *s_w, float *s_red, f32x4 (*s_acc)[kCombineCols4]) {
+    const int row = blockIdx.x;
+    const int H = p.n_q_heads;
+    const int i = row / H;
+    const int h = row - i * H;
+    const int c0 = p.chunk_begin[i];
+    const int nc = in.nc;
     const int tid = threadIdx.x;
     const int col0 = blockIdx.y * 4 * kCombineCols4;
     f32x4 *out = reinterpret_cast<f32x4 *>(p.o + (int64_t)row * width + col0);
-    const float lx = p.lse_x ? p.lse_x[row] : -INFINITY;
-    if (nc == 0 && lx == -INFINITY && s_new == -INFINITY) {
+    if (nc == 0 && in.lx == -INFINITY && s_new == -INFINITY) {
         if (tid < kCombineCols4) out[tid] = f32x4{0.f, 0.f, 0.f, 0.f};
         if (tid == 0 && blockIdx.y == 0) p.lse[row] = -INFINITY;
         return;
     }
     const float *pl = p.part_lse + (int64_t)c0 * H + h;
-    float m = fmaxf(lx, s_new);
-    for (int c = tid; c < nc; c += 256) m = fmaxf(m, pl[(int64_t)c * H]);
+    float m = fmaxf(fmaxf(in.lx, s_new), in.lse_c);
+    for (int c = tid + 256; c < nc; c += 256) m = fmaxf(m, pl[(int64_t)c * H]);
     m = block_reduce(m, true, s_red);
-    // the other partials: weights wx, wn (0 when absent or empty; then they are not read)
-    const float wx = lx == -INFINITY ? 0.f : __expf(lx - m);
+    // the other partials' weights (0 when absent or empty; then their columns are not used)
+    const float wx = in.lx == -INFINITY ? 0.f : __expf(in.lx - m);
     const float wn = s_new == -INFINITY ? 0.f : __expf(s_new - m);
     float dsum = tid == 0 ? wx + wn : 0.f;
-    for (int c = tid; c < nc; c += 256) {
+    if (tid < nc) {
+        const float w = __expf(in.lse_c - m);
+        s_w[tid] = w;
+        dsum += w;
+    }
+    for (int c = tid + 256; c < nc; c += 256) {
         const float w = __expf(pl[(int64_t)c * H] - m);
         if (c < kCombineW) s_w[c] = w;
         dsum += w;
@@ -119,17 +132,18 @@ __device__ __forceinline__ void combine_row(const CombineParams &p, int width, f
     const float den = block_reduce(dsum, false, s_red);   // its barriers also publish s_w
     const int g = tid / kCombineCols4;
     const int c4 = tid - g * kCombineCols4;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (g == 0 && wx != 0.f) acc = wx * in.ox;
+    if (g == 0 && wn != 0.f) acc += wn * in.vn;
+#pragma unroll
+    for (int j = 0; j < kCombineRegs; ++j) {
+        const int c = g + kCombineGroups * j;
+        if (c < nc) acc += s_w[c] * in.po[j];
+    }
     const f32x4 *po = reinterpret_cast<const f32x4 *>(p.part_o + ((int64_t)c0 * H + h) * width + col0) + c4;
     const int64_t cstride = (int64_t)H * width / 4;
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (g == 0 && wx != 0.f) acc = wx * reinterpret_cast<const f32x4 *>(p.o_x + (int64_t)row * width + col0)[c4];
-    if (g == 0 && wn != 0.f) {
-        const uint2 v2 = reinterpret_cast<const uint2 *>(v_new)[c4];
-        acc += wn * f32x4{__uint_as_float(v2.x << 16), __uint_as_float(v2.x & 0xffff0000u),
-                          __uint_as_float(v2.y << 16), __uint_as_float(v2.y & 0xffff0000u)};
-    }
 #pragma unroll 8
-    for (int c = g; c < nc; c += kCombineGroups) {
+    for (int c = g + kCombineGroups * kCombineRegs; c < nc; c += kCombineGroups) {
         const float w = c < kCombineW ? s_w[c] : __expf(pl[(int64_t)c * H] - m);
         acc += w * po[c * cstride];
     }
@@ -148,18 +162,22 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int
     __shared__ float s_w[kCombineW];
     __shared__ float s_red[4];
     __shared__ f32x4 s_acc[kCombineGroups][kCombineCols4];
-    combine_row(p, width, -INFINITY, nullptr, s_w, s_red, s_acc);
+    const CombineIn in = combine_load(p, width, nullptr);
+    combine_finish(p, width, in, -INFINITY, s_w, s_red, s_acc);
 }
 
 // ---------------------------------------------------------------------------
 // Pass 2 of a decode step.  Workgroup (sequence i, head h, column slice) as
-// in combine_kernel; it first scores the step's new token against its query
+// in combine_kernel; it also scores the step's new token against its query
 // row (q . k_new, fp32 from bf16, the whole row, formed by each wavefront
-// with shuffles), merges that token as one
-// more partial, and -- in the workgroup of the first query head of each KV
-// head and the first column slice -- stores the new row into the GPU pool
-// (the decode append; the pass-1 kernels of this step did not read it).
+// with shuffles), merges that token as one more partial, and -- in the
+// workgroup of the first query head of each KV head and the first column
+// slice -- stores the new row into the GPU pool (the decode append; the
+// pass-1 kernels of this step did not read it).  The combine's loads and the
+// dot product's are issued before either is used.
 // ---------------------------------------------------------------------------
+constexpr int kMaxRowPerLane = (kLatent + kRope + 63) / 64;   // 9: the widest row over 64 lanes
+
 __global__ __launch_bounds__(256) void step_combine_kernel(const StepCombineParams sp, int width) {
     __shared__ float s_w[kCombineW];
     __shared__ float s_red[4];
@@ -173,10 +191,20 @@ __global__ __launch_bounds__(256) void step_combine_kernel(const StepCombinePara
     const bool gqa = sp.kind == 0;
     const uint16_t *kr = sp.k_new + (gqa ? ((int64_t)i * sp.n_kv_heads + g) * re : (int64_t)i * re);
     const uint16_t *qr = sp.q + (int64_t)i * sp.q_row + (int64_t)h * re;
+    const uint16_t *vr = gqa ? sp.v_new + ((int64_t)i * sp.n_kv_heads + g) * re : kr;
+    const CombineIn in = combine_load(sp.cp, width, vr + blockIdx.y * 4 * kCombineCols4);
     // every wavefront forms the whole dot product (no barrier on this path)
     const int lane = tid & 63;
+    uint16_t qe[kMaxRowPerLane], ke[kMaxRowPerLane];
+#pragma unroll
+    for (int j = 0; j < kMaxRowPerLane; ++j) {
+        const int e = lane + 64 * j;
+        qe[j] = e < re ? qr[e] : (uint16_t)0;
+        ke[j] = e < re ? kr[e] : (uint16_t)0;
+    }
     float d = 0.f;
-    for (int e = lane; e < re; e += 64) d = fmaf(bf16_to_f32(qr[e]), bf16_to_f32(kr[e]), d);
+#pragma unroll
+    for (int j = 0; j < kMaxRowPerLane; ++j) d = fmaf(bf16_to_f32(qe[j]), bf16_to_f32(ke[j]), d);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) d += __shfl_xor(d, o);
     // the append of the new row
@@ -186,7 +214,6 @@ __global__ __launch_bounds__(256) void step_combine_kernel(const StepCombinePara
         if (tid == 0 && h == 0 && sp.tab_index[i] >= 0) sp.table[sp.tab_index[i]] = sp.tab_slot[i];
         const int row16 = re / 8;
         if (gqa) {
-            const uint16_t *vr = sp.v_new + ((int64_t)i * sp.n_kv_heads + g) * re;
             uint16_t *head = sp.pool + slot0 + (int64_t)g * 2 * sp.block_tokens * re;
             for (int t = tid; t < 2 * row16; t += 256) {
                 const int which = t / row16;
@@ -198,8 +225,7 @@ __global__ __launch_bounds__(256) void step_combine_kernel(const StepCombinePara
                 put_mla32(sp.pool + slot0, row, k, reinterpret_cast<const u32x4 *>(kr)[k]);
         }
     }
-    const uint16_t *vrow = (gqa ? sp.v_new + ((int64_t)i * sp.n_kv_heads + g) * re : kr) + blockIdx.y * 4 * kCombineCols4;
-    combine_row(sp.cp, width, d * sp.scale, vrow, s_w, s_red, s_acc);
+    combine_finish(sp.cp, width, in, d * sp.scale, s_w, s_red, s_acc);
 }
 
 // ---------------------------------------------------------------------------

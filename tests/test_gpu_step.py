@@ -163,6 +163,49 @@ def test_decode_step_many_sequences_and_refusals():
         assert [wsk.wsk_seq_info(sess.h, b)[0] for b in range(2)] == before
 
 
+@pytest.mark.parametrize("all_gpu", [True, False])
+def test_decode_step_full_launch_two_head_groups(all_gpu):
+    """GQA decode steps over 64 sequences (the most one launch takes) with 32
+    query heads per KV head (two head groups share each KV head and its new
+    row), ragged lengths, steps with and without the CPU partial, against the
+    oracle and against a twin cache driven by wsk_append + wsk_attend_gpu:
+    close outputs, byte-identical pools, every step.  all_gpu=False adds a
+    sequence whose GPU range is empty before the first step."""
+    B = 64
+    w = _workload("gqa", B, 64, seed=21)
+    gen = torch.Generator().manual_seed(23)
+    lengths = [int(x) for x in torch.randint(40, 400, (B,), generator=gen)]
+    splits = [L // 3 for L in lengths]
+    if not all_gpu:
+        splits[5] = lengths[5]
+    pf = _prefill(w, lengths, splits, gen)
+    k_all, v_all = list(pf.k), list(pf.v)
+    dv, g = _dims(w)
+    say("case decode step full launch", all_gpu)
+    with DecodeSession(w, pf, DEV, extra_tokens=4) as sess, DecodeSession(w, pf, DEV, extra_tokens=4) as twin:
+        for step in range(3):
+            q_bits = wl.draw_bf16(gen, (B, w.n_q_heads, w.row_elems))
+            kn, vn = _new_rows(w, B, gen)
+            q, knd, vnd = (to_device_bf16(x, sess.dev) for x in (q_bits, kn, vn))
+            o_x, l_x = (None, None) if step == 0 else _cpu_partial(sess, q_bits)
+            o, lse = _step(sess, q, knd, vnd, o_x, l_x)
+            twin.append(knd, vnd)
+            o2, lse2 = twin.attend_gpu(q, o_x=o_x, lse_x=l_x)
+            for b in range(B):
+                k_all[b] = np.concatenate([k_all[b], kn[b:b + 1]])
+                v_all[b] = np.concatenate([v_all[b], vn[b:b + 1]])
+            o, lse, o2, lse2 = (t.cpu().numpy() for t in (o, lse, o2, lse2))
+            for b in range(B):
+                lo = 0 if o_x is not None else splits[b]
+                o_r, l_r = oracle.attend(q_bits[b], k_all[b], v_all[b], lo, sess.lengths[b], w.softmax_scale, g,
+                                         dv=dv)
+                assert_close(o[b], o_r, "full launch step %d b%d" % (step, b))
+                assert_lse(lse[b], l_r, "full launch step %d b%d" % (step, b))
+            assert np.abs(o - o2).max() <= 1e-5 and np.abs(lse - lse2).max() <= 1e-5
+            torch.cuda.synchronize()
+            assert np.array_equal(_gpu_pool(sess), _gpu_pool(twin))
+
+
 @pytest.mark.parametrize("kind", ["gqa", "mla"])
 def test_decode_loop_with_policy_eviction(kind):
     """300 decode steps through wsk_decode_step on a cache whose GPU share
