@@ -12,13 +12,16 @@ synthetic (O, LSE) pair (the merge's cost does not depend on its values).
 Timing: W untimed warmup steps, then K timed steps.  Before each step a
 512 MB buffer is rewritten so the 256 MB Infinity Cache holds no KV.  One
 pair of HIP events on the stream the kernels run on brackets the K
-(flush + step) pairs, and another the same K flushes alone, run right after;
-a step's time is the difference over K.  Events are not recorded between
+(flush + step) pairs, and others the same K flushes alone, run right before
+and right after; a step's time is the difference (from the flushes' mean)
+over K.  Events are not recorded between
 the steps: each record leaves the GPU idle for ~5 us, which a per-step pair
 would count as step time.  The pass-1 kernel alone (the roofline's kernel)
 is timed the same way, K (flush + pass 1) pairs less K flushes.  K more
-diagnostic steps run the pieces as separate calls with events between
-them, for the breakdown.  The algorithmic bytes of a step are the bf16 K
+steps, each between its own pair of events, give the per-step median, p10
+and p90 (each with one event's idle time in it); K more diagnostic steps
+run the pieces as separate calls with events between them, for the
+breakdown.  The algorithmic bytes of a step are the bf16 K
 and V rows (MLA: latent rows) of every attended position, read once.
 
 Prints one JSON line on stdout; progress goes to stderr.
@@ -518,9 +521,9 @@ def main():
         splits = [wl.split_point(args.share, L) for L in pf.lengths]
         pf = wl.Prefill(pf.lengths, splits, pf.k, pf.v, pf.gen)
     F = 5                                    # full CPU + GPU steps after the GPU-only ones
-    steps_in = [wl.draw_step(w, pf.gen) for _ in range(W + 2 * K + F)]
+    steps_in = [wl.draw_step(w, pf.gen) for _ in range(W + 3 * K + F)]
     log("bench: routing the prefill into the cache")
-    sess = DecodeSession(w, pf, 0, extra_tokens=W + 2 * K + F)
+    sess = DecodeSession(w, pf, 0, extra_tokens=W + 3 * K + F)
     B, H = sess.B, w.n_q_heads
     D = sess.out_width                      # attend output width (MLA: the latent)
     qs = [to_device_bf16(s.q, dev) for s in steps_in]
@@ -578,6 +581,8 @@ def main():
     def bracket(fn):   # ms of fn() on the stream, one event pair around it
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
+        for _ in range(3):   # a GPU backlog ahead of the bracket: the host then runs ahead of
+            flush.add_(1)    # the timed launches, and a host stall cannot idle the GPU inside it
         e0.record(stream)
         fn()
         e1.record(stream)
@@ -600,10 +605,11 @@ def main():
         for k in range(K):
             nbytes.append(kv_bytes())
             step(W + k)
+    t_flush_a = bracket(flushes)
     t0 = time.perf_counter()
     t_steps = bracket(timed_steps)
     wall = time.perf_counter() - t0
-    t_flush = bracket(flushes)
+    t_flush = 0.5 * (t_flush_a + bracket(flushes))   # flushes timed before and after: drift cancels
     step_ms = (t_steps - t_flush) / K
 
     # the pass-1 kernel alone, K launches over the current GPU ranges
@@ -615,13 +621,21 @@ def main():
                 flush.add_(1)
             sess.attend_pass1(qs[W + k])
     t_p1 = bracket(pass1s)
-    t_flush2 = bracket(flushes)
+    t_flush2 = 0.5 * (t_flush + bracket(flushes))
     p1_kernel_ms = (t_p1 - t_flush2) / K
+
+    # the per-step distribution: K more steps, each between its own pair of
+    # events (each pair counts one event's idle time, ~5.5 us, as step time)
+    ev_step = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
+    for k in range(K):
+        step(W + K + k, ev=ev_step[k])
+    torch.cuda.synchronize()
+    ev_us = np.array([e[0].elapsed_time(e[1]) for e in ev_step]) * 1e3
 
     d_bytes = []
     for k in range(K):
         d_bytes.append(kv_bytes())
-        step(W + K + k, parts=ev_part[k])
+        step(W + 2 * K + k, parts=ev_part[k])
     torch.cuda.synchronize()
     el = lambda a, b: np.array([e[a].elapsed_time(e[b]) for e in ev_part])
     app_ms, p1_ms, p2_ms = el(0, 1), el(1, 2), el(2, 3)
@@ -639,7 +653,7 @@ def main():
     cpu_engine, full_step, policy = None, None, None
     if not args.no_cpu_engine:
         cpu_engine, full_step, policy = cpu_gpu_steps(
-            w, sess, wsk_mod(), steps_in, W + 2 * K, F, splits, qs, kn, vn, o_m, l_m, flush, dev,
+            w, sess, wsk_mod(), steps_in, W + 3 * K, F, splits, qs, kn, vn, o_m, l_m, flush, dev,
             None,   # MLA: the drawn absorbed query feeds both engines (no absorb launch)
             (lambda: wsk_mod().wsk_mla_expand(o_m, w_uv_d, o_out)) if mla else None,
             gpu_ns_per_token=float(p1_kernel_ms * 1e6 / (p1_bytes / w.token_bytes)),
@@ -719,6 +733,11 @@ def main():
             "flush_plus_step": round(t_steps / K * 1e3, 2),
             "flush": round(t_flush / K * 1e3, 2),
             "pass1_kernel": round(p1_kernel_ms * 1e3, 2),
+            "step_event_pairs": {"median": round(float(np.median(ev_us)), 2),
+                                 "p10": round(float(np.percentile(ev_us, 10)), 2),
+                                 "p90": round(float(np.percentile(ev_us, 90)), 2),
+                                 "what": "K more steps, each between its own pair of events: the per-step "
+                                         "spread; each includes one event record's idle time (~5.5 us)"},
             "wall_per_step_incl_flush": round(wall / K * 1e6, 1),
             "diagnostic_steps": "K more steps with events between the parts (each record adds ~5 us of GPU "
                                 "idle time to the part it closes)",

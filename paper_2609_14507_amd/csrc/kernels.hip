@@ -173,8 +173,9 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int
 // with shuffles), merges that token as one more partial, and -- in the
 // workgroup of the first query head of each KV head and the first column
 // slice -- stores the new row into the GPU pool (the decode append; the
-// pass-1 kernels of this step did not read it).  The combine's loads and the
-// dot product's are issued before either is used.
+// pass-1 kernels of this step did not read it).  The combine's loads, the
+// dot product's and the new row's are issued before any is used; the row is
+// stored after the combine.
 // ---------------------------------------------------------------------------
 constexpr int kMaxRowPerLane = (kLatent + kRope + 63) / 64;   // 9: the widest row over 64 lanes
 
@@ -193,6 +194,15 @@ __global__ __launch_bounds__(256) void step_combine_kernel(const StepCombinePara
     const uint16_t *qr = sp.q + (int64_t)i * sp.q_row + (int64_t)h * re;
     const uint16_t *vr = gqa ? sp.v_new + ((int64_t)i * sp.n_kv_heads + g) * re : kr;
     const CombineIn in = combine_load(sp.cp, width, vr + blockIdx.y * 4 * kCombineCols4);
+    // the append of the new row: its 16-byte pieces are loaded here, with the
+    // rest, and stored after the combine (off the combine's critical path)
+    const bool append = blockIdx.y == 0 && h % sp.group == 0;
+    const int row16 = re / 8;
+    const int n_pieces = gqa ? 2 * row16 : row16;   // GQA: K then V pieces; MLA: the latent row
+    const int which = gqa && tid >= row16 ? 1 : 0;
+    const int piece = tid - which * row16;
+    u32x4 pv = u32x4{0u, 0u, 0u, 0u};
+    if (append && tid < n_pieces) pv = reinterpret_cast<const u32x4 *>(which ? vr : kr)[piece];
     // every wavefront forms the whole dot product (no barrier on this path)
     const int lane = tid & 63;
     uint16_t qe[kMaxRowPerLane], ke[kMaxRowPerLane];
@@ -207,25 +217,17 @@ __global__ __launch_bounds__(256) void step_combine_kernel(const StepCombinePara
     for (int j = 0; j < kMaxRowPerLane; ++j) d = fmaf(bf16_to_f32(qe[j]), bf16_to_f32(ke[j]), d);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) d += __shfl_xor(d, o);
-    // the append of the new row
-    if (blockIdx.y == 0 && h % sp.group == 0) {
-        const int64_t slot0 = sp.slot_elem0[i];
-        const int row = sp.row[i];
+    combine_finish(sp.cp, width, in, d * sp.scale, s_w, s_red, s_acc);
+    if (append) {
         if (tid == 0 && h == 0 && sp.tab_index[i] >= 0) sp.table[sp.tab_index[i]] = sp.tab_slot[i];
-        const int row16 = re / 8;
-        if (gqa) {
-            uint16_t *head = sp.pool + slot0 + (int64_t)g * 2 * sp.block_tokens * re;
-            for (int t = tid; t < 2 * row16; t += 256) {
-                const int which = t / row16;
-                const int k = t - which * row16;
-                put_tiled(head, row, which, k, reinterpret_cast<const u32x4 *>(which ? vr : kr)[k]);
-            }
-        } else {
-            for (int k = tid; k < row16; k += 256)
-                put_mla32(sp.pool + slot0, row, k, reinterpret_cast<const u32x4 *>(kr)[k]);
+        if (tid < n_pieces) {
+            if (gqa)
+                put_tiled(sp.pool + sp.slot_elem0[i] + (int64_t)g * 2 * sp.block_tokens * re, sp.row[i], which,
+                          piece, pv);
+            else
+                put_mla32(sp.pool + sp.slot_elem0[i], sp.row[i], piece, pv);
         }
     }
-    combine_finish(sp.cp, width, in, d * sp.scale, s_w, s_red, s_acc);
 }
 
 // ---------------------------------------------------------------------------
