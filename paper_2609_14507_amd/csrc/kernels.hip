@@ -379,28 +379,34 @@ __global__ __launch_bounds__(256) void proj_kernel(int32_t n, int32_t H, int32_t
         const int k = sl + q * SL;
         wv[q] = (col_ok && k < K) ? *reinterpret_cast<const u32x4 *>(wc + (int64_t)k * C) : u32x4{0u, 0u, 0u, 0u};
     }
-    // the 8 tokens' input rows into LDS as fp32, 16 bytes per load where the width allows
+    // the 8 tokens' input rows into LDS as fp32, 16 bytes per load where the
+    // width allows; a thread's loads (at most kStage) are all issued before
+    // the first is stored, so staging waits for memory once
     constexpr int kVec = 16 / sizeof(Tin);
+    constexpr int kStage = (kProjTok * KMAX / kVec + 255) / 256;
     if (K % kVec == 0 && ((uintptr_t)x & 15) == 0) {
         const int nv = kProjTok * K / kVec;
-        for (int t = threadIdx.x; t < nv; t += 256) {
+        u32x4 raw[kStage];
+#pragma unroll
+        for (int r = 0; r < kStage; ++r) {
+            const int t = threadIdx.x + 256 * r;
             const int e = t * kVec, ii = e / K, k = e - ii * K;
-            float v[kVec];
-            if (ii < nt) {
-                const u32x4 raw = *reinterpret_cast<const u32x4 *>(x + ((int64_t)(i0 + ii) * H + h) * K + k);
+            raw[r] = (t < nv && ii < nt) ? *reinterpret_cast<const u32x4 *>(x + ((int64_t)(i0 + ii) * H + h) * K + k)
+                                         : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int r = 0; r < kStage; ++r) {
+            const int t = threadIdx.x + 256 * r;
+            if (t < nv) {
 #pragma unroll
                 for (int j = 0; j < kVec; ++j) {
                     if constexpr (sizeof(Tin) == 2)
-                        v[j] = __uint_as_float((j & 1) ? (raw[j >> 1] & 0xffff0000u) : (raw[j >> 1] << 16));
+                        sx[t * kVec + j] = __uint_as_float((j & 1) ? (raw[r][j >> 1] & 0xffff0000u)
+                                                                   : (raw[r][j >> 1] << 16));
                     else
-                        v[j] = __uint_as_float(raw[j]);
+                        sx[t * kVec + j] = __uint_as_float(raw[r][j]);
                 }
-            } else {
-#pragma unroll
-                for (int j = 0; j < kVec; ++j) v[j] = 0.f;
             }
-#pragma unroll
-            for (int j = 0; j < kVec; ++j) sx[e + j] = v[j];
         }
     } else {
         for (int t = threadIdx.x; t < kProjTok * K; t += 256) {
