@@ -176,7 +176,7 @@ typedef struct wsk_view {
                              later CPU segments (wsk_seq_segments) use the same table */
     int32_t block_tokens;
     int32_t is_device;
-    int32_t layout;       /* WSK_LAYOUT_ROWS or WSK_LAYOUT_TILED64 */
+    int32_t layout;       /* WSK_LAYOUT_ROWS, WSK_LAYOUT_TILED64 or WSK_LAYOUT_MLA32 */
     int32_t reserved;
 } wsk_view;
 
@@ -290,8 +290,10 @@ int wsk_attend_workspace(const wsk_cache *cache, int32_t n, const int32_t *seq_i
 /*
  * Decode attention over the GPU partition (the GPU engine of Sec. 5.1): for
  * each i < n, every query head of seq_ids[i] attends positions
- * [start[i], end[i]), which must lie in the GPU partition:
- * min(s, L) <= start <= end <= L.  The output
+ * [start[i], end[i]), which must lie in the GPU pool (the D-window):
+ * min(w, L) <= start <= end <= L, where w is the window's start (w = s for
+ * a sequence opened without a load range and never flushed; the load
+ * region is attended by wsk_attend_gpu).  The output
  * is a normalised partial and its log-sum-exp (Sec. 4.2 last paragraph):
  *   O[i][h]   = sum_j softmax_j(scale * q.k_j) v_j
  *   LSE[i][h] = ln sum_j exp(scale * q.k_j)

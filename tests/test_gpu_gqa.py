@@ -316,6 +316,17 @@ def test_c2_qwen3_full():
         for b in (0, 7, 15):
             for p in (0, 9829, 9830, 9831, 32767, 32768):
                 assert wsk.wsk_route(sess.h, b, p) == model.route(b, p)
+    # the same step as the benchmark times it: wsk_decode_step (pass 1, then
+    # pass 2 scoring and storing the new row and merging the CPU partial)
+    with DecodeSession(w, pf, DEV) as sess:
+        o_d, l_d = sess.decode_step(q, to_device_bf16(st.k_new, dev), to_device_bf16(st.v_new, dev),
+                                    o_x=o_cpu, lse_x=l_cpu)
+        o_d, l_d = o_d.cpu().numpy(), l_d.cpu().numpy()
+        _check_step(w, sess, st.q, [st.k_new], [st.v_new], pf, o_g.cpu().numpy(), l_g.cpu().numpy(), o_d, l_d,
+                    ranges, "c2 decode step")
+        assert np.abs(o_d - o_m.cpu().numpy()).max() <= 1e-5 and np.abs(l_d - l_m.cpu().numpy()).max() <= 1e-5
+        for b in (0, 7, 15):
+            assert wsk.wsk_route(sess.h, b, 32768) == model.route(b, 32768)
 
 
 def test_c3_mixtral_sweep_without_data_movement():

@@ -208,6 +208,18 @@ def test_c4_deepseek_v2_lite_full_path():
         for b in (0, 3, 7):
             for p in (0, pf.splits[b] - 1, pf.splits[b], pf.lengths[b] - 1, pf.lengths[b]):
                 assert wsk.wsk_route(sess.h, b, p) == model.route(b, p)
+    # the same step as the benchmark times it: absorb, wsk_decode_step (pass 1,
+    # then pass 2 scoring and storing the new latent row and merging the CPU
+    # partial), expand
+    with DecodeSession(w, pf, DEV) as sess:
+        q_step = q.clone()
+        wsk.wsk_mla_absorb(to_device_bf16(st.q_nope, dev), to_device_bf16(w_uk, dev), q_step, w.row_elems)
+        o_d, _ = sess.decode_step(q_step, to_device_bf16(st.k_new, dev), None, o_x=o_cd, lse_x=l_cd)
+        o_out2 = torch.empty(B, H, w.head_dim, device=dev)
+        wsk.wsk_mla_expand(o_d, to_device_bf16(w_uv, dev), o_out2)
+        assert_close(o_out2.cpu().numpy(), np.stack(ref), "c4 decode step")
+        assert np.abs(o_out2.cpu().numpy() - o_out.cpu().numpy()).max() <= 1e-5
+        _check_pool_bytes(sess, rows_full)
 
 
 def test_alignment_rules():
