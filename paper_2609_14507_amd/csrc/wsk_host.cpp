@@ -3,6 +3,7 @@
 // plumbing of the decode-path kernels.  Implements include/wsk.h.
 
 #include <hip/hip_runtime.h>
+#include <sys/mman.h>
 
 #include <algorithm>
 #include <cmath>
@@ -259,12 +260,18 @@ int wsk_init(const wsk_partition_spec *spec, int device, wsk_cache **out) {
     }
     const size_t slot_bytes = (size_t)c->slot_elems * 2;
     if (spec->host_pool_blocks > 0) {
-        const size_t bytes = ((size_t)spec->host_pool_blocks * slot_bytes + 63) / 64 * 64;
-        c->hpool = (uint16_t *)aligned_alloc(64, bytes);
+        // 2 MB aligned and, where the OS allows, backed by 2 MB pages: the CPU
+        // engine reads each KV head's rows in one-block runs a slot apart, and
+        // fewer page boundaries mean fewer TLB misses and prefetcher restarts
+        // (a hint only; without it the pool is ordinary 4 KB pages)
+        const size_t huge = 2u << 20;
+        const size_t bytes = ((size_t)spec->host_pool_blocks * slot_bytes + huge - 1) / huge * huge;
+        c->hpool = (uint16_t *)aligned_alloc(huge, bytes);
         if (!c->hpool) {
             delete c;
             return fail(WSK_ENOMEM, "host pool of %zu bytes", bytes);
         }
+        (void)madvise(c->hpool, bytes, MADV_HUGEPAGE);
         memset(c->hpool, 0, bytes);
     }
     if (device >= 0) {
