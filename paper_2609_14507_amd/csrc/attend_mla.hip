@@ -27,18 +27,19 @@
 //     A-operand registers (WSK_LAYOUT_MLA32): load (ks, mt) is one fully
 //     coalesced 1 KB read landing in the registers that feed the MFMA.
 //   - P.V contracts over tokens, so its B-operand needs 8 consecutive tokens
-//     of one latent dim per lane: the transpose of what was loaded.  It is
-//     made on the matrix cores: C_mtile [16 tok x 32 dims] . E [32 x 16],
-//     with E a 0/1 selection of 16 dims, gives the 16 x 16 block with each
-//     lane holding 4 consecutive tokens of one dim.  The products are exact
-//     (x * 1 and x * 0 summed in fp32), so the upper halves of the fp32
-//     results are the cached bf16 values bit for bit.
+//     of one latent dim per lane: the transpose of what was loaded.  After
+//     QK each wavefront stores its 8 latent pieces, unchanged, in its own
+//     8 KB of LDS and reads the operand back with ds_read_b64_tr_b16 (two
+//     reads of 4 tokens per N-tile): no other wavefront touches that LDS,
+//     so no barrier guards it.
 //   - The token order inside an M-tile makes the QK accumulator of lane
 //     (g, n) hold tokens 8g..8g+7 of head n, which is exactly the P.V
 //     A-operand: probabilities never leave the registers.
-//   - Each wavefront keeps its pieces of three tiles in registers; a
-//     register is refilled with the tile three ahead as soon as it has been
-//     consumed, so about 200 KB per workgroup is always in flight.
+//   - Each wavefront keeps its pieces of two tiles in registers; once QK
+//     has used (and LDS has taken) a tile's pieces, their registers take the
+//     tile two ahead.  Two tiles in flight per wavefront stream faster here
+//     than three or four: more outstanding reads lower the rate HBM
+//     delivers.
 //   - The only synchronisation is the barrier of the score exchange (one
 //     per round of two tiles, shared by both teams; partial scores are
 //     double-buffered).
@@ -53,13 +54,15 @@ namespace {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(4))) short s16x4;
+typedef __attribute__((ext_vector_type(8))) short s16x8;
 
 constexpr int kRow = kLatent + kRope;          // 576 bf16 per cached token
 constexpr int kSub = 32;                       // tokens per tile
 constexpr int kSubBytes = kSub * kRow * 2;     // 36864
 constexpr int kWaveKS = 5;                     // K-steps per wavefront (4 latent + rope for w < 2)
 constexpr int kWaveNT = 8;                     // P.V N-tiles (128 columns) per wavefront
-constexpr int kDepth = 3;                      // tiles held per wavefront
+constexpr int kDepth = 2;                      // tiles held per wavefront
 constexpr int kOOB = 0x40000000;               // offset past any descriptor extent
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -69,6 +72,7 @@ __device__ __forceinline__ int sub_token(int mt, int r) { return 8 * (r >> 2) + 
 
 __global__ __launch_bounds__(512, 1) void mla_attend_kernel(const AttendParams p) {
     __shared__ f32x4 s_part[2][2][4][2][64];       // 32 KB: partial S^T per team and wavefront, double-buffered
+    __shared__ __attribute__((aligned(16))) uint8_t s_tr[8][8 * 1024];   // 64 KB: each wavefront's latent pieces
     __shared__ float s_m1[16], s_l1[16];
 
     const int lane = threadIdx.x & 63;
@@ -111,13 +115,11 @@ __global__ __launch_bounds__(512, 1) void mla_attend_kernel(const AttendParams p
             qop[j] = as_bf16x8((n < H && (j < 4 || rope)) ? v : u32x4{0u, 0u, 0u, 0u});
         }
     }
-    // selection operands E_half: lane (grp, j) holds E[8grp .. 8grp+7][j],
-    // E[k][j] = 1 iff k = 16 half + j
-    bf16x8 sel[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sel[h][e] = (8 * grp + e == 16 * h + n) ? (__bf16)1.0f : (__bf16)0.0f;
+    // this wavefront's LDS copy of its latent pieces, and the address its
+    // lane reads transposed: lane 16g + 4e + a reads token row 4g + e, dims
+    // 4a .. 4a+3 of an N-tile (see the P.V loop)
+    uint8_t *trbuf = &s_tr[wv][0];
+    const int tr_off = 256 * ((lane & 3) >> 1) + 64 * grp + 16 * ((lane >> 2) & 3) + 8 * (lane & 1);
 
     // ---- tile addressing ----
     struct Src {
@@ -169,7 +171,8 @@ __global__ __launch_bounds__(512, 1) void mla_attend_kernel(const AttendParams p
     float l_lane = 0.f;
 
     // One tile t held in st: partial QK, score exchange, softmax, P.V; each
-    // consumed K-step of st is refilled with tile t + kDepth.
+    // K-step of st is refilled with this team's tile kDepth rounds ahead as
+    // soon as QK has used it.
     auto step = [&](int t, Stage &st) {
         const bool valid = t < sub_end;
         const Src nx = tile_src(t + 2 * kDepth);
@@ -182,6 +185,16 @@ __global__ __launch_bounds__(512, 1) void mla_attend_kernel(const AttendParams p
         for (int j = 0; j < 4; ++j) {
             s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[j][0]), qop[j], s0, 0, 0, 0);
             s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[j][1]), qop[j], s1, 0, 0, 0);
+        }
+        // the latent pieces go to LDS in the order they were loaded (piece
+        // (j, mt) at 1 KB (2j + mt), lane l's 16 bytes at 16 l) for P.V's
+        // transposed reads; their registers take the next tile at once
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt)
+                *reinterpret_cast<u32x4 *>(trbuf + (2 * j + mt) * 1024 + lane * 16) = st[j][mt];
+            load_j(nx, st, j);
         }
         // ---- exchange partial scores; every wavefront sums them in the same order ----
         const int b = (t >> 1) & 1;
@@ -241,40 +254,35 @@ __global__ __launch_bounds__(512, 1) void mla_attend_kernel(const AttendParams p
         }
 
         // ---- O[:, 128w + 16nt ..] += P . c ----
+        // P.V contracts over tokens, so its B-operand is the transpose of the
+        // loaded pieces: lane (grp, j) needs tokens 8grp .. 8grp+7 of dim
+        // 128w + 16nt + j.  ds_read_b64_tr_b16 gives, within each 16-lane
+        // group, element e of lane l from element l % 4 of the 8 bytes at the
+        // address of lane 4e + l / 4; with tr_off, each read returns token
+        // rows 4grp .. 4grp+3 of one M-tile, i.e. tokens 8grp + 4mt + e.
 #pragma unroll
         for (int nt = 0; nt < kWaveNT; ++nt) {
-            const int j = nt >> 1;
-            // transpose on the matrix cores: lane (grp, jj) gets tokens
-            // 8grp + 4mt + r (r = 0..3) of dim 128w + 16nt + jj from M-tile mt
-            const f32x4 zero = f32x4{0.f, 0.f, 0.f, 0.f};
-            const f32x4 t0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[j][0]), sel[nt & 1], zero, 0, 0, 0);
-            const f32x4 t1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(st[j][1]), sel[nt & 1], zero, 0, 0, 0);
-            // exact bf16 values held in fp32: keep the upper halves
-            u32x4 bv;
-            bv[0] = __builtin_amdgcn_perm(__float_as_uint(t0[1]), __float_as_uint(t0[0]), 0x07060302u);
-            bv[1] = __builtin_amdgcn_perm(__float_as_uint(t0[3]), __float_as_uint(t0[2]), 0x07060302u);
-            bv[2] = __builtin_amdgcn_perm(__float_as_uint(t1[1]), __float_as_uint(t1[0]), 0x07060302u);
-            bv[3] = __builtin_amdgcn_perm(__float_as_uint(t1[3]), __float_as_uint(t1[2]), 0x07060302u);
-            o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(phi, as_bf16x8(bv), o[nt], 0, 0, 0);
-            o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo, as_bf16x8(bv), o[nt], 0, 0, 0);
-            if (nt & 1) load_j(nx, st, j);   // K-step j consumed: refill with tile t + kDepth
+            typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+            const uint8_t *src = trbuf + tr_off + 2048 * (nt >> 1) + 512 * (nt & 1);
+            const s16x4 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)src);
+            const s16x4 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(src + 1024));
+            const bf16x8 bv = __builtin_bit_cast(bf16x8, s16x8{b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]});
+            o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(phi, bv, o[nt], 0, 0, 0);
+            o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo, bv, o[nt], 0, 0, 0);
         }
     };
 
-    Stage st0, st1, st2;
+    Stage st0, st1;
     const int t0 = sub_begin + team;
     load_tile(t0, st0);
     load_tile(t0 + 2, st1);
-    load_tile(t0 + 4, st2);
     const int rounds = (sub_end - sub_begin + 1) >> 1;   // same for both teams
     int r = 0;
-    for (; r + 2 < rounds; r += kDepth) {
+    for (; r + 1 < rounds; r += kDepth) {
         step(t0 + 2 * r, st0);
         step(t0 + 2 * r + 2, st1);
-        step(t0 + 2 * r + 4, st2);
     }
     if (r < rounds) step(t0 + 2 * r, st0);
-    if (r + 1 < rounds) step(t0 + 2 * r + 2, st1);
 
     // ---- merge the two teams, normalise, write this wavefront's 128 columns ----
     float l_tot = l_lane + __shfl_xor(l_lane, 16);
