@@ -35,11 +35,11 @@
 //   - The token order inside an M-tile makes the QK accumulator of lane
 //     (g, n) hold tokens 8g..8g+7 of head n, which is exactly the P.V
 //     A-operand: probabilities never leave the registers.
-//   - Each wavefront keeps its pieces of two tiles in registers; once QK
-//     has used (and LDS has taken) a tile's pieces, their registers take the
-//     tile two ahead.  Two tiles in flight per wavefront stream faster here
-//     than three or four: more outstanding reads lower the rate HBM
-//     delivers.
+//   - Each wavefront holds one tile's pieces in registers; once QK has
+//     used them (and LDS has taken the latent ones) they take the team's
+//     next tile, whose reads fly during the score exchange, softmax and P.V.
+//     One tile in flight per wavefront streams faster here than two, three
+//     or four: more outstanding reads lower the rate HBM delivers.
 //   - The only synchronisation is the barrier of the score exchange (one
 //     per round of two tiles, shared by both teams; partial scores are
 //     double-buffered).
@@ -62,7 +62,7 @@ constexpr int kSub = 32;                       // tokens per tile
 constexpr int kSubBytes = kSub * kRow * 2;     // 36864
 constexpr int kWaveKS = 5;                     // K-steps per wavefront (4 latent + rope for w < 2)
 constexpr int kWaveNT = 8;                     // P.V N-tiles (128 columns) per wavefront
-constexpr int kDepth = 2;                      // tiles held per wavefront
+constexpr int kDepth = 1;                      // tiles held per wavefront (in flight while one is used)
 constexpr int kOOB = 0x40000000;               // offset past any descriptor extent
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -272,17 +272,12 @@ __global__ __launch_bounds__(512, 1) void mla_attend_kernel(const AttendParams p
         }
     };
 
-    Stage st0, st1;
+    Stage st0;
     const int t0 = sub_begin + team;
     load_tile(t0, st0);
-    load_tile(t0 + 2, st1);
     const int rounds = (sub_end - sub_begin + 1) >> 1;   // same for both teams
     int r = 0;
-    for (; r + 1 < rounds; r += kDepth) {
-        step(t0 + 2 * r, st0);
-        step(t0 + 2 * r + 2, st1);
-    }
-    if (r < rounds) step(t0 + 2 * r, st0);
+    for (; r < rounds; ++r) step(t0 + 2 * r, st0);
 
     // ---- merge the two teams, normalise, write this wavefront's 128 columns ----
     float l_tot = l_lane + __shfl_xor(l_lane, 16);
