@@ -4,8 +4,9 @@ One step = the whole hot path over one batch (wsk_decode_step): the new
 token's K/V of every sequence is routed to its GPU partition, split-KV
 attention covers the GPU range written so far (pass 1), then one pass 2
 scores and merges the new token, stores it into the pool, and merges the
-chunk partials and the CPU-range partial by their LSE (MLA adds the query
-absorption before and the output expansion after).  Inputs are seeded synthetic tensors already
+chunk partials and the CPU-range partial by their LSE (MLA: the query
+absorption runs before, and wsk_decode_step_mla's pass 2 also expands the
+merged latent output by W_UV).  Inputs are seeded synthetic tensors already
 resident in HBM; the CPU-range partial fed to the merge is a seeded
 synthetic (O, LSE) pair (the merge's cost does not depend on its values).
 
@@ -548,7 +549,8 @@ def main():
         """One decode step.  ev = (start, end) events around the step: the timed
         steps run it as wsk_decode_step (pass 1 over the positions written so
         far, then one pass 2 that folds in the appended row, stores it and
-        merges the CPU partial).  parts = 5 events around its pieces
+        merges the CPU partial; MLA: wsk_decode_step_mla, whose pass 2 also
+        expands the merged latent output by W_UV).  parts = 5 events around its pieces
         (diagnostic steps only, every event record costs GPU time of its own):
         those run the same work as separate calls -- append, pass 1 over
         [s, L + 1), pass 2 -- so that pass 1 is timed on its own."""
@@ -567,9 +569,11 @@ def main():
             mark(2)
             sess.attend_pass2(o=o_m, lse=l_m, o_x=o_cpu, lse_x=l_cpu)
             mark(3)
+        elif mla:
+            sess.decode_step_mla(qs[i], kn[i], w_uv_d, o=o_out, lse=l_m, o_x=o_cpu, lse_x=l_cpu)
         else:
             sess.decode_step(qs[i], kn[i], vn[i], o_x=o_cpu, lse_x=l_cpu, o=o_m, lse=l_m)
-        if mla:   # output-side expansion of the merged latent output
+        if mla and parts:   # output-side expansion of the merged latent output
             wsk.wsk_mla_expand(o_m, w_uv_d, o_out)
             mark(4)
         if ev:
@@ -722,8 +726,8 @@ def main():
             "cpu_share": args.share if args.share is not None else (w.cpu_share or [w.share_lo, w.share_hi]),
             "gpu_tokens_per_step": int(nbytes.mean() / w.token_bytes),
             "kv_bytes_per_step": int(nbytes.mean()),
-            "step": ("absorb + wsk_decode_step (attend pass 1 over [s, L), then one pass 2: the appended row "
-                     "scored, merged and stored, chunk combine, LSE merge with the CPU partial) + expand"
+            "step": ("absorb + wsk_decode_step_mla (attend pass 1 over [s, L), then one pass 2: the appended row "
+                     "scored, merged and stored, chunk combine, LSE merge with the CPU partial, expansion by W_UV)"
                      if mla else "wsk_decode_step: attend pass 1 over [s, L), then one pass 2: the appended row "
                      "scored, merged and stored, chunk combine, LSE merge with the CPU partial"),
             "cache_flush_between_steps": not args.no_flush,

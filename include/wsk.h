@@ -493,6 +493,27 @@ int wsk_decode_step(wsk_cache *cache, int32_t n, const int32_t *seq_ids, const v
                     size_t ws_bytes, void *stream);
 
 /*
+ * One MLA decode step with the output-side expansion folded in (Sec. 6.1:
+ * the latent output is expanded by W_UV per head, a linear map that commutes
+ * with the LSE merge): wsk_decode_step on an MLA cache, then
+ * O[i][h] = W_UV[h]^T O_lat[i][h] (as wsk_mla_expand) in the same workgroups
+ * that merge O_lat, which saves the expansion's own launch.  The new rows
+ * are k_new (bf16 [n][576], latent | rope); there is no v_new.  o_lat (fp32
+ * [n][H][512], 16-byte aligned) receives the merged latent output and may
+ * be NULL when only O is wanted; lse as for wsk_decode_step (natural log, in
+ * the latent attention's scale); w_uv: DEVICE bf16 [H][512][dv], 16-byte
+ * aligned; o: DEVICE fp32 [n][H][dv]; dv one of 64, 128, 256.  q, o_x,
+ * lse_x, ws and the workspace size (wsk_decode_step_workspace) as for
+ * wsk_decode_step; the caller owns every buffer.  All checks happen before
+ * the routing, so a failed call (other than EHIP) changes nothing.
+ * Errors: EINVAL (a GQA cache, an unsupported dv, NULL or misaligned
+ * pointers, as for wsk_decode_step), ESTATE, ERANGE, ENOMEM, EHIP.
+ */
+int wsk_decode_step_mla(wsk_cache *cache, int32_t n, const int32_t *seq_ids, const void *q, const void *k_new,
+                        const float *o_x, const float *lse_x, const uint16_t *w_uv, int32_t dv, float *o_lat,
+                        float *lse, float *o, void *ws, size_t ws_bytes, void *stream);
+
+/*
  * D-window eviction ("flush", Sec. 4.2 and 4.3): for each listed sequence
  * whose D-window [w, L) holds a whole batch, move the batch [w, w') to
  * part[i] (WSK_PART_CPU or WSK_PART_LOAD) and set w = w', where

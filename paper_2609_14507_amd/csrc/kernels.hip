@@ -231,6 +231,180 @@ __global__ __launch_bounds__(256) void step_combine_kernel(const StepCombinePara
 }
 
 // ---------------------------------------------------------------------------
+// Pass 2 of an MLA decode step with the output expansion folded in (Sec. 6.1:
+// the merged latent output is expanded by W_UV[h], which commutes with the
+// merge).  One workgroup per (sequence i, head h) merges all 512 latent
+// columns -- the chunk partials, the CPU partial and the step's new row, as
+// step_combine_kernel does per 128-column slice -- and multiplies the merged
+// row by W_UV[h] (dv columns).  The weight rows are loaded first, together
+// with everything the merge reads, so their latency overlaps the merge; the
+// workgroup of head 0 also stores the new row into the GPU pool.
+// ---------------------------------------------------------------------------
+constexpr int kSxThreads = 512;
+constexpr int kSxWaves = kSxThreads / 64;
+constexpr int kSxCols4 = kLatent / 4;               // 128 float4 columns
+constexpr int kSxGroups = kSxThreads / kSxCols4;    // 4 chunk groups
+constexpr int kSxRegs = 8;                          // chunk partials per thread loaded up front
+
+__device__ __forceinline__ float sx_block_reduce(float v, bool is_max, float *s_red) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+        const float u = __shfl_xor(v, d);
+        v = is_max ? fmaxf(v, u) : v + u;
+    }
+    __syncthreads();                                 // s_red free (earlier use finished)
+    if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    float r = s_red[0];
+#pragma unroll
+    for (int w = 1; w < kSxWaves; ++w) r = is_max ? fmaxf(r, s_red[w]) : r + s_red[w];
+    return r;
+}
+
+template <int DV>
+__global__ __launch_bounds__(kSxThreads) void step_expand_kernel(const StepExpandParams xp) {
+    constexpr int kCg = DV / 8;                      // 16-byte column groups of a W_UV row
+    constexpr int kRg = kSxThreads / kCg;            // row groups
+    constexpr int kRows = kLatent / kRg;             // W_UV rows per thread
+    __shared__ float s_w[kCombineW];
+    __shared__ float s_red[kSxWaves];
+    __shared__ f32x4 s_acc[kSxGroups][kSxCols4];
+    __shared__ float s_lat[kLatent];
+    __shared__ float s_out[kRg][DV];
+    const StepCombineParams &sp = xp.sc;
+    const CombineParams &p = sp.cp;
+    const int H = p.n_q_heads;
+    const int row = blockIdx.x;                      // i * H + h
+    const int i = row / H;
+    const int h = row - i * H;
+    const int tid = threadIdx.x;
+    const int re = sp.row_elems;                     // 576
+    const uint16_t *kr = sp.k_new + (int64_t)i * re;
+    const uint16_t *qr = sp.q + (int64_t)i * sp.q_row + (int64_t)h * re;
+
+    // ---- every load first: W_UV rows, chunk partials and LSEs, CPU partial,
+    //      the new row (its value columns, its score's operands, its pieces) ----
+    const int rg = tid / kCg, cg = tid - (tid / kCg) * kCg;
+    const uint16_t *wrow = xp.w_uv + (int64_t)h * kLatent * DV + 8 * cg;
+    u32x4 wv[kRows];
+#pragma unroll
+    for (int j = 0; j < kRows; ++j) wv[j] = *reinterpret_cast<const u32x4 *>(wrow + (int64_t)(rg + kRg * j) * DV);
+    const int c0 = p.chunk_begin[i];
+    const int nc = p.chunk_begin[i + 1] - c0;
+    const int g = tid / kSxCols4;
+    const int c4 = tid - g * kSxCols4;
+    const f32x4 *po = reinterpret_cast<const f32x4 *>(p.part_o + ((int64_t)c0 * H + h) * kLatent) + c4;
+    const int64_t cstride = (int64_t)H * kLatent / 4;
+    f32x4 pr[kSxRegs];
+#pragma unroll
+    for (int j = 0; j < kSxRegs; ++j) {
+        const int c = g + kSxGroups * j;
+        pr[j] = c < nc ? po[c * cstride] : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    const float lse_c = tid < nc ? p.part_lse[(int64_t)(c0 + tid) * H + h] : -INFINITY;
+    const float lx = p.lse_x ? p.lse_x[row] : -INFINITY;
+    f32x4 ox = f32x4{0.f, 0.f, 0.f, 0.f}, vn = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (g == 0) {
+        if (p.o_x) ox = reinterpret_cast<const f32x4 *>(p.o_x + (int64_t)row * kLatent)[c4];
+        const uint2 v2 = reinterpret_cast<const uint2 *>(kr)[c4];
+        vn = f32x4{__uint_as_float(v2.x << 16), __uint_as_float(v2.x & 0xffff0000u), __uint_as_float(v2.y << 16),
+                   __uint_as_float(v2.y & 0xffff0000u)};
+    }
+    const bool append = h == 0;
+    const int n_pieces = re / 8;
+    u32x4 pv = u32x4{0u, 0u, 0u, 0u};
+    if (append && tid < n_pieces) pv = reinterpret_cast<const u32x4 *>(kr)[tid];
+    const int lane = tid & 63;
+    uint16_t qe[kMaxRowPerLane], ke[kMaxRowPerLane];
+#pragma unroll
+    for (int j = 0; j < kMaxRowPerLane; ++j) {
+        const int e = lane + 64 * j;
+        qe[j] = e < re ? qr[e] : (uint16_t)0;
+        ke[j] = e < re ? kr[e] : (uint16_t)0;
+    }
+
+    // ---- the new row's score (every wavefront forms the whole dot product) ----
+    float d = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMaxRowPerLane; ++j) d = fmaf(bf16_to_f32(qe[j]), bf16_to_f32(ke[j]), d);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) d += __shfl_xor(d, o);
+    const float s_new = d * sp.scale;
+
+    // ---- merge: O_lat = (sum_c w_c O_c + w_x O_x + w_n v_new) / sum w ----
+    const float *pl = p.part_lse + (int64_t)c0 * H + h;
+    float m = fmaxf(fmaxf(lx, s_new), lse_c);
+    for (int c = tid + kSxThreads; c < nc; c += kSxThreads) m = fmaxf(m, pl[(int64_t)c * H]);
+    m = sx_block_reduce(m, true, s_red);
+    const bool empty = m == -INFINITY;               // nothing to merge: O = 0, LSE = -inf
+    const float wx = lx == -INFINITY ? 0.f : __expf(lx - m);
+    const float wn = s_new == -INFINITY ? 0.f : __expf(s_new - m);
+    float dsum = tid == 0 ? wx + wn : 0.f;
+    if (tid < nc) {
+        const float w = __expf(lse_c - m);
+        s_w[tid] = w;
+        dsum += w;
+    }
+    for (int c = tid + kSxThreads; c < nc; c += kSxThreads) {
+        const float w = __expf(pl[(int64_t)c * H] - m);
+        if (c < kCombineW) s_w[c] = w;
+        dsum += w;
+    }
+    const float den = sx_block_reduce(empty ? 0.f : dsum, false, s_red);   // its barriers also publish s_w
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (!empty) {
+        if (g == 0 && wx != 0.f) acc = wx * ox;
+        if (g == 0 && wn != 0.f) acc += wn * vn;
+#pragma unroll
+        for (int j = 0; j < kSxRegs; ++j) {
+            const int c = g + kSxGroups * j;
+            if (c < nc) acc += s_w[c] * pr[j];
+        }
+        for (int c = g + kSxGroups * kSxRegs; c < nc; c += kSxGroups) {
+            const float w = c < kCombineW ? s_w[c] : __expf(pl[(int64_t)c * H] - m);
+            acc += w * po[c * cstride];
+        }
+    }
+    s_acc[g][c4] = acc;
+    __syncthreads();
+    if (tid < kSxCols4) {
+        f32x4 t = s_acc[0][tid];
+#pragma unroll
+        for (int gg = 1; gg < kSxGroups; ++gg) t += s_acc[gg][tid];
+        t = empty ? f32x4{0.f, 0.f, 0.f, 0.f} : t * (1.f / den);
+        reinterpret_cast<f32x4 *>(s_lat)[tid] = t;
+        if (p.o) reinterpret_cast<f32x4 *>(p.o + (int64_t)row * kLatent)[tid] = t;
+    }
+    if (tid == 0) p.lse[row] = empty ? -INFINITY : m + __logf(den);
+    __syncthreads();
+
+    // ---- O[i][h] = W_UV[h]^T O_lat: row group rg sums its rows for 8 columns ----
+    float a8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < kRows; ++j) {
+        const float x = s_lat[rg + kRg * j];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            a8[2 * e] = fmaf(x, __uint_as_float(wv[j][e] << 16), a8[2 * e]);
+            a8[2 * e + 1] = fmaf(x, __uint_as_float(wv[j][e] & 0xffff0000u), a8[2 * e + 1]);
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s_out[rg][8 * cg + e] = a8[e];
+    __syncthreads();
+    if (tid < DV) {
+        float t = s_out[0][tid];
+#pragma unroll 8
+        for (int r = 1; r < kRg; ++r) t += s_out[r][tid];
+        xp.o[(int64_t)row * DV + tid] = t;
+    }
+    if (append) {
+        if (tid == 0 && sp.tab_index[i] >= 0) sp.table[sp.tab_index[i]] = sp.tab_slot[i];
+        if (tid < n_pieces) put_mla32(sp.pool + sp.slot_elem0[i], sp.row[i], tid, pv);
+    }
+}
+
+// ---------------------------------------------------------------------------
 // LSE merge of two partials.  A workgroup owns whole rows: thread t first
 // reads the LSEs of row t into LDS and writes that row's merged LSE, so
 // lse_out may alias lse_a or lse_b; O is then merged 4 elements per thread.
@@ -537,6 +711,18 @@ hipError_t launch_step_combine(const StepCombineParams &p, int width, hipStream_
     if (p.cp.n <= 0) return hipSuccess;
     hipLaunchKernelGGL(step_combine_kernel, dim3(p.cp.n * p.cp.n_q_heads, width / (4 * kCombineCols4)), dim3(256),
                        0, s, p, width);
+    return hipGetLastError();
+}
+
+hipError_t launch_step_expand(const StepExpandParams &p, hipStream_t s) {
+    if (p.sc.cp.n <= 0) return hipSuccess;
+    const dim3 grid(p.sc.cp.n * p.sc.cp.n_q_heads), block(kSxThreads);
+    switch (p.dv) {
+        case 64: hipLaunchKernelGGL(step_expand_kernel<64>, grid, block, 0, s, p); break;
+        case 128: hipLaunchKernelGGL(step_expand_kernel<128>, grid, block, 0, s, p); break;
+        case 256: hipLaunchKernelGGL(step_expand_kernel<256>, grid, block, 0, s, p); break;
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

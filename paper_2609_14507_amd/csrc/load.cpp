@@ -596,9 +596,20 @@ int wsk_decode_step_workspace(const wsk_cache *c, int32_t n, const int32_t *ids,
     return wsk_attend_gpu_workspace(c, n, ids, bytes);
 }
 
-int wsk_decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, const void *k_new, const void *v_new,
-                    const float *o_x, const float *lse_x, float *o, float *lse, void *ws, size_t ws_bytes,
-                    void *stream) {
+}  // extern "C"
+
+namespace {
+
+// The output expansion a decode step may fold into its pass 2 (MLA).
+struct StepExpand {
+    const uint16_t *w_uv;
+    int32_t dv;
+    float *o;   // expanded output; the step's o (the latent output) may then be NULL
+};
+
+int decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, const void *k_new, const void *v_new,
+                const float *o_x, const float *lse_x, float *o, float *lse, void *ws, size_t ws_bytes, void *stream,
+                const StepExpand *ex) {
     int rc = check_ids(c, n, ids);
     if (rc) return rc;
     if (n == 0) return fail(WSK_EINVAL, "n must be positive");
@@ -621,8 +632,9 @@ int wsk_decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, 
     GpuPlan g;
     rc = plan_dense(c, n, ids, g);
     if (rc) return rc;
-    rc = check_run(c, g, q, o_x, lse_x, o, lse, ws, ws_bytes, true, true);
+    rc = check_run(c, g, q, o_x, lse_x, ex ? ex->o : o, lse, ws, ws_bytes, true, true);
     if (rc) return rc;
+    if (ex && !aligned16(o)) return fail(WSK_EINVAL, "o_lat must be 16-byte aligned");
     // routing of the new rows (as wsk_append)
     std::vector<Pending> pend;
     for (int32_t j = 0; j < n; ++j) {
@@ -644,7 +656,7 @@ int wsk_decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, 
         CombineParams &cp = p.cp;
         cp.part_o = part_o + g.pb[i0] * sp.n_q_heads * width;
         cp.part_lse = part_lse + g.pb[i0] * sp.n_q_heads;
-        cp.o = o + (int64_t)i0 * sp.n_q_heads * width;
+        cp.o = o ? o + (int64_t)i0 * sp.n_q_heads * width : nullptr;
         cp.lse = lse + (int64_t)i0 * sp.n_q_heads;
         cp.o_x = o_x ? o_x + (int64_t)i0 * sp.n_q_heads * width : nullptr;
         cp.lse_x = lse_x ? lse_x + (int64_t)i0 * sp.n_q_heads : nullptr;
@@ -676,12 +688,43 @@ int wsk_decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, 
                     p.tab_slot[r] = pd.slot;
                 }
         }
-        e = launch_step_combine(p, width, (hipStream_t)stream);
+        if (ex) {
+            StepExpandParams xp{};
+            xp.sc = p;
+            xp.w_uv = ex->w_uv;
+            xp.o = ex->o + (int64_t)i0 * sp.n_q_heads * ex->dv;
+            xp.dv = ex->dv;
+            e = launch_step_expand(xp, (hipStream_t)stream);
+        } else {
+            e = launch_step_combine(p, width, (hipStream_t)stream);
+        }
     }
     for (int32_t i = 0; i < n; ++i) c->length[ids[i]] += 1;
     if (rc) return rc;
-    if (e != hipSuccess) return hip_fail(e, "wsk_decode_step");
+    if (e != hipSuccess) return hip_fail(e, ex ? "wsk_decode_step_mla" : "wsk_decode_step");
     return WSK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int wsk_decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, const void *k_new, const void *v_new,
+                    const float *o_x, const float *lse_x, float *o, float *lse, void *ws, size_t ws_bytes,
+                    void *stream) {
+    return decode_step(c, n, ids, q, k_new, v_new, o_x, lse_x, o, lse, ws, ws_bytes, stream, nullptr);
+}
+
+int wsk_decode_step_mla(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, const void *k_new,
+                        const float *o_x, const float *lse_x, const uint16_t *w_uv, int32_t dv, float *o_lat,
+                        float *lse, float *o, void *ws, size_t ws_bytes, void *stream) {
+    if (!c) return fail(WSK_EINVAL, "cache is NULL");
+    if (c->spec.kind != WSK_KIND_MLA) return fail(WSK_EINVAL, "wsk_decode_step_mla needs an MLA cache");
+    if (dv != 64 && dv != 128 && dv != 256) return fail(WSK_EINVAL, "dv %d: supported 64, 128, 256", dv);
+    if (!w_uv || !aligned16(w_uv)) return fail(WSK_EINVAL, "w_uv must be non-NULL and 16-byte aligned");
+    if (!o) return fail(WSK_EINVAL, "o must not be NULL");
+    const StepExpand ex{w_uv, dv, o};
+    return decode_step(c, n, ids, q, k_new, nullptr, o_x, lse_x, o_lat, lse, ws, ws_bytes, stream, &ex);
 }
 
 int wsk_attend_blocks_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *sel_begin,

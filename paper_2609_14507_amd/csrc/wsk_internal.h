@@ -91,6 +91,16 @@ struct StepCombineParams {
     int32_t tab_slot[kMaxLaunchSeqs];
 };
 
+// Pass 2 of an MLA decode step with the output expansion: sc as for
+// step_combine (cp.o, the merged latent output, may be NULL), then
+// o[i][h] = W_UV[h]^T O_lat[i][h] for every sequence and head.
+struct StepExpandParams {
+    StepCombineParams sc;
+    const uint16_t *w_uv;    // bf16 [n_q_heads][512][dv]
+    float *o;                // launch-local fp32 [n][n_q_heads][dv]
+    int32_t dv;              // 64, 128 or 256
+};
+
 // Decode append: row r of the source goes to row row[r] of the slot whose
 // first element is slot_elem0[r]; GQA rows carry K and V for every KV head
 // (V stored transposed in the GPU pool).  tab_index[r] >= 0 also stores
@@ -159,6 +169,7 @@ hipError_t launch_gqa_attend(const AttendParams &p, int heads_per_wg, int n_wg, 
 hipError_t launch_mla_attend(const AttendParams &p, int n_wg, hipStream_t s);
 hipError_t launch_combine(const CombineParams &p, int width, hipStream_t s);
 hipError_t launch_step_combine(const StepCombineParams &p, int width, hipStream_t s);
+hipError_t launch_step_expand(const StepExpandParams &p, hipStream_t s);
 hipError_t launch_append(const AppendParams &p, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
 hipError_t launch_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a,

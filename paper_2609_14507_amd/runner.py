@@ -115,6 +115,21 @@ class DecodeSession:
             self.lengths[b] += 1
         return o, lse
 
+    def decode_step_mla(self, q: torch.Tensor, k_new: torch.Tensor, w_uv: torch.Tensor, o: torch.Tensor,
+                        lse: torch.Tensor, o_lat=None, o_x=None, lse_x=None, ids: Optional[List[int]] = None):
+        """MLA decode step with the output expansion folded into its pass 2
+        (wsk_decode_step_mla): o [n, H, dv] = W_UV[h]^T O_lat; o_lat, when
+        given, receives the merged latent output."""
+        ids = self.ids if ids is None else ids
+        need = wsk.wsk_decode_step_workspace(self.h, ids)
+        if self._ws.numel() < need:
+            spare = len(ids) * self.w.n_q_heads * (self.out_width + 1) * 4 + 512
+            self._ws = torch.empty(need + spare, dtype=torch.uint8, device=self.dev)
+        wsk.wsk_decode_step_mla(self.h, ids, q, k_new, w_uv, o, lse, self._ws, o_lat=o_lat, o_x=o_x, lse_x=lse_x)
+        for b in ids:
+            self.lengths[b] += 1
+        return o, lse
+
     def attend_gpu_pass1(self, q: torch.Tensor, ids: Optional[List[int]] = None):
         """Pass 1 of attend_gpu (transfers and kernels enqueued, partials in the
         session workspace); attend_gpu_pass2 with the same ids completes it."""

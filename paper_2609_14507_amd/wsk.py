@@ -84,6 +84,8 @@ _SIGS = {
     "wsk_decode_step_workspace": ([_VP, _I32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
     "wsk_decode_step": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP],
                         ctypes.c_int),
+    "wsk_decode_step_mla": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, _I32, _VP, _VP, _VP, _VP, ctypes.c_size_t,
+                             _VP], ctypes.c_int),
     "wsk_cpu_attend_all": ([_VP, _I32, _PI32, _VP, _VP, _VP, _I32], ctypes.c_int),
     "wsk_load_slot": ([_VP, _I32, ctypes.POINTER(_VP)], ctypes.c_int),
     "wsk_load_stats": ([_VP, ctypes.POINTER(wsk_load_info)], ctypes.c_int),
@@ -252,6 +254,17 @@ def wsk_decode_step(h: int, seq_ids, q, k_new, v_new, o, lse, ws, o_x=None, lse_
     nbytes = ws.numel() * ws.element_size()
     _check(lib().wsk_decode_step(h, len(seq_ids), _i32_array(seq_ids), _ptr(q), _ptr(k_new), _ptr(v_new),
                                  _ptr(o_x), _ptr(lse_x), _ptr(o), _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
+
+
+def wsk_decode_step_mla(h: int, seq_ids, q, k_new, w_uv, o, lse, ws, o_lat=None, o_x=None, lse_x=None,
+                        stream=None):
+    """MLA decode step with the output expansion: o fp32 [n, H, dv] from w_uv bf16 [H, 512, dv];
+    o_lat (optional) receives the merged latent output."""
+    nbytes = ws.numel() * ws.element_size()
+    dv = w_uv.shape[2]
+    _check(lib().wsk_decode_step_mla(h, len(seq_ids), _i32_array(seq_ids), _ptr(q), _ptr(k_new), _ptr(o_x),
+                                     _ptr(lse_x), _ptr(w_uv), dv, _ptr(o_lat), _ptr(lse), _ptr(o), _ptr(ws), nbytes,
+                                     _stream(stream)))
 
 
 def wsk_cpu_attend_all(h: int, seq_ids, q, o, lse, threads: int = 0):

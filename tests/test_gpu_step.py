@@ -260,3 +260,56 @@ def test_decode_loop_with_policy_eviction(kind):
             assert abs(flushed[wsk.PART_CPU] / n - p) <= 0.5 / n + 1e-12
     finally:
         pol.close()
+
+
+@pytest.mark.parametrize("H,bk,dv,load", [(16, 64, 128, False), (5, 256, 64, True), (16, 128, 256, False)])
+def test_decode_step_mla_expand(H, bk, dv, load):
+    """wsk_decode_step_mla: the merged latent output and LSE against the oracle over [0, L], the
+    expanded output against the oracle's expansion of the exact latent output (Sec. 6.1), the latent
+    output within 1e-5 of wsk_decode_step's on a twin cache, the GPU pool byte-identical to the
+    twin's after every step (the fused kernel stores the new row as pass 2 does), and o_lat = NULL
+    leaving the expanded output unchanged."""
+    lengths = [4 * bk - 3, 2 * bk - 3, 3 * bk]
+    splits = [bk + 11, 0, 2 * bk + 5]
+    load_ends = [3 * bk, bk, 3 * bk] if load else None
+    w = _workload("mla", len(lengths), H, seed=bk + dv)
+    w = wl.Workload(w.name, w.kind, batch=w.batch, n_q_heads=H, n_kv_heads=1, head_dim=dv, latent_dim=512,
+                    rope_dim=64, nope_dim=128, context=1, kv_std=0.5, seed=w.seed)
+    gen = torch.Generator().manual_seed(w.seed + 5)
+    pf = _prefill(w, lengths, splits, gen)
+    rows_all = list(pf.k)
+    _, w_uv = wl.draw_mla_weights(w, gen)
+    say("case decode step mla expand H=%d bk=%d dv=%d load=%s" % (H, bk, dv, load))
+    kw = dict(extra_tokens=8, block_tokens=bk, load_ends=load_ends, pingpong_blocks=2, arena_blocks=3)
+    with DecodeSession(w, pf, DEV, **kw) as sess, DecodeSession(w, pf, DEV, **kw) as twin:
+        w_uv_d = to_device_bf16(w_uv, sess.dev)
+        for step in range(5):
+            q_bits = wl.draw_bf16(gen, (sess.B, H, w.row_elems))
+            kn, _ = _new_rows(w, sess.B, gen)
+            q = to_device_bf16(q_bits, sess.dev)
+            knd = to_device_bf16(kn, sess.dev)
+            o_x, l_x = _cpu_partial(sess, q_bits)
+            ws = torch.empty(wsk.wsk_decode_step_workspace(sess.h, sess.ids), dtype=torch.uint8, device=sess.dev)
+            o_lat = torch.empty(sess.B, H, 512, device=sess.dev)
+            lse = torch.empty(sess.B, H, device=sess.dev)
+            o = torch.empty(sess.B, H, dv, device=sess.dev)
+            keep = step == 3   # this step without o_lat: o and lse only
+            wsk.wsk_decode_step_mla(sess.h, sess.ids, q, knd, w_uv_d, o, lse, ws, o_lat=None if keep else o_lat,
+                                    o_x=o_x, lse_x=l_x)
+            for b in sess.ids:
+                sess.lengths[b] += 1
+            o2, lse2 = _step(twin, q, knd, None, o_x, l_x)
+            for b in range(sess.B):
+                rows_all[b] = np.concatenate([rows_all[b], kn[b:b + 1]])
+            o, lse, o_lat, o2, lse2 = (t.cpu().numpy() for t in (o, lse, o_lat, o2, lse2))
+            for b in range(sess.B):
+                L = sess.lengths[b]
+                ol_r, l_r = oracle.attend(q_bits[b], rows_all[b], None, 0, L, w.softmax_scale, H, dv=512)
+                assert_lse(lse[b], l_r, "mla expand step %d b%d" % (step, b))
+                assert_close(o[b], oracle.mla_expand(ol_r, w_uv), "mla expand O step %d b%d" % (step, b))
+                if not keep:
+                    assert_close(o_lat[b], ol_r, "mla expand O_lat step %d b%d" % (step, b))
+                    assert np.abs(o_lat[b] - o2[b]).max() <= 1e-5
+                assert np.abs(lse[b] - lse2[b]).max() <= 1e-5
+            torch.cuda.synchronize()
+            assert np.array_equal(_gpu_pool(sess), _gpu_pool(twin)), "pool differs after step %d" % step

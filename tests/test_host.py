@@ -28,7 +28,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     L = wsk.lib()
     names = _declared_symbols()
-    assert len(names) == 42
+    assert len(names) == 43
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(wsk._SIGS)
@@ -262,6 +262,32 @@ def test_error_codes():
         assert "width" in wsk.wsk_last_error() or wsk.wsk_last_error()
     finally:
         wsk.wsk_destroy(h)
+
+
+def test_decode_step_mla_refusals():
+    """The fused MLA step refuses a GQA cache, an unsupported dv and a NULL w_uv or o before any
+    routing, and a host-only cache (no GPU) with ESTATE, leaving the sequence unchanged."""
+    lib = wsk.lib()
+    ids = (ctypes.c_int32 * 1)(0)
+    g = wsk.wsk_init(_spec(), -1)
+    try:
+        wsk.wsk_seq_open(g, 0, 0)
+        assert lib.wsk_decode_step_mla(g, 1, ids, 16, 16, None, None, 16, 128, None, 16, 16, 256, 1 << 20,
+                                       None) == wsk.WSK_EINVAL
+    finally:
+        wsk.wsk_destroy(g)
+    m = wsk.wsk_init(_spec(kind=wsk.KIND_MLA, n_q_heads=16, n_kv_heads=1, latent_dim=512, rope_dim=64,
+                           softmax_scale=0.072), -1)
+    try:
+        wsk.wsk_seq_open(m, 0, 0)
+        for dv, w_uv, o in ((100, 16, 16), (128, None, 16), (128, 24, 16), (128, 16, None)):
+            assert lib.wsk_decode_step_mla(m, 1, ids, 16, 16, None, None, w_uv, dv, None, 16, o, 256, 1 << 20,
+                                           None) == wsk.WSK_EINVAL, (dv, w_uv, o)
+        assert lib.wsk_decode_step_mla(m, 1, ids, 16, 16, None, None, 16, 128, None, 16, 16, 256, 1 << 20,
+                                       None) == wsk.WSK_ESTATE
+        assert wsk.wsk_seq_info(m, 0)[0] == 0
+    finally:
+        wsk.wsk_destroy(m)
 
 
 def test_workspace_grows_with_range_and_is_aligned():
