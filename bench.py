@@ -125,8 +125,8 @@ TRAFFIC = {
     },
     "deepseek-v2-lite-mla-b8-L65536": {
         "source": "paper_2609_14507_amd/csrc/attend_mla.hip",
-        "sha256": "8251e8c48d8114b3c8cb8934a3d812551091369a3e9732a50b0af12b4010a592",
-        "fetch_bytes": 177708.9 * 1024 * 2.0,
+        "sha256": "4df8a57ec4065ad10e72b3e174e71bce14707792ab7dea83e03b7889f82faa92",
+        "fetch_bytes": 177688.0 * 1024 * 2.0,
         "write_bytes": 7951.5 * 1024 * 1.0,
         "kv_bytes": 362414592,
     },
