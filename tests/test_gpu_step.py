@@ -313,3 +313,43 @@ def test_decode_step_mla_expand(H, bk, dv, load):
                 assert np.abs(lse[b] - lse2[b]).max() <= 1e-5
             torch.cuda.synchronize()
             assert np.array_equal(_gpu_pool(sess), _gpu_pool(twin)), "pool differs after step %d" % step
+
+
+def test_decode_step_mla_expand_many_sequences_and_refusals():
+    """70 MLA sequences (two pass-2 launches, outputs at their offsets) through wsk_decode_step_mla
+    against the oracle; a sequence listed twice and a short workspace are refused with nothing
+    changed."""
+    B, H, dv = 70, 16, 128
+    w = _workload("mla", B, H, seed=9)
+    gen = torch.Generator().manual_seed(10)
+    lengths = [int(x) for x in torch.randint(60, 300, (B,), generator=gen)]
+    splits = [L // 3 for L in lengths]
+    pf = _prefill(w, lengths, splits, gen)
+    _, w_uv = wl.draw_mla_weights(w, gen)
+    say("case decode step mla expand many")
+    with DecodeSession(w, pf, DEV, extra_tokens=2) as sess:
+        q_bits = wl.draw_bf16(gen, (B, H, w.row_elems))
+        kn, _ = _new_rows(w, B, gen)
+        q, knd, w_uv_d = (to_device_bf16(x, sess.dev) for x in (q_bits, kn, w_uv))
+        ws = torch.empty(wsk.wsk_decode_step_workspace(sess.h, sess.ids), dtype=torch.uint8, device=sess.dev)
+        o = torch.empty(B, H, dv, device=sess.dev)
+        o_lat = torch.empty(B, H, 512, device=sess.dev)
+        lse = torch.empty(B, H, device=sess.dev)
+        wsk.wsk_decode_step_mla(sess.h, sess.ids, q, knd, w_uv_d, o, lse, ws, o_lat=o_lat)
+        o, o_lat, lse = o.cpu().numpy(), o_lat.cpu().numpy(), lse.cpu().numpy()
+        for b in range(B):
+            rows = np.concatenate([pf.k[b], kn[b:b + 1]])
+            ol_r, l_r = oracle.attend(q_bits[b], rows, None, splits[b], lengths[b] + 1, w.softmax_scale, H, dv=512)
+            assert_close(o_lat[b], ol_r, "mla many O_lat b%d" % b)
+            assert_close(o[b], oracle.mla_expand(ol_r, w_uv), "mla many O b%d" % b)
+            assert_lse(lse[b], l_r, "mla many b%d" % b)
+        o_t = torch.empty(2, H, dv, device=sess.dev)
+        l_t = torch.empty(2, H, device=sess.dev)
+        before = [wsk.wsk_seq_info(sess.h, b)[0] for b in range(2)]
+        with pytest.raises(wsk.WskError) as ei:                    # a sequence listed twice
+            wsk.wsk_decode_step_mla(sess.h, [1, 1], q[:2], knd[:2], w_uv_d, o_t, l_t, ws)
+        assert ei.value.code == wsk.WSK_EINVAL
+        with pytest.raises(wsk.WskError) as ei:                    # workspace too small
+            wsk.wsk_decode_step_mla(sess.h, [0, 1], q[:2], knd[:2], w_uv_d, o_t, l_t, ws[:256])
+        assert ei.value.code == wsk.WSK_EINVAL
+        assert [wsk.wsk_seq_info(sess.h, b)[0] for b in range(2)] == before
