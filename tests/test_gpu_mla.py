@@ -156,7 +156,9 @@ def test_mla_absorb_and_expand_kernels():
 
 def test_c4_deepseek_v2_lite_full_path():
     """Absorb -> append -> attend the GPU range -> merge with the CPU partial in
-    latent space -> expand, against the oracle doing every step in fp64."""
+    latent space -> expand, against the oracle doing every step in fp64; then
+    the same step through wsk_decode_step (+ expand) and through
+    wsk_decode_step_mla, the benchmark's call."""
     w = wl.C4
     say("case c4", w.name)
     pf = wl.make_prefill(w)
@@ -219,6 +221,18 @@ def test_c4_deepseek_v2_lite_full_path():
         wsk.wsk_mla_expand(o_d, to_device_bf16(w_uv, dev), o_out2)
         assert_close(o_out2.cpu().numpy(), np.stack(ref), "c4 decode step")
         assert np.abs(o_out2.cpu().numpy() - o_out.cpu().numpy()).max() <= 1e-5
+        _check_pool_bytes(sess, rows_full)
+    # the benchmark's own step: absorb, then wsk_decode_step_mla (pass 1, then
+    # one pass 2 that also expands by W_UV), at the full c4 size
+    with DecodeSession(w, pf, DEV) as sess:
+        q_step = q.clone()
+        wsk.wsk_mla_absorb(to_device_bf16(st.q_nope, dev), to_device_bf16(w_uk, dev), q_step, w.row_elems)
+        o_out3 = torch.empty(B, H, w.head_dim, device=dev)
+        l3 = torch.empty(B, H, device=dev)
+        sess.decode_step_mla(q_step, to_device_bf16(st.k_new, dev), to_device_bf16(w_uv, dev), o_out3, l3,
+                             o_x=o_cd, lse_x=l_cd)
+        assert_close(o_out3.cpu().numpy(), np.stack(ref), "c4 decode step with expansion")
+        assert np.abs(o_out3.cpu().numpy() - o_out2.cpu().numpy()).max() <= 1e-5
         _check_pool_bytes(sess, rows_full)
 
 
