@@ -1,4 +1,5 @@
-// Small kernels of the decode path, gfx950: chunk combine, LSE merge,
+// Small kernels of the decode path, gfx950: chunk combine, LSE merge, the
+// decode step's pass 2 (GQA and MLA; the MLA form also expands by W_UV),
 // decode append, bulk scatter, MLA query absorption and output expansion.
 
 #include "device_rows.h"
