@@ -353,3 +353,34 @@ def test_decode_step_mla_expand_many_sequences_and_refusals():
             wsk.wsk_decode_step_mla(sess.h, [0, 1], q[:2], knd[:2], w_uv_d, o_t, l_t, ws[:256])
         assert ei.value.code == wsk.WSK_EINVAL
         assert [wsk.wsk_seq_info(sess.h, b)[0] for b in range(2)] == before
+
+
+def test_decode_step_mla_expand_empty_gpu_side():
+    """Sequences whose GPU side holds nothing before the step (split = L: pass 1 has no chunk for
+    them, so pass 2 merges only the new row and the CPU partial) beside ordinary ones, through
+    wsk_decode_step_mla, against the oracle over [0, L]."""
+    H, dv = 16, 128
+    lengths = [200, 130, 64, 300]
+    splits = [200, 0, 64, 150]          # sequences 0 and 2: every cached position on the CPU side
+    w = _workload("mla", len(lengths), H, seed=31)
+    gen = torch.Generator().manual_seed(32)
+    pf = _prefill(w, lengths, splits, gen)
+    _, w_uv = wl.draw_mla_weights(w, gen)
+    say("case decode step mla expand, empty GPU side")
+    with DecodeSession(w, pf, DEV, extra_tokens=2) as sess:
+        q_bits = wl.draw_bf16(gen, (sess.B, H, w.row_elems))
+        kn, _ = _new_rows(w, sess.B, gen)
+        q, knd, w_uv_d = (to_device_bf16(x, sess.dev) for x in (q_bits, kn, w_uv))
+        o_x, l_x = _cpu_partial(sess, q_bits)
+        ws = torch.empty(wsk.wsk_decode_step_workspace(sess.h, sess.ids), dtype=torch.uint8, device=sess.dev)
+        o = torch.empty(sess.B, H, dv, device=sess.dev)
+        o_lat = torch.empty(sess.B, H, 512, device=sess.dev)
+        lse = torch.empty(sess.B, H, device=sess.dev)
+        wsk.wsk_decode_step_mla(sess.h, sess.ids, q, knd, w_uv_d, o, lse, ws, o_lat=o_lat, o_x=o_x, lse_x=l_x)
+        o, o_lat, lse = o.cpu().numpy(), o_lat.cpu().numpy(), lse.cpu().numpy()
+        for b in range(sess.B):
+            rows = np.concatenate([pf.k[b], kn[b:b + 1]])
+            ol_r, l_r = oracle.attend(q_bits[b], rows, None, 0, lengths[b] + 1, w.softmax_scale, H, dv=512)
+            assert_close(o_lat[b], ol_r, "empty-side O_lat b%d" % b)
+            assert_close(o[b], oracle.mla_expand(ol_r, w_uv), "empty-side O b%d" % b)
+            assert_lse(lse[b], l_r, "empty-side b%d" % b)
