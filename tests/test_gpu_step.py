@@ -384,3 +384,43 @@ def test_decode_step_mla_expand_empty_gpu_side():
             assert_close(o_lat[b], ol_r, "empty-side O_lat b%d" % b)
             assert_close(o[b], oracle.mla_expand(ol_r, w_uv), "empty-side O b%d" % b)
             assert_lse(lse[b], l_r, "empty-side b%d" % b)
+
+
+@pytest.mark.parametrize("kind", ["gqa", "mla"])
+def test_decode_step_more_chunks_than_loaded_up_front(kind):
+    """One long sequence (40 chunk partials: more than the 32 that pass 2 loads before using any, so
+    its loop over the rest runs) and a short one, through wsk_decode_step (GQA) and
+    wsk_decode_step_mla (MLA), against the oracle."""
+    H = 16 if kind == "mla" else 8
+    lengths = [10300, 500]
+    splits = [60, 100]
+    w = _workload(kind, len(lengths), H, seed=41)
+    gen = torch.Generator().manual_seed(42)
+    pf = _prefill(w, lengths, splits, gen)
+    dv, g = _dims(w)
+    say("case decode step, more chunks than loaded up front", kind)
+    with DecodeSession(w, pf, DEV, extra_tokens=2) as sess:
+        q_bits = wl.draw_bf16(gen, (sess.B, H, w.row_elems))
+        kn, vn = _new_rows(w, sess.B, gen)
+        q, knd = to_device_bf16(q_bits, sess.dev), to_device_bf16(kn, sess.dev)
+        o_x, l_x = _cpu_partial(sess, q_bits)
+        if kind == "mla":
+            _, w_uv = wl.draw_mla_weights(w, gen)
+            ws = torch.empty(wsk.wsk_decode_step_workspace(sess.h, sess.ids), dtype=torch.uint8, device=sess.dev)
+            o_lat = torch.empty(sess.B, H, 512, device=sess.dev)
+            lse = torch.empty(sess.B, H, device=sess.dev)
+            o = torch.empty(sess.B, H, w.head_dim, device=sess.dev)
+            wsk.wsk_decode_step_mla(sess.h, sess.ids, q, knd, to_device_bf16(w_uv, sess.dev), o, lse, ws,
+                                    o_lat=o_lat, o_x=o_x, lse_x=l_x)
+            o, out, lse = o.cpu().numpy(), o_lat.cpu().numpy(), lse.cpu().numpy()
+        else:
+            out, lse = _step(sess, q, knd, to_device_bf16(vn, sess.dev), o_x, l_x)
+            out, lse = out.cpu().numpy(), lse.cpu().numpy()
+        for b in range(sess.B):
+            k = np.concatenate([pf.k[b], kn[b:b + 1]])
+            v = None if vn is None else np.concatenate([pf.v[b], vn[b:b + 1]])
+            o_r, l_r = oracle.attend(q_bits[b], k, v, 0, lengths[b] + 1, w.softmax_scale, g, dv=dv)
+            assert_close(out[b], o_r, "%s many chunks b%d" % (kind, b))
+            assert_lse(lse[b], l_r, "%s many chunks b%d" % (kind, b))
+            if kind == "mla":
+                assert_close(o[b], oracle.mla_expand(o_r, w_uv), "mla many chunks O b%d" % b)
