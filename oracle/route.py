@@ -22,9 +22,10 @@ Readings where the paper is silent:
   * an eviction ("flush", Sec. 4.2) moves the whole batch [w, w') of the
     D-window, w' = floor((w + D) / Bk) * Bk, to the CPU partition or the load
     region when w' <= L; the batch's blocks take slots in the destination
-    (lowest free first, sequences in the order listed, blocks ascending; a
-    block that already has a slot there keeps it), their GPU-pool slots are
-    freed, and those positions live in the destination from then on;
+    (lowest free first, sequences in ascending id whatever order the call
+    lists them in, blocks ascending -- the order an append uses; a block
+    that already has a slot there keeps it), their GPU-pool slots are freed,
+    and those positions live in the destination from then on;
   * blocks sit on an absolute grid: logical block k covers [k*Bk, (k+1)*Bk);
     a block straddling s has a slot in both pools, each holding only the
     positions of its own side;
@@ -143,15 +144,17 @@ class RouteModel:
                 raise RouteError("EINVAL", "bad destination")
             if part == LOAD and self.capacity[LOAD] == 0:
                 raise RouteError("ESTATE", "no load region")
-        batches, pending = [], {}
+        dest = dict(zip(seqs, parts))
+        batch, pending = {}, {}
         try:
-            for sq, part in zip(seqs, parts):
+            for sq in sorted(seqs):          # slots are taken in ascending sequence id
+                part = dest[sq]
                 w = self.window[sq]
                 w1 = (w + self.evict) // self.bk * self.bk
                 if w1 > self.length[sq]:
-                    batches.append(None)
+                    batch[sq] = None
                     continue
-                batches.append((w, w1))
+                batch[sq] = (w, w1)
                 for blk in range(w // self.bk, w1 // self.bk):
                     key = (part, sq, blk)
                     if key in self.slot or key in pending:
@@ -164,7 +167,8 @@ class RouteModel:
             raise
         self._commit(pending)
         moved = []
-        for sq, part, b in zip(seqs, parts, batches):
+        for sq, part in zip(seqs, parts):
+            b = batch[sq]
             if b is None:
                 moved.append(0)
                 continue

@@ -264,9 +264,17 @@ def _replay(model, ops):
                 model.append(op["seqs"])
             elif kind == "close":
                 model.close(op["seq"])
+            elif kind == "flush":
+                moved = model.flush(op["seqs"], op["parts"])
+                assert moved == op["moved"], (op, moved)
             elif kind == "expect_route":
                 got = [list(model.route(op["seq"], p)) for p in range(len(op["routes"]))]
                 assert got == op["routes"], (op, got)
+            elif kind == "expect_runs":
+                want = expand_runs(op["runs"], model.bk)
+                got = [list(model.route(op["seq"], p)) for p in range(len(want))]
+                assert model.length[op["seq"]] == len(want), op
+                assert got == want, (op, got)
             elif kind == "expect_length":
                 assert model.length[op["seq"]] == op["length"]
         except RouteError as ex:
@@ -275,10 +283,69 @@ def _replay(model, ops):
         assert err is None, ("expected failure", op)
 
 
+def expand_runs(runs, bk):
+    """[a, e, part, slot] runs -> one (part, logical block, slot, offset) per position."""
+    return [[part, p // bk, slot, p % bk] for a, e, part, slot in runs for p in range(a, e)]
+
+
 def test_route_golden_hand_derived():
     with open(os.path.join(GOLDEN, "route_small.json")) as f:
         g = json.load(f)
     _replay(RouteModel(g["block_tokens"], g["host_blocks"], g["device_blocks"]), g["ops"])
+
+
+def test_route_flush_golden_hand_derived():
+    """Evictions of several sequences listed out of order, both destinations, a
+    straddling block keeping its CPU slot, a batch that is not whole, an
+    exhausted load region that changes nothing, and slot reuse afterwards."""
+    with open(os.path.join(GOLDEN, "route_flush.json")) as f:
+        g = json.load(f)
+    model = RouteModel(g["block_tokens"], g["host_blocks"], g["device_blocks"], g["load_blocks"],
+                       g["evict_tokens"])
+    _replay(model, g["ops"])
+
+
+def test_route_flush_golden_discriminates_slot_order():
+    """The fixture decides the slot order: a model that takes slots in listed
+    order (a planted mistake) fails it at the first out-of-order flush."""
+    import heapq
+
+    class ListedOrder(RouteModel):
+        def flush(self, seqs, parts):
+            batches, pending = [], {}
+            for sq, part in zip(seqs, parts):
+                w = self.window[sq]
+                w1 = (w + self.evict) // self.bk * self.bk
+                if w1 > self.length[sq]:
+                    batches.append(None)
+                    continue
+                batches.append((w, w1))
+                for blk in range(w // self.bk, w1 // self.bk):
+                    if (part, sq, blk) not in self.slot and (part, sq, blk) not in pending:
+                        if not self.free[part]:
+                            self._undo(pending)
+                            raise RouteError("ENOMEM", "pool exhausted")
+                        pending[(part, sq, blk)] = heapq.heappop(self.free[part])
+            self._commit(pending)
+            moved = []
+            for sq, part, b in zip(seqs, parts, batches):
+                if b is None:
+                    moved.append(0)
+                    continue
+                for blk in range(b[0] // self.bk, b[1] // self.bk):
+                    heapq.heappush(self.free[GPU], self.slot.pop((GPU, sq, blk)))
+                for p in range(*b):
+                    self.homes[sq][p] = part
+                self.window[sq] = b[1]
+                moved.append(b[1] - b[0])
+            return moved
+
+    with open(os.path.join(GOLDEN, "route_flush.json")) as f:
+        g = json.load(f)
+    model = ListedOrder(g["block_tokens"], g["host_blocks"], g["device_blocks"], g["load_blocks"],
+                        g["evict_tokens"])
+    with pytest.raises(AssertionError):
+        _replay(model, g["ops"])
 
 
 @pytest.mark.parametrize("bk,L,s", [(4, 13, 6), (4, 16, 0), (4, 9, 9), (8, 30, 17), (2, 7, 3), (4, 12, 8)])
