@@ -519,7 +519,11 @@ int wsk_decode_step_mla(wsk_cache *cache, int32_t n, const int32_t *seq_ids, con
  * part[i] (WSK_PART_CPU or WSK_PART_LOAD) and set w = w', where
  * w' = floor((w + D) / block_tokens) * block_tokens (= w + D once w is
  * block-aligned); a sequence with L < w' is left as it is.  moved[i]
- * (optional, HOST) receives w' - w or 0.  The batch's GPU-pool slots are
+ * (optional, HOST) receives w' - w or 0.  The batch's blocks take slots in
+ * the destination lowest free first, sequences in ascending id (whatever
+ * order seq_ids lists them in), blocks ascending -- the order wsk_append
+ * uses; a block that already has a slot there (the CPU slot of the block
+ * holding s) keeps it.  The batch's GPU-pool slots are
  * freed.  To the load region the slots travel as device -> host DMA into
  * pinned memory, enqueued on stream (the layouts match); to the CPU the
  * rows are copied out on stream, the call waits for them, and the host

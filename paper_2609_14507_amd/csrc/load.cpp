@@ -641,7 +641,11 @@ int decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, cons
         rc = plan(c, sorted[j], c->length[sorted[j]], 1, pend);
         if (rc) return rc;
     }
-    commit(c, pend);
+    // pass 1 reads only positions routed before this call; the new routes are
+    // committed, and the lengths bumped, once both passes are enqueued, so a
+    // failed launch leaves the cache as it was (pass 2 writes a new block's
+    // device table entry, and a later step that routes the block again sends
+    // it again)
     rc = run_plan(c, n, g, false, q, nullptr, nullptr, nullptr, nullptr, ws, ws_bytes, stream, true, false);
     DeviceGuard guard(c->device);
     hipError_t e = guard.err;
@@ -679,14 +683,16 @@ int decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, cons
             const int32_t sq = ids[i0 + r];
             const int32_t pos = c->length[sq];
             const int32_t blk = pos / sp.block_tokens;
-            p.slot_elem0[r] = (int64_t)tab(c, WSK_PART_GPU, sq, blk) * c->slot_elems;
-            p.row[r] = pos % sp.block_tokens;
+            int32_t slot = tab(c, WSK_PART_GPU, sq, blk);
             p.tab_index[r] = -1;
             for (const Pending &pd : pend)
                 if (pd.seq == sq && pd.part == WSK_PART_GPU && pd.blk == blk) {
+                    slot = pd.slot;
                     p.tab_index[r] = (int32_t)((size_t)sq * c->max_blocks + blk);
                     p.tab_slot[r] = pd.slot;
                 }
+            p.slot_elem0[r] = (int64_t)slot * c->slot_elems;
+            p.row[r] = pos % sp.block_tokens;
         }
         if (ex) {
             StepExpandParams xp{};
@@ -699,9 +705,12 @@ int decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, cons
             e = launch_step_combine(p, width, (hipStream_t)stream);
         }
     }
+    if (rc || e != hipSuccess) {
+        undo(c, pend);
+        return rc ? rc : hip_fail(e, ex ? "wsk_decode_step_mla" : "wsk_decode_step");
+    }
+    commit(c, pend);
     for (int32_t i = 0; i < n; ++i) c->length[ids[i]] += 1;
-    if (rc) return rc;
-    if (e != hipSuccess) return hip_fail(e, ex ? "wsk_decode_step_mla" : "wsk_decode_step");
     return WSK_OK;
 }
 
@@ -762,10 +771,14 @@ int wsk_flush(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *part, 
         if (part[i] == WSK_PART_LOAD && !has_load_region(c)) return fail(WSK_ESTATE, "the cache has no load region");
     }
     const int bk = c->spec.block_tokens;
-    // batches and their destination slots (all-or-nothing)
+    // batches and their destination slots (all-or-nothing); slots are taken in
+    // ascending sequence id, whatever order the call lists the sequences in
+    std::vector<int32_t> order(n);
+    for (int32_t i = 0; i < n; ++i) order[i] = i;
+    std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return ids[a] < ids[b]; });
     std::vector<int32_t> w0(n), w1(n);
     std::vector<Pending> pend;
-    for (int32_t i = 0; i < n; ++i) {
+    for (const int32_t i : order) {
         const int32_t sq = ids[i];
         w0[i] = c->window[sq];
         w1[i] = (w0[i] + D) / bk * bk;

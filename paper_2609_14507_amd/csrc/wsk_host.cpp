@@ -550,10 +550,15 @@ int wsk_append(wsk_cache *c, int32_t n, const int32_t *ids, const void *k_new, c
         int rc = plan(c, sq, c->length[sq], 1, pend);
         if (rc) return rc;
     }
-    commit(c, pend);
-
+    // the routes are committed, and the lengths bumped, only once every launch
+    // has been enqueued: a failed launch leaves the cache as it was (a new
+    // block's device table entry is written by the kernel, and a later append
+    // that routes the block again sends it again)
     DeviceGuard guard(c->device);
-    if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+    if (guard.err != hipSuccess) {
+        undo(c, pend);
+        return hip_fail(guard.err, "hipSetDevice");
+    }
     hipStream_t st = (hipStream_t)stream;
     const int hkv = sp.kind == WSK_KIND_GQA ? sp.n_kv_heads : 1;
     hipError_t e = hipSuccess;
@@ -573,20 +578,25 @@ int wsk_append(wsk_cache *c, int32_t n, const int32_t *ids, const void *k_new, c
             const int32_t sq = ids[r0 + r];
             const int32_t pos = c->length[sq];
             const int32_t blk = pos / sp.block_tokens;
-            const int32_t slot = tab(c, WSK_PART_GPU, sq, blk);
-            ap.slot_elem0[r] = (int64_t)slot * c->slot_elems;
-            ap.row[r] = pos % sp.block_tokens;
+            int32_t slot = tab(c, WSK_PART_GPU, sq, blk);
             ap.tab_index[r] = -1;
             for (const Pending &p : pend)
                 if (p.seq == sq && p.part == WSK_PART_GPU && p.blk == blk) {
+                    slot = p.slot;
                     ap.tab_index[r] = (int32_t)((size_t)sq * c->max_blocks + blk);
                     ap.tab_slot[r] = slot;
                 }
+            ap.slot_elem0[r] = (int64_t)slot * c->slot_elems;
+            ap.row[r] = pos % sp.block_tokens;
         }
         e = launch_append(ap, st);
     }
+    if (e != hipSuccess) {
+        undo(c, pend);
+        return hip_fail(e, "wsk_append");
+    }
+    commit(c, pend);
     for (int32_t i = 0; i < n; ++i) c->length[ids[i]] += 1;
-    if (e != hipSuccess) return hip_fail(e, "wsk_append");
     return WSK_OK;
 }
 

@@ -388,9 +388,11 @@ def test_decode_step_mla_expand_empty_gpu_side():
 
 @pytest.mark.parametrize("kind", ["gqa", "mla"])
 def test_decode_step_more_chunks_than_loaded_up_front(kind):
-    """One long sequence (40 chunk partials: more than the 32 that pass 2 loads before using any, so
-    its loop over the rest runs) and a short one, through wsk_decode_step (GQA) and
-    wsk_decode_step_mla (MLA), against the oracle."""
+    """One long sequence (41 chunk partials on a 256-CU device: more than the 32 that pass 2 loads
+    before using any, so its loop over the rest runs) and a short one (at most 2 chunks), through
+    wsk_decode_step (GQA) and wsk_decode_step_mla (MLA), against the oracle.  The chunk count is
+    read back from the workspace size (fp32 O [partials][H][width] then LSE [partials][H], each
+    rounded up to 256 bytes), so the premise is asserted, not assumed."""
     H = 16 if kind == "mla" else 8
     lengths = [10300, 500]
     splits = [60, 100]
@@ -404,6 +406,12 @@ def test_decode_step_more_chunks_than_loaded_up_front(kind):
         kn, vn = _new_rows(w, sess.B, gen)
         q, knd = to_device_bf16(q_bits, sess.dev), to_device_bf16(kn, sess.dev)
         o_x, l_x = _cpu_partial(sess, q_bits)
+        need = wsk.wsk_decode_step_workspace(sess.h, sess.ids)
+        r256 = lambda x: (x + 255) // 256 * 256
+        partials = max(p for p in range(1, 4096) if r256(p * H * dv * 4) + r256(p * H * 4) <= need)
+        short_tiles = -(-lengths[1] // 64) - splits[1] // 64
+        say("  %d chunk partials in all, at most %d of the short sequence" % (partials, -(-short_tiles // 4)))
+        assert partials - -(-short_tiles // 4) > 32, partials
         if kind == "mla":
             _, w_uv = wl.draw_mla_weights(w, gen)
             ws = torch.empty(wsk.wsk_decode_step_workspace(sess.h, sess.ids), dtype=torch.uint8, device=sess.dev)
