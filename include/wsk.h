@@ -493,6 +493,26 @@ int wsk_decode_step(wsk_cache *cache, int32_t n, const int32_t *seq_ids, const v
                     size_t ws_bytes, void *stream);
 
 /*
+ * wsk_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same step, with the same arguments minus the workspace.  The chunk
+ * partials go to a scratch array that the library keeps in device memory,
+ * WSK_NOALLOC_SCRATCH_BYTES per GPU, held from the first wsk_init on that
+ * device until the process ends.  The call allocates nothing (no hipMalloc,
+ * hipFree or other allocating routine).  Every call on one GPU shares that
+ * GPU's array, so calls that overlap on one GPU (different streams, or
+ * different host threads) race and must be serialised by the caller; the
+ * array keeps the last call's contents, none of which a later call reads
+ * before writing it.  Errors: as wsk_decode_step, and ERANGE when the step's
+ * chunk partials (wsk_decode_step_workspace) exceed
+ * WSK_NOALLOC_SCRATCH_BYTES -- then use wsk_decode_step with a workspace.
+ */
+#define WSK_NOALLOC_SCRATCH_BYTES (16u << 20)
+int wsk_decode_step_noalloc(wsk_cache *cache, int32_t n, const int32_t *seq_ids, const void *q, const void *k_new,
+                            const void *v_new, const float *o_x, const float *lse_x, float *o, float *lse,
+                            void *stream);
+
+/*
  * One MLA decode step with the output-side expansion folded in (Sec. 6.1:
  * the latent output is expanded by W_UV per head, a linear map that commutes
  * with the LSE merge): wsk_decode_step on an MLA cache, then

@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libwsk.so")
-SOURCES = ["wsk_host.cpp", "load.cpp", "policy.cpp", "cpu_attend.cpp", "attend_gqa.hip", "attend_mla.hip", "kernels.hip"]
+SOURCES = ["wsk_host.cpp", "load.cpp", "policy.cpp", "cpu_attend.cpp", "attend_gqa.hip", "attend_mla.hip", "kernels.hip", "noalloc.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

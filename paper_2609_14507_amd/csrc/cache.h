@@ -102,6 +102,10 @@ struct DeviceGuard {
 
 int check_seq(const wsk_cache *c, int32_t seq);
 
+// Device address of wsk_decode_step_noalloc's scratch array on `device`,
+// resolved once per device (noalloc.hip).
+int noalloc_scratch(int device, void **out);
+
 inline int32_t &tab(wsk_cache *c, int part, int32_t seq, int32_t blk) {
     return c->htab[part][(size_t)seq * c->max_blocks + blk];
 }

@@ -295,6 +295,16 @@ int wsk_init(const wsk_partition_spec *spec, int device, wsk_cache **out) {
             wsk_destroy(c);
             return r;
         }
+        // the device address of wsk_decode_step_noalloc's scratch array on
+        // this device, resolved here once so the step itself only looks it up
+        void *scratch = nullptr;
+        rc = noalloc_scratch(device, &scratch);
+        if (rc) {
+            const std::string msg = g_err;
+            wsk_destroy(c);
+            g_err = msg;
+            return rc;
+        }
     }
     if (spec->load_pool_blocks > 0) {
         rc = load_init(c);

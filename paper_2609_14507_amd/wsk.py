@@ -82,6 +82,7 @@ _SIGS = {
     "wsk_attend_gpu_pass1": ([_VP, _I32, _PI32, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_attend_gpu_pass2": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP], ctypes.c_int),
     "wsk_decode_step_workspace": ([_VP, _I32, _PI32, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+    "wsk_decode_step_noalloc": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP], ctypes.c_int),
     "wsk_decode_step": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP],
                         ctypes.c_int),
     "wsk_decode_step_mla": ([_VP, _I32, _PI32, _VP, _VP, _VP, _VP, _VP, _I32, _VP, _VP, _VP, _VP, ctypes.c_size_t,
@@ -254,6 +255,12 @@ def wsk_decode_step(h: int, seq_ids, q, k_new, v_new, o, lse, ws, o_x=None, lse_
     nbytes = ws.numel() * ws.element_size()
     _check(lib().wsk_decode_step(h, len(seq_ids), _i32_array(seq_ids), _ptr(q), _ptr(k_new), _ptr(v_new),
                                  _ptr(o_x), _ptr(lse_x), _ptr(o), _ptr(lse), _ptr(ws), nbytes, _stream(stream)))
+
+
+def wsk_decode_step_noalloc(h: int, seq_ids, q, k_new, v_new, o, lse, o_x=None, lse_x=None, stream=None):
+    """wsk_decode_step with its chunk partials in the library's own device scratch (no workspace)."""
+    _check(lib().wsk_decode_step_noalloc(h, len(seq_ids), _i32_array(seq_ids), _ptr(q), _ptr(k_new), _ptr(v_new),
+                                         _ptr(o_x), _ptr(lse_x), _ptr(o), _ptr(lse), _stream(stream)))
 
 
 def wsk_decode_step_mla(h: int, seq_ids, q, k_new, w_uv, o, lse, ws, o_lat=None, o_x=None, lse_x=None,

@@ -28,7 +28,7 @@ def _declared_symbols():
 def test_library_exports_every_declared_symbol():
     L = wsk.lib()
     names = _declared_symbols()
-    assert len(names) == 43
+    assert len(names) == 44
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(wsk._SIGS)
