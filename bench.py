@@ -1,35 +1,55 @@
 """Benchmark of the GPU-partition decode step on one MI355X.
 
-One step = the whole hot path over one batch (wsk_decode_step): the new
-token's K/V of every sequence is routed to its GPU partition, split-KV
-attention covers the GPU range written so far (pass 1), then one pass 2
-scores and merges the new token, stores it into the pool, and merges the
-chunk partials and the CPU-range partial by their LSE (MLA: the query
-absorption runs before, and wsk_decode_step_mla's pass 2 also expands the
-merged latent output by W_UV).  Inputs are seeded synthetic tensors already
-resident in HBM; the CPU-range partial fed to the merge is a seeded
-synthetic (O, LSE) pair (the merge's cost does not depend on its values).
+The headline workload is the largest single-GPU configuration: the ragged
+1M-token aggregate (Qwen3-30B-A3B attention shape, 8 sequences of 98K-164K
+tokens, per-sequence CPU shares of 10-60 %), run as its 64 decode steps.  One
+step = the whole hot path over one batch (wsk_decode_step): the new token's
+K/V of every sequence is routed to its GPU partition, split-KV attention
+covers the GPU range written so far (pass 1), then one pass 2 scores and
+merges the new token, stores it into the pool, and merges the chunk partials
+and the CPU-range partial by their LSE.  The W warmup steps append the last W
+rows of the drawn context, so the K timed steps start exactly at the drawn
+lengths.  Inputs are seeded synthetic tensors already resident in HBM; the
+CPU-range partial fed to the merge is a seeded synthetic (O, LSE) pair (the
+merge's cost does not depend on its values).
 
-Timing: W untimed warmup steps, then K timed steps.  Before each step a
-512 MB buffer is rewritten so the 256 MB Infinity Cache holds no KV.  One
-pair of HIP events on the stream the kernels run on brackets the K
-(flush + step) pairs, and others the same K flushes alone, run right before
-and right after; a step's time is the difference (from the flushes' mean)
-over K.  Events are not recorded between
-the steps: each record leaves the GPU idle for ~5 us, which a per-step pair
-would count as step time.  The pass-1 kernel alone (the roofline's kernel)
-is timed the same way, K (flush + pass 1) pairs less K flushes.  K more
-steps, each between its own pair of events, give the per-step median, p10
-and p90 (each with one event's idle time in it); K more diagnostic steps
-run the pieces as separate calls with events between them, for the
-breakdown.  The algorithmic bytes of a step are the bf16 K
-and V rows (MLA: latent rows) of every attended position, read once.
+The same JSON line carries the other model shapes ("configs"): the
+Mixtral-8x7B shape swept over CPU shares {0, .25, .5, .75} on ONE cache
+written with s = 0 (only the attend range changes between sweep points: pass
+1 over [s', L) and pass 2 merging the CPU partial), the DeepSeek-V2-Lite MLA
+shape (query absorption + wsk_decode_step_mla, whose pass 2 also expands by
+W_UV), the Qwen3 shape at batch 16 x 32K (with the native CPU engine, the
+pinned load region, eviction and the offloaded step measured after it), and
+the tiny single-sequence case.
+
+Timing of every decode workload: before each step a 512 MB buffer is
+rewritten so the 256 MB Infinity Cache holds no KV.  One pair of HIP events on
+the stream the kernels run on brackets the K (flush + step) pairs, and others
+the same K flushes alone, run right before and right after; a step's time is
+the difference (from the flushes' mean) over K.  Events are not recorded
+between the steps: each record leaves the GPU idle for ~5 us, which a
+per-step pair would count as step time.  The pass-1 kernel alone (the
+roofline's kernel) is timed the same way, K (flush + pass 1) pairs less K
+flushes.  More steps, each between its own pair of events, give the per-step
+median, p10 and p90 (each with one event's idle time in it); more diagnostic
+steps run the pieces as separate calls with events between them.  The
+algorithmic bytes of a step are the bf16 K and V rows (MLA: latent rows) of
+every attended position, read once.
+
+Every pass-1 kernel dispatch this process issues is counted per kernel, in
+order ("dispatch_windows"), so that a rocprofv3 trace of the same command can
+be split by section: `python bench.py --trace-summary DIR --bench-json FILE`
+prints, per section, the profiler's mean kernel time (and HBM counters, for a
+--pmc run) over exactly that section's dispatches.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import platform
@@ -43,6 +63,10 @@ sys.path.insert(0, ROOT)
 
 METRIC = "GPU-partition decode attention effective KV GB/s and % of HBM peak"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
+EXTRA_STEPS = 20               # timed steps of each non-headline decode workload
+EXTRA_WARMUP = 3
+EVENT_STEPS = 20               # steps between their own event pairs
+DIAG_STEPS = 20                # steps run as separate calls with events between the parts
 
 
 def log(*a):
@@ -60,105 +84,479 @@ def cpu_model() -> str:
     return platform.processor()
 
 
-def cpu_baseline(w, pf, steps_inputs, budget_s: float):
-    """The fp64 oracle, as it stands, over the same GPU ranges as the timed
-    decode steps (step k attends [s_b, L_b + k + 1) with the appended rows), on
-    the host's cores: steps are taken in order, sequence by sequence, until the
-    time budget is spent."""
-    import oracle
-    B = len(pf.lengths)
-    S = len(steps_inputs)
-    ks, vs = [], []
-    for b in range(B):   # cache rows plus every step's appended row, in place
-        L = pf.lengths[b]
-        k = np.empty((L + S,) + pf.k[b].shape[1:], dtype=pf.k[b].dtype)
-        k[:L] = pf.k[b]
-        for j, st in enumerate(steps_inputs):
-            k[L + j] = st.k_new[b]
-        ks.append(k)
-        if pf.v is not None:
-            v = np.empty((L + S,) + pf.v[b].shape[1:], dtype=pf.v[b].dtype)
-            v[:L] = pf.v[b]
-            for j, st in enumerate(steps_inputs):
-                v[L + j] = st.v_new[b]
-            vs.append(v)
-    t_total, nbytes, done = 0.0, 0, 0
-    for j, st in enumerate(steps_inputs):
-        for b in range(B):
-            L = pf.lengths[b] + j + 1
-            s = min(pf.splits[b], L)
-            t0 = time.perf_counter()
-            if pf.v is None:   # MLA: one latent row per token, values = its latent part
-                oracle.attend(st.q[b], ks[b][:L], None, s, L, w.softmax_scale, w.n_q_heads, dv=w.latent_dim)
-            else:
-                oracle.attend(st.q[b], ks[b][:L], vs[b][:L], s, L, w.softmax_scale, w.group)
-            t_total += time.perf_counter() - t0
-            nbytes += (L - s) * w.token_bytes
-            done += 1
-            if t_total >= budget_s:
-                break
-        if t_total >= budget_s:
-            break
-    return {
-        "value": nbytes / t_total / 1e9,
-        "unit": "GB/s",
-        "cores": oracle.max_threads(),
-        "kind": "oracle",
-        "sample": "fp64 oracle over the GPU ranges of the decode steps in order, %d (sequence, step) ranges "
-                  "of %d sequences x %d steps (%.2f GB of KV, %.1f s); CPU: %s"
-                  % (done, B, S, nbytes / 1e9, t_total, cpu_model()),
-    }
+def gqa_heads_per_workgroup(group: int) -> int:
+    """Query heads one GQA pass-1 workgroup serves (its template argument)."""
+    h = 1
+    while h < min(group, 16):
+        h *= 2
+    return h
+
+
+class Dispatches:
+    """Pass-1 kernel dispatches issued so far, per kernel, in order.  Every
+    pass-1 call of the decode workloads here covers at most 64 sequences with a
+    non-empty range, i.e. exactly one dispatch."""
+
+    def __init__(self):
+        self.n = {}
+
+    @staticmethod
+    def key(w) -> str:
+        from paper_2609_14507_amd import workloads as wl
+        if w.kind == wl.MLA:
+            return "mla_attend_kernel"
+        return "gqa_attend_kernel<%d>" % gqa_heads_per_workgroup(w.group)
+
+    def at(self, w) -> int:
+        return self.n.get(self.key(w), 0)
+
+    def add(self, w, k: int):
+        self.n[self.key(w)] = self.at(w) + k
+
+    def part(self, w, first: int):
+        """[first, count] of the dispatches of w's kernel since `first`."""
+        return [first, self.at(w) - first]
+
+
+def wsk_mod():
+    from paper_2609_14507_amd import wsk
+    return wsk
 
 
 # HBM bytes per launch of the pass-1 kernel, from two rocprofv3 --pmc runs of
-# this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each scaled by
-# what the same counter reads for the plain 256 MiB copy of --copy-calibration
-# (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  Keyed by workload; valid only for the
-# kernel source they were taken on (sha256), null otherwise.
+# this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch, averaged over
+# the section's dispatches), each scaled by what the same counter reads for
+# the plain 256 MiB copy of --copy-calibration (FETCH_SIZE x 2.0,
+# WRITE_SIZE x 1.0).  Keyed by section; valid only for the kernel source they
+# were taken on (sha256), null otherwise.
 TRAFFIC = {
-    "qwen3-30b-a3b-b16-L32768": {
-        "source": "paper_2609_14507_amd/csrc/attend_gqa.hip",
-        "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
-        "fetch_bytes": 368787.1 * 1024 * 2.0,
-        "write_bytes": 774.0 * 1024 * 1.0,
-        "kv_bytes": 751714304,
-    },
-    "deepseek-v2-lite-mla-b8-L65536": {
-        "source": "paper_2609_14507_amd/csrc/attend_mla.hip",
-        "sha256": "4df8a57ec4065ad10e72b3e174e71bce14707792ab7dea83e03b7889f82faa92",
-        "fetch_bytes": 177688.0 * 1024 * 2.0,
-        "write_bytes": 7951.5 * 1024 * 1.0,
-        "kv_bytes": 362414592,
-    },
+    "c5": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
+           "fetch_bytes": 621598.2 * 1024 * 2.0, "write_bytes": 757.9 * 1024 * 1.0, "kv_bytes": 1271121920},
+    "c3 r=0.00": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
+           "fetch_bytes": 1048914.5 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 2147483648},
+    "c3 r=0.25": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
+           "fetch_bytes": 786706.5 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 1610612736},
+    "c3 r=0.50": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
+           "fetch_bytes": 524498.5 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 1073741824},
+    "c3 r=0.75": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
+           "fetch_bytes": 262290.5 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 536870912},
+    "c4": {"source": "paper_2609_14507_amd/csrc/attend_mla.hip", "sha256": "4df8a57ec4065ad10e72b3e174e71bce14707792ab7dea83e03b7889f82faa92",
+           "fetch_bytes": 177748.0 * 1024 * 2.0, "write_bytes": 7951.5 * 1024 * 1.0, "kv_bytes": 362575872},
+    "c2": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
+           "fetch_bytes": 368931.8 * 1024 * 2.0, "write_bytes": 774.0 * 1024 * 1.0, "kv_bytes": 752287744},
+    "c1": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
+           "fetch_bytes": 615.1 * 1024 * 2.0, "write_bytes": 20.3 * 1024 * 1.0, "kv_bytes": 1069056},
 }
 
 
-def roofline(w, kind, achieved_gbs, kv_bytes):
+def roofline(section, kernel, achieved_gbs, kv_bytes):
     """Roofline entry of the pass-1 kernel (the one that streams the KV)."""
-    import hashlib
     traffic = None
-    t = TRAFFIC.get(w.name)
+    t = TRAFFIC.get(section)
     if t is not None:
         with open(os.path.join(ROOT, t["source"]), "rb") as f:
             if hashlib.sha256(f.read()).hexdigest() == t["sha256"]:
                 traffic = t["fetch_bytes"] + t["write_bytes"]
     out = {
         "bound": "hbm",
-        "kernel": "%s_attend_kernel (wsk_attend pass 1)" % kind,
+        "kernel": "%s (pass 1)" % kernel,
         "achieved": round(achieved_gbs, 1),
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
         "frac": round(achieved_gbs / HBM_PEAK_GBS, 4),
         "traffic": None if traffic is None else int(traffic),
+        "kv_bytes_per_launch": int(kv_bytes),
     }
     if traffic is not None:
         out["traffic_per_kv_byte"] = round(traffic / t["kv_bytes"], 4)
     return out
 
 
-def wsk_mod():
-    from paper_2609_14507_amd import wsk
-    return wsk
+class Timer:
+    """Stream-ordered timing with one event pair around a whole bracket."""
+
+    def __init__(self, flush, stream, no_flush):
+        self.flush, self.stream, self.no_flush = flush, stream, no_flush
+
+    def flush_once(self):
+        if not self.no_flush:
+            self.flush.add_(1)
+
+    def bracket(self, fn):
+        """ms of fn() on the stream, one event pair around it."""
+        import torch
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        for _ in range(3):   # a GPU backlog ahead of the bracket: the host then runs ahead of
+            self.flush.add_(1)    # the timed launches, and a host stall cannot idle the GPU inside it
+        e0.record(self.stream)
+        fn()
+        e1.record(self.stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
+    def flushes_ms(self, K):
+        def run():
+            for _ in range(K):
+                self.flush_once()
+        return self.bracket(run)
+
+
+def decode_section(w, K, W, timer, disp, dev, tag, with_cpu_engine=False, keep=False):
+    """K timed decode steps of workload w (after W warmup steps that append the
+    last W rows of the drawn context), then pass 1 alone K times, EVENT_STEPS
+    event-paired steps and DIAG_STEPS diagnostic steps."""
+    import torch
+    from paper_2609_14507_amd import workloads as wl
+    from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
+    wsk = wsk_mod()
+    mla = w.kind == wl.MLA
+    log("%s: drawing %s" % (tag, w.name))
+    pf = wl.make_prefill(w)
+    splits = pf.splits
+    B, H = len(pf.lengths), w.n_q_heads
+    assert all(L - W >= s for L, s in zip(pf.lengths, splits)), "warmup rows must lie on the GPU side"
+    F = 5 if with_cpu_engine else 0
+    n_steps = K + EVENT_STEPS + DIAG_STEPS + F
+    steps_in = [wl.draw_step(w, pf.gen) for _ in range(W + n_steps)]
+    for i in range(W):   # warmup steps append the context's last W rows
+        steps_in[i].k_new = np.stack([pf.k[b][pf.lengths[b] - W + i] for b in range(B)])
+        if not mla:
+            steps_in[i].v_new = np.stack([pf.v[b][pf.lengths[b] - W + i] for b in range(B)])
+    short = wl.Prefill([L - W for L in pf.lengths], splits, [k[:L - W] for k, L in zip(pf.k, pf.lengths)],
+                       None if mla else [v[:L - W] for v, L in zip(pf.v, pf.lengths)], pf.gen)
+    log("%s: routing the prefill into the cache" % tag)
+    sess = DecodeSession(w, short, 0, extra_tokens=W + n_steps)
+    D = sess.out_width                      # attend output width (MLA: the latent)
+    qs = [to_device_bf16(s.q, dev) for s in steps_in]
+    kn = [to_device_bf16(s.k_new, dev) for s in steps_in]
+    vn = [None if mla else to_device_bf16(s.v_new, dev) for s in steps_in]
+    if mla:
+        w_uk, w_uv = wl.draw_mla_weights(w, pf.gen)
+        w_uk_d, w_uv_d = to_device_bf16(w_uk, dev), to_device_bf16(w_uv, dev)
+        qn = [to_device_bf16(s.q_nope, dev) for s in steps_in]
+        o_out = torch.empty(B, H, w.head_dim, device=dev)
+    o_c, l_c = wl.draw_cpu_partial(pf.gen, B * H, D)
+    o_cpu = torch.from_numpy(o_c).to(dev).view(B, H, D)
+    l_cpu = torch.from_numpy(l_c).to(dev).view(B, H)
+    o_m = torch.empty(B, H, D, device=dev)
+    l_m = torch.empty(B, H, device=dev)
+    sess.workspace(sess.ids, [min(s, L) for s, L in zip(splits, sess.lengths)], list(sess.lengths))
+    stream = timer.stream
+
+    def step(i, ev=None, parts=None):
+        """One decode step.  ev = (start, end) events around the step: the timed
+        steps run it as wsk_decode_step (pass 1 over the positions written so
+        far, then one pass 2 that folds in the appended row, stores it and
+        merges the CPU partial; MLA: wsk_decode_step_mla, whose pass 2 also
+        expands the merged latent output by W_UV).  parts = 5 events around its
+        pieces (diagnostic steps only, every event record costs GPU time of its
+        own): those run the same work as separate calls -- append, pass 1 over
+        [s, L + 1), pass 2 -- so that pass 1 is timed on its own."""
+        timer.flush_once()
+        mark = (lambda k: parts[k].record(stream)) if parts else (lambda k: None)
+        if ev:
+            ev[0].record(stream)
+        mark(0)
+        if mla:   # query-side projection into the latent space, in place
+            wsk.wsk_mla_absorb(qn[i], w_uk_d, qs[i], w.row_elems)
+        if parts:
+            sess.append(kn[i], vn[i])
+            mark(1)
+            sess.attend_pass1(qs[i])
+            mark(2)
+            sess.attend_pass2(o=o_m, lse=l_m, o_x=o_cpu, lse_x=l_cpu)
+            mark(3)
+        elif mla:
+            sess.decode_step_mla(qs[i], kn[i], w_uv_d, o=o_out, lse=l_m, o_x=o_cpu, lse_x=l_cpu)
+        else:
+            sess.decode_step(qs[i], kn[i], vn[i], o_x=o_cpu, lse_x=l_cpu, o=o_m, lse=l_m)
+        if mla and parts:   # output-side expansion of the merged latent output
+            wsk.wsk_mla_expand(o_m, w_uv_d, o_out)
+            mark(4)
+        if ev:
+            ev[1].record(stream)
+        disp.add(w, 1)
+
+    def kv_bytes():   # algorithmic bytes of the next step: [s_b, L_b + 1) of every sequence
+        return sum((sess.lengths[b] + 1 - min(splits[b], sess.lengths[b])) * w.token_bytes for b in range(B))
+
+    win = {"kernel": disp.key(w)}
+    log("%s: %d warmup + %d timed steps" % (tag, W, K))
+    d0 = disp.at(w)
+    for i in range(W):
+        step(i)
+    torch.cuda.synchronize()
+    win["warmup"] = disp.part(w, d0)
+    assert list(sess.lengths) == list(pf.lengths)
+    contexts = list(sess.lengths)
+    nbytes = []
+
+    def timed_steps():
+        for k in range(K):
+            nbytes.append(kv_bytes())
+            step(W + k)
+    t_flush_a = timer.flushes_ms(K)
+    t0 = time.perf_counter()
+    d0 = disp.at(w)
+    t_steps = timer.bracket(timed_steps)
+    win["timed_steps"] = disp.part(w, d0)
+    wall = time.perf_counter() - t0
+    t_flush = 0.5 * (t_flush_a + timer.flushes_ms(K))   # flushes timed before and after: drift cancels
+    step_ms = (t_steps - t_flush) / K
+
+    # the pass-1 kernel alone, K launches over the current GPU ranges
+    p1_bytes = float(sum((sess.lengths[b] - min(splits[b], sess.lengths[b])) * w.token_bytes for b in range(B)))
+
+    def pass1s():
+        for k in range(K):
+            timer.flush_once()
+            sess.attend_pass1(qs[W + k])
+            disp.add(w, 1)
+    d0 = disp.at(w)
+    t_p1 = timer.bracket(pass1s)
+    win["pass1_alone"] = disp.part(w, d0)
+    t_flush2 = 0.5 * (t_flush + timer.flushes_ms(K))
+    p1_kernel_ms = (t_p1 - t_flush2) / K
+
+    # the per-step distribution: steps each between their own pair of events
+    # (each pair counts one event's idle time, ~5.5 us, as step time)
+    ev_step = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(EVENT_STEPS)]
+    d0 = disp.at(w)
+    for k in range(EVENT_STEPS):
+        step(W + K + k, ev=ev_step[k])
+    torch.cuda.synchronize()
+    win["event_pairs"] = disp.part(w, d0)
+    ev_us = np.array([e[0].elapsed_time(e[1]) for e in ev_step]) * 1e3
+
+    ev_part = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(DIAG_STEPS)]
+    d_bytes = []
+    d0 = disp.at(w)
+    for k in range(DIAG_STEPS):
+        d_bytes.append(kv_bytes())
+        step(W + K + EVENT_STEPS + k, parts=ev_part[k])
+    torch.cuda.synchronize()
+    win["diagnostic"] = disp.part(w, d0)
+    el = lambda a, b: np.array([e[a].elapsed_time(e[b]) for e in ev_part])
+    app_ms, p1_ms, p2_ms = el(0, 1), el(1, 2), el(2, 3)
+    exp_ms = el(3, 4) if mla else np.zeros(DIAG_STEPS)
+    nbytes = np.array(nbytes, dtype=np.float64)
+    d_bytes = np.array(d_bytes, dtype=np.float64)
+    value = float(nbytes.mean() / (step_ms * 1e-3) / 1e9)
+    att_gbs = float(d_bytes.sum() / ((p1_ms + p2_ms).sum() * 1e-3) / 1e9)
+    p1_gbs = float(p1_bytes / (p1_kernel_ms * 1e-3) / 1e9)
+    log("%s: step %.1f us (%.1f GB/s); pass 1 alone %.1f us, %.0f GB/s; diagnostic parts: absorb+append %.1f, "
+        "pass 1 %.1f, pass 2 %.1f, expand %.1f us"
+        % (tag, step_ms * 1e3, value, p1_kernel_ms * 1e3, p1_gbs, app_ms.mean() * 1e3, p1_ms.mean() * 1e3,
+           p2_ms.mean() * 1e3, exp_ms.mean() * 1e3))
+    out = {
+        "workload": w.name,
+        "config": {
+            "batch": B, "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+            **({"latent_dim": w.latent_dim, "rope_dim": w.rope_dim, "nope_dim": w.nope_dim} if mla else {}),
+            "context": contexts if w.ragged_hi else w.context,
+            "cpu_split": list(splits) if w.ragged_hi else splits[0],
+            "cpu_share": [w.share_lo, w.share_hi] if w.ragged_hi else w.cpu_share,
+            "gpu_tokens_per_step": int(nbytes.mean() / w.token_bytes),
+            "kv_bytes_per_step": int(nbytes.mean()),
+            "step": ("absorb + wsk_decode_step_mla (attend pass 1 over [s, L), then one pass 2: the appended row "
+                     "scored, merged and stored, chunk combine, LSE merge with the CPU partial, expansion by W_UV)"
+                     if mla else "wsk_decode_step: attend pass 1 over [s, L), then one pass 2: the appended row "
+                     "scored, merged and stored, chunk combine, LSE merge with the CPU partial"),
+            "cache_flush_between_steps": not timer.no_flush,
+        },
+        "steps": K, "warmup": W,
+        "step_us": round(step_ms * 1e3, 2),
+        "step_gbs": round(value, 1),
+        "step_frac_of_peak": round(value / HBM_PEAK_GBS, 4),
+        "breakdown_us": {
+            "step": round(step_ms * 1e3, 2),
+            "flush_plus_step": round(t_steps / K * 1e3, 2),
+            "flush": round(t_flush / K * 1e3, 2),
+            "pass1_kernel": round(p1_kernel_ms * 1e3, 2),
+            "step_event_pairs": {"median": round(float(np.median(ev_us)), 2),
+                                 "p10": round(float(np.percentile(ev_us, 10)), 2),
+                                 "p90": round(float(np.percentile(ev_us, 90)), 2),
+                                 "what": "steps each between their own pair of events: the per-step spread; each "
+                                         "includes one event record's idle time (~5.5 us)"},
+            "wall_per_step_incl_flush": round(wall / K * 1e6, 1),
+            "diagnostic_steps": "steps with events between the parts (each record adds ~5 us of GPU idle time to "
+                                "the part it closes)",
+            ("absorb_append" if mla else "append"): round(float(app_ms.mean() * 1e3), 2),
+            "attend_pass1": round(float(p1_ms.mean() * 1e3), 2),
+            "attend_pass2_combine_merge": round(float(p2_ms.mean() * 1e3), 2),
+            **({"expand": round(float(exp_ms.mean() * 1e3), 2)} if mla else {}),
+            "attend_gbs": round(att_gbs, 1),
+        },
+        "roofline": roofline(tag, disp.key(w), p1_gbs, p1_bytes),
+        "dispatch_window": win,
+        "_ms_per_step": float(step_ms),
+    }
+    state = None
+    if with_cpu_engine or keep:
+        state = dict(pf=pf, sess=sess if with_cpu_engine else None, steps_in=steps_in,
+                     i0=W + K + EVENT_STEPS + DIAG_STEPS, F=F, splits=splits, qs=qs, kn=kn, vn=vn, o_m=o_m,
+                     l_m=l_m, p1_kernel_ms=p1_kernel_ms, p1_bytes=p1_bytes, step_ms=step_ms, K=K, W=W)
+    if not with_cpu_engine:
+        sess.close()
+    return out, state
+
+
+def sweep_section(w, K, W, timer, disp, dev, tag="c3"):
+    """The CPU share swept over w.sweep on ONE cache written once with s = 0:
+    between sweep points only the attend range [s', L) changes (no data is
+    written or moved).  A point's step is pass 1 over [s', L) plus pass 2
+    merging the CPU partial of [0, s') (a synthetic stand-in here), timed as
+    K (flush + step) pairs less K flushes; pass 1 alone the same way."""
+    import torch
+    from paper_2609_14507_amd import workloads as wl
+    from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
+    log("%s: drawing %s" % (tag, w.name))
+    pf = wl.make_prefill(w)
+    assert all(s == 0 for s in pf.splits), "the sweep cache is written with s = 0"
+    B, H, L = len(pf.lengths), w.n_q_heads, w.context
+    st = wl.draw_step(w, pf.gen)
+    log("%s: routing the prefill into the cache (s = 0, once)" % tag)
+    sess = DecodeSession(w, pf, 0, extra_tokens=0)
+    q = to_device_bf16(st.q, dev)
+    o_c, l_c = wl.draw_cpu_partial(pf.gen, B * H, w.head_dim)
+    o_x = torch.from_numpy(o_c).to(dev).view(B, H, w.head_dim)
+    l_x = torch.from_numpy(l_c).to(dev).view(B, H)
+    o = torch.empty(B, H, w.head_dim, device=dev)
+    lse = torch.empty(B, H, device=dev)
+    points = []
+    win = {"kernel": disp.key(w)}
+    for share in w.sweep:
+        s = wl.split_point(share, L)
+        start, end = [s] * B, [L] * B
+        sess.workspace(sess.ids, start, end)
+
+        def one_step():
+            timer.flush_once()
+            sess.attend_pass1(q, start, end)
+            sess.attend_pass2(start, end, o=o, lse=lse, o_x=o_x, lse_x=l_x)
+            disp.add(w, 1)
+        d0 = disp.at(w)
+        for _ in range(W):
+            one_step()
+        torch.cuda.synchronize()
+        fa = timer.flushes_ms(K)
+        d1 = disp.at(w)
+        t_steps = timer.bracket(lambda: [one_step() for _ in range(K)])
+        d2 = disp.at(w)
+        t_flush = 0.5 * (fa + timer.flushes_ms(K))
+
+        def p1():
+            for _ in range(K):
+                timer.flush_once()
+                sess.attend_pass1(q, start, end)
+                disp.add(w, 1)
+        t_p1 = timer.bracket(p1)
+        t_flush2 = 0.5 * (t_flush + timer.flushes_ms(K))
+        step_ms = (t_steps - t_flush) / K
+        p1_ms = (t_p1 - t_flush2) / K
+        kvb = float(B * (L - s) * w.token_bytes)
+        key = "%s r=%.2f" % (tag, share)
+        points.append({
+            "cpu_share": share, "split": s, "kv_bytes_per_step": int(kvb),
+            "step_us": round(step_ms * 1e3, 2), "step_gbs": round(kvb / (step_ms * 1e-3) / 1e9, 1),
+            "step_frac_of_peak": round(kvb / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "pass1_us": round(p1_ms * 1e3, 2),
+            "roofline": roofline(key, disp.key(w), kvb / (p1_ms * 1e-3) / 1e9, kvb),
+        })
+        win["r=%.2f" % share] = {"warmup": [d0, d1 - d0], "timed_steps": [d1, d2 - d1], "pass1_alone": [d2, K]}
+        log("%s: r = %.2f (s' = %d): step %.1f us (%.0f GB/s), pass 1 %.1f us (%.0f GB/s)"
+            % (tag, share, s, step_ms * 1e3, kvb / (step_ms * 1e-3) / 1e9, p1_ms * 1e3, kvb / (p1_ms * 1e-3) / 1e9))
+    sess.close()
+    return {
+        "workload": w.name,
+        "config": {"batch": B, "q_heads": H, "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "context": L,
+                   "written_with_split": 0, "sweep": list(w.sweep),
+                   "step": "wsk_attend_pass1 over [s', L) + wsk_attend_pass2 (chunk combine and LSE merge of the "
+                           "CPU partial of [0, s')); one cache, written once, no data moved between points",
+                   "cache_flush_between_steps": not timer.no_flush},
+        "steps": K, "warmup": W,
+        "sweep": points,
+        "dispatch_window": win,
+    }
+
+
+def cpu_baseline(w5, pf5, steps5, W, K, w1, budget_s: float):
+    """The fp64 oracle, as it stands, on the host's cores: the headline's GPU
+    ranges [s_b, L_b + k + 1) of all sequences at timed decode steps 0, 31 and
+    63 first (and their CPU ranges [0, s_b), which feed the merge), then
+    further steps in order until the time budget is spent; also the tiny
+    single-sequence case on one thread and on all of them."""
+    import oracle
+    B = len(pf5.lengths)
+    timed = steps5[W:W + K]
+    ks, vs = [], []
+    for b in range(B):   # cache rows plus every timed step's appended row, in place
+        L = pf5.lengths[b]
+        k = np.empty((L + K,) + pf5.k[b].shape[1:], dtype=pf5.k[b].dtype)
+        v = np.empty_like(k)
+        k[:L], v[:L] = pf5.k[b], pf5.v[b]
+        for j, st in enumerate(timed):
+            k[L + j], v[L + j] = st.k_new[b], st.v_new[b]
+        ks.append(k)
+        vs.append(v)
+    threads = oracle.max_threads()
+    order = [j for j in (0, 31, 63) if j < K] + [j for j in range(K) if j not in (0, 31, 63)]
+    t_total, nbytes, done, first = 0.0, 0, 0, []
+    for j in order:
+        st = timed[j]
+        tg, bg, tc, bc = 0.0, 0, 0.0, 0
+        for b in range(B):
+            L = pf5.lengths[b] + j + 1
+            s = pf5.splits[b]
+            t0 = time.perf_counter()
+            oracle.attend(st.q[b], ks[b][:L], vs[b][:L], s, L, w5.softmax_scale, w5.group)
+            t1 = time.perf_counter()
+            tg += t1 - t0
+            bg += (L - s) * w5.token_bytes
+            if j in (0, 31, 63):
+                oracle.attend(st.q[b], ks[b][:L], vs[b][:L], 0, s, w5.softmax_scale, w5.group)
+                tc += time.perf_counter() - t1
+                bc += s * w5.token_bytes
+        t_total += tg
+        nbytes += bg
+        done += 1
+        if j in (0, 31, 63):
+            first.append({"step": j, "gpu_range_s": round(tg, 3), "gpu_range_gbs": round(bg / tg / 1e9, 3),
+                          "cpu_range_s": round(tc, 3), "cpu_range_gbs": round(bc / tc / 1e9, 3)})
+        elif t_total >= budget_s:
+            break
+    # the tiny case: one sequence, [s, L + 1) after its append, single thread and all threads
+    from paper_2609_14507_amd import workloads as wl
+    pf1 = wl.make_prefill(w1)
+    st1 = wl.draw_step(w1, pf1.gen)
+    k1 = np.concatenate([pf1.k[0], st1.k_new[0][None]])
+    v1 = np.concatenate([pf1.v[0], st1.v_new[0][None]])
+    s1, L1 = pf1.splits[0], k1.shape[0]
+    c1 = {}
+    for label, n in (("threads_1", 1), ("threads_all", threads)):
+        oracle.set_threads(n)
+        reps, t = 0, 0.0
+        while t < 1.0:
+            t0 = time.perf_counter()
+            oracle.attend(st1.q[0], k1, v1, s1, L1, w1.softmax_scale, w1.group)
+            t += time.perf_counter() - t0
+            reps += 1
+        c1[label] = {"threads": n, "ms": round(t / reps * 1e3, 3),
+                     "gbs": round((L1 - s1) * w1.token_bytes * reps / t / 1e9, 3)}
+    oracle.set_threads(threads)
+    return {
+        "value": nbytes / t_total / 1e9,
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": "fp64 oracle over the GPU ranges [s_b, L_b + k + 1) of all %d sequences of the headline "
+                  "workload at timed decode steps 0, 31, 63, then further steps in order until %.0f s were spent: "
+                  "%d steps, %.2f GB of KV in %.1f s; CPU: %s"
+                  % (B, budget_s, done, nbytes / 1e9, t_total, cpu_model()),
+        "steps_0_31_63": first,
+        "tiny_c1": dict(c1, what="one sequence, L 2048 + 1 appended, GPU range [1024, 2049), fp64 oracle"),
+    }
 
 
 def cpu_gpu_steps(w, sess, wsk, steps_in, i0, F, splits, qs, kn, vn, o_m, l_m, flush, dev, absorb, expand,
@@ -481,13 +879,93 @@ def offload_section(w, pf, steps_in, dev, flush, A_s, c_cpu_s, B_s, n_steps=3):
     return out
 
 
+
+
+def _read_rows(pattern):
+    paths = sorted(glob.glob(pattern, recursive=True))
+    rows = []
+    for p in paths:
+        with open(p, newline="") as f:
+            rows.extend(csv.DictReader(f))
+    return rows
+
+
+def trace_summary(trace_dir, bench_json):
+    """Markdown summary of a rocprofv3 run of this script: for every section
+    of the JSON line the same run printed, the profiler's mean duration (kernel
+    trace) or counter value (--pmc, KiB per dispatch) over exactly that
+    section's pass-1 dispatches, matched by kernel name in dispatch order."""
+    with open(bench_json) as f:
+        line = [ln for ln in f if ln.startswith("{")][-1]
+    out = json.loads(line)
+    trace = _read_rows(os.path.join(trace_dir, "**", "*kernel_trace.csv"))
+    counters = _read_rows(os.path.join(trace_dir, "**", "*counter_collection.csv"))
+
+    def per_kernel(rows, key):
+        sel = [r for r in rows if (key + "(") in r["Kernel_Name"]]
+        return sorted(sel, key=lambda r: int(r["Dispatch_Id"]))
+
+    sections = []
+    for name, sec in [("headline", out)] + sorted(out.get("configs", {}).items()):
+        win = sec.get("dispatch_window")
+        if not win:
+            continue
+        if "timed_steps" in win:
+            sections.append((name, sec["workload"], win["kernel"], win, sec["roofline"]["kv_bytes_per_launch"],
+                             sec["breakdown_us"]["pass1_kernel"]))
+        for label, sub in sorted(win.items()):
+            if isinstance(sub, dict):
+                pt = [p for p in sec["sweep"] if "r=%.2f" % p["cpu_share"] == label][0]
+                sections.append(("%s %s" % (name, label), sec["workload"], win["kernel"], sub,
+                                 pt["roofline"]["kv_bytes_per_launch"], pt["pass1_us"]))
+    lines = []
+    if trace:
+        lines += ["| section | kernel | part | dispatches | mean us | min us | max us | KV MB per launch | "
+                  "TB/s at mean | % of 8 TB/s | bench.py pass-1 us |", "|---|---|---|---|---|---|---|---|---|---|---|"]
+        cache = {}
+        for name, wl_name, key, win, kvb, bench_us in sections:
+            d = cache.setdefault(key, per_kernel(trace, key))
+            for part in ("timed_steps", "pass1_alone", "event_pairs", "diagnostic"):
+                if part not in win:
+                    continue
+                a, n = win[part]
+                us = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in d[a:a + n]]
+                if len(us) != n:
+                    lines.append("| %s | %s | %s | %d of %d found | | | | | | | |" % (name, key, part, len(us), n))
+                    continue
+                m = float(np.mean(us))
+                lines.append("| %s | %s | %s | %d | %.2f | %.2f | %.2f | %.1f | %.2f | %.1f | %s |"
+                             % (name, key, part, n, m, min(us), max(us), kvb / 1e6, kvb / (m * 1e-6) / 1e12,
+                                100 * kvb / (m * 1e-6) / 8e12, bench_us if part == "pass1_alone" else ""))
+    if counters:
+        names = sorted({r["Counter_Name"] for r in counters})
+        copies = [r for r in counters if "__amd_rocclr_copyBuffer" in r["Kernel_Name"]]
+        lines += ["", "Counters (KiB per dispatch); copy calibration (%d dispatches of __amd_rocclr_copyBuffer, "
+                  "the last three are the 256 MiB copies): %s" % (len(copies), ", ".join(
+                      "%s %s" % (c, [round(float(r["Counter_Value"]), 1) for r in copies if r["Counter_Name"] == c][-3:])
+                      for c in names)), "",
+                  "| section | kernel | part | dispatches | " + " | ".join(names) + " | KV MB per launch |",
+                  "|---|---|---|---|" + "---|" * len(names) + "---|"]
+        for name, wl_name, key, win, kvb, _ in sections:
+            for part in ("timed_steps", "pass1_alone"):
+                if part not in win:
+                    continue
+                a, n = win[part]
+                vals = []
+                for c in names:
+                    d = per_kernel([r for r in counters if r["Counter_Name"] == c], key)[a:a + n]
+                    vals.append("%.1f" % np.mean([float(r["Counter_Value"]) for r in d]) if len(d) == n else "-")
+                lines.append("| %s | %s | %s | %d | %s | %.1f |" % (name, key, part, n, " | ".join(vals), kvb / 1e6))
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="c2", help="workload: c2 (default, the metric's), c1, c3, c4, c5")
-    ap.add_argument("--share", type=float, default=None, help="override the CPU share (sweep configs)")
+    ap.add_argument("--steps", type=int, default=64, help="timed decode steps of the headline workload")
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c5", help="headline workload: c5 (default), c2, c4 or c1")
+    ap.add_argument("--headline-only", action="store_true", help="skip the other configurations")
     ap.add_argument("--no-flush", action="store_true", help="skip the Infinity Cache flush between steps")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -496,10 +974,16 @@ def main():
     ap.add_argument("--no-load-region", action="store_true",
                     help="skip the streamed load-region step, eviction and transfer measurements")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="after the timed steps, run a plain 256 MiB device copy three times (the reference "
-                         "dispatch that scales HBM byte counters)")
+                    help="at the end, run a plain 256 MiB device copy three times (the reference dispatch that "
+                         "scales HBM byte counters)")
+    ap.add_argument("--trace-summary", default=None, help="summarise a rocprofv3 output directory of this script "
+                    "(needs --bench-json) and exit; uses no GPU")
+    ap.add_argument("--bench-json", default=None, help="file holding the JSON line of the profiled run")
     args = ap.parse_args()
 
+    if args.trace_summary:
+        trace_summary(args.trace_summary, args.bench_json)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
@@ -507,167 +991,58 @@ def main():
 
     import torch
     from paper_2609_14507_amd import workloads as wl
-    from paper_2609_14507_amd.runner import DecodeSession, to_device_bf16
 
-    w = wl.CONFIGS[args.config]
-    mla = w.kind == wl.MLA
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    K, W = args.steps, args.warmup
-
-    log("bench: drawing %s" % w.name)
-    pf = wl.make_prefill(w)
-    splits = pf.splits
-    if args.share is not None:
-        splits = [wl.split_point(args.share, L) for L in pf.lengths]
-        pf = wl.Prefill(pf.lengths, splits, pf.k, pf.v, pf.gen)
-    F = 5                                    # full CPU + GPU steps after the GPU-only ones
-    steps_in = [wl.draw_step(w, pf.gen) for _ in range(W + 3 * K + F)]
-    log("bench: routing the prefill into the cache")
-    sess = DecodeSession(w, pf, 0, extra_tokens=W + 3 * K + F)
-    B, H = sess.B, w.n_q_heads
-    D = sess.out_width                      # attend output width (MLA: the latent)
-    qs = [to_device_bf16(s.q, dev) for s in steps_in]
-    kn = [to_device_bf16(s.k_new, dev) for s in steps_in]
-    vn = [None if mla else to_device_bf16(s.v_new, dev) for s in steps_in]
-    if mla:
-        from paper_2609_14507_amd import wsk
-        w_uk, w_uv = wl.draw_mla_weights(w, pf.gen)
-        w_uk_d, w_uv_d = to_device_bf16(w_uk, dev), to_device_bf16(w_uv, dev)
-        qn = [to_device_bf16(s.q_nope, dev) for s in steps_in]
-        o_out = torch.empty(B, H, w.head_dim, device=dev)
-    o_c, l_c = wl.draw_cpu_partial(pf.gen, B * H, D)
-    o_cpu = torch.from_numpy(o_c).to(dev).view(B, H, D)
-    l_cpu = torch.from_numpy(l_c).to(dev).view(B, H)
-    o_m = torch.empty(B, H, D, device=dev)
-    l_m = torch.empty(B, H, device=dev)
-    sess.workspace(sess.ids, [min(s, L) for s, L in zip(splits, pf.lengths)], list(pf.lengths))
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-    stream = torch.cuda.current_stream()
+    timer = Timer(flush, torch.cuda.current_stream(), args.no_flush)
+    disp = Dispatches()
+    K, W = args.steps, args.warmup
+    w = wl.CONFIGS[args.config]
+    if w.sweep:
+        raise SystemExit("the swept configuration is reported under 'configs'; pick c5, c2, c4 or c1")
 
-    def step(i, ev=None, parts=None):
-        """One decode step.  ev = (start, end) events around the step: the timed
-        steps run it as wsk_decode_step (pass 1 over the positions written so
-        far, then one pass 2 that folds in the appended row, stores it and
-        merges the CPU partial; MLA: wsk_decode_step_mla, whose pass 2 also
-        expands the merged latent output by W_UV).  parts = 5 events around its pieces
-        (diagnostic steps only, every event record costs GPU time of its own):
-        those run the same work as separate calls -- append, pass 1 over
-        [s, L + 1), pass 2 -- so that pass 1 is timed on its own."""
-        if not args.no_flush:
-            flush.add_(1)
-        mark = (lambda k: parts[k].record(stream)) if parts else (lambda k: None)
-        if ev:
-            ev[0].record(stream)
-        mark(0)
-        if mla:   # query-side projection into the latent space, in place
-            wsk.wsk_mla_absorb(qn[i], w_uk_d, qs[i], w.row_elems)
-        if parts:
-            sess.append(kn[i], vn[i])
-            mark(1)
-            sess.attend_pass1(qs[i])
-            mark(2)
-            sess.attend_pass2(o=o_m, lse=l_m, o_x=o_cpu, lse_x=l_cpu)
-            mark(3)
-        elif mla:
-            sess.decode_step_mla(qs[i], kn[i], w_uv_d, o=o_out, lse=l_m, o_x=o_cpu, lse_x=l_cpu)
-        else:
-            sess.decode_step(qs[i], kn[i], vn[i], o_x=o_cpu, lse_x=l_cpu, o=o_m, lse=l_m)
-        if mla and parts:   # output-side expansion of the merged latent output
-            wsk.wsk_mla_expand(o_m, w_uv_d, o_out)
-            mark(4)
-        if ev:
-            ev[1].record(stream)
-
-    def kv_bytes():   # algorithmic bytes of the next step: [s_b, L_b + 1) of every sequence
-        return sum((sess.lengths[b] + 1 - min(splits[b], sess.lengths[b])) * w.token_bytes for b in range(B))
-
-    def bracket(fn):   # ms of fn() on the stream, one event pair around it
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        for _ in range(3):   # a GPU backlog ahead of the bracket: the host then runs ahead of
-            flush.add_(1)    # the timed launches, and a host stall cannot idle the GPU inside it
-        e0.record(stream)
-        fn()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1)
-
-    def flushes():
-        if not args.no_flush:
-            for _ in range(K):
-                flush.add_(1)
-
-    ev_part = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
-    log("bench: %d warmup + %d timed steps (+ %d diagnostic steps with per-part events)" % (W, K, K))
-    for i in range(W):
-        step(i)
-    torch.cuda.synchronize()
-    nbytes = []
-
-    def timed_steps():
-        for k in range(K):
-            nbytes.append(kv_bytes())
-            step(W + k)
-    t_flush_a = bracket(flushes)
-    t0 = time.perf_counter()
-    t_steps = bracket(timed_steps)
-    wall = time.perf_counter() - t0
-    t_flush = 0.5 * (t_flush_a + bracket(flushes))   # flushes timed before and after: drift cancels
-    step_ms = (t_steps - t_flush) / K
-
-    # the pass-1 kernel alone, K launches over the current GPU ranges
-    p1_bytes = float(sum((sess.lengths[b] - min(splits[b], sess.lengths[b])) * w.token_bytes for b in range(B)))
-
-    def pass1s():
-        for k in range(K):
-            if not args.no_flush:
-                flush.add_(1)
-            sess.attend_pass1(qs[W + k])
-    t_p1 = bracket(pass1s)
-    t_flush2 = 0.5 * (t_flush + bracket(flushes))
-    p1_kernel_ms = (t_p1 - t_flush2) / K
-
-    # the per-step distribution: K more steps, each between its own pair of
-    # events (each pair counts one event's idle time, ~5.5 us, as step time)
-    ev_step = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
-    for k in range(K):
-        step(W + K + k, ev=ev_step[k])
-    torch.cuda.synchronize()
-    ev_us = np.array([e[0].elapsed_time(e[1]) for e in ev_step]) * 1e3
-
-    d_bytes = []
-    for k in range(K):
-        d_bytes.append(kv_bytes())
-        step(W + 2 * K + k, parts=ev_part[k])
-    torch.cuda.synchronize()
-    el = lambda a, b: np.array([e[a].elapsed_time(e[b]) for e in ev_part])
-    app_ms, p1_ms, p2_ms = el(0, 1), el(1, 2), el(2, 3)
-    exp_ms = el(3, 4) if mla else np.zeros(K)
-    nbytes = np.array(nbytes, dtype=np.float64)
-    d_bytes = np.array(d_bytes, dtype=np.float64)
-    value = float(nbytes.mean() / (step_ms * 1e-3) / 1e9)
-    att_gbs = float(d_bytes.sum() / ((p1_ms + p2_ms).sum() * 1e-3) / 1e9)
-    p1_gbs = float(p1_bytes / (p1_kernel_ms * 1e-3) / 1e9)
-    log("bench: step %.1f us (%.1f us per flush + step less %.1f us per flush); pass 1 alone %.1f us, %.0f GB/s; "
-        "diagnostic steps (events between parts): absorb+append %.1f, attend pass 1 %.1f, pass 2 with merge %.1f, "
-        "expand %.1f us; wall %.1f ms/step"
-        % (step_ms * 1e3, t_steps / K * 1e3, t_flush / K * 1e3, p1_kernel_ms * 1e3, p1_gbs, app_ms.mean() * 1e3,
-           p1_ms.mean() * 1e3, p2_ms.mean() * 1e3, exp_ms.mean() * 1e3, wall / K * 1e3))
-    cpu_engine, full_step, policy = None, None, None
-    if not args.no_cpu_engine:
+    # headline: K timed decode steps
+    cpu_c2 = not args.no_cpu_engine
+    head, head_state = decode_section(w, K, W, timer, disp, dev, args.config,
+                                      with_cpu_engine=(args.config == "c2" and cpu_c2), keep=True)
+    configs, c2_state = {}, (head_state if args.config == "c2" else None)
+    if not args.headline_only:
+        configs["c3"] = sweep_section(wl.C3, EXTRA_STEPS, EXTRA_WARMUP, timer, disp, dev)
+        for tag in ("c4", "c2", "c1"):
+            if tag == args.config:
+                continue
+            res, st = decode_section(wl.CONFIGS[tag], EXTRA_STEPS, EXTRA_WARMUP, timer, disp, dev, tag,
+                                     with_cpu_engine=(tag == "c2" and cpu_c2), keep=(tag == "c2"))
+            configs[tag] = res
+            if tag == "c2":
+                c2_state = st
+    # the native CPU engine and the full CPU + GPU step (the Qwen3 shape at
+    # batch 16), on that workload's decode session
+    cpu_engine = full_step = policy = None
+    wc = wl.C2
+    if c2_state is not None and c2_state["sess"] is not None:
+        st = c2_state
+        d0 = disp.at(wc)
         cpu_engine, full_step, policy = cpu_gpu_steps(
-            w, sess, wsk_mod(), steps_in, W + 3 * K, F, splits, qs, kn, vn, o_m, l_m, flush, dev,
-            None,   # MLA: the drawn absorbed query feeds both engines (no absorb launch)
-            (lambda: wsk_mod().wsk_mla_expand(o_m, w_uv_d, o_out)) if mla else None,
-            gpu_ns_per_token=float(p1_kernel_ms * 1e6 / (p1_bytes / w.token_bytes)),
-            gpu_fixed_us=float((step_ms - p1_kernel_ms) * 1e3))
-    sess.close()
-    load_region = None if args.no_load_region else load_region_section(w, pf, steps_in, dev, flush)
-    offload = None
-    if load_region is not None and policy is not None:
-        offload = offload_section(w, pf, steps_in, dev, flush, policy["A_ns_per_token"] * 1e-9,
-                                  policy["c_cpu_us"] * 1e-6, w.token_bytes / (load_region["achieved"] * 1e9))
+            wc, st["sess"], wsk_mod(), st["steps_in"], st["i0"], st["F"], st["splits"], st["qs"], st["kn"],
+            st["vn"], st["o_m"], st["l_m"], flush, dev, None, None,
+            gpu_ns_per_token=float(st["p1_kernel_ms"] * 1e6 / (st["p1_bytes"] / wc.token_bytes)),
+            gpu_fixed_us=float((st["step_ms"] - st["p1_kernel_ms"]) * 1e3))
+        disp.add(wc, st["F"])
+        (configs.get("c2") or head)["dispatch_window"]["cpu_gpu_steps"] = disp.part(wc, d0)
+        st["sess"].close()
+        st["sess"] = None
+    # after every counted dispatch: the pinned load region, eviction, the
+    # offloaded step (their streamed pass-1 launches are not counted)
+    load_region = offload = None
+    if not args.no_load_region and c2_state is not None:
+        load_region = load_region_section(wc, c2_state["pf"], c2_state["steps_in"], dev, flush)
+        if policy is not None:
+            offload = offload_section(wc, c2_state["pf"], c2_state["steps_in"], dev, flush,
+                                      policy["A_ns_per_token"] * 1e-9, policy["c_cpu_us"] * 1e-6,
+                                      wc.token_bytes / (load_region["achieved"] * 1e9))
+    c2_state = None
     # plain streaming read of 2 GiB with the attention kernels' load pattern:
     # the practical HBM read ceiling the pass-1 rate is compared with
     from paper_2609_14507_amd import wsk as _wsk
@@ -675,6 +1050,7 @@ def main():
     probe.fill_(3)
     fold = torch.zeros(1, dtype=torch.int32, device=dev)
     cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    stream = timer.stream
 
     def read_gbs(workgroups):
         ms = []
@@ -702,56 +1078,29 @@ def main():
         torch.cuda.synchronize()
         log("bench: copy calibration: 3 x %d bytes read + written" % src.numel())
 
+    step_ms = head.pop("_ms_per_step")
+    for c in configs.values():
+        c.pop("_ms_per_step", None)
     out = {
         "metric": METRIC,
-        "value": round(value, 1),
+        "value": head["step_gbs"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": W,
-        "ms_per_step": round(float(step_ms), 4),
+        "ms_per_step": round(step_ms, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {
-            "workload": w.name,
-            "batch": B,
-            "q_heads": w.n_q_heads,
-            "kv_heads": w.n_kv_heads,
-            "head_dim": w.head_dim,
-            **({"latent_dim": w.latent_dim, "rope_dim": w.rope_dim, "nope_dim": w.nope_dim} if mla else {}),
-            "context": w.context if w.context else [w.ragged_lo, w.ragged_hi],
-            "cpu_share": args.share if args.share is not None else (w.cpu_share or [w.share_lo, w.share_hi]),
-            "gpu_tokens_per_step": int(nbytes.mean() / w.token_bytes),
-            "kv_bytes_per_step": int(nbytes.mean()),
-            "step": ("absorb + wsk_decode_step_mla (attend pass 1 over [s, L), then one pass 2: the appended row "
-                     "scored, merged and stored, chunk combine, LSE merge with the CPU partial, expansion by W_UV)"
-                     if mla else "wsk_decode_step: attend pass 1 over [s, L), then one pass 2: the appended row "
-                     "scored, merged and stored, chunk combine, LSE merge with the CPU partial"),
-            "cache_flush_between_steps": not args.no_flush,
-        },
-        "breakdown_us": {
-            "step": round(step_ms * 1e3, 2),
-            "flush_plus_step": round(t_steps / K * 1e3, 2),
-            "flush": round(t_flush / K * 1e3, 2),
-            "pass1_kernel": round(p1_kernel_ms * 1e3, 2),
-            "step_event_pairs": {"median": round(float(np.median(ev_us)), 2),
-                                 "p10": round(float(np.percentile(ev_us, 10)), 2),
-                                 "p90": round(float(np.percentile(ev_us, 90)), 2),
-                                 "what": "K more steps, each between its own pair of events: the per-step "
-                                         "spread; each includes one event record's idle time (~5.5 us)"},
-            "wall_per_step_incl_flush": round(wall / K * 1e6, 1),
-            "diagnostic_steps": "K more steps with events between the parts (each record adds ~5 us of GPU "
-                                "idle time to the part it closes)",
-            ("absorb_append" if mla else "append"): round(float(app_ms.mean() * 1e3), 2),
-            "attend_pass1": round(float(p1_ms.mean() * 1e3), 2),
-            "attend_pass2_combine_merge": round(float(p2_ms.mean() * 1e3), 2),
-            **({"expand": round(float(exp_ms.mean() * 1e3), 2)} if mla else {}),
-            "attend_gbs": round(att_gbs, 1),
-        },
-        "roofline": roofline(w, "mla" if mla else "gqa", p1_gbs, p1_bytes),
+        "config": dict(workload=head["workload"], decode_steps=K, **head["config"]),
+        "frac_of_peak": head["step_frac_of_peak"],
+        "breakdown_us": head["breakdown_us"],
+        "roofline": head["roofline"],
+        "workload": head["workload"],
+        "dispatch_window": head["dispatch_window"],
+        "configs": configs,
         "stream_read_probe": {"value": round(probe_gbs, 1), "unit": "GB/s", "bytes": 2 << 30,
                               "by_workgroups": probe_sweep,
                               "what": "wsk_stream_read: one plain read of 2 GiB with the attention kernels' "
@@ -766,9 +1115,14 @@ def main():
         out["cpu_engine"] = cpu_engine
         out["full_step"] = full_step
         out["split_policy"] = policy
-    if not args.no_cpu_baseline:
-        log("bench: timing the oracle on the host (%.0f s budget)" % args.cpu_budget)
-        out["cpu_baseline"] = cpu_baseline(w, pf, steps_in, args.cpu_budget)
+    if head_state is not None:
+        if not args.no_cpu_baseline:
+            if w is wl.C5:
+                log("bench: timing the oracle on the host (%.0f s budget)" % args.cpu_budget)
+                out["cpu_baseline"] = cpu_baseline(w, head_state["pf"], head_state["steps_in"], W, K, wl.C1,
+                                                   args.cpu_budget)
+            else:
+                log("bench: cpu_baseline is taken on the ragged 1M-token workload only")
     print(json.dumps(out), flush=True)
 
 

@@ -47,8 +47,9 @@ def lib():
         L.oracle_mla_absorb.argtypes = [i32, i32, i32, u16, u16, d]
         L.oracle_mla_expand.argtypes = [i32, i32, i32, d, u16, d]
         L.oracle_round_bf16.argtypes = [i64, d, u16]
+        L.oracle_set_threads.argtypes = [i32]
         for f in (L.oracle_attend, L.oracle_merge, L.oracle_mla_absorb,
-                  L.oracle_mla_expand, L.oracle_round_bf16, L.oracle_max_threads):
+                  L.oracle_mla_expand, L.oracle_round_bf16, L.oracle_max_threads, L.oracle_set_threads):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -150,3 +151,8 @@ def round_bf16(x) -> np.ndarray:
 
 def max_threads() -> int:
     return int(lib().oracle_max_threads())
+
+
+def set_threads(n: int):
+    """OpenMP threads of later oracle calls (timing only)."""
+    assert lib().oracle_set_threads(int(n)) == 0

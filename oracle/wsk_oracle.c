@@ -233,3 +233,13 @@ int oracle_max_threads(void)
     return 1;
 #endif
 }
+
+/* Threads of the following calls (timing only; results do not depend on it). */
+int oracle_set_threads(int n)
+{
+    if (n < 1) return -1;
+#ifdef _OPENMP
+    omp_set_num_threads(n);
+#endif
+    return 0;
+}
