@@ -22,13 +22,19 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (IEEE fp64: no fast-math)."""
+def build(force: bool = True, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc (IEEE fp64: no fast-math).  sanitize=True
+    builds it with clang's ASan and UBSan instead (the runtime the sanitized
+    HIP library uses, so that one process can load both)."""
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
-                               "-fno-fast-math", "-ffp-contract=off",
-                               "-o", tmp, _SRC, "-lm"])
+        if sanitize:
+            cc = ["/opt/rocm/llvm/bin/clang", "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+                  "-fno-omit-frame-pointer", "-g", "-fopenmp=libgomp"]
+        else:
+            cc = ["gcc", "-fopenmp"]
+        subprocess.check_call(cc + ["-O2", "-std=c11", "-fPIC", "-shared", "-fno-fast-math", "-ffp-contract=off",
+                                    "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 

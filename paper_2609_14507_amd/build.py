@@ -21,10 +21,24 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source into libwsk.so (always recompiles)."""
+# Host-code sanitizers (the device passes are unchanged): AddressSanitizer
+# and UndefinedBehaviorSanitizer, for the host-only cache path.  The library
+# then needs the clang ASan runtime loaded first (LD_PRELOAD of
+# libclang_rt.asan-x86_64.so), since the Python interpreter is not built
+# with it.
+SANITIZE_FLAGS = [
+    "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+    "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+    "-Xarch_host", "-g",
+]
+
+
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    """Compile every source into libwsk.so (always recompiles); sanitize=True
+    builds the host code with ASan and UBSan."""
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + [os.path.join(CSRC, s) for s in SOURCES] + ["-o", tmp]
+    cmd = [HIPCC] + FLAGS + (SANITIZE_FLAGS if sanitize else []) + [os.path.join(CSRC, s) for s in SOURCES] + \
+        ["-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -36,4 +50,4 @@ def build(verbose: bool = False) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose=True, sanitize="--sanitize" in sys.argv))
