@@ -671,7 +671,7 @@ def load_region_section(w, pf, steps_in, dev, flush, n_steps=5):
     B, H = len(pf.lengths), w.n_q_heads
     load_ends = [max(s, (L - D) // bk * bk) for s, L in zip(pf.splits, pf.lengths)]
     log("load region: routing the prefill (GPU share below the last %d positions pinned)" % D)
-    sess = DecodeSession(w, pf, 0, extra_tokens=D + 2, load_ends=load_ends, evict_tokens=D, pingpong_blocks=512,
+    sess = DecodeSession(w, pf, 0, extra_tokens=5 * D + 2, load_ends=load_ends, evict_tokens=D, pingpong_blocks=512,
                          arena_blocks=1024)
     info0 = wsk.wsk_load_stats(sess.h)
     q = to_device_bf16(steps_in[0].q, dev)
@@ -717,19 +717,22 @@ def load_region_section(w, pf, steps_in, dev, flush, n_steps=5):
     h2d_sparse = (wsk.wsk_load_stats(sess.h).h2d_bytes - h0) / n_steps
     # D-window eviction: one batch of D per sequence to the load region, then
     # (after D more appends) one to the CPU partition
-    d0 = wsk.wsk_load_stats(sess.h).d2h_bytes
-    t_fl = timed(lambda: sess.flush([wsk.PART_LOAD] * B), 1)
-    d_fl = wsk.wsk_load_stats(sess.h).d2h_bytes - d0
+    # (three of each; D more rows are appended to every sequence before each)
     if w.kind == wl.MLA:
         kn, vn = torch.zeros(B, w.row_elems, dtype=torch.bfloat16, device=dev), None
     else:
         kn = torch.zeros(B, w.n_kv_heads, w.head_dim, dtype=torch.bfloat16, device=dev)
         vn = torch.zeros_like(kn)
-    for _ in range(D):
-        sess.append(kn, vn)
-    d0 = wsk.wsk_load_stats(sess.h).d2h_bytes
-    t_fc = timed(lambda: sess.flush([wsk.PART_CPU] * B), 1)
-    d_fc = wsk.wsk_load_stats(sess.h).d2h_bytes - d0
+    fl_t, fl_b = {wsk.PART_LOAD: [], wsk.PART_CPU: []}, {wsk.PART_LOAD: [], wsk.PART_CPU: []}
+    for k, dest in enumerate([wsk.PART_LOAD, wsk.PART_CPU] * 3):
+        if k:
+            for _ in range(D):
+                sess.append(kn, vn)
+        d0 = wsk.wsk_load_stats(sess.h).d2h_bytes
+        fl_t[dest].append(timed(lambda: sess.flush([dest] * B), 1))
+        fl_b[dest].append(wsk.wsk_load_stats(sess.h).d2h_bytes - d0)
+    t_fl, d_fl = float(np.median(fl_t[wsk.PART_LOAD])), int(np.median(fl_b[wsk.PART_LOAD]))
+    t_fc, d_fc = float(np.median(fl_t[wsk.PART_CPU])), int(np.median(fl_b[wsk.PART_CPU]))
     info = wsk.wsk_load_stats(sess.h)
     sess.close()
 
@@ -746,6 +749,16 @@ def load_region_section(w, pf, steps_in, dev, flush, n_steps=5):
     micro = {"pinned_256MiB": round(ceiling, 2), "pageable_256MiB": round(h2d_gbs(256 << 20, pinned=False), 2)}
     for label, n in (("192KiB", 192 << 10), ("1MiB", 1 << 20), ("8MiB", 8 << 20), ("64MiB", 64 << 20)):
         micro["pinned_" + label] = round(h2d_gbs(n, reps=5), 2)
+
+    def d2h_gbs(nbytes, reps=5):   # device -> pinned host: the eviction direction
+        src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        src.fill_(1)
+        dst = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+        dst.copy_(src, non_blocking=True)
+        torch.cuda.synchronize()
+        return nbytes / timed(lambda: dst.copy_(src, non_blocking=True), reps) / 1e9
+    for label, n in (("8MiB", 8 << 20), ("256MiB", 256 << 20)):
+        micro["d2h_pinned_" + label] = round(d2h_gbs(n), 2)
     # 64 MiB as one DMA versus one DMA per 128 KiB block from scattered offsets
     blk = 128 << 10
     src = torch.empty(128 << 20, dtype=torch.uint8, pin_memory=True)
@@ -780,8 +793,9 @@ def load_region_section(w, pf, steps_in, dev, flush, n_steps=5):
                                   "per block, one DMA per buffer) plus the D-window blocks in place"},
         "flush": {"to_load": {"ms": round(t_fl * 1e3, 3), "bytes": int(d_fl), "gbs": round(d_fl / t_fl / 1e9, 2)},
                   "to_cpu": {"ms": round(t_fc * 1e3, 3), "bytes": int(d_fc), "gbs": round(d_fc / t_fc / 1e9, 2)},
-                  "what": "wsk_flush of one D = %d batch of every sequence; to the CPU includes the host's "
-                          "token-major rewrite" % D},
+                  "what": "wsk_flush of one D = %d batch of every sequence (median of 3 each, alternating); to "
+                          "the CPU includes the token-major rewrite (on the GPU) and the host's copy into the "
+                          "slots" % D},
         "pinning": {"pinned_bytes": int(info0.pinned_bytes), "arenas": int(info0.arenas),
                     "ms_per_MiB": round(info0.pin_seconds * 1e3 / max(info0.pinned_bytes / 2 ** 20, 1e-9), 4)},
         "transfer_micro_gbs": micro,

@@ -89,7 +89,9 @@ extern "C" {
  *   host_pool_blocks   slots in the CPU pool (pageable host memory), >= 0
  *   softmax_scale      multiplier of q.k before the softmax, finite and > 0
  *   evict_tokens       D, the eviction batch of wsk_flush (Sec. 4.2): a
- *                      multiple of block_tokens, or 0 (no eviction)
+ *                      multiple of block_tokens, or 0 (no eviction); a
+ *                      device cache with D > 0 pins, at init, a host bounce
+ *                      for one batch of every sequence (at most 64 MB)
  *   load_arena_blocks  load-region slots pinned by one host allocation; the
  *                      region is pinned arena by arena as it fills, one
  *                      arena ahead of use (Sec. 4.3 end, Sec. 5)
@@ -544,10 +546,15 @@ int wsk_decode_step_mla(wsk_cache *cache, int32_t n, const int32_t *seq_ids, con
  * order seq_ids lists them in), blocks ascending -- the order wsk_append
  * uses; a block that already has a slot there (the CPU slot of the block
  * holding s) keeps it.  The batch's GPU-pool slots are
- * freed.  To the load region the slots travel as device -> host DMA into
- * pinned memory, enqueued on stream (the layouts match); to the CPU the
- * rows are copied out on stream, the call waits for them, and the host
- * writes them token-major into the CPU pool.  The part chosen per batch is
+ * freed.  A kernel on stream first gathers the batch's slots, scattered
+ * in HBM, into the cache's device staging buffer in destination order.  To
+ * the load region they then travel unchanged (the layouts match) as one
+ * device -> host DMA per run of consecutive load slots, straight into the
+ * pinned slots.  To the CPU the same kernel rewrites them into the CPU
+ * pool's token-major rows; they are sent in ~2 MB pieces into a pinned
+ * bounce (pinned once, at wsk_init, for caches with evict_tokens > 0), and
+ * the host copies each piece's rows into their slots as soon as it lands;
+ * the call returns when they are in place.  The part chosen per batch is
  * the caller's: wsk_policy_route_batch gives the paper's roofline routing.
  * Later writes that reuse the freed slots must be ordered after this call on
  * stream.  seq_ids (distinct, open), part, moved: HOST arrays.  Needs

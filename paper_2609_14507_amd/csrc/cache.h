@@ -76,6 +76,7 @@ struct wsk_cache {
     uint16_t *hgather[2] = {nullptr, nullptr};     // pinned gather staging (sparse selections), on first use
     uint16_t *hbounce = nullptr;          // pinned bounce of evictions into the CPU pool
     size_t hbounce_bytes = 0;
+    hipEvent_t bounce_ev[8] = {};         // pieces of one eviction round landed in the bounce
     int64_t h2d_bytes = 0, d2h_bytes = 0; // load-region traffic since init
 };
 
@@ -187,6 +188,7 @@ int check_outputs(const void *q, const float *o, const float *lse, const float *
 uint16_t *load_slot_ptr(const wsk_cache *c, int32_t slot);
 int load_ensure(wsk_cache *c, const std::vector<Pending> &pend);   // pins the arenas new slots fall in
 int load_init(wsk_cache *c);                                       // ping-pong, streams, events
+int evict_init(wsk_cache *c);                                      // bounce of evictions to the CPU pool
 void load_destroy(wsk_cache *c);
 // Copies positions [p0, p1) of the host rows (layout as wsk_write's k/v,
 // row 0 = position pos0) into their load-region slots (GPU slot layout).

@@ -520,6 +520,39 @@ __global__ __launch_bounds__(256) void scatter_kernel(const ScatterParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// Eviction gather: whole GPU-pool slots into contiguous staging, unchanged
+// or as the CPU pool's token-major rows.  One 16-byte output piece per
+// thread and step; the writes are coalesced, the reads stay inside one slot.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void evict_kernel(const EvictParams p) {
+    const int64_t units = p.slot_elems / 8;           // 16-byte pieces per slot
+    const int64_t total = (int64_t)p.m * units;
+    const int bk = p.block_tokens;
+    const int row16 = p.row_elems / 8;
+    for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < total; u += (int64_t)gridDim.x * blockDim.x) {
+        const int j = (int)(u / units);
+        const int64_t x = u - (int64_t)j * units;
+        const uint16_t *src = p.pool + (int64_t)p.src_slot[j] * p.slot_elems;
+        u32x4 v;
+        if (!p.to_rows) {
+            v = reinterpret_cast<const u32x4 *>(src)[x];
+        } else if (p.kind == 1) {   // MLA: row r, piece c
+            const int r = (int)(x / row16), c = (int)(x - (int64_t)r * row16);
+            v = get_mla32(src, r, c);
+        } else {                     // GQA: head g, K or V, row r, piece k
+            const int per_head = 2 * bk * row16;
+            const int g = (int)(x / per_head);
+            int q = (int)(x - (int64_t)g * per_head);
+            const int which = q / (bk * row16);
+            q -= which * bk * row16;
+            const int r = q / row16, k = q - r * row16;
+            v = get_tiled(src + (int64_t)g * 2 * bk * p.row_elems, r, which, k);
+        }
+        reinterpret_cast<u32x4 *>(p.stage + (int64_t)j * p.slot_elems)[x] = v;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // MLA absorption and expansion: per head, a batch of up to 8 token rows times
 // a bf16 weight matrix, fp32 accumulation:
 //   absorb  q_lat[i][h][l] = sum_k q_nope[i][h][k] W_UK[h][k][l]  (bf16 out, one rounding)
@@ -740,6 +773,15 @@ hipError_t launch_scatter(const ScatterParams &p, hipStream_t s) {
     int64_t blocks = ((int64_t)p.m * per_pos + 255) / 256;
     if (blocks > 65536) blocks = 65536;
     hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_evict(const EvictParams &p, hipStream_t s) {
+    if (p.m <= 0) return hipSuccess;
+    if (p.m > kEvictMax) return hipErrorInvalidValue;
+    int64_t blocks = ((int64_t)p.m * (p.slot_elems / 8) + 255) / 256;
+    if (blocks > 2048) blocks = 2048;
+    hipLaunchKernelGGL(evict_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p);
     return hipGetLastError();
 }
 

@@ -14,6 +14,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <cstdlib>
 #include <cstring>
@@ -66,24 +67,6 @@ void put_position(const wsk_cache *c, uint16_t *slot, int off, const uint16_t *c
 }
 
 // The inverse: reads the rows of one position out of a slot of GPU layout.
-void get_position(const wsk_cache *c, const uint16_t *slot, int off, uint16_t *const *k, uint16_t *const *v) {
-    const int bk = c->spec.block_tokens;
-    if (c->spec.kind == WSK_KIND_MLA) {
-        const uint16_t *tile = slot + (int64_t)(off / 32) * kMlaTilePieces * kPiece;
-        const int u = off % 32;
-        for (int p = 0; p < (kLatent + kRope) / kPiece; ++p)
-            memcpy(k[0] + p * kPiece, tile + (int64_t)mla_piece(u, p) * kPiece, 16);
-        return;
-    }
-    const int t = off % 64;
-    for (int g = 0; g < c->spec.n_kv_heads; ++g) {
-        const uint16_t *tile = slot + ((int64_t)g * (bk / 64) + off / 64) * kGqaTilePieces * kPiece;
-        for (int j = 0; j < kHeadDim / kPiece; ++j) memcpy(k[g] + j * kPiece, tile + (int64_t)gqa_k_piece(t, j) * kPiece, 16);
-        const uint16_t *vt = tile + 1024 * kPiece;
-        for (int d = 0; d < kHeadDim; ++d) v[g][d] = vt[gqa_v_elem(t, d)];
-    }
-}
-
 int32_t arena_blocks(const wsk_cache *c) { return c->spec.load_arena_blocks; }
 int32_t sp_pingpong(const wsk_cache *c) { return c->spec.pingpong_blocks; }
 
@@ -124,25 +107,6 @@ int pin_arena(wsk_cache *c, size_t k) {
     c->pinned_bytes += (int64_t)bytes;
     c->arenas[k] = (uint16_t *)p;
     return WSK_OK;
-}
-
-// Writes the rows of positions [a, e) of sequence seq, read out of bounce
-// (GPU layout; block first_blk + j at slot j of bounce), token-major into
-// the CPU pool.
-void untile_to_cpu(wsk_cache *c, int32_t seq, int32_t a, int32_t e, const uint16_t *bounce, int32_t first_blk) {
-    const int bk = c->spec.block_tokens;
-    const int hkv = c->spec.kind == WSK_KIND_GQA ? c->spec.n_kv_heads : 1;
-    std::vector<uint16_t *> kp(hkv), vp(hkv);
-    for (int32_t p = a; p < e; ++p) {
-        const int32_t blk = p / bk;
-        const uint16_t *src = bounce + (int64_t)(blk - first_blk) * c->slot_elems;
-        uint16_t *dst = c->hpool + (int64_t)tab(c, WSK_PART_CPU, seq, blk) * c->slot_elems;
-        for (int g = 0; g < hkv; ++g) {
-            kp[g] = dst + row_offset(c, p, g, 0);
-            vp[g] = c->spec.kind == WSK_KIND_GQA ? dst + row_offset(c, p, g, 1) : nullptr;
-        }
-        get_position(c, src, p % bk, kp.data(), vp.data());
-    }
 }
 
 }  // namespace
@@ -199,6 +163,33 @@ int wsk::load_init(wsk_cache *c) {
     return WSK_OK;
 }
 
+// Blocks of one eviction round: what the device staging holds, at most
+// kEvictMax (the gather kernel's argument list).
+static size_t evict_round_blocks(const wsk_cache *c) {
+    return std::max<size_t>(1, std::min<size_t>(kEvictMax, kStageBytes / slot_bytes(c)));
+}
+
+// The pinned bounce that evictions to the CPU pool land in, sized for one
+// batch of every sequence (capped at one round), and its piece events:
+// allocated and touched here, so a flush does not pin memory on its way.
+int wsk::evict_init(wsk_cache *c) {
+    DeviceGuard guard(c->device);
+    if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
+    const int bk = c->spec.block_tokens;
+    const size_t blocks = std::min<size_t>(evict_round_blocks(c),
+                                           (size_t)c->spec.max_seqs * (size_t)(c->spec.evict_tokens / bk + 1));
+    const size_t bytes = blocks * slot_bytes(c);
+    hipError_t e = hipHostMalloc((void **)&c->hbounce, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) return hip_fail(e, "pinned eviction bounce");
+    c->hbounce_bytes = bytes;
+    memset(c->hbounce, 0, bytes);
+    for (hipEvent_t &ev : c->bounce_ev) {
+        e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+        if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+    }
+    return WSK_OK;
+}
+
 void wsk::load_destroy(wsk_cache *c) {
     if (c->device >= 0) {
         DeviceGuard guard(c->device);
@@ -214,6 +205,8 @@ void wsk::load_destroy(wsk_cache *c) {
         hipEvent_t evs[] = {c->filled[0], c->filled[1], c->consumed[0], c->consumed[1],
                             c->staged[0], c->staged[1], c->flush_ev};
         for (hipEvent_t ev : evs)
+            if (ev) (void)hipEventDestroy(ev);
+        for (hipEvent_t ev : c->bounce_ev)
             if (ev) (void)hipEventDestroy(ev);
         if (c->copy_stream) (void)hipStreamDestroy(c->copy_stream);
         for (uint16_t *a : c->arenas)
@@ -810,68 +803,102 @@ int wsk_flush(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *part, 
     hipStream_t st = (hipStream_t)stream;
     const size_t sb = slot_bytes(c);
     hipError_t e = hipSuccess;
-    // to the load region: device -> host DMA straight into the pinned slots
-    bool any_load = false;
-    for (int32_t i = 0; i < n && e == hipSuccess; ++i) {
-        if (part[i] != WSK_PART_LOAD || w1[i] == w0[i]) continue;
-        any_load = true;
-        const int32_t sq = ids[i];
-        // one DMA per run of blocks consecutive in both pools (and in one arena)
-        for (int32_t blk = w0[i] / bk; blk < w1[i] / bk && e == hipSuccess;) {
-            const int32_t ls = tab(c, WSK_PART_LOAD, sq, blk), gs = tab(c, WSK_PART_GPU, sq, blk);
-            int32_t r = 1;
-            while (blk + r < w1[i] / bk && tab(c, WSK_PART_LOAD, sq, blk + r) == ls + r &&
-                   tab(c, WSK_PART_GPU, sq, blk + r) == gs + r && (ls + r) % arena_blocks(c) != 0)
+    // the evicted blocks: destination slot, GPU-pool slot, first row held
+    // (rows below it belong to the CPU side of the block holding s)
+    struct Mv {
+        int32_t dst, src, lo;
+    };
+    std::vector<Mv> to_load, to_cpu;
+    for (int32_t i = 0; i < n; ++i)
+        for (int32_t blk = w0[i] / bk; blk < w1[i] / bk; ++blk) {
+            const Mv m{tab(c, part[i], ids[i], blk), tab(c, WSK_PART_GPU, ids[i], blk), std::max(w0[i] - blk * bk, 0)};
+            (part[i] == WSK_PART_LOAD ? to_load : to_cpu).push_back(m);
+        }
+    const auto by_dst = [](const Mv &x, const Mv &y) { return x.dst < y.dst; };
+    std::sort(to_load.begin(), to_load.end(), by_dst);
+    std::sort(to_cpu.begin(), to_cpu.end(), by_dst);
+    // blocks gathered per round into the device staging buffer, in
+    // destination order (one kernel for all of them, HBM-resident slots are
+    // scattered), then sent device -> host
+    const size_t cap = evict_round_blocks(c);
+    const auto gather = [&](const std::vector<Mv> &v, size_t j0, size_t m, bool rows) {
+        EvictParams ep{};
+        ep.pool = c->dpool;
+        ep.stage = c->dstage;
+        ep.slot_elems = c->slot_elems;
+        ep.m = (int32_t)m;
+        ep.kind = c->spec.kind;
+        ep.n_kv_heads = c->spec.kind == WSK_KIND_GQA ? c->spec.n_kv_heads : 1;
+        ep.block_tokens = bk;
+        ep.row_elems = c->row_elems;
+        ep.to_rows = rows;
+        for (size_t k = 0; k < m; ++k) ep.src_slot[k] = v[j0 + k].src;
+        return launch_evict(ep, st);
+    };
+    // to the load region (same slot layout): one DMA per run of consecutive
+    // load slots of one arena, straight into the pinned slots
+    for (size_t j0 = 0; j0 < to_load.size() && e == hipSuccess; j0 += cap) {
+        const size_t m = std::min(cap, to_load.size() - j0);
+        e = gather(to_load, j0, m, false);
+        for (size_t j = 0; j < m && e == hipSuccess;) {
+            size_t r = j + 1;
+            while (r < m && to_load[j0 + r].dst == to_load[j0 + r - 1].dst + 1 &&
+                   to_load[j0 + r].dst % arena_blocks(c) != 0)
                 ++r;
-            e = hipMemcpyAsync(load_slot_ptr(c, ls), c->dpool + (int64_t)gs * c->slot_elems, r * sb,
-                               hipMemcpyDeviceToHost, st);
-            c->d2h_bytes += (int64_t)(r * sb);
-            blk += r;
+            e = hipMemcpyAsync(load_slot_ptr(c, to_load[j0 + j].dst), c->dstage + (int64_t)j * c->slot_elems,
+                               (r - j) * sb, hipMemcpyDeviceToHost, st);
+            c->d2h_bytes += (int64_t)((r - j) * sb);
+            j = r;
         }
     }
-    if (any_load && e == hipSuccess) e = hipEventRecord(c->flush_ev, st);
-    // to the CPU pool: device -> host into the pinned bounce, then the host
-    // writes the rows token-major
-    size_t cpu_blocks = 0;
-    for (int32_t i = 0; i < n; ++i)
-        if (part[i] == WSK_PART_CPU) cpu_blocks += (size_t)(w1[i] / bk - w0[i] / bk);
-    if (cpu_blocks && e == hipSuccess) {
-        const size_t bytes = cpu_blocks * sb;
-        if (c->hbounce_bytes < bytes) {
+    if (!to_load.empty() && e == hipSuccess) e = hipEventRecord(c->flush_ev, st);
+    // to the CPU pool: rewritten into its token-major rows by the same
+    // kernel and sent into the pinned bounce in pieces of ~2 MB, each piece's
+    // rows copied into their slots on the host's threads as soon as it has
+    // landed, while the next pieces are still on the link
+    if (!to_cpu.empty() && e == hipSuccess) {
+        const size_t bytes = std::min(cap, to_cpu.size()) * sb;
+        if (c->hbounce_bytes < bytes) {   // more blocks than one batch of every sequence
             if (c->hbounce) (void)hipHostFree(c->hbounce);
             c->hbounce = nullptr;
             c->hbounce_bytes = 0;
             e = hipHostMalloc((void **)&c->hbounce, bytes, hipHostMallocDefault);
             if (e == hipSuccess) c->hbounce_bytes = bytes;
         }
-        size_t at = 0;
-        for (int32_t i = 0; i < n && e == hipSuccess; ++i) {
-            if (part[i] != WSK_PART_CPU) continue;
-            for (int32_t blk = w0[i] / bk; blk < w1[i] / bk && e == hipSuccess; ++blk, ++at) {
-                e = hipMemcpyAsync(c->hbounce + (int64_t)at * c->slot_elems,
-                                   c->dpool + (int64_t)tab(c, WSK_PART_GPU, ids[i], blk) * c->slot_elems, sb,
-                                   hipMemcpyDeviceToHost, st);
-                c->d2h_bytes += (int64_t)sb;
+        const bool mla = c->spec.kind == WSK_KIND_MLA;
+        const int runs = mla ? 1 : 2 * c->spec.n_kv_heads;   // (head, K | V) row runs per slot
+        const size_t n_ev = sizeof(c->bounce_ev) / sizeof(c->bounce_ev[0]);
+        for (size_t j0 = 0; j0 < to_cpu.size() && e == hipSuccess; j0 += cap) {
+            const size_t m = std::min(cap, to_cpu.size() - j0);
+            const size_t per = std::max((m + n_ev - 1) / n_ev, std::max<size_t>(1, (2u << 20) / sb));
+            e = gather(to_cpu, j0, m, true);
+            size_t pieces = 0;
+            for (size_t a = 0; a < m && e == hipSuccess; a += per, ++pieces) {
+                const size_t k = std::min(per, m - a);
+                e = hipMemcpyAsync(c->hbounce + (int64_t)a * c->slot_elems, c->dstage + (int64_t)a * c->slot_elems,
+                                   k * sb, hipMemcpyDeviceToHost, st);
+                if (e == hipSuccess) e = hipEventRecord(c->bounce_ev[pieces], st);
             }
+            // one parallel region for the round: the tasks are the blocks in
+            // bounce order, and each waits for its piece's event first
+            std::atomic<int> bad{0};
+            if (e == hipSuccess)
+                parallel_tasks((int)m, gather_threads(), [&](int t) {
+                    if (hipEventSynchronize(c->bounce_ev[t / per]) != hipSuccess) {
+                        bad = 1;
+                        return;
+                    }
+                    const Mv &mv = to_cpu[j0 + t];
+                    const int64_t off = (int64_t)mv.lo * c->row_elems, len = (int64_t)(bk - mv.lo) * c->row_elems;
+                    for (int r = 0; r < runs; ++r) {
+                        const int64_t base = (int64_t)r * bk * c->row_elems + off;
+                        memcpy(c->hpool + (int64_t)mv.dst * c->slot_elems + base,
+                               c->hbounce + (int64_t)t * c->slot_elems + base, (size_t)len * 2);
+                    }
+                });
+            if (e == hipSuccess && bad) e = hipErrorUnknown;
+            if (e == hipSuccess) c->d2h_bytes += (int64_t)(m * sb);
         }
-        if (e == hipSuccess) e = hipStreamSynchronize(st);
-        // one task per evicted block: rows [max(w0, blk Bk), (blk + 1) Bk)
-        struct Task {
-            int32_t seq, a, e;
-            size_t at;
-        };
-        std::vector<Task> tasks;
-        at = 0;
-        for (int32_t i = 0; i < n; ++i) {
-            if (part[i] != WSK_PART_CPU) continue;
-            for (int32_t blk = w0[i] / bk; blk < w1[i] / bk; ++blk, ++at)
-                tasks.push_back({ids[i], std::max(w0[i], blk * bk), (blk + 1) * bk, at});
-        }
-        if (e == hipSuccess)
-            parallel_tasks((int)tasks.size(), gather_threads(), [&](int t) {
-                const Task &k = tasks[t];
-                untile_to_cpu(c, k.seq, k.a, k.e, c->hbounce + (int64_t)k.at * c->slot_elems, k.a / bk);
-            });
     }
     // the batch now lives in its new home: free the GPU-pool slots, extend
     // the segments, move the window

@@ -306,6 +306,15 @@ int wsk_init(const wsk_partition_spec *spec, int device, wsk_cache **out) {
             return rc;
         }
     }
+    if (device >= 0 && spec->evict_tokens > 0) {
+        rc = evict_init(c);
+        if (rc) {
+            const std::string msg = g_err;
+            wsk_destroy(c);
+            g_err = msg;
+            return rc;
+        }
+    }
     if (spec->load_pool_blocks > 0) {
         rc = load_init(c);
         if (rc) {

@@ -137,6 +137,25 @@ struct ScatterParams {
     int32_t row_elems;
 };
 
+// Eviction gather: copies whole GPU-pool slots src_slot[0 .. m) into a
+// contiguous device staging buffer (slot j at j * slot_elems), either
+// unchanged (to_rows = 0: the load region keeps the GPU slot layout) or
+// rewritten into the CPU pool's token-major rows (to_rows = 1: GQA
+// [n_kv_heads][K | V][block_tokens][128], MLA [block_tokens][576]).
+constexpr int kEvictMax = 256;
+struct EvictParams {
+    const uint16_t *pool;
+    uint16_t *stage;
+    int64_t slot_elems;
+    int32_t m;
+    int32_t kind;
+    int32_t n_kv_heads;
+    int32_t block_tokens;
+    int32_t row_elems;
+    int32_t to_rows;
+    int32_t src_slot[kEvictMax];
+};
+
 // In-place CPU attention over host-pool rows (cpu_attend.cpp).
 struct CpuAttendArgs {
     const uint16_t *pool;          // host pool base
@@ -172,6 +191,7 @@ hipError_t launch_step_combine(const StepCombineParams &p, int width, hipStream_
 hipError_t launch_step_expand(const StepExpandParams &p, hipStream_t s);
 hipError_t launch_append(const AppendParams &p, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
+hipError_t launch_evict(const EvictParams &p, hipStream_t s);
 hipError_t launch_merge(int32_t rows, int32_t width, const float *o_a, const float *lse_a,
                         const float *o_b, const float *lse_b, float *o_out, float *lse_out,
                         uint16_t *o_bf16, hipStream_t s);
