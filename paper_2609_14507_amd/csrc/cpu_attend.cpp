@@ -272,18 +272,31 @@ __attribute__((target("avx512f,avx512bw,avx512bf16"))) void run_item_bf16(const 
             else
                 krow[t] = vrow[t] = zero_row;
         }
-        // prefetch the next tile's rows: a KV head's rows come in runs of one
-        // block, a slot apart, which the hardware prefetchers (page-bound)
-        // pick up late; one tile ahead nearly halves the time from DRAM
+        // prefetch: the next tile's rows into L1 and the rows one block ahead
+        // into L2.  A KV head's rows come in runs of one block a slot apart,
+        // which the hardware prefetchers pick up late; the L2 stream keeps
+        // the L1 prefetches short (measured on the GPU machines' hosts: 15.0 ->
+        // 17.0 GB/s on one thread, +3-20 % on 16, against L1 only)
         {
-            const int tp = t0 + 16;
+            const int tq = t0 + 16;
+            const int nq = std::min(16, it.b - tq);
+            for (int t = 0; t < nq; ++t) {
+                const uint16_t *pk, *pv;
+                rows_of(x, it.i, it.g, tq + t, pk, pv);
+                for (int off = 0; off < dk * 2; off += 64) _mm_prefetch((const char *)pk + off, _MM_HINT_T0);
+                if (!x.mla)
+                    for (int off = 0; off < dv * 2; off += 64) _mm_prefetch((const char *)pv + off, _MM_HINT_T0);
+            }
+        }
+        {
+            const int tp = t0 + x.block_tokens;
             const int np = std::min(16, it.b - tp);
             for (int t = 0; t < np; ++t) {
                 const uint16_t *pk, *pv;
                 rows_of(x, it.i, it.g, tp + t, pk, pv);
-                for (int off = 0; off < dk * 2; off += 64) _mm_prefetch((const char *)pk + off, _MM_HINT_T0);
+                for (int off = 0; off < dk * 2; off += 64) _mm_prefetch((const char *)pk + off, _MM_HINT_T1);
                 if (!x.mla)
-                    for (int off = 0; off < dv * 2; off += 64) _mm_prefetch((const char *)pv + off, _MM_HINT_T0);
+                    for (int off = 0; off < dv * 2; off += 64) _mm_prefetch((const char *)pv + off, _MM_HINT_T1);
             }
         }
         // K tile -> dim pairs x tokens
