@@ -3,11 +3,12 @@
 The headline workload is the largest single-GPU configuration: the ragged
 1M-token aggregate (Qwen3-30B-A3B attention shape, 8 sequences of 98K-164K
 tokens, per-sequence CPU shares of 10-60 %), run as its 64 decode steps.  One
-step = the whole hot path over one batch (wsk_decode_step): the new token's
-K/V of every sequence is routed to its GPU partition, split-KV attention
-covers the GPU range written so far (pass 1), then one pass 2 scores and
+step = the whole hot path over one batch (wsk_decode_step, one kernel launch
+for GQA): the new token's K/V of every sequence is routed to its GPU
+partition, split-KV attention covers the GPU range written so far (pass 1),
+and the last workgroup of each (sequence, KV head, head group) scores and
 merges the new token, stores it into the pool, and merges the chunk partials
-and the CPU-range partial by their LSE.  The W warmup steps append the last W
+and the CPU-range partial by their LSE (pass 2).  The W warmup steps append the last W
 rows of the drawn context, so the K timed steps start exactly at the drawn
 lengths.  Inputs are seeded synthetic tensors already resident in HBM; the
 CPU-range partial fed to the merge is a seeded synthetic (O, LSE) pair (the
@@ -30,13 +31,14 @@ the difference (from the flushes' mean) over K.  Events are not recorded
 between the steps: each record leaves the GPU idle for ~5 us, which a
 per-step pair would count as step time.  The pass-1 kernel alone (the
 roofline's kernel) is timed the same way, K (flush + pass 1) pairs less K
-flushes.  More steps, each between its own pair of events, give the per-step
+flushes; for GQA the step itself is one launch of the step kernel, which is
+then the roofline's kernel.  More steps, each between its own pair of events, give the per-step
 median, p10 and p90 (each with one event's idle time in it); more diagnostic
 steps run the pieces as separate calls with events between them.  The
 algorithmic bytes of a step are the bf16 K and V rows (MLA: latent rows) of
 every attended position, read once.
 
-Every pass-1 kernel dispatch this process issues is counted per kernel, in
+Every KV-streaming kernel dispatch this process issues is counted per kernel, in
 order ("dispatch_windows"), so that a rocprofv3 trace of the same command can
 be split by section: `python bench.py --trace-summary DIR --bench-json FILE`
 prints, per section, the profiler's mean kernel time (and HBM counters, for a
@@ -93,29 +95,32 @@ def gqa_heads_per_workgroup(group: int) -> int:
 
 
 class Dispatches:
-    """Pass-1 kernel dispatches issued so far, per kernel, in order.  Every
-    pass-1 call of the decode workloads here covers at most 64 sequences with a
-    non-empty range, i.e. exactly one dispatch."""
+    """Dispatches of the KV-streaming kernels issued so far, per kernel, in
+    order.  Every call of the decode workloads here covers at most 64
+    sequences, i.e. exactly one dispatch: a GQA decode step (no load region)
+    is one gqa_step_kernel launch (pass 1 with pass 2 in its last
+    workgroups); pass 1 alone, and every MLA pass 1, one attend-kernel
+    launch."""
 
     def __init__(self):
         self.n = {}
 
     @staticmethod
-    def key(w) -> str:
+    def key(w, step: bool = False) -> str:
         from paper_2609_14507_amd import workloads as wl
         if w.kind == wl.MLA:
             return "mla_attend_kernel"
-        return "gqa_attend_kernel<%d>" % gqa_heads_per_workgroup(w.group)
+        return "gqa_%s_kernel<%d>" % ("step" if step else "attend", gqa_heads_per_workgroup(w.group))
 
-    def at(self, w) -> int:
-        return self.n.get(self.key(w), 0)
+    def at(self, w, step: bool = False) -> int:
+        return self.n.get(self.key(w, step), 0)
 
-    def add(self, w, k: int):
-        self.n[self.key(w)] = self.at(w) + k
+    def add(self, w, k: int, step: bool = False):
+        self.n[self.key(w, step)] = self.at(w, step) + k
 
-    def part(self, w, first: int):
-        """[first, count] of the dispatches of w's kernel since `first`."""
-        return [first, self.at(w) - first]
+    def part(self, w, first: int, step: bool = False):
+        """[first, count, kernel] of the dispatches of w's kernel since `first`."""
+        return [first, self.at(w, step) - first, self.key(w, step)]
 
 
 def wsk_mod():
@@ -149,8 +154,8 @@ TRAFFIC = {
 }
 
 
-def roofline(section, kernel, achieved_gbs, kv_bytes):
-    """Roofline entry of the pass-1 kernel (the one that streams the KV)."""
+def roofline(section, kernel, achieved_gbs, kv_bytes, what="pass 1"):
+    """Roofline entry of the kernel that streams the KV."""
     traffic = None
     t = TRAFFIC.get(section)
     if t is not None:
@@ -159,7 +164,7 @@ def roofline(section, kernel, achieved_gbs, kv_bytes):
                 traffic = t["fetch_bytes"] + t["write_bytes"]
     out = {
         "bound": "hbm",
-        "kernel": "%s (pass 1)" % kernel,
+        "kernel": "%s (%s)" % (kernel, what),
         "achieved": round(achieved_gbs, 1),
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
@@ -246,10 +251,11 @@ def decode_section(w, K, W, timer, disp, dev, tag, with_cpu_engine=False, keep=F
 
     def step(i, ev=None, parts=None):
         """One decode step.  ev = (start, end) events around the step: the timed
-        steps run it as wsk_decode_step (pass 1 over the positions written so
-        far, then one pass 2 that folds in the appended row, stores it and
-        merges the CPU partial; MLA: wsk_decode_step_mla, whose pass 2 also
-        expands the merged latent output by W_UV).  parts = 5 events around its
+        steps run it as wsk_decode_step (GQA: one launch, pass 1 over the
+        positions written so far with pass 2 -- the appended row scored,
+        merged and stored, the CPU partial merged -- in its last workgroups;
+        MLA: wsk_decode_step_mla, pass 1 then a pass 2 that also expands the
+        merged latent output by W_UV).  parts = 5 events around its
         pieces (diagnostic steps only, every event record costs GPU time of its
         own): those run the same work as separate calls -- append, pass 1 over
         [s, L + 1), pass 2 -- so that pass 1 is timed on its own."""
@@ -276,18 +282,21 @@ def decode_section(w, K, W, timer, disp, dev, tag, with_cpu_engine=False, keep=F
             mark(4)
         if ev:
             ev[1].record(stream)
-        disp.add(w, 1)
+        disp.add(w, 1, step=fused and not parts)
 
     def kv_bytes():   # algorithmic bytes of the next step: [s_b, L_b + 1) of every sequence
         return sum((sess.lengths[b] + 1 - min(splits[b], sess.lengths[b])) * w.token_bytes for b in range(B))
 
-    win = {"kernel": disp.key(w)}
+    # a GQA step is one launch of the step kernel, the roofline's kernel;
+    # an MLA step's KV-streaming kernel is its pass 1
+    fused = not mla
+    win = {"kernel": disp.key(w, fused)}
     log("%s: %d warmup + %d timed steps" % (tag, W, K))
-    d0 = disp.at(w)
+    d0 = disp.at(w, fused)
     for i in range(W):
         step(i)
     torch.cuda.synchronize()
-    win["warmup"] = disp.part(w, d0)
+    win["warmup"] = disp.part(w, d0, fused)
     assert list(sess.lengths) == list(pf.lengths)
     contexts = list(sess.lengths)
     nbytes = []
@@ -298,9 +307,9 @@ def decode_section(w, K, W, timer, disp, dev, tag, with_cpu_engine=False, keep=F
             step(W + k)
     t_flush_a = timer.flushes_ms(K)
     t0 = time.perf_counter()
-    d0 = disp.at(w)
+    d0 = disp.at(w, fused)
     t_steps = timer.bracket(timed_steps)
-    win["timed_steps"] = disp.part(w, d0)
+    win["timed_steps"] = disp.part(w, d0, fused)
     wall = time.perf_counter() - t0
     t_flush = 0.5 * (t_flush_a + timer.flushes_ms(K))   # flushes timed before and after: drift cancels
     step_ms = (t_steps - t_flush) / K
@@ -322,11 +331,11 @@ def decode_section(w, K, W, timer, disp, dev, tag, with_cpu_engine=False, keep=F
     # the per-step distribution: steps each between their own pair of events
     # (each pair counts one event's idle time, ~5.5 us, as step time)
     ev_step = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(EVENT_STEPS)]
-    d0 = disp.at(w)
+    d0 = disp.at(w, fused)
     for k in range(EVENT_STEPS):
         step(W + K + k, ev=ev_step[k])
     torch.cuda.synchronize()
-    win["event_pairs"] = disp.part(w, d0)
+    win["event_pairs"] = disp.part(w, d0, fused)
     ev_us = np.array([e[0].elapsed_time(e[1]) for e in ev_step]) * 1e3
 
     ev_part = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(DIAG_STEPS)]
@@ -361,8 +370,9 @@ def decode_section(w, K, W, timer, disp, dev, tag, with_cpu_engine=False, keep=F
             "kv_bytes_per_step": int(nbytes.mean()),
             "step": ("absorb + wsk_decode_step_mla (attend pass 1 over [s, L), then one pass 2: the appended row "
                      "scored, merged and stored, chunk combine, LSE merge with the CPU partial, expansion by W_UV)"
-                     if mla else "wsk_decode_step: attend pass 1 over [s, L), then one pass 2: the appended row "
-                     "scored, merged and stored, chunk combine, LSE merge with the CPU partial"),
+                     if mla else "wsk_decode_step, one launch: attend pass 1 over [s, L); the last workgroup of "
+                     "each (sequence, KV head, head group) scores, merges and stores the appended row, combines "
+                     "the chunks and merges the CPU partial by LSE"),
             "cache_flush_between_steps": not timer.no_flush,
         },
         "steps": K, "warmup": W,
@@ -374,6 +384,7 @@ def decode_section(w, K, W, timer, disp, dev, tag, with_cpu_engine=False, keep=F
             "flush_plus_step": round(t_steps / K * 1e3, 2),
             "flush": round(t_flush / K * 1e3, 2),
             "pass1_kernel": round(p1_kernel_ms * 1e3, 2),
+            "pass1_kv_bytes": int(p1_bytes),
             "step_event_pairs": {"median": round(float(np.median(ev_us)), 2),
                                  "p10": round(float(np.percentile(ev_us, 10)), 2),
                                  "p90": round(float(np.percentile(ev_us, 90)), 2),
@@ -388,7 +399,8 @@ def decode_section(w, K, W, timer, disp, dev, tag, with_cpu_engine=False, keep=F
             **({"expand": round(float(exp_ms.mean() * 1e3), 2)} if mla else {}),
             "attend_gbs": round(att_gbs, 1),
         },
-        "roofline": roofline(tag, disp.key(w), p1_gbs, p1_bytes),
+        "roofline": (roofline(tag, disp.key(w), p1_gbs, p1_bytes) if mla else
+                     roofline(tag, disp.key(w, True), value, float(nbytes.mean()), "the whole step")),
         "dispatch_window": win,
         "_ms_per_step": float(step_ms),
     }
@@ -919,30 +931,41 @@ def trace_summary(trace_dir, bench_json):
         sel = [r for r in rows if (key + "(") in r["Kernel_Name"]]
         return sorted(sel, key=lambda r: int(r["Dispatch_Id"]))
 
+    # per section: its windows, and per part the algorithmic KV bytes of one
+    # dispatch and bench.py's own time of it (event-timed parts only)
     sections = []
     for name, sec in [("headline", out)] + sorted(out.get("configs", {}).items()):
         win = sec.get("dispatch_window")
         if not win:
             continue
         if "timed_steps" in win:
-            sections.append((name, sec["workload"], win["kernel"], win, sec["roofline"]["kv_bytes_per_launch"],
-                             sec["breakdown_us"]["pass1_kernel"]))
+            bd = sec["breakdown_us"]
+            kv_step = sec["config"]["kv_bytes_per_step"]
+            kv_p1 = bd.get("pass1_kv_bytes", sec["roofline"]["kv_bytes_per_launch"])
+            kv = {"timed_steps": kv_step, "event_pairs": kv_step, "diagnostic": kv_step, "pass1_alone": kv_p1}
+            us = {"pass1_alone": bd["pass1_kernel"]}
+            if "step" in win["kernel"]:
+                us["timed_steps"] = bd["step"]
+            sections.append((name, win["kernel"], win, kv, us))
         for label, sub in sorted(win.items()):
             if isinstance(sub, dict):
                 pt = [p for p in sec["sweep"] if "r=%.2f" % p["cpu_share"] == label][0]
-                sections.append(("%s %s" % (name, label), sec["workload"], win["kernel"], sub,
-                                 pt["roofline"]["kv_bytes_per_launch"], pt["pass1_us"]))
+                kvp = pt["roofline"]["kv_bytes_per_launch"]
+                sections.append(("%s %s" % (name, label), win["kernel"], sub, {"timed_steps": kvp, "pass1_alone": kvp},
+                                 {"pass1_alone": pt["pass1_us"]}))
     lines = []
     if trace:
         lines += ["| section | kernel | part | dispatches | mean us | min us | max us | KV MB per launch | "
-                  "TB/s at mean | % of 8 TB/s | bench.py pass-1 us |", "|---|---|---|---|---|---|---|---|---|---|---|"]
+                  "TB/s at mean | % of 8 TB/s | bench.py us |", "|---|---|---|---|---|---|---|---|---|---|---|"]
         cache = {}
-        for name, wl_name, key, win, kvb, bench_us in sections:
-            d = cache.setdefault(key, per_kernel(trace, key))
+        for name, kernel, win, kv, bench_us in sections:
             for part in ("timed_steps", "pass1_alone", "event_pairs", "diagnostic"):
                 if part not in win:
                     continue
-                a, n = win[part]
+                a, n = win[part][:2]
+                key = win[part][2] if len(win[part]) > 2 else kernel
+                kvb = kv[part]
+                d = cache.setdefault(key, per_kernel(trace, key))
                 us = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in d[a:a + n]]
                 if len(us) != n:
                     lines.append("| %s | %s | %s | %d of %d found | | | | | | | |" % (name, key, part, len(us), n))
@@ -950,7 +973,7 @@ def trace_summary(trace_dir, bench_json):
                 m = float(np.mean(us))
                 lines.append("| %s | %s | %s | %d | %.2f | %.2f | %.2f | %.1f | %.2f | %.1f | %s |"
                              % (name, key, part, n, m, min(us), max(us), kvb / 1e6, kvb / (m * 1e-6) / 1e12,
-                                100 * kvb / (m * 1e-6) / 8e12, bench_us if part == "pass1_alone" else ""))
+                                100 * kvb / (m * 1e-6) / 8e12, bench_us.get(part, "")))
     if counters:
         names = sorted({r["Counter_Name"] for r in counters})
         copies = [r for r in counters if "__amd_rocclr_copyBuffer" in r["Kernel_Name"]]
@@ -960,11 +983,13 @@ def trace_summary(trace_dir, bench_json):
                       for c in names)), "",
                   "| section | kernel | part | dispatches | " + " | ".join(names) + " | KV MB per launch |",
                   "|---|---|---|---|" + "---|" * len(names) + "---|"]
-        for name, wl_name, key, win, kvb, _ in sections:
+        for name, kernel, win, kv, _ in sections:
             for part in ("timed_steps", "pass1_alone"):
                 if part not in win:
                     continue
-                a, n = win[part]
+                a, n = win[part][:2]
+                key = win[part][2] if len(win[part]) > 2 else kernel
+                kvb = kv[part]
                 vals = []
                 for c in names:
                     d = per_kernel([r for r in counters if r["Counter_Name"] == c], key)[a:a + n]

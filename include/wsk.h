@@ -477,10 +477,15 @@ int wsk_attend_gpu_pass2(wsk_cache *cache, int32_t n, const int32_t *seq_ids, co
  * sequence's new row at position L (as wsk_append), then every query head
  * attends all its GPU-side positions [.., L] -- the new row included -- and
  * the result is merged with o_x / lse_x when given (as wsk_attend_gpu).
- * Same result as wsk_append followed by wsk_attend_gpu, in one launch less:
- * pass 1 covers the positions written before the call, and pass 2 scores the
- * new row straight from k_new (q . k_new), merges it as one more partial and
- * stores it into the GPU pool.  seq_ids: HOST array of n > 0 distinct open
+ * Same result as wsk_append followed by wsk_attend_gpu: pass 1 covers the
+ * positions written before the call, and pass 2 scores the new row straight
+ * from k_new (q . k_new), merges it as one more partial and stores it into
+ * the GPU pool.  GQA without load-region positions: one kernel launch per 64
+ * sequences, pass 2 done by the last workgroup of each (sequence, KV head,
+ * head group) to finish its pass-1 chunk (counted with device-scope atomics
+ * on counters the cache keeps, which are back at zero after every launch, so
+ * two steps on one cache must not overlap in time); otherwise pass 1 and
+ * pass 2 are separate launches.  seq_ids: HOST array of n > 0 distinct open
  * sequences; q, k_new, v_new, o_x, lse_x, o, lse, ws: DEVICE pointers laid out
  * as for wsk_append and wsk_attend_gpu; ws of at least
  * wsk_decode_step_workspace() bytes, queried before the call (it does not

@@ -31,17 +31,21 @@
 // chunk with their own online softmax and are merged through LDS at the end.
 // Each wavefront issues the next tile's K loads as soon as QK has consumed
 // the current ones, and the next V loads right after P.V.
+//
+// gqa_step_kernel is the same pass 1 with a decode step's pass 2 folded in
+// (Sec. 4.2: one LSE join per step): the last workgroup of each (sequence,
+// KV head, head group) to finish -- counted with a device-scope atomic after
+// a device-scope fence -- merges the chunk partials of its heads with the
+// step's new token and the CPU partial and stores the new row into the pool.
+// The step then costs one launch instead of two.
 
-#include "wsk_internal.h"
+#include "device_rows.h"
 
 namespace wsk {
 namespace {
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(4))) float f32x4;
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
-
 constexpr int kWaves = 4;
+constexpr int kTailW = 64;   // chunk weights per head the step's last workgroup keeps in LDS
 constexpr int kTileBytes = 2 * kTile * kHeadDim * 2;   // K and V pieces of one 64-token tile: 32 KB
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -52,8 +56,175 @@ __device__ __forceinline__ int tile_token(int mt, int r) {
     return 32 * (mt >> 1) + 8 * (r >> 2) + 4 * (mt & 1) + (r & 3);
 }
 
+// A load that sees what another XCD stored device-coherent in this launch.
+__device__ __forceinline__ float coherent_load(const float *a) {
+    return __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// What pass 2 of a decode step reads besides the chunk partials, for heads
+// h0 .. h0 + GH - 1 of launch-local sequence i (KV head g): loaded by every
+// workgroup before it is counted, so that these loads overlap the wait for
+// its partial stores; only the last workgroup uses them.
 template <int GH>
-__global__ __launch_bounds__(256, 2) void gqa_attend_kernel(const AttendParams p) {
+struct TailIn {
+    static constexpr int kItems = (GH * 32 + 255) / 256;           // float4 output columns per thread
+    static constexpr int kHeads = (GH + kWaves - 1) / kWaves;      // heads scored per wavefront
+    uint32_t kw;                 // k_new[2 lane .. 2 lane + 1]
+    uint32_t qw[kHeads];         // q of head wave + 4 k, same two dims
+    float lx[kHeads];            // lse_x of that head
+    uint2 vn[kItems];            // v_new columns 4 c4 .. 4 c4 + 3
+    f32x4 ox[kItems];            // o_x of (head, column) item
+    u32x4 piece;                 // 16-byte piece of the new K/V row this thread stores
+};
+
+template <int GH>
+__device__ __forceinline__ TailIn<GH> tail_load(const AttendParams &p, const StepTail &t, int i, int g, int h0) {
+    TailIn<GH> in;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int H = p.n_q_heads;
+    const int64_t kv_row = ((int64_t)i * p.n_kv_heads + g) * kHeadDim;
+    in.kw = reinterpret_cast<const uint32_t *>(t.k_new + kv_row)[lane];
+#pragma unroll
+    for (int k = 0; k < TailIn<GH>::kHeads; ++k) {
+        const int hh = wave + kWaves * k;
+        in.qw[k] = 0u;
+        in.lx[k] = -INFINITY;
+        if (hh < GH) {
+            const int h = h0 + hh;
+            in.qw[k] = reinterpret_cast<const uint32_t *>(p.q + (int64_t)i * p.q_row + (int64_t)h * kHeadDim)[lane];
+            if (t.lse_x) in.lx[k] = t.lse_x[(int64_t)i * H + h];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < TailIn<GH>::kItems; ++j) {
+        const int idx = threadIdx.x + 256 * j;
+        in.vn[j] = uint2{0u, 0u};
+        in.ox[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (idx < GH * 32) {
+            const int hh = idx >> 5, c4 = idx & 31;
+            in.vn[j] = reinterpret_cast<const uint2 *>(t.v_new + kv_row)[c4];
+            if (t.o_x) in.ox[j] = reinterpret_cast<const f32x4 *>(t.o_x + ((int64_t)i * H + h0 + hh) * kHeadDim)[c4];
+        }
+    }
+    in.piece = u32x4{0u, 0u, 0u, 0u};
+    if (threadIdx.x < 32)
+        in.piece = reinterpret_cast<const u32x4 *>((threadIdx.x >> 4 ? t.v_new : t.k_new) + kv_row)[threadIdx.x & 15];
+    return in;
+}
+
+// Pass 2 of a decode step for heads h0 .. h0 + GH - 1 of launch-local
+// sequence i (KV head g, head group hg), by the workgroup that finished the
+// last of its nc chunk partials (partials pb .. pb + nc - 1, all visible).
+// Same arithmetic as the separate pass-2 kernel: the new token enters as a
+// partial of one key (score q . k_new * scale, value v_new), the CPU partial
+// as one more; weights exp(lse - max), natural-log domain.  The first
+// kTailRegs partials of every output column are loaded together with the
+// LSEs, in one round trip.
+constexpr int kTailRegs = 8;
+
+template <int GH>
+__device__ __forceinline__ void step_tail(const AttendParams &p, const StepTail &t, const TailIn<GH> &in, int i,
+                                          int g, int hg, int h0, int nc, int pb) {
+    __shared__ float s_w[GH][kTailW];
+    __shared__ float s_sc[GH][4];   // per head: max, CPU-partial weight, new-token weight, 1 / normaliser
+    constexpr int kItems = TailIn<GH>::kItems;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int H = p.n_q_heads;
+    const float *po = p.part_o + ((int64_t)pb * H + h0) * kHeadDim;
+    const int64_t cstride = (int64_t)H * kHeadDim;   // floats between chunks
+    f32x4 pr[kItems][kTailRegs];
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        const int idx = threadIdx.x + 256 * j;
+        const float *e0 = po + (int64_t)(idx >> 5) * kHeadDim + 4 * (idx & 31);
+#pragma unroll
+        for (int c = 0; c < kTailRegs; ++c) {
+            pr[j][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (idx < GH * 32 && c < nc) {
+                const float *e = e0 + c * cstride;
+                pr[j][c] = f32x4{coherent_load(e), coherent_load(e + 1), coherent_load(e + 2), coherent_load(e + 3)};
+            }
+        }
+    }
+    // ---- per head: new-token score, maximum, weights, normaliser ----
+#pragma unroll
+    for (int k = 0; k < TailIn<GH>::kHeads; ++k) {
+        const int hh = wave + kWaves * k;
+        if (hh >= GH) break;
+        const int64_t row = (int64_t)i * H + h0 + hh;
+        const float *pl = p.part_lse + (int64_t)pb * H + h0 + hh;
+        const float l0 = lane < nc ? coherent_load(pl + (int64_t)lane * H) : -INFINITY;
+        const float lx = in.lx[k];
+        const uint32_t qw = in.qw[k];
+        float d = __uint_as_float(qw << 16) * __uint_as_float(in.kw << 16);
+        d = fmaf(__uint_as_float(qw & 0xffff0000u), __uint_as_float(in.kw & 0xffff0000u), d);
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) d += __shfl_xor(d, o);
+        const float s_new = d * t.scale;
+        float m = fmaxf(fmaxf(s_new, lx), l0);
+        for (int c = lane + 64; c < nc; c += 64) m = fmaxf(m, coherent_load(pl + (int64_t)c * H));
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+        float den = 0.f;
+        if (lane < nc) {
+            const float w = __expf(l0 - m);
+            s_w[hh][lane] = w;
+            den = w;
+        }
+        for (int c = lane + 64; c < nc; c += 64) den += __expf(coherent_load(pl + (int64_t)c * H) - m);
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) den += __shfl_xor(den, o);
+        const float wx = lx == -INFINITY ? 0.f : __expf(lx - m);
+        const float wn = __expf(s_new - m);
+        den += wx + wn;
+        if (lane == 0) {
+            s_sc[hh][0] = m;
+            s_sc[hh][1] = wx;
+            s_sc[hh][2] = wn;
+            s_sc[hh][3] = 1.f / den;
+            t.lse[row] = m + __logf(den);
+        }
+    }
+    __syncthreads();
+    // ---- merged rows: 32 float4 columns per head ----
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        const int idx = threadIdx.x + 256 * j;
+        if (idx >= GH * 32) break;
+        const int hh = idx >> 5;
+        const int c4 = idx & 31;
+        const int64_t row = (int64_t)i * H + h0 + hh;
+        const float m = s_sc[hh][0], wx = s_sc[hh][1], wn = s_sc[hh][2], inv = s_sc[hh][3];
+        const uint2 v2 = in.vn[j];
+        f32x4 acc = wn * f32x4{__uint_as_float(v2.x << 16), __uint_as_float(v2.x & 0xffff0000u),
+                               __uint_as_float(v2.y << 16), __uint_as_float(v2.y & 0xffff0000u)};
+        if (wx != 0.f) acc += wx * in.ox[j];
+#pragma unroll
+        for (int c = 0; c < kTailRegs; ++c)
+            if (c < nc) acc += s_w[hh][c] * pr[j][c];
+        const float *e0 = po + (int64_t)hh * kHeadDim + 4 * c4;
+        for (int c = kTailRegs; c < nc; ++c) {
+            const float w = c < kTailW ? s_w[hh][c]
+                                       : __expf(coherent_load(p.part_lse + (int64_t)(pb + c) * H + h0 + hh) - m);
+            const float *e = e0 + c * cstride;
+            acc += w * f32x4{coherent_load(e), coherent_load(e + 1), coherent_load(e + 2), coherent_load(e + 3)};
+        }
+        reinterpret_cast<f32x4 *>(t.o + row * kHeadDim)[c4] = acc * inv;
+    }
+    // ---- the new row into the pool (once per KV head: head group 0) ----
+    // No workgroup of this KV head reads it this launch: the chunks of head
+    // group 0 are done, and those of other head groups mask every position
+    // at or past the step's start length.
+    if (hg == 0 && threadIdx.x < 32)
+        put_tiled(t.pool + t.slot_elem0[i] + (int64_t)g * 2 * p.block_tokens * kHeadDim, t.row[i], threadIdx.x >> 4,
+                  threadIdx.x & 15, in.piece);
+    if (hg == 0 && g == 0 && threadIdx.x == 0 && t.tab_index[i] >= 0) t.table[t.tab_index[i]] = t.tab_slot[i];
+}
+
+template <int GH, bool STEP>
+__device__ __forceinline__ void attend(const AttendParams &p, const StepTail *st) {
     __shared__ float s_o[kWaves][GH][kHeadDim];
     __shared__ float s_m[kWaves][GH];
     __shared__ float s_l[kWaves][GH];
@@ -260,9 +431,55 @@ __global__ __launch_bounds__(256, 2) void gqa_attend_kernel(const AttendParams p
             den = fmaf(a, s_l[w][h], den);
         }
         const int64_t row = (int64_t)part * p.n_q_heads + h0 + h;
-        p.part_o[row * kHeadDim + d] = num / den;
-        if (d == 0) p.part_lse[row] = (M + __log2f(den)) * 0.69314718055994530942f;
+        // an empty chunk (a decode step's sequence with no GPU-pool
+        // positions before the step) leaves a zero row of weight 0
+        const bool any = den > 0.f;
+        const float ov = any ? num / den : 0.f;
+        const float lv = any ? (M + __log2f(den)) * 0.69314718055994530942f : -INFINITY;
+        if constexpr (STEP) {
+            // device-coherent stores: another XCD's workgroup reads them this launch
+            __hip_atomic_store(p.part_o + row * kHeadDim + d, ov, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (d == 0) __hip_atomic_store(p.part_lse + row, lv, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            p.part_o[row * kHeadDim + d] = ov;
+            if (d == 0) p.part_lse[row] = lv;
+        }
     }
+
+    if constexpr (STEP) {
+        // Arrival.  The partials were stored device-coherent (written
+        // through the XCD's L2, which the other XCDs do not share); every
+        // wavefront waits until its stores are complete, and only then is
+        // the workgroup counted.  The last arrival reads the partials with
+        // device-coherent loads.  No L2-wide writeback or invalidation: the
+        // other workgroups of the XCD keep streaming undisturbed.
+        __shared__ uint32_t s_last;
+        const TailIn<GH> tin = tail_load<GH>(p, *st, i, g, h0);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        const int nc = (p.wg_begin[i + 1] - p.wg_begin[i]) / units;
+        if (threadIdx.x == 0) {
+            uint32_t *cnt = st->done + i * units + u;
+            const uint32_t prev = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const bool last = prev == (uint32_t)(nc - 1);
+            // every arrival is in: reset for the next launch
+            if (last) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_last = last ? 1u : 0u;
+        }
+        __syncthreads();
+        if (!s_last) return;
+        step_tail<GH>(p, *st, tin, i, g, hg, h0, nc, p.chunk_begin[i]);
+    }
+}
+
+template <int GH>
+__global__ __launch_bounds__(256, 2) void gqa_attend_kernel(const AttendParams p) {
+    attend<GH, false>(p, nullptr);
+}
+
+template <int GH>
+__global__ __launch_bounds__(256, 2) void gqa_step_kernel(const AttendParams p, const StepTail t) {
+    attend<GH, true>(p, &t);
 }
 
 }  // namespace
@@ -276,6 +493,20 @@ hipError_t launch_gqa_attend(const AttendParams &p, int heads_per_wg, int n_wg, 
         case 4: hipLaunchKernelGGL(gqa_attend_kernel<4>, grid, block, 0, s, p); break;
         case 8: hipLaunchKernelGGL(gqa_attend_kernel<8>, grid, block, 0, s, p); break;
         case 16: hipLaunchKernelGGL(gqa_attend_kernel<16>, grid, block, 0, s, p); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_gqa_step(const AttendParams &p, const StepTail &t, int heads_per_wg, int n_wg, hipStream_t s) {
+    if (n_wg <= 0) return hipSuccess;
+    const dim3 grid(n_wg), block(256);
+    switch (heads_per_wg) {
+        case 1: hipLaunchKernelGGL(gqa_step_kernel<1>, grid, block, 0, s, p, t); break;
+        case 2: hipLaunchKernelGGL(gqa_step_kernel<2>, grid, block, 0, s, p, t); break;
+        case 4: hipLaunchKernelGGL(gqa_step_kernel<4>, grid, block, 0, s, p, t); break;
+        case 8: hipLaunchKernelGGL(gqa_step_kernel<8>, grid, block, 0, s, p, t); break;
+        case 16: hipLaunchKernelGGL(gqa_step_kernel<16>, grid, block, 0, s, p, t); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -50,6 +50,7 @@ struct wsk_cache {
     uint16_t *dpool = nullptr;    // GPU partition pool (HBM)
     int32_t *dtab = nullptr;      // device copy of the GPU block table
     uint16_t *dstage = nullptr;   // device staging for wsk_write
+    uint32_t *dstep_done = nullptr; // GQA decode step: arrival counters [kMaxLaunchSeqs][n_q_heads], zero between launches
     int32_t *hsel = nullptr;      // pinned host staging of block-selection tables
     size_t hsel_bytes = 0;
     hipEvent_t hsel_ev = nullptr; // marks the end of the last selection-table upload
@@ -154,7 +155,10 @@ struct AttendPlan {
     size_t bytes = 0;
 };
 inline int64_t n_tiles(int32_t a, int32_t e) { return e > a ? (int64_t)((e - 1) / kTile - a / kTile + 1) : 0; }
-void plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const int32_t *end, AttendPlan &pl);
+// min_one: every range gets at least one chunk, an empty range an empty
+// chunk (a decode step's pass 2 runs in the workgroups of its pass 1).
+void plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const int32_t *end, AttendPlan &pl,
+                 bool min_one = false);
 
 // Fills the launch-invariant fields of AttendParams (strides, head counts,
 // scale) for this cache.
@@ -175,6 +179,10 @@ struct RowLaunch {
 };
 hipError_t launch_rows(const wsk_cache *c, const RowLaunch &rl, int32_t n, const void *q, float *part_o,
                        float *part_lse, hipStream_t st);
+// The pass-1 parameters of call rows i0 .. i0 + m - 1 (m <= kMaxLaunchSeqs)
+// of rl; returns the launch's workgroup count.
+int fill_attend(const wsk_cache *c, const RowLaunch &rl, int32_t i0, int32_t m, const void *q, float *part_o,
+                float *part_lse, AttendParams &ap);
 // Pass 2: merges partials [pb[i], pb[i + 1]) of every sequence i (and, if
 // given, o_x / lse_x as one more partial) into o / lse.
 hipError_t launch_combine_all(const wsk_cache *c, int32_t n, const std::vector<int64_t> &pb, const float *part_o,

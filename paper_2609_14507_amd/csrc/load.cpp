@@ -326,8 +326,10 @@ int check_ids(const wsk_cache *c, int32_t n, const int32_t *ids) {
 }
 
 // Every GPU-side position of each sequence: the D-window in place, every
-// load-region block streamed.
-int plan_dense(const wsk_cache *c, int32_t n, const int32_t *ids, GpuPlan &g) {
+// load-region block streamed.  fused_step: the plan of a GQA decode step,
+// whose pass 2 runs inside its pass-1 launch when nothing is streamed (then
+// every sequence gets at least one chunk).
+int plan_dense(const wsk_cache *c, int32_t n, const int32_t *ids, GpuPlan &g, bool fused_step = false) {
     int rc = check_ids(c, n, ids);
     if (rc) return rc;
     const int bk = c->spec.block_tokens;
@@ -347,7 +349,7 @@ int plan_dense(const wsk_cache *c, int32_t n, const int32_t *ids, GpuPlan &g) {
             }
         }
     }
-    plan_chunks(c, n, g.hbm.start.data(), g.hbm.end.data(), g.hbm.plan);
+    plan_chunks(c, n, g.hbm.start.data(), g.hbm.end.data(), g.hbm.plan, fused_step && g.pieces.empty());
     finish_plan(c, n, g);
     return WSK_OK;
 }
@@ -586,7 +588,12 @@ int wsk_attend_gpu_pass2(wsk_cache *c, int32_t n, const int32_t *ids, const floa
 }
 
 int wsk_decode_step_workspace(const wsk_cache *c, int32_t n, const int32_t *ids, size_t *bytes) {
-    return wsk_attend_gpu_workspace(c, n, ids, bytes);
+    if (!bytes) return fail(WSK_EINVAL, "bytes is NULL");
+    GpuPlan g;
+    int rc = plan_dense(c, n, ids, g, c && c->spec.kind == WSK_KIND_GQA);
+    if (rc) return rc;
+    *bytes = g.bytes;
+    return WSK_OK;
 }
 
 }  // extern "C"
@@ -623,7 +630,7 @@ int decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, cons
     }
     // pass 1 covers the positions written so far; the new row joins in pass 2
     GpuPlan g;
-    rc = plan_dense(c, n, ids, g);
+    rc = plan_dense(c, n, ids, g, gqa);
     if (rc) return rc;
     rc = check_run(c, g, q, o_x, lse_x, ex ? ex->o : o, lse, ws, ws_bytes, true, true);
     if (rc) return rc;
@@ -639,14 +646,69 @@ int decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, cons
     // failed launch leaves the cache as it was (pass 2 writes a new block's
     // device table entry, and a later step that routes the block again sends
     // it again)
-    rc = run_plan(c, n, g, false, q, nullptr, nullptr, nullptr, nullptr, ws, ws_bytes, stream, true, false);
-    DeviceGuard guard(c->device);
-    hipError_t e = guard.err;
+    // The slot and row of each sequence's new position (launch-local r of
+    // the launch that starts at call row i0), and the device table entry of
+    // a block the step opens.
+    auto place = [&](int32_t i0, int32_t m, int64_t *slot_elem0, int32_t *row, int32_t *tab_index,
+                     int32_t *tab_slot) {
+        for (int32_t r = 0; r < m; ++r) {
+            const int32_t sq = ids[i0 + r];
+            const int32_t pos = c->length[sq];
+            const int32_t blk = pos / sp.block_tokens;
+            int32_t slot = tab(c, WSK_PART_GPU, sq, blk);
+            tab_index[r] = -1;
+            for (const Pending &pd : pend)
+                if (pd.seq == sq && pd.part == WSK_PART_GPU && pd.blk == blk) {
+                    slot = pd.slot;
+                    tab_index[r] = (int32_t)((size_t)sq * c->max_blocks + blk);
+                    tab_slot[r] = pd.slot;
+                }
+            slot_elem0[r] = (int64_t)slot * c->slot_elems;
+            row[r] = pos % sp.block_tokens;
+        }
+    };
     const int hkv = gqa ? sp.n_kv_heads : 1;
     const int width = gqa ? kHeadDim : kLatent;
     const int re = c->row_elems;
     float *part_o = (float *)ws;
     float *part_lse = (float *)((char *)ws + g.part_o_bytes);
+    if (gqa && g.chunks.empty()) {
+        // one launch per (up to) kMaxLaunchSeqs sequences: pass 1 with pass 2
+        // in the last workgroup of each (sequence, KV head, head group)
+        DeviceGuard guard(c->device);
+        hipError_t e = guard.err;
+        g.hbm.pool = c->dpool;
+        g.hbm.table = c->dtab;
+        g.hbm.table_stride = c->max_blocks;
+        for (int32_t i0 = 0; i0 < n && e == hipSuccess; i0 += kMaxLaunchSeqs) {
+            const int32_t m = std::min(kMaxLaunchSeqs, n - i0);
+            AttendParams ap;
+            const int n_wg = fill_attend(c, g.hbm, i0, m, q, part_o, part_lse, ap);
+            StepTail t{};
+            t.done = c->dstep_done;
+            t.o = o + (int64_t)i0 * sp.n_q_heads * width;
+            t.lse = lse + (int64_t)i0 * sp.n_q_heads;
+            t.o_x = o_x ? o_x + (int64_t)i0 * sp.n_q_heads * width : nullptr;
+            t.lse_x = lse_x ? lse_x + (int64_t)i0 * sp.n_q_heads : nullptr;
+            t.k_new = (const uint16_t *)k_new + (int64_t)i0 * hkv * re;
+            t.v_new = (const uint16_t *)v_new + (int64_t)i0 * hkv * re;
+            t.pool = c->dpool;
+            t.table = c->dtab;
+            t.scale = sp.softmax_scale;
+            place(i0, m, t.slot_elem0, t.row, t.tab_index, t.tab_slot);
+            e = launch_gqa_step(ap, t, g.hbm.plan.heads_per_wg, n_wg, (hipStream_t)stream);
+        }
+        if (e != hipSuccess) {
+            undo(c, pend);
+            return hip_fail(e, "wsk_decode_step");
+        }
+        commit(c, pend);
+        for (int32_t i = 0; i < n; ++i) c->length[ids[i]] += 1;
+        return WSK_OK;
+    }
+    rc = run_plan(c, n, g, false, q, nullptr, nullptr, nullptr, nullptr, ws, ws_bytes, stream, true, false);
+    DeviceGuard guard(c->device);
+    hipError_t e = guard.err;
     for (int32_t i0 = 0; i0 < n && !rc && e == hipSuccess; i0 += kMaxLaunchSeqs) {
         const int32_t m = std::min(kMaxLaunchSeqs, n - i0);
         StepCombineParams p{};
@@ -672,21 +734,7 @@ int decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, cons
         p.row_elems = re;
         p.block_tokens = sp.block_tokens;
         p.scale = sp.softmax_scale;
-        for (int32_t r = 0; r < m; ++r) {
-            const int32_t sq = ids[i0 + r];
-            const int32_t pos = c->length[sq];
-            const int32_t blk = pos / sp.block_tokens;
-            int32_t slot = tab(c, WSK_PART_GPU, sq, blk);
-            p.tab_index[r] = -1;
-            for (const Pending &pd : pend)
-                if (pd.seq == sq && pd.part == WSK_PART_GPU && pd.blk == blk) {
-                    slot = pd.slot;
-                    p.tab_index[r] = (int32_t)((size_t)sq * c->max_blocks + blk);
-                    p.tab_slot[r] = pd.slot;
-                }
-            p.slot_elem0[r] = (int64_t)slot * c->slot_elems;
-            p.row[r] = pos % sp.block_tokens;
-        }
+        place(i0, m, p.slot_elem0, p.row, p.tab_index, p.tab_slot);
         if (ex) {
             StepExpandParams xp{};
             xp.sc = p;

@@ -6,6 +6,7 @@
 #include <sys/mman.h>
 
 #include <algorithm>
+#include <queue>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -178,9 +179,8 @@ int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *
 
 // Chunking of valid ranges (positions on the tile grid of the table the
 // kernels will read: the cache's, or a compacted one for block selections).
-void wsk::plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const int32_t *end, AttendPlan &pl) {
-    int64_t total_tiles = 0;
-    for (int32_t i = 0; i < n; ++i) total_tiles += n_tiles(start[i], end[i]);
+void wsk::plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const int32_t *end, AttendPlan &pl,
+                      bool min_one) {
     const wsk_partition_spec &sp = c->spec;
     int units = 1;
     if (sp.kind == WSK_KIND_GQA) {
@@ -197,16 +197,38 @@ void wsk::plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const
     pl.tpc.assign(n, 1);
     pl.nchunks.assign(n, 0);
     pl.partials = 0;
+    // Chunk counts, min-max: every non-empty range starts with one chunk, and
+    // each further chunk of the budget goes to the range whose chunks are
+    // currently the largest (never below 4 tiles, one per wavefront, per
+    // chunk).  The launch lasts as long as its largest chunk, so on ragged
+    // batches this beats counts in proportion to the ranges' tiles.
+    std::vector<int64_t> T(n);
+    std::priority_queue<std::pair<int64_t, int32_t>> big;   // (tiles per chunk now, range)
+    int64_t spent = 0;
     for (int32_t i = 0; i < n; ++i) {
-        const int64_t T = n_tiles(start[i], end[i]);
-        if (T == 0) continue;
-        // chunks in proportion to this sequence's tiles, at least one, and at
-        // least 4 tiles (one per wavefront) per chunk when the range allows
-        int64_t want = total_tiles ? (budget * T + total_tiles / 2) / total_tiles : 1;
-        want = std::max<int64_t>(1, std::min<int64_t>(want, (T + 3) / 4));
-        const int64_t tpc = (T + want - 1) / want;
+        T[i] = n_tiles(start[i], end[i]);
+        if (T[i] == 0) continue;
+        pl.nchunks[i] = 1;
+        ++spent;
+        big.push({T[i], i});
+    }
+    while (spent < budget && !big.empty()) {
+        const int32_t i = big.top().second;
+        big.pop();
+        if (pl.nchunks[i] + 1 > (T[i] + 3) / 4) continue;
+        ++pl.nchunks[i];
+        ++spent;
+        big.push({(T[i] + pl.nchunks[i] - 1) / pl.nchunks[i], i});
+    }
+    for (int32_t i = 0; i < n; ++i) {
+        if (T[i] == 0) {
+            pl.nchunks[i] = min_one ? 1 : 0;
+            pl.partials += pl.nchunks[i];
+            continue;
+        }
+        const int64_t tpc = (T[i] + pl.nchunks[i] - 1) / pl.nchunks[i];
         pl.tpc[i] = (int32_t)tpc;
-        pl.nchunks[i] = (int32_t)((T + tpc - 1) / tpc);
+        pl.nchunks[i] = (int32_t)((T[i] + tpc - 1) / tpc);
         pl.partials += pl.nchunks[i];
     }
     const int width = sp.kind == WSK_KIND_GQA ? kHeadDim : kLatent;
@@ -289,6 +311,9 @@ int wsk_init(const wsk_partition_spec *spec, int device, wsk_cache **out) {
         if (e == hipSuccess) e = hipMalloc((void **)&c->dtab, tab_bytes);
         if (e == hipSuccess) e = hipMemset(c->dtab, 0xff, tab_bytes);
         if (e == hipSuccess) e = hipMalloc((void **)&c->dstage, kStageBytes);
+        const size_t done_bytes = (size_t)kMaxLaunchSeqs * spec->n_q_heads * sizeof(uint32_t);
+        if (e == hipSuccess && spec->kind == WSK_KIND_GQA) e = hipMalloc((void **)&c->dstep_done, done_bytes);
+        if (e == hipSuccess && c->dstep_done) e = hipMemset(c->dstep_done, 0, done_bytes);
         if (e == hipSuccess) e = hipDeviceSynchronize();
         if (e != hipSuccess) {
             const int r = hip_fail(e, "device allocation");
@@ -335,6 +360,7 @@ int wsk_destroy(wsk_cache *c) {
         if (c->dpool) (void)hipFree(c->dpool);
         if (c->dtab) (void)hipFree(c->dtab);
         if (c->dstage) (void)hipFree(c->dstage);
+        if (c->dstep_done) (void)hipFree(c->dstep_done);
         if (c->hsel_ev) (void)hipEventSynchronize(c->hsel_ev);
         if (c->hsel) (void)hipHostFree(c->hsel);
         if (c->hsel_ev) (void)hipEventDestroy(c->hsel_ev);
@@ -693,34 +719,42 @@ void wsk::attend_params(const wsk_cache *c, const AttendPlan &pl, AttendParams &
     ap.scale_log2 = sp.softmax_scale * 1.4426950408889634f;
 }
 
+int wsk::fill_attend(const wsk_cache *c, const RowLaunch &rl, int32_t i0, int32_t m, const void *q, float *part_o,
+                     float *part_lse, AttendParams &ap) {
+    ap = AttendParams{};
+    attend_params(c, rl.plan, ap);
+    ap.pool = rl.pool;
+    ap.table = rl.table;
+    ap.table_stride = rl.table_stride;
+    ap.q = (const uint16_t *)q + (int64_t)i0 * ap.q_row;
+    ap.part_o = part_o;
+    ap.part_lse = part_lse;
+    ap.n = m;
+    const int units = ap.n_kv_heads * ap.head_groups;
+    ap.wg_begin[0] = 0;
+    for (int32_t r = 0; r < m; ++r) {
+        const int32_t i = i0 + r;
+        const int32_t nc = rl.plan.nchunks[i];
+        // an empty range (an empty chunk of a decode step) reads no tile
+        const bool live = nc && rl.end[i] > rl.start[i];
+        ap.seq[r] = live ? rl.trow[i] : 0;
+        ap.start[r] = live ? rl.start[i] : 0;
+        ap.end[r] = live ? rl.end[i] : 0;
+        ap.tpc[r] = rl.plan.tpc[i];
+        ap.chunk_begin[r] = (int32_t)rl.pbase[i];
+        ap.wg_begin[r + 1] = ap.wg_begin[r] + nc * units;
+    }
+    for (int32_t r = m + 1; r <= kMaxLaunchSeqs; ++r) ap.wg_begin[r] = ap.wg_begin[m];
+    return ap.wg_begin[m];
+}
+
 hipError_t wsk::launch_rows(const wsk_cache *c, const RowLaunch &rl, int32_t n, const void *q, float *part_o,
                             float *part_lse, hipStream_t st) {
     hipError_t e = hipSuccess;
     for (int32_t i0 = 0; i0 < n && e == hipSuccess; i0 += kMaxLaunchSeqs) {
         const int32_t m = std::min(kMaxLaunchSeqs, n - i0);
-        AttendParams ap{};
-        attend_params(c, rl.plan, ap);
-        ap.pool = rl.pool;
-        ap.table = rl.table;
-        ap.table_stride = rl.table_stride;
-        ap.q = (const uint16_t *)q + (int64_t)i0 * ap.q_row;
-        ap.part_o = part_o;
-        ap.part_lse = part_lse;
-        ap.n = m;
-        const int units = ap.n_kv_heads * ap.head_groups;
-        ap.wg_begin[0] = 0;
-        for (int32_t r = 0; r < m; ++r) {
-            const int32_t i = i0 + r;
-            const int32_t nc = rl.plan.nchunks[i];
-            ap.seq[r] = nc ? rl.trow[i] : 0;
-            ap.start[r] = nc ? rl.start[i] : 0;
-            ap.end[r] = nc ? rl.end[i] : 0;
-            ap.tpc[r] = rl.plan.tpc[i];
-            ap.chunk_begin[r] = (int32_t)rl.pbase[i];
-            ap.wg_begin[r + 1] = ap.wg_begin[r] + nc * units;
-        }
-        for (int32_t r = m + 1; r <= kMaxLaunchSeqs; ++r) ap.wg_begin[r] = ap.wg_begin[m];
-        const int n_wg = ap.wg_begin[m];
+        AttendParams ap;
+        const int n_wg = fill_attend(c, rl, i0, m, q, part_o, part_lse, ap);
         if (n_wg == 0) continue;
         if (c->spec.kind == WSK_KIND_GQA)
             e = launch_gqa_attend(ap, rl.plan.heads_per_wg, n_wg, st);

@@ -54,6 +54,29 @@ struct AttendParams {
     int32_t chunk_begin[kMaxLaunchSeqs + 1];
 };
 
+// A GQA decode step in one launch: pass 1 as AttendParams describes it, and
+// the work of pass 2 (the chunk combine, the step's new token scored and
+// merged, the merge of the CPU partial, the new row stored into the pool)
+// done by the last workgroup of each (sequence, KV head, head group) to
+// finish its chunk.  done[] counts those arrivals and is back at zero when
+// the launch ends.
+struct StepTail {
+    uint32_t *done;          // [kMaxLaunchSeqs][units] arrival counters
+    float *o;                // launch-local [n][n_q_heads][128]
+    float *lse;              // launch-local [n][n_q_heads]
+    const float *o_x;        // optional CPU partial, launch-local; NULL when absent
+    const float *lse_x;
+    const uint16_t *k_new;   // launch-local [n][n_kv_heads][128]
+    const uint16_t *v_new;
+    uint16_t *pool;
+    int32_t *table;
+    float scale;             // softmax scale (natural-log domain)
+    int64_t slot_elem0[kMaxLaunchSeqs];
+    int32_t row[kMaxLaunchSeqs];
+    int32_t tab_index[kMaxLaunchSeqs];
+    int32_t tab_slot[kMaxLaunchSeqs];
+};
+
 // Chunk combine (pass 2): merges the partials of each (sequence, head).
 struct CombineParams {
     const float *part_o;
@@ -185,6 +208,7 @@ uint64_t host_read(const void *p, size_t bytes, int threads);
 int policy_fail(int code, const char *msg);
 
 hipError_t launch_gqa_attend(const AttendParams &p, int heads_per_wg, int n_wg, hipStream_t s);
+hipError_t launch_gqa_step(const AttendParams &p, const StepTail &t, int heads_per_wg, int n_wg, hipStream_t s);
 hipError_t launch_mla_attend(const AttendParams &p, int n_wg, hipStream_t s);
 hipError_t launch_combine(const CombineParams &p, int width, hipStream_t s);
 hipError_t launch_step_combine(const StepCombineParams &p, int width, hipStream_t s);
