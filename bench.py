@@ -128,29 +128,31 @@ def wsk_mod():
     return wsk
 
 
-# HBM bytes per launch of the pass-1 kernel, from two rocprofv3 --pmc runs of
-# this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch, averaged over
-# the section's dispatches), each scaled by what the same counter reads for
+# HBM bytes per launch of each section's roofline kernel, from two rocprofv3
+# --pmc runs of this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch,
+# averaged over the section's dispatches), each scaled by what the same counter reads for
 # the plain 256 MiB copy of --copy-calibration (FETCH_SIZE x 2.0,
 # WRITE_SIZE x 1.0).  Keyed by section; valid only for the kernel source they
 # were taken on (sha256), null otherwise.
 TRAFFIC = {
-    "c5": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
-           "fetch_bytes": 621598.2 * 1024 * 2.0, "write_bytes": 757.9 * 1024 * 1.0, "kv_bytes": 1271121920},
-    "c3 r=0.00": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
-           "fetch_bytes": 1048914.5 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 2147483648},
-    "c3 r=0.25": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
-           "fetch_bytes": 786706.5 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 1610612736},
-    "c3 r=0.50": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
-           "fetch_bytes": 524498.5 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 1073741824},
-    "c3 r=0.75": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
-           "fetch_bytes": 262290.5 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 536870912},
+    # the decode steps' roofline kernel: gqa_step_kernel (timed steps)
+    "c5": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "678b3495ea6445d672e5d30dc65ea847bf5141faca3ad5859f125eced8b94955",
+           "fetch_bytes": 621923.6 * 1024 * 2.0, "write_bytes": 1032.0 * 1024 * 1.0, "kv_bytes": 1270605824},
+    "c2": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "678b3495ea6445d672e5d30dc65ea847bf5141faca3ad5859f125eced8b94955",
+           "fetch_bytes": 369624.7 * 1024 * 2.0, "write_bytes": 1242.0 * 1024 * 1.0, "kv_bytes": 751976448},
+    "c1": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "678b3495ea6445d672e5d30dc65ea847bf5141faca3ad5859f125eced8b94955",
+           "fetch_bytes": 655.1 * 1024 * 2.0, "write_bytes": 30.5 * 1024 * 1.0, "kv_bytes": 1059328},
+    # the sweep's and the MLA step's roofline kernel: pass 1 (launches alone)
+    "c3 r=0.00": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "678b3495ea6445d672e5d30dc65ea847bf5141faca3ad5859f125eced8b94955",
+           "fetch_bytes": 1048914.0 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 2147483648},
+    "c3 r=0.25": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "678b3495ea6445d672e5d30dc65ea847bf5141faca3ad5859f125eced8b94955",
+           "fetch_bytes": 786706.0 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 1610612736},
+    "c3 r=0.50": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "678b3495ea6445d672e5d30dc65ea847bf5141faca3ad5859f125eced8b94955",
+           "fetch_bytes": 524498.0 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 1073741824},
+    "c3 r=0.75": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "678b3495ea6445d672e5d30dc65ea847bf5141faca3ad5859f125eced8b94955",
+           "fetch_bytes": 262290.0 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 536870912},
     "c4": {"source": "paper_2609_14507_amd/csrc/attend_mla.hip", "sha256": "4df8a57ec4065ad10e72b3e174e71bce14707792ab7dea83e03b7889f82faa92",
-           "fetch_bytes": 177748.0 * 1024 * 2.0, "write_bytes": 7951.5 * 1024 * 1.0, "kv_bytes": 362575872},
-    "c2": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
-           "fetch_bytes": 368931.8 * 1024 * 2.0, "write_bytes": 774.0 * 1024 * 1.0, "kv_bytes": 752287744},
-    "c1": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "3c5725ebbdfd995009107330266a6eea2eec21b5d5791d7493b3e17112d7b199",
-           "fetch_bytes": 615.1 * 1024 * 2.0, "write_bytes": 20.3 * 1024 * 1.0, "kv_bytes": 1069056},
+           "fetch_bytes": 177748.1 * 1024 * 2.0, "write_bytes": 8208.0 * 1024 * 1.0, "kv_bytes": 362575872},
 }
 
 
