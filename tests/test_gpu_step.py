@@ -386,6 +386,44 @@ def test_decode_step_mla_expand_empty_gpu_side():
             assert_lse(lse[b], l_r, "empty-side b%d" % b)
 
 
+def test_decode_step_more_chunks_than_weights_kept():
+    """GQA decode step with one KV head (one (KV head, head group) unit, so the whole grid serves
+    one sequence): a long sequence cut into more than 64 chunk partials -- more than the weights
+    the last workgroup keeps per head and more than the partials it loads before the merge, so
+    both of its loops over the rest run -- and a short one, against the oracle; the chunk count
+    is read back from the workspace size, so the premise is asserted."""
+    H = 8
+    lengths = [20100, 700]
+    splits = [37, 130]
+    w = wl.Workload("step-gqa-one-kv-head", wl.GQA, batch=len(lengths), n_q_heads=H, n_kv_heads=1, head_dim=128,
+                    context=1, seed=43)
+    gen = torch.Generator().manual_seed(44)
+    pf = _prefill(w, lengths, splits, gen)
+    dv, g = _dims(w)
+    say("case decode step, more chunks than weights kept")
+    with DecodeSession(w, pf, DEV, extra_tokens=2) as sess:
+        for step in range(2):
+            q_bits = wl.draw_bf16(gen, (sess.B, H, w.row_elems))
+            kn, vn = _new_rows(w, sess.B, gen)
+            need = wsk.wsk_decode_step_workspace(sess.h, sess.ids)
+            r256 = lambda x: (x + 255) // 256 * 256
+            partials = max(p for p in range(1, 4096) if r256(p * H * dv * 4) + r256(p * H * 4) <= need)
+            short_tiles = -(-(lengths[1] + step) // 64) - splits[1] // 64
+            say("  step %d: %d chunk partials in all" % (step, partials))
+            assert partials - -(-short_tiles // 4) > 64, partials
+            o_x, l_x = _cpu_partial(sess, q_bits)
+            out, lse = _step(sess, to_device_bf16(q_bits, sess.dev), to_device_bf16(kn, sess.dev),
+                             to_device_bf16(vn, sess.dev), o_x, l_x)
+            out, lse = out.cpu().numpy(), lse.cpu().numpy()
+            for b in range(sess.B):
+                pf.k[b] = np.concatenate([pf.k[b], kn[b:b + 1]])
+                pf.v[b] = np.concatenate([pf.v[b], vn[b:b + 1]])
+                o_r, l_r = oracle.attend(q_bits[b], pf.k[b], pf.v[b], 0, sess.lengths[b], w.softmax_scale, g,
+                                         dv=dv)
+                assert_close(out[b], o_r, "more than 64 chunks step %d b%d" % (step, b))
+                assert_lse(lse[b], l_r, "more than 64 chunks step %d b%d" % (step, b))
+
+
 @pytest.mark.parametrize("kind", ["gqa", "mla"])
 def test_decode_step_more_chunks_than_loaded_up_front(kind):
     """One long sequence (41 chunk partials on a 256-CU device: more than the 32 that pass 2 loads
