@@ -55,6 +55,7 @@ import hashlib
 import json
 import os
 import platform
+import re
 import sys
 import time
 
@@ -930,7 +931,9 @@ def trace_summary(trace_dir, bench_json):
     counters = _read_rows(os.path.join(trace_dir, "**", "*counter_collection.csv"))
 
     def per_kernel(rows, key):
-        sel = [r for r in rows if (key + "(") in r["Kernel_Name"]]
+        # the GQA kernels come as a per-sequence-chunk and a flat-split
+        # instantiation ("<8, false>", "<8, true>"): one key, dispatch order
+        sel = [r for r in rows if (key + "(") in re.sub(r", (true|false)>", ">", r["Kernel_Name"])]
         return sorted(sel, key=lambda r: int(r["Dispatch_Id"]))
 
     # per section: its windows, and per part the algorithmic KV bytes of one

@@ -26,11 +26,14 @@
 // bf16 hi + lo parts (two MFMAs), which keeps P.V accurate to ~2^-16
 // relative, like fp32 probabilities.
 //
-// Work mapping: workgroup = (sequence, KV head, group of GH <= 16 query
-// heads, chunk of 64-token tiles); its 4 wavefronts take every 4th tile of the
-// chunk with their own online softmax and are merged through LDS at the end.
-// Each wavefront issues the next tile's K loads as soon as QK has consumed
-// the current ones, and the next V loads right after P.V.
+// Work mapping: workgroup = (KV head, group of GH <= 16 query heads, a run
+// of 64-token tiles): a chunk of one sequence (per-sequence chunks), or, for
+// ragged batches, an equal share of the launch's tiles that may cross from
+// one sequence into the next (the flat split: one partial per sequence it
+// reads).  Its 4 wavefronts take every 4th tile of a run with their own
+// online softmax and are merged through LDS at the end of each sequence's
+// part.  Each wavefront issues the next tile's K loads as soon as QK has
+// consumed the current ones, and the next V loads right after P.V.
 //
 // gqa_step_kernel is the same pass 1 with a decode step's pass 2 folded in
 // (Sec. 4.2: one LSE join per step): the last workgroup of each (sequence,
@@ -223,34 +226,22 @@ __device__ __forceinline__ void step_tail(const AttendParams &p, const StepTail 
     if (hg == 0 && g == 0 && threadIdx.x == 0 && t.tab_index[i] >= 0) t.table[t.tab_index[i]] = t.tab_slot[i];
 }
 
+// Pass 1 over tiles [tile0, tile_end) of launch-local sequence i for query
+// heads h0 .. h0 + GH - 1 of KV head g: writes partial `part` (an empty
+// range writes a zero row of LSE -inf); device-coherent stores for a decode
+// step, whose last workgroups read the partials back in the same launch.
 template <int GH, bool STEP>
-__device__ __forceinline__ void attend(const AttendParams &p, const StepTail *st) {
-    __shared__ float s_o[kWaves][GH][kHeadDim];
-    __shared__ float s_m[kWaves][GH];
-    __shared__ float s_l[kWaves][GH];
-
+__device__ __forceinline__ void attend_segment(const AttendParams &p, int i, int g, int h0, int tile0, int tile_end,
+                                               int part, float (*s_o)[GH][kHeadDim], float (*s_m)[GH],
+                                               float (*s_l)[GH]) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n = lane & 15;     // MFMA column: query head (QK) / dim within an N-tile (P.V)
     const int grp = lane >> 4;   // MFMA k-group 0..3
 
-    // ---- work item of this workgroup (uniform) ----
-    const int wg = blockIdx.x;
-    int i = 0;
-    while (wg >= p.wg_begin[i + 1]) ++i;
-    const int rel = wg - p.wg_begin[i];
-    const int units = p.n_kv_heads * p.head_groups;
-    const int c = rel / units;
-    const int u = rel - c * units;
-    const int g = u / p.head_groups;
-    const int hg = u - g * p.head_groups;
     const int seq = p.seq[i];
     const int t_start = p.start[i];
     const int t_end = p.end[i];
-    const int tpc = p.tpc[i];
-    const int tile0 = (t_start >> 6) + c * tpc;
-    const int tile_end = min(tile0 + tpc, ((t_end - 1) >> 6) + 1);
-    const int h0 = g * p.group + hg * GH;
     typedef const __attribute__((address_space(4))) int32_t ci32;
     ci32 *trow = (ci32 *)(p.table + (int64_t)seq * p.table_stride);   // read-only here
     const int bk = p.block_tokens;
@@ -416,7 +407,6 @@ __device__ __forceinline__ void attend(const AttendParams &p, const StepTail *st
     }
     __syncthreads();
 
-    const int part = p.chunk_begin[i] + c;
     for (int idx = threadIdx.x; idx < GH * kHeadDim; idx += 256) {
         const int h = idx / kHeadDim;
         const int d = idx - h * kHeadDim;
@@ -445,71 +435,182 @@ __device__ __forceinline__ void attend(const AttendParams &p, const StepTail *st
             if (d == 0) p.part_lse[row] = lv;
         }
     }
+}
 
-    if constexpr (STEP) {
-        // Arrival.  The partials were stored device-coherent (written
-        // through the XCD's L2, which the other XCDs do not share); every
-        // wavefront waits until its stores are complete, and only then is
-        // the workgroup counted.  The last arrival reads the partials with
-        // device-coherent loads.  No L2-wide writeback or invalidation: the
-        // other workgroups of the XCD keep streaming undisturbed.
-        __shared__ uint32_t s_last;
-        const TailIn<GH> tin = tail_load<GH>(p, *st, i, g, h0);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        const int nc = (p.wg_begin[i + 1] - p.wg_begin[i]) / units;
-        if (threadIdx.x == 0) {
-            uint32_t *cnt = st->done + i * units + u;
-            const uint32_t prev = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            const bool last = prev == (uint32_t)(nc - 1);
-            // every arrival is in: reset for the next launch
-            if (last) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            s_last = last ? 1u : 0u;
+// Arrival of a decode step's workgroup for sequence i, unit u, after its
+// partial for them is stored.  The partials are stored device-coherent
+// (written through the XCD's L2, which the other XCDs do not share); every
+// wavefront waits until its stores are complete, and only then is the
+// workgroup counted.  Returns whether it is the last arrival for the
+// (sequence, unit), which then reads the partials with device-coherent
+// loads and finishes pass 2.  No L2-wide writeback or invalidation: the
+// other workgroups of the XCD keep streaming undisturbed.
+__device__ __forceinline__ bool count_in(const AttendParams &p, const StepTail &t, int i, int u, int units) {
+    __shared__ uint32_t s_last;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t *cnt = t.done + i * units + u;
+        const uint32_t nc = p.chunk_begin[i + 1] - p.chunk_begin[i];
+        const uint32_t prev = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const bool last = prev == nc - 1;
+        // every arrival is in: reset for the next launch
+        if (last) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = last ? 1u : 0u;
+    }
+    __syncthreads();
+    const bool last = s_last != 0u;
+    __syncthreads();   // s_last is free again
+    return last;
+}
+
+// Pass 2 for sequence i, unit u, by its last arrival (its inputs loaded in `in`).
+template <int GH>
+__device__ __forceinline__ void finish(const AttendParams &p, const StepTail &t, const TailIn<GH> &in, int i, int u) {
+    const int g = u / p.head_groups;
+    const int hg = u - g * p.head_groups;
+    step_tail<GH>(p, t, in, i, g, hg, g * p.group + hg * GH, p.chunk_begin[i + 1] - p.chunk_begin[i],
+                  p.chunk_begin[i]);
+}
+
+template <int GH>
+__device__ __forceinline__ TailIn<GH> tail_inputs(const AttendParams &p, const StepTail &t, int i, int u) {
+    const int g = u / p.head_groups;
+    return tail_load<GH>(p, t, i, g, g * p.group + (u - g * p.head_groups) * GH);
+}
+
+// Tiles of launch-local sequence i's range.
+__device__ __forceinline__ int seq_tiles(const AttendParams &p, int i) {
+    return p.end[i] > p.start[i] ? ((p.end[i] - 1) >> 6) - (p.start[i] >> 6) + 1 : 0;
+}
+
+// One workgroup's work.  Per-sequence chunks (FLAT false): one segment,
+// tiles [c tpc, (c + 1) tpc) of sequence i for unit u, partial
+// chunk_begin[i] + c.  The flat split (FLAT true): workgroup w * units + u
+// reads flat positions [lo, hi) of unit u, one segment per sequence they
+// cross, in sequence order, each with its own partial
+// chunk_begin[i] + w - wfirst[i]; an empty sequence of a decode step is an
+// empty segment of the one workgroup wfirst names.  A decode step counts
+// the workgroup in after each segment, so a workgroup that crosses into the
+// next sequence has already arrived for the previous one.
+template <int GH, bool STEP, bool FLAT>
+__device__ __forceinline__ void attend(const AttendParams &p, const StepTail *st) {
+    __shared__ float s_o[kWaves][GH][kHeadDim];
+    __shared__ float s_m[kWaves][GH];
+    __shared__ float s_l[kWaves][GH];
+    const int units = p.n_kv_heads * p.head_groups;
+    auto segment = [&](int i, int u, int a, int b, int part) {
+        const int g = u / p.head_groups;
+        const int h0 = g * p.group + (u - g * p.head_groups) * GH;
+        const int first = p.start[i] >> 6;
+        attend_segment<GH, STEP>(p, i, g, h0, first + a, first + b, part, s_o, s_m, s_l);
+    };
+    if constexpr (FLAT) {
+        // Segments in sequence order; a decode step counts the workgroup in
+        // after each, so a workgroup that crosses into the next sequence has
+        // arrived for the previous one before it streams on, and finishes
+        // pass 2 of the sequences it arrived last for after its last segment.
+        __shared__ int s_fin[kMaxLaunchSeqs];
+        int n_fin = 0;
+        const int w = blockIdx.x / units;
+        const int u = blockIdx.x - w * units;
+        const int64_t total = p.flat_begin[p.n];
+        const int lo = (int)(w * total / p.flat_wgs);
+        const int hi = (int)((w + 1) * total / p.flat_wgs);
+        for (int i = 0; i < p.n; ++i) {
+            const int fb = p.flat_begin[i];
+            const int nt = seq_tiles(p, i);
+            const int a = nt ? max(fb, lo) - fb : 0;
+            const int b = nt ? min(fb + nt, hi) - fb : 0;
+            const bool go = nt ? a < b : STEP && p.wfirst[i] == w;
+            if (!go) continue;
+            segment(i, u, a, b, p.chunk_begin[i] + (w - p.wfirst[i]));
+            __syncthreads();   // s_o, s_m, s_l are free again
+            if constexpr (STEP) {
+                if (count_in(p, *st, i, u, units)) {
+                    if (threadIdx.x == 0) s_fin[n_fin] = i;
+                    ++n_fin;
+                }
+            }
         }
-        __syncthreads();
-        if (!s_last) return;
-        step_tail<GH>(p, *st, tin, i, g, hg, h0, nc, p.chunk_begin[i]);
+        if constexpr (STEP) {
+            __syncthreads();
+            for (int k = 0; k < n_fin; ++k) {
+                const int i = s_fin[k];
+                finish<GH>(p, *st, tail_inputs<GH>(p, *st, i, u), i, u);
+                __syncthreads();   // the tail's LDS is free again
+            }
+        }
+    } else {
+        int i = 0;
+        while ((int)blockIdx.x >= p.wg_begin[i + 1]) ++i;
+        const int rel = blockIdx.x - p.wg_begin[i];
+        const int c = rel / units;
+        const int u = rel - c * units;
+        const int nt = seq_tiles(p, i);
+        const int a = min(c * p.tpc[i], nt);
+        segment(i, u, a, min(a + p.tpc[i], nt), p.chunk_begin[i] + c);
+        if constexpr (STEP) {
+            // the loads pass 2 needs besides the partials overlap the wait in count_in
+            const TailIn<GH> tin = tail_inputs<GH>(p, *st, i, u);
+            if (count_in(p, *st, i, u, units)) finish<GH>(p, *st, tin, i, u);
+        }
     }
 }
 
-template <int GH>
+template <int GH, bool FLAT>
 __global__ __launch_bounds__(256, 2) void gqa_attend_kernel(const AttendParams p) {
-    attend<GH, false>(p, nullptr);
+    attend<GH, false, FLAT>(p, nullptr);
 }
 
-template <int GH>
+template <int GH, bool FLAT>
 __global__ __launch_bounds__(256, 2) void gqa_step_kernel(const AttendParams p, const StepTail t) {
-    attend<GH, true>(p, &t);
+    attend<GH, true, FLAT>(p, &t);
+}
+
+}  // namespace
+
+namespace {
+
+template <bool FLAT>
+hipError_t attend_launch(const AttendParams &p, int heads_per_wg, int n_wg, hipStream_t s) {
+    const dim3 grid(n_wg), block(256);
+    switch (heads_per_wg) {
+        case 1: hipLaunchKernelGGL((gqa_attend_kernel<1, FLAT>), grid, block, 0, s, p); break;
+        case 2: hipLaunchKernelGGL((gqa_attend_kernel<2, FLAT>), grid, block, 0, s, p); break;
+        case 4: hipLaunchKernelGGL((gqa_attend_kernel<4, FLAT>), grid, block, 0, s, p); break;
+        case 8: hipLaunchKernelGGL((gqa_attend_kernel<8, FLAT>), grid, block, 0, s, p); break;
+        case 16: hipLaunchKernelGGL((gqa_attend_kernel<16, FLAT>), grid, block, 0, s, p); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <bool FLAT>
+hipError_t step_launch(const AttendParams &p, const StepTail &t, int heads_per_wg, int n_wg, hipStream_t s) {
+    const dim3 grid(n_wg), block(256);
+    switch (heads_per_wg) {
+        case 1: hipLaunchKernelGGL((gqa_step_kernel<1, FLAT>), grid, block, 0, s, p, t); break;
+        case 2: hipLaunchKernelGGL((gqa_step_kernel<2, FLAT>), grid, block, 0, s, p, t); break;
+        case 4: hipLaunchKernelGGL((gqa_step_kernel<4, FLAT>), grid, block, 0, s, p, t); break;
+        case 8: hipLaunchKernelGGL((gqa_step_kernel<8, FLAT>), grid, block, 0, s, p, t); break;
+        case 16: hipLaunchKernelGGL((gqa_step_kernel<16, FLAT>), grid, block, 0, s, p, t); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gqa_attend(const AttendParams &p, int heads_per_wg, int n_wg, hipStream_t s) {
     if (n_wg <= 0) return hipSuccess;
-    const dim3 grid(n_wg), block(256);
-    switch (heads_per_wg) {
-        case 1: hipLaunchKernelGGL(gqa_attend_kernel<1>, grid, block, 0, s, p); break;
-        case 2: hipLaunchKernelGGL(gqa_attend_kernel<2>, grid, block, 0, s, p); break;
-        case 4: hipLaunchKernelGGL(gqa_attend_kernel<4>, grid, block, 0, s, p); break;
-        case 8: hipLaunchKernelGGL(gqa_attend_kernel<8>, grid, block, 0, s, p); break;
-        case 16: hipLaunchKernelGGL(gqa_attend_kernel<16>, grid, block, 0, s, p); break;
-        default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
+    return p.flat_wgs > 0 ? attend_launch<true>(p, heads_per_wg, n_wg, s) : attend_launch<false>(p, heads_per_wg, n_wg, s);
 }
 
 hipError_t launch_gqa_step(const AttendParams &p, const StepTail &t, int heads_per_wg, int n_wg, hipStream_t s) {
     if (n_wg <= 0) return hipSuccess;
-    const dim3 grid(n_wg), block(256);
-    switch (heads_per_wg) {
-        case 1: hipLaunchKernelGGL(gqa_step_kernel<1>, grid, block, 0, s, p, t); break;
-        case 2: hipLaunchKernelGGL(gqa_step_kernel<2>, grid, block, 0, s, p, t); break;
-        case 4: hipLaunchKernelGGL(gqa_step_kernel<4>, grid, block, 0, s, p, t); break;
-        case 8: hipLaunchKernelGGL(gqa_step_kernel<8>, grid, block, 0, s, p, t); break;
-        case 16: hipLaunchKernelGGL(gqa_step_kernel<16>, grid, block, 0, s, p, t); break;
-        default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
+    return p.flat_wgs > 0 ? step_launch<true>(p, t, heads_per_wg, n_wg, s)
+                          : step_launch<false>(p, t, heads_per_wg, n_wg, s);
 }
 
 }  // namespace wsk

@@ -148,8 +148,13 @@ bool range_in(const wsk_cache *c, int32_t seq, int32_t a, int32_t e, int part);
 struct AttendPlan {
     int heads_per_wg = 1;
     int head_groups = 1;
-    std::vector<int32_t> tpc;       // tiles per chunk, per sequence
-    std::vector<int32_t> nchunks;   // per sequence
+    std::vector<int32_t> tpc;       // tiles per chunk, per sequence (per-sequence chunks)
+    std::vector<int32_t> nchunks;   // partials per sequence
+    // the flat split (GQA), per launch of kMaxLaunchSeqs sequences: the
+    // sequence's first flat position within its launch, the first
+    // workgroup that reads it; per launch: its flat positions and its
+    // workgroups per unit (0: per-sequence chunks)
+    std::vector<int32_t> flat_first, wfirst, launch_tiles, launch_wgs;
     int64_t partials = 0;           // sum of nchunks
     size_t part_o_bytes = 0;
     size_t bytes = 0;

@@ -177,61 +177,121 @@ int make_plan(const wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *
 
 }  // namespace
 
+namespace {
+
+// Per-sequence chunks of ranges [i0, i0 + m), min-max: every non-empty range
+// starts with one chunk, and each further chunk of the budget goes to the
+// range whose chunks are currently the largest (never below 4 tiles, one per
+// wavefront, per chunk).  A launch lasts as long as its largest chunk, so on
+// ragged batches this beats counts in proportion to the ranges' tiles.  Sets
+// nchunks and tpc of those ranges; returns the largest chunk's tiles.
+int64_t chunks_per_range(const int32_t *start, const int32_t *end, int32_t i0, int32_t m, int64_t budget,
+                         bool min_one, AttendPlan &pl) {
+    std::vector<int64_t> T(m);
+    std::priority_queue<std::pair<int64_t, int32_t>> big;   // (tiles per chunk now, range)
+    int64_t spent = 0;
+    for (int32_t r = 0; r < m; ++r) {
+        T[r] = n_tiles(start[i0 + r], end[i0 + r]);
+        pl.nchunks[i0 + r] = 0;
+        pl.tpc[i0 + r] = 1;
+        if (T[r] == 0) continue;
+        pl.nchunks[i0 + r] = 1;
+        ++spent;
+        big.push({T[r], r});
+    }
+    while (spent < budget && !big.empty()) {
+        const int32_t r = big.top().second;
+        big.pop();
+        int32_t &nc = pl.nchunks[i0 + r];
+        if (nc + 1 > (T[r] + 3) / 4) continue;
+        ++nc;
+        ++spent;
+        big.push({(T[r] + nc - 1) / nc, r});
+    }
+    int64_t worst = 0;
+    for (int32_t r = 0; r < m; ++r) {
+        int32_t &nc = pl.nchunks[i0 + r];
+        if (T[r] == 0) {
+            nc = min_one ? 1 : 0;
+            continue;
+        }
+        const int64_t tpc = (T[r] + nc - 1) / nc;
+        pl.tpc[i0 + r] = (int32_t)tpc;
+        nc = (int32_t)((T[r] + tpc - 1) / tpc);
+        worst = std::max(worst, tpc);
+    }
+    return worst;
+}
+
+}  // namespace
+
 // Chunking of valid ranges (positions on the tile grid of the table the
-// kernels will read: the cache's, or a compacted one for block selections).
+// kernels will read: the cache's, or a compacted one for block selections),
+// per launch of up to kMaxLaunchSeqs ranges, each launch aiming at the whole
+// GPU.
 void wsk::plan_chunks(const wsk_cache *c, int32_t n, const int32_t *start, const int32_t *end, AttendPlan &pl,
                       bool min_one) {
     const wsk_partition_spec &sp = c->spec;
+    const bool gqa = sp.kind == WSK_KIND_GQA;
     int units = 1;
-    if (sp.kind == WSK_KIND_GQA) {
+    if (gqa) {
         const int G = sp.n_q_heads / sp.n_kv_heads;
         pl.heads_per_wg = gqa_heads_per_wg(G);
         pl.head_groups = G / pl.heads_per_wg;
         units = sp.n_kv_heads * pl.head_groups;
     }
-    // workgroups the grid aims at (GQA: 3/4 per CU; MLA, whose workgroups
-    // are twice as wide: 1 per CU); the chunk budget per (KV head, head
-    // group) unit follows from it
-    const int64_t slots = sp.kind == WSK_KIND_GQA ? gqa_resident_slots(c->cu_count) : (int64_t)c->cu_count;
+    // workgroups a launch aims at (GQA: 3/4 per CU; MLA, whose workgroups
+    // are twice as wide: 1 per CU); the budget per (KV head, head group)
+    // unit follows from it
+    const int64_t slots = gqa ? gqa_resident_slots(c->cu_count) : (int64_t)c->cu_count;
     const int64_t budget = std::max<int64_t>(1, slots / units);
     pl.tpc.assign(n, 1);
     pl.nchunks.assign(n, 0);
-    pl.partials = 0;
-    // Chunk counts, min-max: every non-empty range starts with one chunk, and
-    // each further chunk of the budget goes to the range whose chunks are
-    // currently the largest (never below 4 tiles, one per wavefront, per
-    // chunk).  The launch lasts as long as its largest chunk, so on ragged
-    // batches this beats counts in proportion to the ranges' tiles.
-    std::vector<int64_t> T(n);
-    std::priority_queue<std::pair<int64_t, int32_t>> big;   // (tiles per chunk now, range)
-    int64_t spent = 0;
-    for (int32_t i = 0; i < n; ++i) {
-        T[i] = n_tiles(start[i], end[i]);
-        if (T[i] == 0) continue;
-        pl.nchunks[i] = 1;
-        ++spent;
-        big.push({T[i], i});
-    }
-    while (spent < budget && !big.empty()) {
-        const int32_t i = big.top().second;
-        big.pop();
-        if (pl.nchunks[i] + 1 > (T[i] + 3) / 4) continue;
-        ++pl.nchunks[i];
-        ++spent;
-        big.push({(T[i] + pl.nchunks[i] - 1) / pl.nchunks[i], i});
-    }
-    for (int32_t i = 0; i < n; ++i) {
-        if (T[i] == 0) {
-            pl.nchunks[i] = min_one ? 1 : 0;
-            pl.partials += pl.nchunks[i];
-            continue;
+    pl.flat_first.assign(n, 0);
+    pl.wfirst.assign(n, 0);
+    pl.launch_tiles.clear();
+    pl.launch_wgs.clear();
+    for (int32_t i0 = 0; i0 < n; i0 += kMaxLaunchSeqs) {
+        const int32_t m = std::min(kMaxLaunchSeqs, n - i0);
+        const int64_t worst = chunks_per_range(start, end, i0, m, budget, min_one, pl);
+        pl.launch_tiles.push_back(0);
+        pl.launch_wgs.push_back(0);   // 0: per-range chunks
+        if (!gqa) continue;
+        // GQA, the flat split: the launch's tiles in range order, a gap of
+        // kSegmentTiles before each non-empty range, cut into equal runs, one
+        // per workgroup of each unit, whatever the ranges' lengths.  A run
+        // that crosses into a range pays for the restart with the gap.  Taken
+        // when its runs are shorter than the largest per-range chunk.
+        int64_t total = 0, tiles = 0;
+        for (int32_t r = 0; r < m; ++r) {
+            const int64_t t = n_tiles(start[i0 + r], end[i0 + r]);
+            if (t > 0) total += kSegmentTiles;
+            pl.flat_first[i0 + r] = (int32_t)total;
+            total += t;
+            tiles += t;
         }
-        const int64_t tpc = (T[i] + pl.nchunks[i] - 1) / pl.nchunks[i];
-        pl.tpc[i] = (int32_t)tpc;
-        pl.nchunks[i] = (int32_t)((T[i] + tpc - 1) / tpc);
-        pl.partials += pl.nchunks[i];
+        if (tiles == 0) continue;
+        const int64_t nw = std::max<int64_t>(1, std::min<int64_t>(budget, (tiles + 3) / 4));
+        if ((total + nw - 1) / nw >= worst) continue;
+        pl.launch_tiles.back() = (int32_t)total;
+        pl.launch_wgs.back() = (int32_t)nw;
+        // the run holding flat position x: the last w with w * total / nw <= x
+        auto owner = [&](int64_t x) { return (int32_t)(((x + 1) * nw + total - 1) / total - 1); };
+        for (int32_t r = 0; r < m; ++r) {
+            const int32_t i = i0 + r;
+            const int64_t f = pl.flat_first[i], t = n_tiles(start[i], end[i]);
+            if (t > 0) {
+                pl.wfirst[i] = owner(f);
+                pl.nchunks[i] = owner(f + t - 1) - pl.wfirst[i] + 1;
+            } else {   // an empty range: its one empty partial (min_one) comes from the run at f
+                pl.wfirst[i] = f < total ? owner(f) : (int32_t)nw - 1;
+                pl.nchunks[i] = min_one ? 1 : 0;
+            }
+        }
     }
-    const int width = sp.kind == WSK_KIND_GQA ? kHeadDim : kLatent;
+    pl.partials = 0;
+    for (int32_t i = 0; i < n; ++i) pl.partials += pl.nchunks[i];
+    const int width = gqa ? kHeadDim : kLatent;
     pl.part_o_bytes = ((size_t)pl.partials * sp.n_q_heads * width * sizeof(float) + 255) / 256 * 256;
     pl.bytes = pl.part_o_bytes + ((size_t)pl.partials * sp.n_q_heads * sizeof(float) + 255) / 256 * 256;
 }
@@ -731,19 +791,31 @@ int wsk::fill_attend(const wsk_cache *c, const RowLaunch &rl, int32_t i0, int32_
     ap.part_lse = part_lse;
     ap.n = m;
     const int units = ap.n_kv_heads * ap.head_groups;
-    ap.wg_begin[0] = 0;
     for (int32_t r = 0; r < m; ++r) {
         const int32_t i = i0 + r;
         const int32_t nc = rl.plan.nchunks[i];
-        // an empty range (an empty chunk of a decode step) reads no tile
+        // an empty range (an empty partial of a decode step) reads no tile
         const bool live = nc && rl.end[i] > rl.start[i];
         ap.seq[r] = live ? rl.trow[i] : 0;
         ap.start[r] = live ? rl.start[i] : 0;
         ap.end[r] = live ? rl.end[i] : 0;
         ap.tpc[r] = rl.plan.tpc[i];
         ap.chunk_begin[r] = (int32_t)rl.pbase[i];
-        ap.wg_begin[r + 1] = ap.wg_begin[r] + nc * units;
     }
+    // one past the last sequence's partials (contiguous when nothing is streamed)
+    ap.chunk_begin[m] = (int32_t)(rl.pbase[i0 + m - 1] + rl.plan.nchunks[i0 + m - 1]);
+    const size_t k = (size_t)(i0 / kMaxLaunchSeqs);
+    ap.flat_wgs = rl.plan.launch_wgs[k];
+    if (ap.flat_wgs > 0) {   // the flat split (GQA)
+        for (int32_t r = 0; r < m; ++r) {
+            ap.flat_begin[r] = rl.plan.flat_first[i0 + r];
+            ap.wfirst[r] = rl.plan.wfirst[i0 + r];
+        }
+        ap.flat_begin[m] = rl.plan.launch_tiles[k];
+        return ap.flat_wgs * units;
+    }
+    ap.wg_begin[0] = 0;
+    for (int32_t r = 0; r < m; ++r) ap.wg_begin[r + 1] = ap.wg_begin[r] + rl.plan.nchunks[i0 + r] * units;
     for (int32_t r = m + 1; r <= kMaxLaunchSeqs; ++r) ap.wg_begin[r] = ap.wg_begin[m];
     return ap.wg_begin[m];
 }

@@ -11,6 +11,11 @@ namespace wsk {
 
 // Sequences handled by one kernel launch; a call with more is split.
 constexpr int kMaxLaunchSeqs = 64;
+// What starting one more range costs a GQA pass-1 workgroup (the query
+// load, the refill of its load pipeline, one more partial and, in a decode
+// step, one more arrival), in tiles of streaming: the flat split's gap
+// before each range.
+constexpr int kSegmentTiles = 8;
 // Tokens per attention tile: one token per lane of a 64-wide wavefront.
 constexpr int kTile = 64;
 // GQA key/value width.
@@ -24,11 +29,20 @@ constexpr int kRope = 64;
 constexpr int kStreamLoad = 2;
 
 // ---------------------------------------------------------------------------
-// Split-KV attention (pass 1).  One workgroup = (sequence i, KV head g, query
-// head group hg, chunk c); a chunk is tpc[i] consecutive 64-token tiles of
-// [start, end) on the absolute tile grid.  Each workgroup writes a
-// normalised partial O and its LSE for its heads into part_o / part_lse at
-// partial index chunk_begin[i] + c.
+// Split-KV attention (pass 1).  Sequence i attends positions [start, end) on
+// the absolute 64-token tile grid; every workgroup writes a normalised
+// partial O and its LSE per (sequence it reads, head) into part_o /
+// part_lse, sequence i's partials numbered from chunk_begin[i].
+//   Per-sequence chunks (flat_wgs == 0): workgroup (sequence i, chunk c,
+//   unit u) reads tpc[i] tiles from the sequence's first + c * tpc[i], for
+//   partial chunk_begin[i] + c; sequence i's workgroups are
+//   [wg_begin[i], wg_begin[i + 1]), unit fastest.
+//   The flat split (GQA, flat_wgs > 0): the launch's tiles in sequence order,
+//   sequence i's from flat position flat_begin[i] (after a gap of
+//   kSegmentTiles), flat_begin[n] positions in all, are cut into flat_wgs
+//   equal runs per (KV head, head group) unit; workgroup w * units + u reads
+//   run w for unit u, one segment per sequence it crosses, and writes
+//   partial chunk_begin[i] + w - wfirst[i] of each.
 // ---------------------------------------------------------------------------
 struct AttendParams {
     const uint16_t *pool;    // device pool base (bf16)
@@ -52,6 +66,9 @@ struct AttendParams {
     int32_t end[kMaxLaunchSeqs];
     int32_t wg_begin[kMaxLaunchSeqs + 1];
     int32_t chunk_begin[kMaxLaunchSeqs + 1];
+    int32_t flat_begin[kMaxLaunchSeqs + 1];
+    int32_t wfirst[kMaxLaunchSeqs];
+    int32_t flat_wgs;
 };
 
 // A GQA decode step in one launch: pass 1 as AttendParams describes it, and
