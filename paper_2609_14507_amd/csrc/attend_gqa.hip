@@ -207,12 +207,26 @@ __device__ __forceinline__ void step_tail(const AttendParams &p, const StepTail 
 #pragma unroll
         for (int c = 0; c < kTailRegs; ++c)
             if (c < nc) acc += s_w[hh][c] * pr[j][c];
+        // the rest, kTailRegs partials at a time, every load of a batch
+        // issued before any is used
         const float *e0 = po + (int64_t)hh * kHeadDim + 4 * c4;
-        for (int c = kTailRegs; c < nc; ++c) {
-            const float w = c < kTailW ? s_w[hh][c]
+        for (int c0 = kTailRegs; c0 < nc; c0 += kTailRegs) {
+            f32x4 b[kTailRegs];
+            float wb[kTailRegs];
+#pragma unroll
+            for (int k = 0; k < kTailRegs; ++k) {
+                const int c = c0 + k;
+                b[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+                wb[k] = 0.f;
+                if (c < nc) {
+                    const float *e = e0 + c * cstride;
+                    b[k] = f32x4{coherent_load(e), coherent_load(e + 1), coherent_load(e + 2), coherent_load(e + 3)};
+                    wb[k] = c < kTailW ? s_w[hh][c]
                                        : __expf(coherent_load(p.part_lse + (int64_t)(pb + c) * H + h0 + hh) - m);
-            const float *e = e0 + c * cstride;
-            acc += w * f32x4{coherent_load(e), coherent_load(e + 1), coherent_load(e + 2), coherent_load(e + 3)};
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kTailRegs; ++k) acc += wb[k] * b[k];
         }
         reinterpret_cast<f32x4 *>(t.o + row * kHeadDim)[c4] = acc * inv;
     }
@@ -508,8 +522,9 @@ __device__ __forceinline__ void attend(const AttendParams &p, const StepTail *st
     if constexpr (FLAT) {
         // Segments in sequence order; a decode step counts the workgroup in
         // after each, so a workgroup that crosses into the next sequence has
-        // arrived for the previous one before it streams on, and finishes
-        // pass 2 of the sequences it arrived last for after its last segment.
+        // arrived for the previous one before it streams on.  Pass 2 of the
+        // last segment's sequence follows at once when it is the last
+        // arrival; that of an earlier one, after the last segment.
         __shared__ int s_fin[kMaxLaunchSeqs];
         int n_fin = 0;
         const int w = blockIdx.x / units;
@@ -517,13 +532,25 @@ __device__ __forceinline__ void attend(const AttendParams &p, const StepTail *st
         const int64_t total = p.flat_begin[p.n];
         const int lo = (int)(w * total / p.flat_wgs);
         const int hi = (int)((w + 1) * total / p.flat_wgs);
-        for (int i = 0; i < p.n; ++i) {
+        auto has_segment = [&](int i, int &a, int &b) {
             const int fb = p.flat_begin[i];
             const int nt = seq_tiles(p, i);
-            const int a = nt ? max(fb, lo) - fb : 0;
-            const int b = nt ? min(fb + nt, hi) - fb : 0;
-            const bool go = nt ? a < b : STEP && p.wfirst[i] == w;
-            if (!go) continue;
+            a = nt ? max(fb, lo) - fb : 0;
+            b = nt ? min(fb + nt, hi) - fb : 0;
+            return nt ? a < b : STEP && p.wfirst[i] == w;
+        };
+        // a decode step takes its last segment out of the loop, so that the
+        // register-heavy pass 2 is not inside it
+        int i_last = p.n;
+        if constexpr (STEP) {
+            for (int i = 0; i < p.n; ++i) {
+                int a, b;
+                if (has_segment(i, a, b)) i_last = i;
+            }
+        }
+        for (int i = 0; i < i_last; ++i) {
+            int a, b;
+            if (!has_segment(i, a, b)) continue;
             segment(i, u, a, b, p.chunk_begin[i] + (w - p.wfirst[i]));
             __syncthreads();   // s_o, s_m, s_l are free again
             if constexpr (STEP) {
@@ -531,6 +558,19 @@ __device__ __forceinline__ void attend(const AttendParams &p, const StepTail *st
                     if (threadIdx.x == 0) s_fin[n_fin] = i;
                     ++n_fin;
                 }
+            }
+        }
+        if constexpr (STEP) {
+            if (i_last < p.n) {
+                const int i = i_last;
+                int a, b;
+                has_segment(i, a, b);
+                segment(i, u, a, b, p.chunk_begin[i] + (w - p.wfirst[i]));
+                __syncthreads();
+                // pass 2's inputs overlap the wait, as for per-sequence chunks
+                const TailIn<GH> tin = tail_inputs<GH>(p, *st, i, u);
+                if (count_in(p, *st, i, u, units)) finish<GH>(p, *st, tin, i, u);
+                __syncthreads();
             }
         }
         if constexpr (STEP) {
