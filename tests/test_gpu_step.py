@@ -386,6 +386,54 @@ def test_decode_step_mla_expand_empty_gpu_side():
             assert_lse(lse[b], l_r, "empty-side b%d" % b)
 
 
+def test_decode_step_flat_split_many_short_one_long():
+    """A batch the per-sequence chunking handles badly: 70 sequences (two launches), most with a
+    few GPU-side tiles, one of ~610 tiles in each launch, and one with nothing on the GPU side
+    before the step.  Every non-empty range starting with a chunk of its own leaves the first
+    launch's long sequence a single chunk, so the planner takes the flat split there (its runs
+    cross from short sequence to short sequence, several segments per workgroup); the premise is
+    asserted from the workspace size (the flat split writes more partials).  Two decode steps
+    against the fp64 oracle, and a twin cache driven by wsk_append + wsk_attend_gpu (pass 1 alone,
+    the same split) with close outputs and a byte-identical pool."""
+    B, H = 70, 8
+    gen = torch.Generator().manual_seed(51)
+    lengths = [int(x) for x in torch.randint(100, 330, (B,), generator=gen)]
+    splits = [int(x) for x in torch.randint(0, 64, (B,), generator=gen)]
+    for b in (3, 66):
+        lengths[b], splits[b] = 40000, 1000
+    lengths[9], splits[9] = 700, 700          # nothing on the GPU side before the first step
+    w = wl.Workload("step-gqa-flat", wl.GQA, batch=B, n_q_heads=H, n_kv_heads=4, head_dim=128, context=1, seed=52)
+    pf = _prefill(w, lengths, splits, gen)
+    k_all, v_all = list(pf.k), list(pf.v)
+    dv, g = _dims(w)
+    say("case decode step, flat split")
+    with DecodeSession(w, pf, DEV, extra_tokens=3) as sess, DecodeSession(w, pf, DEV, extra_tokens=3) as twin:
+        need = wsk.wsk_decode_step_workspace(sess.h, sess.ids)
+        r256 = lambda x: (x + 255) // 256 * 256
+        partials = max(p for p in range(1, 8192) if r256(p * H * dv * 4) + r256(p * H * 4) <= need)
+        say("  %d chunk partials (one per range would be %d)" % (partials, B))
+        assert partials >= B + 20, partials
+        for step in range(2):
+            q_bits = wl.draw_bf16(gen, (B, H, w.row_elems))
+            kn, vn = _new_rows(w, B, gen)
+            q, knd, vnd = (to_device_bf16(x, sess.dev) for x in (q_bits, kn, vn))
+            o_x, l_x = _cpu_partial(sess, q_bits)
+            o, lse = _step(sess, q, knd, vnd, o_x, l_x)
+            twin.append(knd, vnd)
+            o2, lse2 = twin.attend_gpu(q, o_x=o_x, lse_x=l_x)
+            o, lse, o2, lse2 = (t.cpu().numpy() for t in (o, lse, o2, lse2))
+            for b in range(B):
+                k_all[b] = np.concatenate([k_all[b], kn[b:b + 1]])
+                v_all[b] = np.concatenate([v_all[b], vn[b:b + 1]])
+                o_r, l_r = oracle.attend(q_bits[b], k_all[b], v_all[b], 0, sess.lengths[b], w.softmax_scale, g,
+                                         dv=dv)
+                assert_close(o[b], o_r, "flat split step %d b%d" % (step, b))
+                assert_lse(lse[b], l_r, "flat split step %d b%d" % (step, b))
+            assert np.abs(o - o2).max() <= 1e-5 and np.abs(lse - lse2).max() <= 1e-5
+            torch.cuda.synchronize()
+            assert np.array_equal(_gpu_pool(sess), _gpu_pool(twin))
+
+
 def test_decode_step_more_chunks_than_weights_kept():
     """GQA decode step with one KV head (one (KV head, head group) unit, so the whole grid serves
     one sequence): a long sequence cut into more than 64 chunk partials -- more than the weights
