@@ -36,11 +36,12 @@
 // consumed the current ones, and the next V loads right after P.V.
 //
 // gqa_step_kernel is the same pass 1 with a decode step's pass 2 folded in
-// (Sec. 4.2: one LSE join per step): the last workgroup of each (sequence,
-// KV head, head group) to finish -- counted with a device-scope atomic after
-// a device-scope fence -- merges the chunk partials of its heads with the
-// step's new token and the CPU partial and stores the new row into the pool.
-// The step then costs one launch instead of two.
+// (Sec. 4.2: one LSE join per step): every workgroup stores its partial
+// device-coherent, waits for the stores and counts itself on a device-scope
+// atomic; the last of each (sequence, KV head, head group) merges the chunk
+// partials of its heads with the step's new token and the CPU partial and
+// stores the new row into the pool.  The step then costs one launch instead
+// of two, and no L2-wide fence.
 
 #include "device_rows.h"
 
@@ -65,9 +66,10 @@ __device__ __forceinline__ float coherent_load(const float *a) {
 }
 
 // What pass 2 of a decode step reads besides the chunk partials, for heads
-// h0 .. h0 + GH - 1 of launch-local sequence i (KV head g): loaded by every
-// workgroup before it is counted, so that these loads overlap the wait for
-// its partial stores; only the last workgroup uses them.
+// h0 .. h0 + GH - 1 of launch-local sequence i (KV head g): loaded after a
+// workgroup's last segment, before it is counted, so that these loads
+// overlap the wait for its partial stores; only the last workgroup uses
+// them.
 template <int GH>
 struct TailIn {
     static constexpr int kItems = (GH * 32 + 255) / 256;           // float4 output columns per thread

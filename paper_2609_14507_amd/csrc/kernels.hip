@@ -168,7 +168,9 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int
 }
 
 // ---------------------------------------------------------------------------
-// Pass 2 of a decode step.  Workgroup (sequence i, head h, column slice) as
+// Pass 2 of a decode step run as two launches (GQA with load-region blocks
+// streamed, MLA inside step_expand_kernel; a GQA step over HBM alone folds
+// this into gqa_step_kernel).  Workgroup (sequence i, head h, column slice) as
 // in combine_kernel; it also scores the step's new token against its query
 // row (q . k_new, fp32 from bf16, the whole row, formed by each wavefront
 // with shuffles), merges that token as one more partial, and -- in the

@@ -107,10 +107,11 @@ struct CombineParams {
     int32_t chunk_begin[kMaxLaunchSeqs + 1];
 };
 
-// Pass 2 of a decode step: the chunk combine, plus the step's new token of
-// every sequence taken straight from its input row (its score q.k_new and its
-// value row enter as one more partial), plus the append of that row into the
-// GPU pool (as AppendParams describes it).
+// Pass 2 of a decode step run as its own launch (a GQA step that streams
+// load-region blocks; the MLA step's step_expand_kernel): the chunk combine,
+// plus the step's new token of every sequence taken straight from its input
+// row (its score q.k_new and its value row enter as one more partial), plus
+// the append of that row into the GPU pool (as AppendParams describes it).
 struct StepCombineParams {
     CombineParams cp;
     const uint16_t *q;       // launch-local query rows, q_row elements per sequence
