@@ -551,15 +551,17 @@ int wsk_decode_step_mla(wsk_cache *cache, int32_t n, const int32_t *seq_ids, con
  * order seq_ids lists them in), blocks ascending -- the order wsk_append
  * uses; a block that already has a slot there (the CPU slot of the block
  * holding s) keeps it.  The batch's GPU-pool slots are
- * freed.  A kernel on stream first gathers the batch's slots, scattered
- * in HBM, into the cache's device staging buffer in destination order.  To
- * the load region they then travel unchanged (the layouts match) as one
- * device -> host DMA per run of consecutive load slots, straight into the
- * pinned slots.  To the CPU the same kernel rewrites them into the CPU
- * pool's token-major rows; they are sent in ~2 MB pieces into a pinned
- * bounce (pinned once, at wsk_init, for caches with evict_tokens > 0), and
- * the host copies each piece's rows into their slots as soon as it lands;
- * the call returns when they are in place.  The part chosen per batch is
+ * freed.  A kernel on stream gathers the batch's slots, scattered in HBM,
+ * in destination order and stores them straight into pinned host memory
+ * over the link (where that memory is mapped for the device at its host
+ * address; else into the cache's device staging buffer, followed by
+ * device -> host DMAs).  To the load region they travel unchanged (the
+ * layouts match), one kernel per run of consecutive load slots, into the
+ * pinned slots.  To the CPU the kernel rewrites them into the CPU pool's
+ * token-major rows, in ~2 MB pieces into a pinned bounce (pinned once, at
+ * wsk_init, for caches with evict_tokens > 0), and the host copies each
+ * piece's rows into their slots as soon as it lands; the call returns when
+ * they are in place.  The part chosen per batch is
  * the caller's: wsk_policy_route_batch gives the paper's roofline routing.
  * Later writes that reuse the freed slots must be ordered after this call on
  * stream.  seq_ids (distinct, open), part, moved: HOST arrays.  Needs

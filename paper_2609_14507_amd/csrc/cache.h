@@ -65,6 +65,7 @@ struct wsk_cache {
 
     // ---- load region (pinned host, GPU slot layout) and its streaming ----
     std::vector<uint16_t *> arenas;       // arena k holds slots [k * A, (k + 1) * A)
+    std::vector<uint8_t> arena_mapped;    // arena k is mapped for the device at its host address
     int64_t pinned_bytes = 0;
     double pin_seconds = 0.0;
     int32_t *dident = nullptr;            // device identity table 0 .. pingpong_blocks - 1
@@ -78,6 +79,7 @@ struct wsk_cache {
     uint16_t *hbounce = nullptr;          // pinned bounce of evictions into the CPU pool
     size_t hbounce_bytes = 0;
     hipEvent_t bounce_ev[8] = {};         // pieces of one eviction round landed in the bounce
+    bool bounce_mapped = false;           // the bounce is mapped for the device at its host address
     int64_t h2d_bytes = 0, d2h_bytes = 0; // load-region traffic since init
 };
 

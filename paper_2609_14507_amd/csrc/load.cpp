@@ -27,6 +27,13 @@ using namespace wsk;
 
 namespace {
 
+// Whether pinned host memory at p is mapped for the device at the same
+// address, so that a kernel can store into it directly.
+bool device_maps(void *p) {
+    void *d = nullptr;
+    return hipHostGetDevicePointer(&d, p, 0) == hipSuccess && d == p;
+}
+
 // ---- GPU slot layouts, host side -------------------------------------------
 // Pieces are 16 bytes (8 bf16).  GQA (64-token tiles, per KV head): K piece j
 // (dims 8j..8j+7) of token t, and V element (t, d); MLA (32-token tiles):
@@ -106,6 +113,7 @@ int pin_arena(wsk_cache *c, size_t k) {
     c->pin_seconds += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
     c->pinned_bytes += (int64_t)bytes;
     c->arenas[k] = (uint16_t *)p;
+    c->arena_mapped[k] = c->device >= 0 && device_maps(p);
     return WSK_OK;
 }
 
@@ -137,6 +145,7 @@ int wsk::load_ensure(wsk_cache *c, const std::vector<Pending> &pend) {
 int wsk::load_init(wsk_cache *c) {
     const int64_t A = arena_blocks(c);
     c->arenas.assign((size_t)((c->spec.load_pool_blocks + A - 1) / A), nullptr);
+    c->arena_mapped.assign(c->arenas.size(), 0);
     if (c->device < 0) return WSK_OK;
     DeviceGuard guard(c->device);
     if (guard.err != hipSuccess) return hip_fail(guard.err, "hipSetDevice");
@@ -183,6 +192,7 @@ int wsk::evict_init(wsk_cache *c) {
     if (e != hipSuccess) return hip_fail(e, "pinned eviction bounce");
     c->hbounce_bytes = bytes;
     memset(c->hbounce, 0, bytes);
+    c->bounce_mapped = device_maps(c->hbounce);
     for (hipEvent_t &ev : c->bounce_ev) {
         e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
         if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
@@ -869,10 +879,12 @@ int wsk_flush(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *part, 
     // destination order (one kernel for all of them, HBM-resident slots are
     // scattered), then sent device -> host
     const size_t cap = evict_round_blocks(c);
-    const auto gather = [&](const std::vector<Mv> &v, size_t j0, size_t m, bool rows) {
+    // blocks j0 .. j0 + m - 1 of v, one after another from dst (the device
+    // staging buffer, or pinned host memory mapped for the device)
+    const auto gather = [&](const std::vector<Mv> &v, size_t j0, size_t m, bool rows, uint16_t *dst) {
         EvictParams ep{};
         ep.pool = c->dpool;
-        ep.stage = c->dstage;
+        ep.stage = dst;
         ep.slot_elems = c->slot_elems;
         ep.m = (int32_t)m;
         ep.kind = c->spec.kind;
@@ -883,18 +895,28 @@ int wsk_flush(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *part, 
         for (size_t k = 0; k < m; ++k) ep.src_slot[k] = v[j0 + k].src;
         return launch_evict(ep, st);
     };
-    // to the load region (same slot layout): one DMA per run of consecutive
-    // load slots of one arena, straight into the pinned slots
+    // to the load region (same slot layout), per run of consecutive load
+    // slots of one arena: the gather kernel stores the run straight into the
+    // pinned slots over the link when the arena is mapped for the device;
+    // else it gathers into the device staging buffer and one DMA per run
+    // follows.  (A copy launched after the kernel leaves the link idle for
+    // tens of microseconds first.)
     for (size_t j0 = 0; j0 < to_load.size() && e == hipSuccess; j0 += cap) {
         const size_t m = std::min(cap, to_load.size() - j0);
-        e = gather(to_load, j0, m, false);
+        bool all_mapped = true;
+        for (size_t j = 0; j < m; ++j) all_mapped &= c->arena_mapped[to_load[j0 + j].dst / arena_blocks(c)] != 0;
+        if (!all_mapped) e = gather(to_load, j0, m, false, c->dstage);
         for (size_t j = 0; j < m && e == hipSuccess;) {
             size_t r = j + 1;
             while (r < m && to_load[j0 + r].dst == to_load[j0 + r - 1].dst + 1 &&
                    to_load[j0 + r].dst % arena_blocks(c) != 0)
                 ++r;
-            e = hipMemcpyAsync(load_slot_ptr(c, to_load[j0 + j].dst), c->dstage + (int64_t)j * c->slot_elems,
-                               (r - j) * sb, hipMemcpyDeviceToHost, st);
+            uint16_t *slot = load_slot_ptr(c, to_load[j0 + j].dst);
+            if (all_mapped)
+                e = gather(to_load, j0 + j, r - j, false, slot);
+            else
+                e = hipMemcpyAsync(slot, c->dstage + (int64_t)j * c->slot_elems, (r - j) * sb, hipMemcpyDeviceToHost,
+                                   st);
             c->d2h_bytes += (int64_t)((r - j) * sb);
             j = r;
         }
@@ -912,6 +934,7 @@ int wsk_flush(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *part, 
             c->hbounce_bytes = 0;
             e = hipHostMalloc((void **)&c->hbounce, bytes, hipHostMallocDefault);
             if (e == hipSuccess) c->hbounce_bytes = bytes;
+            c->bounce_mapped = e == hipSuccess && device_maps(c->hbounce);
         }
         const bool mla = c->spec.kind == WSK_KIND_MLA;
         const int runs = mla ? 1 : 2 * c->spec.n_kv_heads;   // (head, K | V) row runs per slot
@@ -919,12 +942,19 @@ int wsk_flush(wsk_cache *c, int32_t n, const int32_t *ids, const int32_t *part, 
         for (size_t j0 = 0; j0 < to_cpu.size() && e == hipSuccess; j0 += cap) {
             const size_t m = std::min(cap, to_cpu.size() - j0);
             const size_t per = std::max((m + n_ev - 1) / n_ev, std::max<size_t>(1, (2u << 20) / sb));
-            e = gather(to_cpu, j0, m, true);
+            // the rows go straight into the bounce, a kernel per piece, when
+            // it is mapped for the device; else through the device staging
+            // buffer and one DMA per piece
+            const bool direct = c->bounce_mapped;
+            if (!direct) e = gather(to_cpu, j0, m, true, c->dstage);
             size_t pieces = 0;
             for (size_t a = 0; a < m && e == hipSuccess; a += per, ++pieces) {
                 const size_t k = std::min(per, m - a);
-                e = hipMemcpyAsync(c->hbounce + (int64_t)a * c->slot_elems, c->dstage + (int64_t)a * c->slot_elems,
-                                   k * sb, hipMemcpyDeviceToHost, st);
+                if (direct)
+                    e = gather(to_cpu, j0 + a, k, true, c->hbounce + (int64_t)a * c->slot_elems);
+                else
+                    e = hipMemcpyAsync(c->hbounce + (int64_t)a * c->slot_elems, c->dstage + (int64_t)a * c->slot_elems,
+                                       k * sb, hipMemcpyDeviceToHost, st);
                 if (e == hipSuccess) e = hipEventRecord(c->bounce_ev[pieces], st);
             }
             // one parallel region for the round: the tasks are the blocks in
