@@ -137,20 +137,20 @@ def wsk_mod():
 # were taken on (sha256), null otherwise.
 TRAFFIC = {
     # the decode steps' roofline kernel: gqa_step_kernel (timed steps)
-    "c5": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "70b3c53db3ce5d1408d4cce0d32bc8173363306641602cb5adbd6142e59c1962",
-           "fetch_bytes": 622067.2 * 1024 * 2.0, "write_bytes": 1151.9 * 1024 * 1.0, "kv_bytes": 1270605824},
-    "c2": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "70b3c53db3ce5d1408d4cce0d32bc8173363306641602cb5adbd6142e59c1962",
-           "fetch_bytes": 369621.9 * 1024 * 2.0, "write_bytes": 1242.0 * 1024 * 1.0, "kv_bytes": 751976448},
-    "c1": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "70b3c53db3ce5d1408d4cce0d32bc8173363306641602cb5adbd6142e59c1962",
+    "c5": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
+           "fetch_bytes": 622066.2 * 1024 * 2.0, "write_bytes": 1151.9 * 1024 * 1.0, "kv_bytes": 1270605824},
+    "c2": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
+           "fetch_bytes": 369622.1 * 1024 * 2.0, "write_bytes": 1242.0 * 1024 * 1.0, "kv_bytes": 751976448},
+    "c1": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
            "fetch_bytes": 647.4 * 1024 * 2.0, "write_bytes": 30.5 * 1024 * 1.0, "kv_bytes": 1059328},
     # the sweep's and the MLA step's roofline kernel: pass 1 (launches alone)
-    "c3 r=0.00": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "70b3c53db3ce5d1408d4cce0d32bc8173363306641602cb5adbd6142e59c1962",
+    "c3 r=0.00": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
            "fetch_bytes": 1048909.0 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 2147483648},
-    "c3 r=0.25": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "70b3c53db3ce5d1408d4cce0d32bc8173363306641602cb5adbd6142e59c1962",
+    "c3 r=0.25": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
            "fetch_bytes": 786701.0 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 1610612736},
-    "c3 r=0.50": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "70b3c53db3ce5d1408d4cce0d32bc8173363306641602cb5adbd6142e59c1962",
+    "c3 r=0.50": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
            "fetch_bytes": 524493.0 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 1073741824},
-    "c3 r=0.75": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "70b3c53db3ce5d1408d4cce0d32bc8173363306641602cb5adbd6142e59c1962",
+    "c3 r=0.75": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
            "fetch_bytes": 262285.0 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 536870912},
     "c4": {"source": "paper_2609_14507_amd/csrc/attend_mla.hip", "sha256": "4df8a57ec4065ad10e72b3e174e71bce14707792ab7dea83e03b7889f82faa92",
            "fetch_bytes": 177748.1 * 1024 * 2.0, "write_bytes": 8208.0 * 1024 * 1.0, "kv_bytes": 362575872},
