@@ -180,7 +180,42 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams p, int
 // dot product's and the new row's are issued before any is used; the row is
 // stored after the combine.
 // ---------------------------------------------------------------------------
-constexpr int kMaxRowPerLane = (kLatent + kRope + 63) / 64;   // 9: the widest row over 64 lanes
+// The two rows of a q . k product, as 16-byte pieces: lane l holds pieces l
+// and l + 64 (zero past the row's re / 8; re <= 1024, the widest row here is
+// MLA's 576).  Rows start 16-byte aligned.
+struct RowPair {
+    u32x4 q0, k0, q1, k1;
+};
+__device__ __forceinline__ RowPair load_row_pair(const uint16_t *q, const uint16_t *k, int re) {
+    const int lane = threadIdx.x & 63;
+    const int np = re / 8;
+    const u32x4 *q16 = reinterpret_cast<const u32x4 *>(q), *k16 = reinterpret_cast<const u32x4 *>(k);
+    RowPair r;
+    r.q0 = r.k0 = r.q1 = r.k1 = u32x4{0u, 0u, 0u, 0u};
+    if (lane < np) {
+        r.q0 = q16[lane];
+        r.k0 = k16[lane];
+    }
+    if (lane + 64 < np) {
+        r.q1 = q16[lane + 64];
+        r.k1 = k16[lane + 64];
+    }
+    return r;
+}
+// q . k in fp32 from the bf16 pieces, the same sum in every lane
+__device__ __forceinline__ float row_dot(const RowPair &r) {
+    float d = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        d = fmaf(__uint_as_float(r.q0[e] << 16), __uint_as_float(r.k0[e] << 16), d);
+        d = fmaf(__uint_as_float(r.q0[e] & 0xffff0000u), __uint_as_float(r.k0[e] & 0xffff0000u), d);
+        d = fmaf(__uint_as_float(r.q1[e] << 16), __uint_as_float(r.k1[e] << 16), d);
+        d = fmaf(__uint_as_float(r.q1[e] & 0xffff0000u), __uint_as_float(r.k1[e] & 0xffff0000u), d);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) d += __shfl_xor(d, o);
+    return d;
+}
 
 __global__ __launch_bounds__(256) void step_combine_kernel(const StepCombineParams sp, int width) {
     __shared__ float s_w[kCombineW];
@@ -207,19 +242,7 @@ __global__ __launch_bounds__(256) void step_combine_kernel(const StepCombinePara
     u32x4 pv = u32x4{0u, 0u, 0u, 0u};
     if (append && tid < n_pieces) pv = reinterpret_cast<const u32x4 *>(which ? vr : kr)[piece];
     // every wavefront forms the whole dot product (no barrier on this path)
-    const int lane = tid & 63;
-    uint16_t qe[kMaxRowPerLane], ke[kMaxRowPerLane];
-#pragma unroll
-    for (int j = 0; j < kMaxRowPerLane; ++j) {
-        const int e = lane + 64 * j;
-        qe[j] = e < re ? qr[e] : (uint16_t)0;
-        ke[j] = e < re ? kr[e] : (uint16_t)0;
-    }
-    float d = 0.f;
-#pragma unroll
-    for (int j = 0; j < kMaxRowPerLane; ++j) d = fmaf(bf16_to_f32(qe[j]), bf16_to_f32(ke[j]), d);
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) d += __shfl_xor(d, o);
+    const float d = row_dot(load_row_pair(qr, kr, re));
     combine_finish(sp.cp, width, in, d * sp.scale, s_w, s_red, s_acc);
     if (append) {
         if (tid == 0 && h == 0 && sp.tab_index[i] >= 0) sp.table[sp.tab_index[i]] = sp.tab_slot[i];
@@ -236,12 +259,16 @@ __global__ __launch_bounds__(256) void step_combine_kernel(const StepCombinePara
 // ---------------------------------------------------------------------------
 // Pass 2 of an MLA decode step with the output expansion folded in (Sec. 6.1:
 // the merged latent output is expanded by W_UV[h], which commutes with the
-// merge).  One workgroup per (sequence i, head h) merges all 512 latent
-// columns -- the chunk partials, the CPU partial and the step's new row, as
-// step_combine_kernel does per 128-column slice -- and multiplies the merged
-// row by W_UV[h] (dv columns).  The weight rows are loaded first, together
-// with everything the merge reads, so their latency overlaps the merge; the
-// workgroup of head 0 also stores the new row into the GPU pool.
+// merge).  Workgroup (sequence i, head h, slice y of DVS output columns)
+// merges all 512 latent columns -- the chunk partials, the CPU partial and
+// the step's new row, as step_combine_kernel does per 128-column slice -- and
+// multiplies the merged row by columns [y DVS, (y + 1) DVS) of W_UV[h].  The
+// slices of one (i, h) repeat the merge, which reads far less than W_UV[h]:
+// slicing spreads the weight reads over more compute units when the batch
+// leaves some idle.  Loads go out in the order they are used -- the merge's
+// scalars, the chunk partials, the weights -- so the merge runs while the
+// weights arrive; slice 0 stores the latent row and its LSE, and that of
+// head 0 also stores the new row into the GPU pool.
 // ---------------------------------------------------------------------------
 constexpr int kSxThreads = 512;
 constexpr int kSxWaves = kSxThreads / 64;
@@ -264,75 +291,69 @@ __device__ __forceinline__ float sx_block_reduce(float v, bool is_max, float *s_
     return r;
 }
 
-template <int DV>
+template <int DVS>
 __global__ __launch_bounds__(kSxThreads) void step_expand_kernel(const StepExpandParams xp) {
-    constexpr int kCg = DV / 8;                      // 16-byte column groups of a W_UV row
+    constexpr int kCg = DVS / 8;                     // 16-byte column groups of a W_UV row slice
     constexpr int kRg = kSxThreads / kCg;            // row groups
     constexpr int kRows = kLatent / kRg;             // W_UV rows per thread
+    constexpr int kParts = kSxThreads / DVS;         // threads per output column in the final sum
+    static_assert(kRg % kParts == 0 && kRg / kParts == 8, "each first-level sum adds 8 row groups");
     __shared__ float s_w[kCombineW];
     __shared__ float s_red[kSxWaves];
     __shared__ f32x4 s_acc[kSxGroups][kSxCols4];
     __shared__ float s_lat[kLatent];
-    __shared__ float s_out[kRg][DV];
+    __shared__ float s_out[kRg][DVS];
     const StepCombineParams &sp = xp.sc;
     const CombineParams &p = sp.cp;
     const int H = p.n_q_heads;
     const int row = blockIdx.x;                      // i * H + h
     const int i = row / H;
     const int h = row - i * H;
+    const int col0 = blockIdx.y * DVS;
+    const bool lead = blockIdx.y == 0;               // stores the latent row, its LSE and the new row
     const int tid = threadIdx.x;
     const int re = sp.row_elems;                     // 576
     const uint16_t *kr = sp.k_new + (int64_t)i * re;
     const uint16_t *qr = sp.q + (int64_t)i * sp.q_row + (int64_t)h * re;
 
-    // ---- every load first: W_UV rows, chunk partials and LSEs, CPU partial,
-    //      the new row (its value columns, its score's operands, its pieces) ----
-    const int rg = tid / kCg, cg = tid - (tid / kCg) * kCg;
-    const uint16_t *wrow = xp.w_uv + (int64_t)h * kLatent * DV + 8 * cg;
-    u32x4 wv[kRows];
-#pragma unroll
-    for (int j = 0; j < kRows; ++j) wv[j] = *reinterpret_cast<const u32x4 *>(wrow + (int64_t)(rg + kRg * j) * DV);
+    // ---- loads, in the order they are used: the new row's score operands,
+    //      chunk LSEs, CPU partial, new row; chunk partials; W_UV rows ----
+    // (loads whose lanes differ in whether they are needed read a valid
+    // stand-in address instead, and their values are then left unused: no
+    // branch, so none waits for the loads issued before it)
+    const RowPair qk = load_row_pair(qr, kr, re);
     const int c0 = p.chunk_begin[i];
     const int nc = p.chunk_begin[i + 1] - c0;
+    const float lse_r = *(tid < nc ? p.part_lse + (int64_t)(c0 + tid) * H + h : p.lse + row);
+    const float lse_c = tid < nc ? lse_r : -INFINITY;
+    const float lx = p.lse_x ? p.lse_x[row] : -INFINITY;
     const int g = tid / kSxCols4;
     const int c4 = tid - g * kSxCols4;
+    const f32x4 ox = p.o_x ? reinterpret_cast<const f32x4 *>(p.o_x + (int64_t)row * kLatent)[c4]
+                           : f32x4{0.f, 0.f, 0.f, 0.f};
+    const uint2 v2 = reinterpret_cast<const uint2 *>(kr)[c4];
+    const f32x4 vn = f32x4{__uint_as_float(v2.x << 16), __uint_as_float(v2.x & 0xffff0000u),
+                           __uint_as_float(v2.y << 16), __uint_as_float(v2.y & 0xffff0000u)};
+    const bool append = lead && h == 0;
+    const int n_pieces = re / 8;
+    const u32x4 pv = reinterpret_cast<const u32x4 *>(kr)[min(tid, n_pieces - 1)];
     const f32x4 *po = reinterpret_cast<const f32x4 *>(p.part_o + ((int64_t)c0 * H + h) * kLatent) + c4;
+    const f32x4 *stand_in = reinterpret_cast<const f32x4 *>(xp.w_uv);
     const int64_t cstride = (int64_t)H * kLatent / 4;
     f32x4 pr[kSxRegs];
 #pragma unroll
     for (int j = 0; j < kSxRegs; ++j) {
         const int c = g + kSxGroups * j;
-        pr[j] = c < nc ? po[c * cstride] : f32x4{0.f, 0.f, 0.f, 0.f};
+        pr[j] = *(c < nc ? po + c * cstride : stand_in);
     }
-    const float lse_c = tid < nc ? p.part_lse[(int64_t)(c0 + tid) * H + h] : -INFINITY;
-    const float lx = p.lse_x ? p.lse_x[row] : -INFINITY;
-    f32x4 ox = f32x4{0.f, 0.f, 0.f, 0.f}, vn = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (g == 0) {
-        if (p.o_x) ox = reinterpret_cast<const f32x4 *>(p.o_x + (int64_t)row * kLatent)[c4];
-        const uint2 v2 = reinterpret_cast<const uint2 *>(kr)[c4];
-        vn = f32x4{__uint_as_float(v2.x << 16), __uint_as_float(v2.x & 0xffff0000u), __uint_as_float(v2.y << 16),
-                   __uint_as_float(v2.y & 0xffff0000u)};
-    }
-    const bool append = h == 0;
-    const int n_pieces = re / 8;
-    u32x4 pv = u32x4{0u, 0u, 0u, 0u};
-    if (append && tid < n_pieces) pv = reinterpret_cast<const u32x4 *>(kr)[tid];
-    const int lane = tid & 63;
-    uint16_t qe[kMaxRowPerLane], ke[kMaxRowPerLane];
+    const int rg = tid / kCg, cg = tid - (tid / kCg) * kCg;
+    const uint16_t *wrow = xp.w_uv + (int64_t)h * kLatent * xp.dv + col0 + 8 * cg;
+    u32x4 wv[kRows];
 #pragma unroll
-    for (int j = 0; j < kMaxRowPerLane; ++j) {
-        const int e = lane + 64 * j;
-        qe[j] = e < re ? qr[e] : (uint16_t)0;
-        ke[j] = e < re ? kr[e] : (uint16_t)0;
-    }
+    for (int j = 0; j < kRows; ++j) wv[j] = *reinterpret_cast<const u32x4 *>(wrow + (int64_t)(rg + kRg * j) * xp.dv);
 
     // ---- the new row's score (every wavefront forms the whole dot product) ----
-    float d = 0.f;
-#pragma unroll
-    for (int j = 0; j < kMaxRowPerLane; ++j) d = fmaf(bf16_to_f32(qe[j]), bf16_to_f32(ke[j]), d);
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) d += __shfl_xor(d, o);
-    const float s_new = d * sp.scale;
+    const float s_new = row_dot(qk) * sp.scale;
 
     // ---- merge: O_lat = (sum_c w_c O_c + w_x O_x + w_n v_new) / sum w ----
     const float *pl = p.part_lse + (int64_t)c0 * H + h;
@@ -376,12 +397,12 @@ __global__ __launch_bounds__(kSxThreads) void step_expand_kernel(const StepExpan
         for (int gg = 1; gg < kSxGroups; ++gg) t += s_acc[gg][tid];
         t = empty ? f32x4{0.f, 0.f, 0.f, 0.f} : t * (1.f / den);
         reinterpret_cast<f32x4 *>(s_lat)[tid] = t;
-        if (p.o) reinterpret_cast<f32x4 *>(p.o + (int64_t)row * kLatent)[tid] = t;
+        if (lead && p.o) reinterpret_cast<f32x4 *>(p.o + (int64_t)row * kLatent)[tid] = t;
     }
-    if (tid == 0) p.lse[row] = empty ? -INFINITY : m + __logf(den);
+    if (lead && tid == 0) p.lse[row] = empty ? -INFINITY : m + __logf(den);
     __syncthreads();
 
-    // ---- O[i][h] = W_UV[h]^T O_lat: row group rg sums its rows for 8 columns ----
+    // ---- O[i][h][col0 ..] = W_UV[h]^T O_lat: row group rg sums its rows for 8 columns ----
     float a8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < kRows; ++j) {
@@ -395,11 +416,20 @@ __global__ __launch_bounds__(kSxThreads) void step_expand_kernel(const StepExpan
 #pragma unroll
     for (int e = 0; e < 8; ++e) s_out[rg][8 * cg + e] = a8[e];
     __syncthreads();
-    if (tid < DV) {
+    // the row groups' sums: 8 per thread into the first of them, then kParts per column
+    {
+        const int c = tid % DVS, q = tid / DVS;
+        float t = s_out[8 * q][c];
+#pragma unroll
+        for (int r = 1; r < 8; ++r) t += s_out[8 * q + r][c];
+        s_out[8 * q][c] = t;
+    }
+    __syncthreads();
+    if (tid < DVS) {
         float t = s_out[0][tid];
-#pragma unroll 8
-        for (int r = 1; r < kRg; ++r) t += s_out[r][tid];
-        xp.o[(int64_t)row * DV + tid] = t;
+#pragma unroll
+        for (int q = 1; q < kParts; ++q) t += s_out[8 * q][tid];
+        xp.o[(int64_t)row * xp.dv + col0 + tid] = t;
     }
     if (append) {
         if (tid == 0 && sp.tab_index[i] >= 0) sp.table[sp.tab_index[i]] = sp.tab_slot[i];
@@ -750,10 +780,12 @@ hipError_t launch_step_combine(const StepCombineParams &p, int width, hipStream_
     return hipGetLastError();
 }
 
-hipError_t launch_step_expand(const StepExpandParams &p, hipStream_t s) {
+hipError_t launch_step_expand(const StepExpandParams &p, int slices, hipStream_t s) {
     if (p.sc.cp.n <= 0) return hipSuccess;
-    const dim3 grid(p.sc.cp.n * p.sc.cp.n_q_heads), block(kSxThreads);
-    switch (p.dv) {
+    if (slices <= 0 || p.dv % slices) return hipErrorInvalidValue;
+    const dim3 grid(p.sc.cp.n * p.sc.cp.n_q_heads, slices), block(kSxThreads);
+    switch (p.dv / slices) {
+        case 32: hipLaunchKernelGGL(step_expand_kernel<32>, grid, block, 0, s, p); break;
         case 64: hipLaunchKernelGGL(step_expand_kernel<64>, grid, block, 0, s, p); break;
         case 128: hipLaunchKernelGGL(step_expand_kernel<128>, grid, block, 0, s, p); break;
         case 256: hipLaunchKernelGGL(step_expand_kernel<256>, grid, block, 0, s, p); break;

@@ -751,7 +751,12 @@ int decode_step(wsk_cache *c, int32_t n, const int32_t *ids, const void *q, cons
             xp.w_uv = ex->w_uv;
             xp.o = ex->o + (int64_t)i0 * sp.n_q_heads * ex->dv;
             xp.dv = ex->dv;
-            e = launch_step_expand(xp, (hipStream_t)stream);
+            // split each (sequence, head) over up to 4 workgroups of >= 32
+            // output columns while the grid still fits the compute units
+            const int64_t rows = (int64_t)m * sp.n_q_heads;
+            int slices = 1;
+            while (slices < 4 && rows * slices * 2 <= c->cu_count && ex->dv / (slices * 2) >= 32) slices *= 2;
+            e = launch_step_expand(xp, slices, (hipStream_t)stream);
         } else {
             e = launch_step_combine(p, width, (hipStream_t)stream);
         }

@@ -230,7 +230,9 @@ hipError_t launch_gqa_step(const AttendParams &p, const StepTail &t, int heads_p
 hipError_t launch_mla_attend(const AttendParams &p, int n_wg, hipStream_t s);
 hipError_t launch_combine(const CombineParams &p, int width, hipStream_t s);
 hipError_t launch_step_combine(const StepCombineParams &p, int width, hipStream_t s);
-hipError_t launch_step_expand(const StepExpandParams &p, hipStream_t s);
+// slices: workgroups per (sequence, head), each expanding dv / slices columns
+// (32, 64, 128 or 256 of them)
+hipError_t launch_step_expand(const StepExpandParams &p, int slices, hipStream_t s);
 hipError_t launch_append(const AppendParams &p, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
 hipError_t launch_evict(const EvictParams &p, hipStream_t s);
