@@ -73,19 +73,24 @@ __device__ __forceinline__ CombineIn combine_load(const CombineParams &p, int wi
     const int col0 = blockIdx.y * 4 * kCombineCols4;
     CombineIn in;
     in.nc = p.chunk_begin[i + 1] - c0;
+    // loads that only some lanes need read a valid stand-in address (this
+    // workgroup's own output row) in the others, whose values go unused: no
+    // branch, so none waits for the loads issued before it
     const f32x4 *po = reinterpret_cast<const f32x4 *>(p.part_o + ((int64_t)c0 * H + h) * width + col0) + c4;
+    const f32x4 *stand_in = reinterpret_cast<const f32x4 *>(p.o + (int64_t)row * width + col0) + c4;
     const int64_t cstride = (int64_t)H * width / 4;
 #pragma unroll
     for (int j = 0; j < kCombineRegs; ++j) {
         const int c = g + kCombineGroups * j;
-        in.po[j] = c < in.nc ? po[c * cstride] : f32x4{0.f, 0.f, 0.f, 0.f};
+        in.po[j] = *(c < in.nc ? po + c * cstride : stand_in);
     }
-    in.lse_c = tid < in.nc ? p.part_lse[(int64_t)(c0 + tid) * H + h] : -INFINITY;
+    const float lse_r = *(tid < in.nc ? p.part_lse + (int64_t)(c0 + tid) * H + h : p.lse + row);
+    in.lse_c = tid < in.nc ? lse_r : -INFINITY;
     in.lx = p.lse_x ? p.lse_x[row] : -INFINITY;
-    in.ox = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (p.o_x && g == 0) in.ox = reinterpret_cast<const f32x4 *>(p.o_x + (int64_t)row * width + col0)[c4];
+    // (used by the lanes of chunk group 0 only)
+    in.ox = p.o_x ? reinterpret_cast<const f32x4 *>(p.o_x + (int64_t)row * width + col0)[c4] : f32x4{0.f, 0.f, 0.f, 0.f};
     in.vn = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (v_new && g == 0) {
+    if (v_new) {
         const uint2 v2 = reinterpret_cast<const uint2 *>(v_new)[c4];
         in.vn = f32x4{__uint_as_float(v2.x << 16), __uint_as_float(v2.x & 0xffff0000u),
                       __uint_as_float(v2.y << 16), __uint_as_float(v2.y & 0xffff0000u)};
