@@ -23,8 +23,10 @@ W_UV), the Qwen3 shape at batch 16 x 32K (with the native CPU engine, the
 pinned load region, eviction and the offloaded step measured after it), and
 the tiny single-sequence case.
 
-Timing of every decode workload: before each step a 512 MB buffer is
-rewritten so the 256 MB Infinity Cache holds no KV.  One pair of HIP events on
+Timing of every decode workload: before each step a 512 MB buffer is read
+through the caches so that neither L2 nor the 256 MB Infinity Cache holds
+any KV (a read, not a rewrite, so that no dirty lines are left to be written
+back during the step).  One pair of HIP events on
 the stream the kernels run on brackets the K (flush + step) pairs, and others
 the same K flushes alone, run right before and right after; a step's time is
 the difference (from the flushes' mean) over K.  Events are not recorded
@@ -180,6 +182,16 @@ def roofline(section, kernel, achieved_gbs, kv_bytes, what="pass 1"):
     return out
 
 
+def evict(buf):
+    """Read a 512 MiB buffer through the caches (its maximum, as int32), so
+    that neither L2 nor the 256 MB Infinity Cache holds any KV when the next
+    launch starts.  A read leaves the caches clean: a buffer rewrite would
+    also leave up to 256 MB of dirty lines whose write-back lands in the next
+    timed launch, which is the flush's cost, not the step's."""
+    import torch
+    return buf.view(torch.int32).amax()
+
+
 class Timer:
     """Stream-ordered timing with one event pair around a whole bracket."""
 
@@ -188,7 +200,7 @@ class Timer:
 
     def flush_once(self):
         if not self.no_flush:
-            self.flush.add_(1)
+            evict(self.flush)
 
     def bracket(self, fn):
         """ms of fn() on the stream, one event pair around it."""
@@ -196,7 +208,7 @@ class Timer:
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         for _ in range(3):   # a GPU backlog ahead of the bracket: the host then runs ahead of
-            self.flush.add_(1)    # the timed launches, and a host stall cannot idle the GPU inside it
+            evict(self.flush)    # the timed launches, and a host stall cannot idle the GPU inside it
         e0.record(self.stream)
         fn()
         e1.record(self.stream)
@@ -597,7 +609,7 @@ def cpu_gpu_steps(w, sess, wsk, steps_in, i0, F, splits, qs, kn, vn, o_m, l_m, f
     for f in range(F):
         i = i0 + f
         ce = [min(splits[b], sess.lengths[b]) for b in range(B)]
-        flush.add_(1)
+        evict(flush)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         if absorb:
@@ -700,7 +712,7 @@ def load_region_section(w, pf, steps_in, dev, flush, n_steps=5):
     def timed(fn, reps):
         ts = []
         for _ in range(reps):
-            flush.add_(1)
+            evict(flush)
             torch.cuda.synchronize()
             t = time.perf_counter()
             fn()
@@ -875,7 +887,7 @@ def offload_section(w, pf, steps_in, dev, flush, A_s, c_cpu_s, B_s, n_steps=3):
 
         ts = []
         for it in range(n_steps + 1):
-            flush.add_(1)
+            evict(flush)
             torch.cuda.synchronize()
             t = time.perf_counter()
             full_step()
@@ -1099,7 +1111,7 @@ def main():
     def read_gbs(workgroups):
         ms = []
         for it in range(6):
-            flush.add_(1)
+            evict(flush)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             _wsk.wsk_stream_read(probe, fold, workgroups)
@@ -1117,7 +1129,7 @@ def main():
         dst = torch.empty_like(src)
         src.fill_(1)
         for _ in range(3):
-            flush.add_(1)
+            evict(flush)
             dst.copy_(src)
         torch.cuda.synchronize()
         log("bench: copy calibration: 3 x %d bytes read + written" % src.numel())
