@@ -142,7 +142,7 @@ TRAFFIC = {
     "c5": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
            "fetch_bytes": 622066.2 * 1024 * 2.0, "write_bytes": 1151.9 * 1024 * 1.0, "kv_bytes": 1270605824},
     "c2": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
-           "fetch_bytes": 369622.1 * 1024 * 2.0, "write_bytes": 1242.0 * 1024 * 1.0, "kv_bytes": 751976448},
+           "fetch_bytes": 369622.0 * 1024 * 2.0, "write_bytes": 1242.0 * 1024 * 1.0, "kv_bytes": 751976448},
     "c1": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
            "fetch_bytes": 647.4 * 1024 * 2.0, "write_bytes": 30.5 * 1024 * 1.0, "kv_bytes": 1059328},
     # the sweep's and the MLA step's roofline kernel: pass 1 (launches alone)
