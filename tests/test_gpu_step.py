@@ -315,12 +315,17 @@ def test_decode_step_mla_expand(H, bk, dv, load):
             assert np.array_equal(_gpu_pool(sess), _gpu_pool(twin)), "pool differs after step %d" % step
 
 
-def test_decode_step_mla_expand_many_sequences_and_refusals():
+@pytest.mark.parametrize("dv", [128, 256])
+def test_decode_step_mla_expand_many_sequences_and_refusals(dv):
     """70 MLA sequences (two pass-2 launches, outputs at their offsets) through wsk_decode_step_mla
     against the oracle; a sequence listed twice and a short workspace are refused with nothing
-    changed."""
-    B, H, dv = 70, 16, 128
+    changed.  The launch of 64 sequences expands each (sequence, head) in one workgroup, that of
+    the other 6 in slices of dv / 2 columns (with dv = 256: every slice width the kernel has, with
+    the three-sequence cases above)."""
+    B, H = 70, 16
     w = _workload("mla", B, H, seed=9)
+    w = wl.Workload(w.name, w.kind, batch=w.batch, n_q_heads=H, n_kv_heads=1, head_dim=dv, latent_dim=512,
+                    rope_dim=64, nope_dim=128, context=1, kv_std=0.5, seed=w.seed)
     gen = torch.Generator().manual_seed(10)
     lengths = [int(x) for x in torch.randint(60, 300, (B,), generator=gen)]
     splits = [L // 3 for L in lengths]
