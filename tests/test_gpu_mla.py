@@ -154,6 +154,35 @@ def test_mla_absorb_and_expand_kernels():
     assert_close(o.cpu().numpy(), ref, "expand")
 
 
+@pytest.mark.parametrize("dn", [40, 64, 192, 256])
+def test_mla_absorb_widths(dn):
+    """Query absorption at other q_nope widths (1/4 to 2x the model's, and one that is not a multiple
+    of 64), 11 tokens (a partial group of 8), 3 heads, into rows wider than the latent width: each
+    bf16 output within the fp32-sum bound of the fp64 oracle's, the rest of the rows untouched."""
+    gen = torch.Generator().manual_seed(60 + dn)
+    n, H, dl, stride = 11, 3, 512, 576
+    w = wl.Workload("absorb", wl.MLA, batch=n, n_q_heads=H, n_kv_heads=1, head_dim=128, latent_dim=dl,
+                    rope_dim=64, nope_dim=dn, context=1, kv_std=0.5, seed=dn)
+    q_nope = wl.draw_bf16(gen, (n, H, dn))
+    w_uk, _ = wl.draw_mla_weights(w, gen)
+    dev = torch.device("cuda", DEV)
+    say("case absorb dn=%d" % dn)
+    out = torch.zeros(n, H, stride, dtype=torch.bfloat16, device=dev)
+    wsk.wsk_mla_absorb(to_device_bf16(q_nope, dev), to_device_bf16(w_uk, dev), out, stride)
+    got = out.cpu().view(torch.int16).numpy().view(np.uint16)
+    assert not got[:, :, dl:].any()
+    got = got[:, :, :dl]
+    for i in range(n):
+        ref = oracle.mla_absorb(q_nope[i], w_uk)
+        diff = got[i] != oracle.round_bf16(ref)
+        g = oracle.bf16_to_f64(got[i][diff])
+        r = ref[diff]
+        ulp = 2.0 ** (np.floor(np.log2(np.abs(r))) - 7)
+        s_abs = np.einsum("hk,hkl->hl", np.abs(oracle.bf16_to_f64(q_nope[i])), np.abs(oracle.bf16_to_f64(w_uk)))[diff]
+        assert np.all(np.abs(g - r) <= ulp * 0.5 + dn * 2.0 ** -24 * s_abs), (dn, i)
+        assert int(diff.sum()) <= got[i].size // 100, (dn, i, int(diff.sum()))
+
+
 def test_c4_deepseek_v2_lite_full_path():
     """Absorb -> append -> attend the GPU range -> merge with the CPU partial in
     latent space -> expand, against the oracle doing every step in fp64; then
