@@ -588,7 +588,7 @@ def cpu_baseline(w5, pf5, steps5, W, K, w1, budget_s: float):
 
 def cpu_gpu_steps(w, sess, wsk, steps_in, i0, F, splits, qs, kn, vn, o_m, l_m, flush, dev, absorb, expand,
                   gpu_ns_per_token, gpu_fixed_us):
-    """The paper's whole decode step on this box: the GPU appends and runs pass 1
+    """The paper's whole decode step on this machine: the GPU appends and runs pass 1
     over [s_b, L_b + 1) while the native CPU engine (wsk_cpu_attend) attends
     [0, s_b) in place in the host pool on every available core; the CPU partial
     is copied to the device and pass 2 merges it with the GPU chunks.  Timed on
@@ -840,7 +840,7 @@ def offload_section(w, pf, steps_in, dev, flush, A_s, c_cpu_s, B_s, n_steps=3):
     the GPU streams its share from the pinned load region (plus the D-window)
     and attends it; one LSE join.  Timed on the host clock at the all-GPU
     split (s = 0) and at CPU shares around the one Eq. 2 gives with A (CPU
-    engine) and B (streamed GPU side) measured on this box, next to Eq. 1's
+    engine) and B (streamed GPU side) measured on this machine, next to Eq. 1's
     prediction max(r A L, (1 - r) B L) + C for each share (the paper's Fig. 7
     comparison of the model with measured optima)."""
     import torch
@@ -1041,7 +1041,7 @@ def main():
         trace_summary(args.trace_summary, args.bench_json)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 

@@ -275,7 +275,7 @@ __attribute__((target("avx512f,avx512bw,avx512bf16"))) void run_item_bf16(const 
         // prefetch: the next tile's rows into L1 and the rows one block ahead
         // into L2.  A KV head's rows come in runs of one block a slot apart,
         // which the hardware prefetchers pick up late; the L2 stream keeps
-        // the L1 prefetches short (measured on the GPU machines' hosts: 15.0 ->
+        // the L1 prefetches short (measured on MI355X servers' EPYC hosts: 15.0 ->
         // 17.0 GB/s on one thread, +3-20 % on 16, against L1 only)
         {
             const int tq = t0 + 16;
