@@ -73,7 +73,7 @@ __device__ __forceinline__ int sub_token(int mt, int r) { return 8 * (r >> 2) + 
 __global__ __launch_bounds__(512, 1) void mla_attend_kernel(const AttendParams p) {
     __shared__ f32x4 s_part[2][2][4][2][64];       // 32 KB: partial S^T per team and wavefront, double-buffered
     __shared__ __attribute__((aligned(16))) uint8_t s_tr[8][8 * 1024];   // 64 KB: each wavefront's latent pieces
-    __shared__ float s_m1[16], s_l1[16];
+    __shared__ float s_mt[2][16], s_lt[2][16];      // per team: running max and normaliser of each head
 
     const int lane = threadIdx.x & 63;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -280,42 +280,46 @@ __global__ __launch_bounds__(512, 1) void mla_attend_kernel(const AttendParams p
     for (; r < rounds; ++r) step(t0 + 2 * r, st0);
 
     // ---- merge the two teams, normalise, write this wavefront's 128 columns ----
+    // Each lane holds rows r = 0..3 (heads 4 grp + r) of 8 columns; team t
+    // merges and stores rows 2t and 2t + 1, the other team's values of
+    // those rows coming through LDS, so both teams share the stores.
     float l_tot = l_lane + __shfl_xor(l_lane, 16);
     l_tot += __shfl_xor(l_tot, 32);                  // head n, in every lane of column n
     __syncthreads();                                 // s_part is free
-    float *sx = reinterpret_cast<float *>(&s_part[0][0][0][0][0]) + wave * 16 * 128;
-    if (team == 1) {
+    float *xs = reinterpret_cast<float *>(&s_part[0][0][0][0][0]);
+    // rows of merging team mt, row rr (of its two), N-tile nt: 64 lanes contiguous
+    auto slot = [&](int mt, int rr, int nt) { return xs + (((mt * 4 + wave) * 2 + rr) * kWaveNT + nt) * 64 + lane; };
 #pragma unroll
-        for (int nt = 0; nt < kWaveNT; ++nt)
+    for (int rr = 0; rr < 2; ++rr)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) sx[(4 * grp + r) * 128 + 16 * nt + n] = o[nt][r];
-        if (wave == 0 && grp == 0) {
-            s_m1[n] = m_run;
-            s_l1[n] = l_tot;
-        }
+        for (int nt = 0; nt < kWaveNT; ++nt) *slot(1 - team, rr, nt) = team == 0 ? o[nt][2 + rr] : o[nt][rr];
+    if (wave == 0 && grp == 0) {
+        s_mt[team][n] = m_run;
+        s_lt[team][n] = l_tot;
     }
     __syncthreads();
-    if (team == 1) return;
     const int part = p.chunk_begin[i] + c;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int h = 4 * grp + r;
-        const float m0 = __shfl(m_run, h), l0 = __shfl(l_tot, h);
-        const float m1 = s_m1[h], l1 = s_l1[h];
-        const float M = fmaxf(m0, m1);
-        const float w0 = __builtin_amdgcn_exp2f(m0 - M);
+    for (int rr = 0; rr < 2; ++rr) {
+        const int h = 4 * grp + 2 * team + rr;
+        const float m0 = __shfl(m_run, h), l0 = __shfl(l_tot, h);   // this team's (-inf if it read no tile)
+        const float m1 = s_mt[1 - team][h], l1 = s_lt[1 - team][h];
+        const float M = fmaxf(m0, m1);                  // finite: team 0 reads at least one tile
+        const float w0 = m0 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m0 - M);
         const float w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
         const float den = w0 * l0 + w1 * l1;
         const float inv = 1.f / den;
         if (h < H) {
             float *dst = p.part_o + ((int64_t)part * H + h) * kLatent + 128 * wave + n;
 #pragma unroll
-            for (int nt = 0; nt < kWaveNT; ++nt)
-                dst[16 * nt] = (w0 * o[nt][r] + w1 * sx[h * 128 + 16 * nt + n]) * inv;
+            for (int nt = 0; nt < kWaveNT; ++nt) {
+                const float own = team == 0 ? o[nt][rr] : o[nt][2 + rr];
+                dst[16 * nt] = (w0 * own + w1 * *slot(team, rr, nt)) * inv;
+            }
         }
     }
-    if (wave == 0 && grp == 0 && n < H) {
-        const float m1 = s_m1[n], l1 = s_l1[n];
+    if (team == 0 && wave == 0 && grp == 0 && n < H) {
+        const float m1 = s_mt[1][n], l1 = s_lt[1][n];
         const float M = fmaxf(m_run, m1);
         const float den = __builtin_amdgcn_exp2f(m_run - M) * l_tot +
                           (m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M) * l1);
