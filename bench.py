@@ -140,9 +140,9 @@ def wsk_mod():
 TRAFFIC = {
     # the decode steps' roofline kernel: gqa_step_kernel (timed steps)
     "c5": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
-           "fetch_bytes": 622066.2 * 1024 * 2.0, "write_bytes": 1151.9 * 1024 * 1.0, "kv_bytes": 1270605824},
+           "fetch_bytes": 622065.4 * 1024 * 2.0, "write_bytes": 1151.9 * 1024 * 1.0, "kv_bytes": 1270605824},
     "c2": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
-           "fetch_bytes": 369622.0 * 1024 * 2.0, "write_bytes": 1242.0 * 1024 * 1.0, "kv_bytes": 751976448},
+           "fetch_bytes": 369623.6 * 1024 * 2.0, "write_bytes": 1242.0 * 1024 * 1.0, "kv_bytes": 751976448},
     "c1": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
            "fetch_bytes": 647.4 * 1024 * 2.0, "write_bytes": 30.5 * 1024 * 1.0, "kv_bytes": 1059328},
     # the sweep's and the MLA step's roofline kernel: pass 1 (launches alone)
@@ -154,7 +154,7 @@ TRAFFIC = {
            "fetch_bytes": 524493.0 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 1073741824},
     "c3 r=0.75": {"source": "paper_2609_14507_amd/csrc/attend_gqa.hip", "sha256": "dd13240b9482a9c2d0850924fc7ec9e9ae79171c2f848167129493327e6cfac1",
            "fetch_bytes": 262285.0 * 1024 * 2.0, "write_bytes": 390.0 * 1024 * 1.0, "kv_bytes": 536870912},
-    "c4": {"source": "paper_2609_14507_amd/csrc/attend_mla.hip", "sha256": "4df8a57ec4065ad10e72b3e174e71bce14707792ab7dea83e03b7889f82faa92",
+    "c4": {"source": "paper_2609_14507_amd/csrc/attend_mla.hip", "sha256": "fc7de28eef1c19d2054c21535bb9ce8b390632da3c964280ae047638d62b3edb",
            "fetch_bytes": 177748.1 * 1024 * 2.0, "write_bytes": 8208.0 * 1024 * 1.0, "kv_bytes": 362575872},
 }
 
